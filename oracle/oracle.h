@@ -1,0 +1,81 @@
+/*
+ * oracle.h -- serial CPU reference for the scan hot path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path (the HIP library and
+ * its Python binding) includes, links or calls this code.  Only the tests, the
+ * smoke check and the benchmark's CPU-baseline leg use it.
+ *
+ * Each function is the plain definition of what an operation of
+ * "Parallel Scan on Ascend AI Accelerators" (Wroblewski, Gottardo, Zouzias)
+ * computes, written as one serial loop: no tiling, no reordering.
+ *   - integer sums wrap modulo 2^32 (accumulated in uint32_t);
+ *   - floating-point sums are accumulated in double and returned in double,
+ *     together with the running sum of |x| that the float tolerance uses.
+ * All pointers are host pointers owned by the caller; nothing is allocated
+ * except the temporary array of oracle_sort_u32.
+ */
+#ifndef LIBSCAN_ORACLE_H
+#define LIBSCAN_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Section 2 (Background): the inclusive prefix sum y_i = x_1 + ... + x_i. */
+void oracle_scan_inclusive_i32(const int32_t* x, uint32_t* y, int64_t n);
+/* Appendix "Exclusive and int8 scan": the inclusive result shifted right by
+ * one, the last value dropped, zero in front. */
+void oracle_scan_exclusive_i32(const int32_t* x, uint32_t* y, int64_t n);
+
+/* Float scans: y = prefix sums in double, a = prefix sums of |x| in double
+ * (a may be NULL). */
+void oracle_scan_inclusive_f32(const float* x, double* y, double* a, int64_t n);
+void oracle_scan_exclusive_f32(const float* x, double* y, double* a, int64_t n);
+
+/* IEEE 754 binary16 bit pattern -> exact double value. */
+double oracle_half_to_double(uint16_t h);
+/* fp16 input (raw bit patterns), every value converted exactly to double. */
+void oracle_scan_inclusive_f16(const uint16_t* x, double* y, double* a, int64_t n);
+void oracle_scan_exclusive_f16(const uint16_t* x, double* y, double* a, int64_t n);
+
+/* Appendix "Exclusive and int8 scan": 8-bit inputs summed as integers into a
+ * 32-bit result (mod 2^32).  *total (may be NULL) receives the full sum. */
+void oracle_scan_exclusive_u8(const uint8_t* x, uint32_t* y, int64_t n, uint32_t* total);
+void oracle_scan_inclusive_u8(const uint8_t* x, uint32_t* y, int64_t n);
+
+/* Appendix "Multiple (Batched) Scans": an independent scan of every row of a
+ * row-major rows x len matrix. */
+void oracle_scan_rows_i32(const int32_t* x, uint32_t* y, int64_t rows, int64_t len, int exclusive);
+void oracle_scan_rows_f32(const float* x, double* y, double* a, int64_t rows, int64_t len,
+                          int exclusive);
+
+/* Section 5 "Compress": keep x_i where mask_i != 0, in index order; idx (may
+ * be NULL) receives the source indices.  Returns the number kept. */
+int64_t oracle_compact_f32(const float* x, const uint8_t* mask, float* out, int32_t* idx,
+                           int64_t n);
+
+/* Section 5 "Split": the flagged items first, then the unflagged ones, each
+ * group in index order.  idx_in NULL means the identity.  Returns the number
+ * flagged. */
+int64_t oracle_split_u32(const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags,
+                         uint32_t* keys_out, int32_t* idx_out, int64_t n);
+
+/* Section 5 "Radix Sort": the result radix sort must reach -- a stable
+ * ascending sort of unsigned keys.  perm_out[i] is the source index of
+ * keys_out[i].  Defined as the lexicographic order of (key, source index).
+ * Returns 0, or -1 if the temporary array cannot be allocated. */
+int oracle_sort_u32(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out, int64_t n);
+
+/* Section 5 "Top-p or Nucleus Sampling": per row of probabilities already
+ * sorted in descending order, the first index whose inclusive running sum
+ * (in double) reaches p, or len - 1 if it never does. */
+void oracle_topp_cutoff_f32(const float* probs, int32_t* cutoff, int64_t rows, int64_t len,
+                            float p);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif

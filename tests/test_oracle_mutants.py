@@ -1,0 +1,79 @@
+"""Planted mistakes in the oracle (on the CPU) must fail at least one pin.
+
+Each mutant is oracle.c with one plausible slip -- a dropped term, a wrong sign
+or index, an operand swapped, a comparison flipped -- compiled into a temporary
+library and run through the pins of oracle_pins.py.  A mutant that passes every
+pin would show a blind spot in the pins.
+"""
+import os
+
+import pytest
+
+import oracle
+from oracle import build as obuild
+import oracle_pins as P
+
+MUTANTS = {
+    "inclusive_i32_off_by_one": (
+        "        acc += (uint32_t)x[i];\n        y[i] = acc;\n    }\n}\n\n/* ---- Appendix \"Exclusive",
+        "        y[i] = acc;\n        acc += (uint32_t)x[i];\n    }\n}\n\n/* ---- Appendix \"Exclusive"),
+    "exclusive_i32_wrong_index": (
+        "        y[i] = acc;\n        acc += (uint32_t)x[i];\n    }\n}\n\nvoid oracle_scan_inclusive_f32",
+        "        y[i] = acc;\n        acc += (uint32_t)x[i > 0 ? i - 1 : 0];\n    }\n}\n\nvoid oracle_scan_inclusive_f32"),
+    "inclusive_f32_sign": (
+        "        acc += (double)x[i];\n        aacc += fabs((double)x[i]);\n        y[i] = acc;",
+        "        acc -= (double)x[i];\n        aacc += fabs((double)x[i]);\n        y[i] = acc;"),
+    "inclusive_f32_float_accumulator": (
+        "        acc += (double)x[i];\n        aacc += fabs((double)x[i]);\n        y[i] = acc;",
+        "        acc = (float)(acc + (double)x[i]);\n        aacc += fabs((double)x[i]);\n        y[i] = acc;"),
+    "abs_prefix_dropped_fabs": (
+        "        acc += (double)x[i];\n        aacc += fabs((double)x[i]);\n        y[i] = acc;",
+        "        acc += (double)x[i];\n        aacc += (double)x[i];\n        y[i] = acc;"),
+    "exclusive_f32_inclusive_order": (
+        "        y[i] = acc;\n        if (a) a[i] = aacc;\n        acc += (double)x[i];",
+        "        acc += (double)x[i];\n        y[i] = acc;\n        if (a) a[i] = aacc;"),
+    "half_exponent_bias": ("(1024 + f), e - 25)", "(1024 + f), e - 24)"),
+    "half_subnormal_scale": ("ldexp((double)f, -24)", "ldexp((double)f, -25)"),
+    "inclusive_f16_dropped_term": (
+        "        const double v = oracle_half_to_double(x[i]);\n        acc += v;",
+        "        const double v = oracle_half_to_double(x[i]);\n        acc += (i > 0) ? v : 0.0;"),
+    "u8_signed_bytes": (
+        "        y[i] = acc;\n        acc += (uint32_t)x[i];\n    }\n    if (total)",
+        "        y[i] = acc;\n        acc += (uint32_t)(int8_t)x[i];\n    }\n    if (total)"),
+    "rows_wrong_input_offset": (
+        "oracle_scan_inclusive_i32(x + r * len, y + r * len, len);",
+        "oracle_scan_inclusive_i32(x + r, y + r * len, len);"),
+    "compact_only_ones": ("if (mask[i] != 0) {", "if (mask[i] == 1) {"),
+    "split_unstable_second_part": (
+        "for (int64_t i = 0; i < n; ++i) { /* second pass",
+        "for (int64_t i = n - 1; i >= 0; --i) { /* second pass"),
+    "split_ignores_idx_in": (
+        "            if (idx_out) idx_out[c] = idx_in ? idx_in[i] : (int32_t)i;\n            ++c;\n        }\n    }\n    const int64_t",
+        "            if (idx_out) idx_out[c] = (int32_t)i;\n            ++c;\n        }\n    }\n    const int64_t"),
+    "sort_descending": ("return a->key < b->key ? -1 : 1;", "return a->key < b->key ? 1 : -1;"),
+    "sort_ties_reversed": ("return a->index < b->index ? -1 : (a->index > b->index ? 1 : 0);",
+                           "return a->index < b->index ? 1 : (a->index > b->index ? -1 : 0);"),
+    "topp_strict_comparison": ("if (c >= pd) {", "if (c > pd) {"),
+    "topp_default_len": ("int64_t k = len - 1;", "int64_t k = len;"),
+    "topp_exclusive_sum": ("            c += (double)row[i];\n            if (c >= pd) {",
+                           "            if (c >= pd) {\n                k = i;\n                break;\n"
+                           "            }\n            c += (double)row[i];\n            if (0) {"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, tmp_path):
+    old, new = MUTANTS[name]
+    src = open(obuild.SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique/found"
+    mutated = tmp_path / "oracle_mutant.c"
+    mutated.write_text(src.replace(old, new))
+    lib = obuild.compile_source(str(mutated), str(tmp_path / "liboracle_mutant.so"))
+    o = oracle.Oracle(lib)
+    failed = []
+    for check in P.ALL_CHECKS:
+        try:
+            check(o)
+        except AssertionError:
+            failed.append(check.__name__)
+    assert failed, f"mutant {name} passed every pin"
