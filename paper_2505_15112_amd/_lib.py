@@ -1,0 +1,95 @@
+"""ctypes loader for libscan.so: signatures mirror include/libscan.h exactly.
+
+The library is loaded after ``import torch`` so that it binds to the HIP
+runtime torch has already loaded (same soname) instead of a second copy; the
+stream handles torch hands out are then valid inside the library.
+"""
+import ctypes
+import os
+import re
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libscan.so")
+HEADER = os.path.join(os.path.dirname(PKG), "include", "libscan.h")
+
+_p = ctypes.c_void_p
+_i64 = ctypes.c_int64
+_int = ctypes.c_int
+_sz = ctypes.c_size_t
+
+# name -> (restype, argtypes)
+SIGNATURES = {
+    "libscan_version": (_int, []),
+    "libscan_status_string": (ctypes.c_char_p, [_int]),
+    "libscan_workspace_bytes": (_int, [_int, _i64, _i64, _i64, _int, ctypes.POINTER(_sz)]),
+    "libscan_workspace_init": (_int, [_p, _sz, _p]),
+    "scan_inclusive_i32": (_int, [_p, _p, _i64, _p, _sz, _p]),
+    "scan_exclusive_i32": (_int, [_p, _p, _i64, _p, _sz, _p]),
+    "scan_inclusive_f32": (_int, [_p, _p, _i64, _p, _sz, _p]),
+    "scan_exclusive_f32": (_int, [_p, _p, _i64, _p, _sz, _p]),
+    "scan_inclusive_f16f32": (_int, [_p, _p, _i64, _p, _sz, _p]),
+    "scan_exclusive_f16f32": (_int, [_p, _p, _i64, _p, _sz, _p]),
+    "scan_exclusive_u8i32": (_int, [_p, _p, _i64, _p, _p, _sz, _p]),
+    "scan_inclusive_i32_carry": (_int, [_p, _p, _i64, _p, _p, _p, _sz, _p]),
+    "scan_exclusive_i32_carry": (_int, [_p, _p, _i64, _p, _p, _p, _sz, _p]),
+    "scan_inclusive_f32_carry": (_int, [_p, _p, _i64, _p, _p, _p, _sz, _p]),
+    "scan_exclusive_f32_carry": (_int, [_p, _p, _i64, _p, _p, _p, _sz, _p]),
+    "scan_inclusive_rss_i32": (_int, [_p, _p, _i64, _p, _sz, _p]),
+    "scan_inclusive_rss_f32": (_int, [_p, _p, _i64, _p, _sz, _p]),
+}
+
+OK, EINVAL, ENOSPACE, EHIP, ERANGE = 0, -1, -2, -3, -4
+OP_SCAN, OP_SCAN_RSS = 1, 2
+
+_LIB = None
+
+
+class LibscanError(RuntimeError):
+    def __init__(self, name, status, lib):
+        msg = lib.libscan_status_string(status).decode() if lib is not None else "?"
+        super().__init__(f"{name} failed: {status} ({msg})")
+        self.status = status
+
+
+def header_functions(path: str = HEADER):
+    """Names of the functions include/libscan.h declares."""
+    text = open(path).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+def load(path: str = LIB_PATH):
+    """Load libscan.so once (after torch, see module docstring)."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    import torch  # noqa: F401  -- bind to torch's HIP runtime (see module docstring)
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"{path} is not built; run `python -m paper_2505_15112_amd.build` "
+            "(there is no fallback path)")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _LIB = lib
+    return lib
+
+
+def call(name: str, *args):
+    """Call an entry point; raise LibscanError on a non-zero status."""
+    lib = load()
+    st = getattr(lib, name)(*args)
+    if st != OK:
+        raise LibscanError(name, st, lib)
+    return st
+
+
+def workspace_bytes(op: int, n: int = 0, rows: int = 0, length: int = 0, bits: int = 0) -> int:
+    lib = load()
+    out = _sz(0)
+    st = lib.libscan_workspace_bytes(op, n, rows, length, bits, ctypes.byref(out))
+    if st != OK:
+        raise LibscanError("libscan_workspace_bytes", st, lib)
+    return out.value

@@ -1,0 +1,173 @@
+// tile.hpp -- the workgroup tile shared by every scan kernel.
+//
+// A tile is WAVES wavefronts x J chunks x 64 lanes x V elements, laid out so
+// that chunk j of wave w covers 64*V contiguous elements and lane l owns V
+// contiguous elements of it:
+//     element(w, j, l, e) = tile_base + ((w*J + j)*64 + l)*V + e.
+// One chunk is therefore one fully coalesced vector load per lane (16 bytes
+// for 32-bit data with V = 4), and a wave reads J*64*V contiguous elements.
+// The tile scan is: serial scan of the V elements in each lane, a DPP
+// wavefront scan of the 64 lane totals per chunk, a running carry over the J
+// chunks of the wave, and the wave totals combined through LDS.
+#pragma once
+
+#include "device.hpp"
+
+namespace ls {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// ---------------------------------------------------------------- conversion
+
+template <class In, class T>
+struct Conv;
+template <>
+struct Conv<uint32_t, uint32_t> {
+    __device__ static uint32_t f(uint32_t v) { return v; }
+};
+template <>
+struct Conv<float, float> {
+    __device__ static float f(float v) { return v; }
+};
+template <>
+struct Conv<uint16_t, float> {  // IEEE binary16 bits -> fp32 (exact)
+    __device__ static float f(uint16_t v) { return (float)__builtin_bit_cast(_Float16, v); }
+};
+template <>
+struct Conv<uint8_t, uint32_t> {  // unsigned byte value
+    __device__ static uint32_t f(uint8_t v) { return v; }
+};
+
+// Aligned vector load of V elements of In, converted to T.
+template <class In, class T, int V>
+__device__ __forceinline__ void load_vec(const In* p, T (&out)[V]) {
+    constexpr int kBytes = V * (int)sizeof(In);
+    In e[V];
+    if constexpr (kBytes == 16) {
+        const u32x4 r = *reinterpret_cast<const u32x4*>(p);
+        __builtin_memcpy(e, &r, 16);
+    } else if constexpr (kBytes == 8) {
+        const u32x2 r = *reinterpret_cast<const u32x2*>(p);
+        __builtin_memcpy(e, &r, 8);
+    } else if constexpr (kBytes == 4) {
+        const uint32_t r = *reinterpret_cast<const uint32_t*>(p);
+        __builtin_memcpy(e, &r, 4);
+    } else {
+        static_assert(kBytes == 16 || kBytes == 8 || kBytes == 4, "unsupported vector width");
+    }
+#pragma unroll
+    for (int i = 0; i < V; ++i) out[i] = Conv<In, T>::f(e[i]);
+}
+
+// Aligned vector store of V 32-bit elements (V = 4: one 16-byte store).
+template <class T, int V>
+__device__ __forceinline__ void store_vec(T* p, const T (&v)[V]) {
+    static_assert(sizeof(T) == 4 && V == 4, "16-byte stores of 32-bit elements");
+    u32x4 r;
+    __builtin_memcpy(&r, v, 16);
+    __builtin_nontemporal_store(r, reinterpret_cast<u32x4*>(p));
+}
+
+// ---------------------------------------------------------------- the tile
+
+template <class In_, class T_, int V_, int J_, int WAVES_>
+struct Tile {
+    using In = In_;
+    using T = T_;
+    static constexpr int V = V_;
+    static constexpr int J = J_;
+    static constexpr int WAVES = WAVES_;
+    static constexpr int kThreads = WAVES * kWave;
+    static constexpr int kElems = WAVES * J * kWave * V;
+
+    __device__ static int64_t offset(int64_t base, int j) {
+        const int w = threadIdx.x / kWave;
+        return base + ((int64_t)(w * J + j) * kWave + lane_id()) * V;
+    }
+
+    // Load the tile starting at `base`; elements at or past n read as zero.
+    template <bool VEC>
+    __device__ static void load(const In* x, int64_t n, int64_t base, T (&v)[J][V]) {
+        if (VEC && base + kElems <= n) {  // uniform: all vector loads issued back to back
+#pragma unroll
+            for (int j = 0; j < J; ++j) load_vec<In, T, V>(x + offset(base, j), v[j]);
+        } else {
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                const int64_t off = offset(base, j);
+#pragma unroll
+                for (int e = 0; e < V; ++e)
+                    v[j][e] = (off + e < n) ? Conv<In, T>::f(x[off + e]) : T(0);
+            }
+        }
+    }
+
+    // In-lane inclusive scans and wavefront scans.  Afterwards v[j][e] is the
+    // inclusive prefix of the lane's own elements and lane_off[j] the sum of
+    // everything in the wave before the lane's chunk-j elements.  Returns the
+    // wave's total (uniform).
+    __device__ static T wave_scan(T (&v)[J][V], T (&lane_off)[J]) {
+        T run = T(0);
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+#pragma unroll
+            for (int e = 1; e < V; ++e) v[j][e] = v[j][e - 1] + v[j][e];
+            const T inc = wave_incl_scan(v[j][V - 1]);
+            lane_off[j] = run + wave_shr1(inc);
+            run = run + lane_read(inc, kWave - 1);
+        }
+        return run;
+    }
+
+    // Sum of the lane's elements (no scan), for reductions.
+    __device__ static T lane_sum(const T (&v)[J][V]) {
+        T s = T(0);
+#pragma unroll
+        for (int j = 0; j < J; ++j)
+#pragma unroll
+            for (int e = 0; e < V; ++e) s = s + v[j][e];
+        return s;
+    }
+
+    // Combine wave totals through LDS: returns the tile aggregate; *wofs gets
+    // the sum of the waves before this one.  Contains a barrier.
+    __device__ static T combine_waves(T wave_total, T* s_wtot, T* wofs) {
+        const int w = threadIdx.x / kWave;
+        if (lane_id() == 0) s_wtot[w] = wave_total;
+        __syncthreads();
+        T before = T(0), agg = T(0);
+#pragma unroll
+        for (int k = 0; k < WAVES; ++k) {
+            const T t = s_wtot[k];
+            if (k < w) before = before + t;
+            agg = agg + t;
+        }
+        *wofs = before;
+        return agg;
+    }
+
+    // Store carry + scanned values (inclusive or exclusive); only i < n.
+    template <bool EXCL, bool VEC>
+    __device__ static void store(T* y, int64_t n, int64_t base, const T (&v)[J][V],
+                                 const T (&lane_off)[J], T carry) {
+        const bool full = VEC && base + kElems <= n;
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const int64_t off = offset(base, j);
+            const T lb = carry + lane_off[j];
+            T o[V];
+#pragma unroll
+            for (int e = 0; e < V; ++e) o[e] = EXCL ? (e == 0 ? lb : lb + v[j][e - 1]) : lb + v[j][e];
+            if (full) {
+                store_vec<T, V>(y + off, o);
+            } else {
+#pragma unroll
+                for (int e = 0; e < V; ++e)
+                    if (off + e < n) y[off + e] = o[e];
+            }
+        }
+    }
+};
+
+}  // namespace ls

@@ -1,0 +1,101 @@
+"""libscan.so on the CPU: it loads without a GPU, exports every function that
+include/libscan.h declares, and rejects bad arguments before any HIP call.
+
+No call here reaches a kernel launch: every call made with fake device
+addresses fails validation first, by construction of its arguments.
+"""
+import ctypes
+import os
+
+import pytest
+
+from paper_2505_15112_amd import _lib
+
+if not os.path.exists(_lib.LIB_PATH):  # load what is built; build only if nothing is
+    from paper_2505_15112_amd import build as _build
+    _build.build()
+
+P = ctypes.c_void_p
+X = P(0x100000)      # fake, never dereferenced
+Y = P(0x900000)
+WS = P(0x4000000)
+BIG = 1 << 30
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return _lib.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    declared = _lib.header_functions()
+    assert len(declared) >= 16
+    for name in declared:
+        assert hasattr(lib, name), name
+        assert name in _lib.SIGNATURES, f"{name} missing from the binding"
+    assert sorted(_lib.SIGNATURES) == declared
+
+
+def test_version_and_strings(lib):
+    assert lib.libscan_version() >= 100
+    for st in (0, -1, -2, -3, -4, 7):
+        assert isinstance(lib.libscan_status_string(st), bytes)
+    assert lib.libscan_status_string(-2) == b"workspace too small"
+
+
+def test_workspace_bytes(lib):
+    out = ctypes.c_size_t(0)
+    assert lib.libscan_workspace_bytes(_lib.OP_SCAN, 0, 0, 0, 0, ctypes.byref(out)) == 0
+    small = out.value
+    assert lib.libscan_workspace_bytes(_lib.OP_SCAN, 1 << 28, 0, 0, 0, ctypes.byref(out)) == 0
+    assert out.value >= small + 8 * ((1 << 28) // 8192)
+    assert lib.libscan_workspace_bytes(_lib.OP_SCAN_RSS, 1 << 20, 0, 0, 0, ctypes.byref(out)) == 0
+    assert lib.libscan_workspace_bytes(99, 10, 0, 0, 0, ctypes.byref(out)) == _lib.EINVAL
+    assert lib.libscan_workspace_bytes(_lib.OP_SCAN, -1, 0, 0, 0, ctypes.byref(out)) == _lib.EINVAL
+    assert lib.libscan_workspace_bytes(_lib.OP_SCAN, 10, 0, 0, 0, None) == _lib.EINVAL
+    assert lib.libscan_workspace_bytes(_lib.OP_SCAN, 1 << 40, 0, 0, 0,
+                                       ctypes.byref(out)) == _lib.ERANGE
+
+
+SCANS = ["scan_inclusive_i32", "scan_exclusive_i32", "scan_inclusive_f32", "scan_exclusive_f32",
+         "scan_inclusive_f16f32", "scan_exclusive_f16f32", "scan_inclusive_rss_i32",
+         "scan_inclusive_rss_f32"]
+
+
+@pytest.mark.parametrize("name", SCANS)
+def test_scan_validation(lib, name):
+    fn = getattr(lib, name)
+    assert fn(X, Y, -1, WS, BIG, None) == _lib.EINVAL           # negative size
+    assert fn(None, Y, 10, WS, BIG, None) == _lib.EINVAL        # NULL input
+    assert fn(X, None, 10, WS, BIG, None) == _lib.EINVAL        # NULL output
+    assert fn(X, P(0x100004), 100, WS, BIG, None) == _lib.EINVAL  # partial overlap
+    assert fn(X, Y, 1 << 40, WS, BIG, None) == _lib.ERANGE      # too long
+    assert fn(X, Y, 1 << 20, WS, 8, None) == _lib.ENOSPACE      # workspace too small
+    assert fn(X, Y, 1 << 20, P(0x4000004), BIG, None) == _lib.EINVAL  # misaligned workspace
+    assert fn(X, Y, 1 << 20, None, BIG, None) == _lib.EINVAL    # NULL workspace
+    assert fn(None, None, 0, None, 0, None) == _lib.OK          # empty: nothing to do
+
+
+def test_mixed_type_scans_reject_any_overlap(lib):
+    # fp16 in / fp32 out may not alias at all, not even exactly
+    assert lib.scan_inclusive_f16f32(X, X, 100, WS, BIG, None) == _lib.EINVAL
+    assert lib.scan_exclusive_u8i32(X, X, 100, None, WS, BIG, None) == _lib.EINVAL
+
+
+def test_carry_validation(lib):
+    for name in ("scan_inclusive_i32_carry", "scan_exclusive_i32_carry",
+                 "scan_inclusive_f32_carry", "scan_exclusive_f32_carry"):
+        fn = getattr(lib, name)
+        assert fn(X, Y, -5, None, None, WS, BIG, None) == _lib.EINVAL
+        # total written inside the output range
+        assert fn(X, Y, 100, None, P(0x900008), WS, BIG, None) == _lib.EINVAL
+        assert fn(X, Y, 1 << 20, None, None, WS, 16, None) == _lib.ENOSPACE
+
+
+def test_python_binding_needs_gpu_tensors():
+    import torch
+    from paper_2505_15112_amd import ops
+    with pytest.raises(ValueError):
+        ops.scan_inclusive_i32(torch.zeros(10, dtype=torch.int32))
+    with pytest.raises(TypeError):
+        ops.scan_inclusive_i32(torch.zeros(10, dtype=torch.int64))

@@ -1,0 +1,206 @@
+"""GPU parity of the 1-D scans against the CPU oracle, through the C ABI.
+
+Integers: bit-exact.  Floats: |y - ref| <= 1e-5 * prefix(|x|) + 1e-6 against
+the float64 oracle, plus bit-exact runs on {-1, 0, 1} inputs (every partial
+sum is an integer far below 2^24, so any summation order is exact).
+Sizes span sub-wave, sub-tile, several tiles with ragged tails (tile = 4096
+elements), the workloads' full sizes, misaligned views and in-place calls.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import (FULL, announce, assert_equal_first_diff, assert_float_close, to_dev,
+                      to_host)
+from paper_2505_15112_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+SIZES = [1, 2, 63, 64, 65, 255, 256, 257, 1023, 4095, 4096, 4097, 3 * 4096 + 5, 65536,
+         (1 << 20) + 17]
+
+
+@pytest.fixture(scope="module")
+def ops():
+    from paper_2505_15112_amd import ops
+    return ops
+
+
+@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("excl", [False, True])
+def test_i32(ops, n, excl):
+    announce("i32", n, excl)
+    x = W.scan_i32_full_range(n, seed=n)
+    fn = ops.scan_exclusive_i32 if excl else ops.scan_inclusive_i32
+    y = to_host(fn(to_dev(x)))
+    assert_equal_first_diff(y, oracle.scan_i32(x, exclusive=excl), f"i32 n={n}")
+
+
+@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("excl", [False, True])
+def test_f32(ops, n, excl):
+    announce("f32", n, excl)
+    x = W.scan_f32(n, seed=n)
+    fn = ops.scan_exclusive_f32 if excl else ops.scan_inclusive_f32
+    y = to_host(fn(to_dev(x)))
+    ref, a = oracle.scan_f32(x, exclusive=excl)
+    assert_float_close(y, ref, a, f"f32 n={n}")
+    xe = W.exact_pm1(n, seed=n + 1)
+    ye = to_host(fn(to_dev(xe)))
+    refe, _ = oracle.scan_f32(xe, exclusive=excl)
+    assert_equal_first_diff(ye.astype(np.float64), refe, f"f32 exact n={n}")
+
+
+@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("excl", [False, True])
+def test_f16f32(ops, n, excl):
+    announce("f16f32", n, excl)
+    x = W.scan_f16(n, seed=n)
+    fn = ops.scan_exclusive_f16f32 if excl else ops.scan_inclusive_f16f32
+    y = to_host(fn(to_dev(x)))
+    ref, a = oracle.scan_f16(x, exclusive=excl)
+    assert_float_close(y, ref, a, f"f16 n={n}")
+    xe = W.exact_pm1(n, seed=n + 2, dtype=np.float16)
+    ye = to_host(fn(to_dev(xe)))
+    refe, _ = oracle.scan_f16(xe, exclusive=excl)
+    assert_equal_first_diff(ye.astype(np.float64), refe, f"f16 exact n={n}")
+
+
+@pytest.mark.parametrize("n", SIZES)
+def test_u8i32(ops, n):
+    announce("u8i32", n)
+    x = W.bytes_u8(n, seed=n)
+    y, total = ops.scan_exclusive_u8i32(to_dev(x))
+    ref, rtot = oracle.scan_u8(x)
+    assert_equal_first_diff(to_host(y), ref, f"u8 n={n}")
+    assert int(to_host(total)[0]) == rtot
+
+
+def test_empty(ops):
+    import torch
+    announce("empty")
+    e = torch.empty(0, dtype=torch.int32, device="cuda")
+    assert ops.scan_inclusive_i32(e).numel() == 0
+    y, tot = ops.scan_exclusive_u8i32(torch.empty(0, dtype=torch.uint8, device="cuda"))
+    assert y.numel() == 0 and int(tot.item()) == 0
+    cin = torch.tensor([7], dtype=torch.int32, device="cuda")
+    _, t = ops.scan_inclusive_i32_carry(e, carry_in=cin)
+    assert int(t.item()) == 7
+
+
+@pytest.mark.parametrize("n", [5, 4097, 100_003])
+def test_misaligned_and_inplace(ops, n):
+    import torch
+    announce("misaligned/inplace", n)
+    x = W.scan_i32_full_range(n + 1, seed=3)
+    xd = to_dev(x)
+    y = torch.empty(n + 1, dtype=torch.int32, device="cuda")
+    ops.scan_inclusive_i32(xd[1:], out=y[1:])  # both 4 bytes off 16-byte alignment
+    assert_equal_first_diff(to_host(y[1:]), oracle.scan_i32(x[1:]), "misaligned")
+    z = xd.clone()
+    ops.scan_inclusive_i32(z, out=z)  # in place
+    assert_equal_first_diff(to_host(z), oracle.scan_i32(x), "in-place")
+    xf = W.scan_f32(n + 1, seed=4)
+    yf = ops.scan_exclusive_f32(to_dev(xf)[1:])
+    ref, a = oracle.scan_f32(xf[1:], exclusive=True)
+    assert_float_close(to_host(yf), ref, a, "misaligned f32")
+
+
+@pytest.mark.parametrize("excl", [False, True])
+def test_carry_chunks(ops, excl):
+    """Three chunked calls chained through carry_in / total_out equal one call."""
+    import torch
+    announce("carry chunks", excl)
+    n = 3 * 4096 * 7 + 123
+    x = W.scan_i32_full_range(n, seed=9)
+    xd = to_dev(x)
+    y = torch.empty_like(xd)
+    carry = torch.zeros(1, dtype=torch.int32, device="cuda")
+    fn = ops.scan_exclusive_i32_carry if excl else ops.scan_inclusive_i32_carry
+    cuts = [0, 4096 * 5 + 7, 4096 * 13, n]
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        fn(xd[a:b], carry_in=carry, out=y[a:b], total_out=carry)
+    assert_equal_first_diff(to_host(y), oracle.scan_i32(x, exclusive=excl), "carry chunks")
+    assert int(to_host(carry)[0]) == int(oracle.scan_i32(x)[-1])
+    xf = W.exact_pm1(n, seed=10)
+    xfd = to_dev(xf)
+    yf = torch.empty_like(xfd)
+    cf = torch.tensor([0.5], dtype=torch.float32, device="cuda")
+    fnf = ops.scan_exclusive_f32_carry if excl else ops.scan_inclusive_f32_carry
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        fnf(xfd[a:b], carry_in=cf, out=yf[a:b], total_out=cf)
+    ref, _ = oracle.scan_f32(xf, exclusive=excl)
+    assert_equal_first_diff(to_host(yf).astype(np.float64), ref + 0.5, "carry chunks f32")
+
+
+@pytest.mark.parametrize("n", [1, 4096, 4097, 65536 + 3, (1 << 20) + 17])
+def test_rss_matches_lookback(ops, n):
+    announce("rss", n)
+    x = W.scan_i32_full_range(n, seed=11)
+    xd = to_dev(x)
+    a = to_host(ops.scan_inclusive_rss_i32(xd))
+    b = to_host(ops.scan_inclusive_i32(xd))
+    assert_equal_first_diff(a, oracle.scan_i32(x), "rss")
+    assert_equal_first_diff(a, b, "rss vs lookback")
+    xf = W.scan_f32(n, seed=12)
+    yf = to_host(ops.scan_inclusive_rss_f32(to_dev(xf)))
+    ref, ab = oracle.scan_f32(xf)
+    assert_float_close(yf, ref, ab, "rss f32")
+
+
+def test_repeat_no_race(ops):
+    """The same input 100 times: the look-back must give one result every time."""
+    import torch
+    announce("repeat x100")
+    n = (1 << 22) + 9
+    x = W.scan_i32_full_range(n, seed=13)
+    xd = to_dev(x)
+    ref = to_dev(oracle.scan_i32(x))
+    y = torch.empty_like(xd)
+    ws = ops.workspace(1, xd.device, n)
+    bad = 0
+    for _ in range(100):
+        ops.scan_inclusive_i32(xd, out=y, ws=ws)
+        bad += int((y != ref).sum().item())
+    assert bad == 0
+
+
+def test_config_scan_i32_n2_16(ops):
+    announce("config i32 n=2^16")
+    x = W.scan_i32(1 << 16, seed=0)
+    assert_equal_first_diff(to_host(ops.scan_inclusive_i32(to_dev(x))), oracle.scan_i32(x), "c1")
+
+
+def test_config_f16f32_n2_24(ops):
+    announce("config f16f32 n=2^24")
+    for seed in (0, 1, 2):
+        x = W.scan_f16(1 << 24, seed=seed)
+        y = to_host(ops.scan_inclusive_f16f32(to_dev(x)))
+        ref, a = oracle.scan_f16(x)
+        assert_float_close(y, ref, a, f"c2 seed {seed}")
+    xe = W.exact_pm1(1 << 24, seed=5, dtype=np.float16)
+    ye = to_host(ops.scan_inclusive_f16f32(to_dev(xe)))
+    assert_equal_first_diff(ye.astype(np.float64), oracle.scan_f16(xe)[0], "c2 exact")
+
+
+@pytest.mark.skipif(not FULL, reason="full-size cases disabled")
+def test_metric_n2_28_i32(ops):
+    announce("metric i32 n=2^28")
+    n = W.METRIC_N
+    x = W.scan_i32(n, seed=0)
+    y = to_host(ops.scan_inclusive_i32(to_dev(x)))
+    assert_equal_first_diff(y, oracle.scan_i32(x), "metric i32")
+
+
+@pytest.mark.skipif(not FULL, reason="full-size cases disabled")
+def test_metric_n2_28_f32(ops):
+    announce("metric f32 n=2^28")
+    n = W.METRIC_N
+    x = W.scan_f32(n, seed=0)
+    y = to_host(ops.scan_inclusive_f32(to_dev(x)))
+    ref, a = oracle.scan_f32(x)
+    assert_float_close(y, ref, a, "metric f32")
+    del ref, a
+    xe = W.exact_pm1(n, seed=1)
+    ye = to_host(ops.scan_inclusive_f32(to_dev(xe)))
+    assert_equal_first_diff(ye.astype(np.float64), oracle.scan_f32(xe)[0], "metric f32 exact")
