@@ -65,6 +65,9 @@ int libscan_workspace_init(void* ws, size_t ws_bytes, void* stream);
 /* Operation codes for libscan_workspace_bytes. */
 #define LIBSCAN_OP_SCAN 1     /* every 1-D scan_* entry point (look-back) */
 #define LIBSCAN_OP_SCAN_RSS 2 /* scan_inclusive_rss_* (reduce-then-scan) */
+#define LIBSCAN_OP_SCAN_ROWS 3 /* scan_rows_* and topp_cutoff_f32 (rows, len) */
+#define LIBSCAN_OP_COMPACT 4   /* compact_by_mask_f32 and split_by_flags_u32 (n) */
+#define LIBSCAN_OP_RADIX_SORT 5 /* radix_sort_u32 (n, bits = bits_per_pass) */
 
 /*
  * Workspace size in bytes that op needs for n elements (rows/len/bits are
@@ -129,6 +132,65 @@ int scan_inclusive_rss_i32(const int32_t* x, int32_t* y, int64_t n, void* ws, si
                            void* stream);
 int scan_inclusive_rss_f32(const float* x, float* y, int64_t n, void* ws, size_t ws_bytes,
                            void* stream);
+
+/* ------------------------------------------------------------------------
+ * Batched scans (appendix "Multiple (Batched) Scans"): every row of the
+ * row-major rows x len matrix x is scanned on its own (inclusive, or
+ * exclusive when `exclusive` != 0) into y of the same layout.  In-place
+ * (x == y) is allowed.  rows * len <= 2^35 and rows * ceil(len / 4096) <=
+ * 2^24.  Workspace: LIBSCAN_OP_SCAN_ROWS with (rows, len).
+ * ------------------------------------------------------------------------ */
+int scan_rows_i32(const int32_t* x, int32_t* y, int64_t rows, int64_t len, int exclusive, void* ws,
+                  size_t ws_bytes, void* stream);
+int scan_rows_f32(const float* x, float* y, int64_t rows, int64_t len, int exclusive, void* ws,
+                  size_t ws_bytes, void* stream);
+
+/* Top-p (nucleus) cutoff (Section 5 "Top-p or Nucleus Sampling": sort, then
+ * cumulative sum, then cut at p).  probs: rows x len, every row already sorted
+ * in descending order.  cutoff (device, rows int32) receives, per row, the
+ * smallest 0-based index i with probs[r][0] + ... + probs[r][i] >= p, the
+ * running sum taken in fp32; len - 1 if no prefix reaches p (so p <= 0 gives
+ * 0 for non-negative rows); -1 for len == 0.  Tokens 0..cutoff[r] are kept.
+ * p must not be NaN; len <= INT32_MAX.  Workspace: LIBSCAN_OP_SCAN_ROWS. */
+int topp_cutoff_f32(const float* probs, int32_t* cutoff, int64_t rows, int64_t len, float p,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Scan-based data movement (Section 5).  n <= INT32_MAX (positions, counts
+ * and indices are int32).  No output may overlap any input or another
+ * output.  Workspace: LIBSCAN_OP_COMPACT with n.
+ * ------------------------------------------------------------------------ */
+
+/* Compress (Section 5 "Compress", i.e. torch.masked_select): out receives the
+ * x_i whose mask byte is non-zero, in index order, as bit copies; idx_out
+ * (nullable) their source indices; count_dev (device, one int32, required)
+ * their number.  out and idx_out need room for n elements (only the first
+ * count are written).  Single pass: mask and x read once. */
+int compact_by_mask_f32(const float* x, const uint8_t* mask, float* out, int32_t* idx_out,
+                        int32_t* count_dev, int64_t n, void* ws, size_t ws_bytes, void* stream);
+
+/* Split (Section 5 "Split", the SplitInd operator): a stable partition of keys
+ * -- every key whose flag byte is non-zero first, then all the others, each
+ * group in index order.  idx_out (nullable) receives idx_in[i] of every moved
+ * key, or i when idx_in is NULL; n_true_dev (nullable, device, one int32) the
+ * number of flagged keys. */
+int split_by_flags_u32(const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags,
+                       uint32_t* keys_out, int32_t* idx_out, int32_t* n_true_dev, int64_t n,
+                       void* ws, size_t ws_bytes, void* stream);
+
+/* LSD radix sort (Section 5 "Radix Sort": a loop over the key bits from the
+ * least significant one, each step a stable split; Section 6 returns source
+ * indices like PyTorch's sort()).  keys_out receives the n keys in ascending
+ * order, stably; perm_out (nullable) the source index of each, so that
+ * keys_out[i] == keys[perm_out[i]].  bits_per_pass: 1 (32 split passes) or 4
+ * (8 passes of 16-way stable splits); both give the same output.  keys_tmp
+ * (and perm_tmp when perm_out is given) are caller-provided n-element
+ * ping-pong buffers whose contents are clobbered.  No two of keys, keys_out,
+ * perm_out, keys_tmp, perm_tmp may overlap.  n <= INT32_MAX.  Workspace:
+ * LIBSCAN_OP_RADIX_SORT with n and bits = bits_per_pass. */
+int radix_sort_u32(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out, uint32_t* keys_tmp,
+                   int32_t* perm_tmp, int64_t n, int bits_per_pass, void* ws, size_t ws_bytes,
+                   void* stream);
 
 #ifdef __cplusplus
 }

@@ -36,10 +36,16 @@ SIGNATURES = {
     "scan_exclusive_f32_carry": (_int, [_p, _p, _i64, _p, _p, _p, _sz, _p]),
     "scan_inclusive_rss_i32": (_int, [_p, _p, _i64, _p, _sz, _p]),
     "scan_inclusive_rss_f32": (_int, [_p, _p, _i64, _p, _sz, _p]),
+    "scan_rows_i32": (_int, [_p, _p, _i64, _i64, _int, _p, _sz, _p]),
+    "scan_rows_f32": (_int, [_p, _p, _i64, _i64, _int, _p, _sz, _p]),
+    "topp_cutoff_f32": (_int, [_p, _p, _i64, _i64, ctypes.c_float, _p, _sz, _p]),
+    "compact_by_mask_f32": (_int, [_p, _p, _p, _p, _p, _i64, _p, _sz, _p]),
+    "split_by_flags_u32": (_int, [_p, _p, _p, _p, _p, _p, _i64, _p, _sz, _p]),
+    "radix_sort_u32": (_int, [_p, _p, _p, _p, _p, _i64, _int, _p, _sz, _p]),
 }
 
 OK, EINVAL, ENOSPACE, EHIP, ERANGE = 0, -1, -2, -3, -4
-OP_SCAN, OP_SCAN_RSS = 1, 2
+OP_SCAN, OP_SCAN_RSS, OP_SCAN_ROWS, OP_COMPACT, OP_RADIX_SORT = 1, 2, 3, 4, 5
 
 _LIB = None
 

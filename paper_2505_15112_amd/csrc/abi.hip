@@ -2,6 +2,7 @@
 //
 // Each entry point checks its arguments on the host, before any HIP call, and
 // then enqueues the kernels through the launchers of launch.hpp.
+#include <limits.h>
 #include <string.h>
 
 #include "../../include/libscan.h"
@@ -72,6 +73,29 @@ int scan1d_rss(Kind kind, const void* x, void* y, int64_t n, void* ws, size_t ws
     return hip_status(ls::launch_scan1d_rss(kind, x, y, n, ws, (hipStream_t)stream));
 }
 
+// rows x len must describe at most kMaxScanElems elements and a tile grid
+// that fits one launch.
+int check_rows(int64_t rows, int64_t len) {
+    if (rows < 0 || len < 0) return LIBSCAN_EINVAL;
+    if (rows > 0 && len > ls::kMaxScanElems / rows) return LIBSCAN_ERANGE;
+    if (rows > 0 && len > 0 && rows * ((len + 4095) / 4096) > ls::kMaxGridTiles) return LIBSCAN_ERANGE;
+    return LIBSCAN_OK;
+}
+
+int scan_rows(Kind kind, const void* x, void* y, int64_t rows, int64_t len, int exclusive,
+              void* ws, size_t ws_bytes, void* stream) {
+    const int r = check_rows(rows, len);
+    if (r != LIBSCAN_OK) return r;
+    const size_t bytes = (size_t)rows * (size_t)len * 4;
+    if (bytes > 0 && (!x || !y)) return LIBSCAN_EINVAL;
+    if (bad_alias(x, bytes, y, bytes, true)) return LIBSCAN_EINVAL;
+    if (bytes == 0) return LIBSCAN_OK;
+    const int w = check_ws(ws, ws_bytes, ls::scan_rows_ws_bytes(rows, len));
+    if (w != LIBSCAN_OK) return w;
+    return hip_status(ls::launch_scan_rows(kind, exclusive != 0, x, y, rows, len, ws, ws_bytes,
+                                           (hipStream_t)stream));
+}
+
 }  // namespace
 
 extern "C" {
@@ -102,7 +126,6 @@ int libscan_workspace_init(void* ws, size_t ws_bytes, void* stream) {
 }
 
 int libscan_workspace_bytes(int op, int64_t n, int64_t rows, int64_t len, int bits, size_t* bytes) {
-    (void)bits;
     if (!bytes || n < 0 || rows < 0 || len < 0) return LIBSCAN_EINVAL;
     switch (op) {
         case LIBSCAN_OP_SCAN:
@@ -113,6 +136,21 @@ int libscan_workspace_bytes(int op, int64_t n, int64_t rows, int64_t len, int bi
             if (n > ls::kMaxScanElems) return LIBSCAN_ERANGE;
             *bytes = ls::scan1d_rss_ws_bytes(n);
             return LIBSCAN_OK;
+        case LIBSCAN_OP_COMPACT:
+            if (n > INT32_MAX) return LIBSCAN_ERANGE;
+            *bytes = ls::compact_ws_bytes(n);
+            return LIBSCAN_OK;
+        case LIBSCAN_OP_RADIX_SORT:
+            if (n > INT32_MAX) return LIBSCAN_ERANGE;
+            if (bits != 1 && bits != 4) return LIBSCAN_EINVAL;
+            *bytes = ls::radix_ws_bytes(n, bits);
+            return LIBSCAN_OK;
+        case LIBSCAN_OP_SCAN_ROWS: {
+            const int r = check_rows(rows, len);
+            if (r != LIBSCAN_OK) return r;
+            *bytes = ls::scan_rows_ws_bytes(rows, len);
+            return LIBSCAN_OK;
+        }
         default:
             return LIBSCAN_EINVAL;
     }
@@ -169,6 +207,96 @@ int scan_inclusive_rss_i32(const int32_t* x, int32_t* y, int64_t n, void* ws, si
 int scan_inclusive_rss_f32(const float* x, float* y, int64_t n, void* ws, size_t ws_bytes,
                            void* stream) {
     return scan1d_rss(Kind::F32, x, y, n, ws, ws_bytes, stream);
+}
+
+int scan_rows_i32(const int32_t* x, int32_t* y, int64_t rows, int64_t len, int exclusive, void* ws,
+                  size_t ws_bytes, void* stream) {
+    return scan_rows(Kind::I32, x, y, rows, len, exclusive, ws, ws_bytes, stream);
+}
+int scan_rows_f32(const float* x, float* y, int64_t rows, int64_t len, int exclusive, void* ws,
+                  size_t ws_bytes, void* stream) {
+    return scan_rows(Kind::F32, x, y, rows, len, exclusive, ws, ws_bytes, stream);
+}
+
+int topp_cutoff_f32(const float* probs, int32_t* cutoff, int64_t rows, int64_t len, float p,
+                    void* ws, size_t ws_bytes, void* stream) {
+    const int r = check_rows(rows, len);
+    if (r != LIBSCAN_OK) return r;
+    if (len > INT32_MAX) return LIBSCAN_ERANGE;
+    if (p != p) return LIBSCAN_EINVAL;  // NaN
+    if (rows > 0 && !cutoff) return LIBSCAN_EINVAL;
+    const size_t bytes = (size_t)rows * (size_t)len * 4;
+    if (bytes > 0 && !probs) return LIBSCAN_EINVAL;
+    if (overlaps(probs, bytes, cutoff, (size_t)rows * 4)) return LIBSCAN_EINVAL;
+    if (rows == 0) return LIBSCAN_OK;
+    const int w = check_ws(ws, ws_bytes, ls::scan_rows_ws_bytes(rows, len));
+    if (w != LIBSCAN_OK) return w;
+    return hip_status(ls::launch_topp_cutoff(probs, cutoff, rows, len, p, ws, ws_bytes,
+                                             (hipStream_t)stream));
+}
+
+int compact_by_mask_f32(const float* x, const uint8_t* mask, float* out, int32_t* idx_out,
+                        int32_t* count_dev, int64_t n, void* ws, size_t ws_bytes, void* stream) {
+    if (n < 0 || !count_dev) return LIBSCAN_EINVAL;
+    if (n > INT32_MAX) return LIBSCAN_ERANGE;
+    if (n > 0 && (!x || !mask || !out)) return LIBSCAN_EINVAL;
+    const size_t b4 = (size_t)n * 4, b1 = (size_t)n;
+    if (overlaps(out, b4, x, b4) || overlaps(out, b4, mask, b1) || overlaps(out, b4, count_dev, 4) ||
+        overlaps(idx_out, b4, x, b4) || overlaps(idx_out, b4, mask, b1) ||
+        overlaps(idx_out, b4, out, b4) || overlaps(idx_out, b4, count_dev, 4) ||
+        overlaps(count_dev, 4, x, b4) || overlaps(count_dev, 4, mask, b1))
+        return LIBSCAN_EINVAL;
+    if (n > 0) {
+        const int w = check_ws(ws, ws_bytes, ls::compact_ws_bytes(n));
+        if (w != LIBSCAN_OK) return w;
+    }
+    return hip_status(ls::launch_compact(x, mask, out, idx_out, count_dev, n, ws, ws_bytes,
+                                         (hipStream_t)stream));
+}
+
+int split_by_flags_u32(const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags,
+                       uint32_t* keys_out, int32_t* idx_out, int32_t* n_true_dev, int64_t n,
+                       void* ws, size_t ws_bytes, void* stream) {
+    if (n < 0) return LIBSCAN_EINVAL;
+    if (n > INT32_MAX) return LIBSCAN_ERANGE;
+    if (n > 0 && (!keys || !flags || !keys_out)) return LIBSCAN_EINVAL;
+    const size_t b4 = (size_t)n * 4, b1 = (size_t)n;
+    const void* ins[3] = {keys, idx_in, flags};
+    const size_t inb[3] = {b4, idx_in ? b4 : 0, b1};
+    void* outs[3] = {keys_out, idx_out, n_true_dev};
+    const size_t outb[3] = {b4, idx_out ? b4 : 0, n_true_dev ? 4u : 0u};
+    for (int o = 0; o < 3; ++o) {
+        for (int i = 0; i < 3; ++i)
+            if (overlaps(outs[o], outb[o], ins[i], inb[i])) return LIBSCAN_EINVAL;
+        for (int p = o + 1; p < 3; ++p)
+            if (overlaps(outs[o], outb[o], outs[p], outb[p])) return LIBSCAN_EINVAL;
+    }
+    if (n > 0) {
+        const int w = check_ws(ws, ws_bytes, ls::compact_ws_bytes(n));
+        if (w != LIBSCAN_OK) return w;
+    } else if (!n_true_dev) {
+        return LIBSCAN_OK;
+    }
+    return hip_status(ls::launch_split(keys, idx_in, flags, 0, keys_out, idx_out, n_true_dev, n, ws,
+                                       ws_bytes, (hipStream_t)stream));
+}
+
+int radix_sort_u32(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out, uint32_t* keys_tmp,
+                   int32_t* perm_tmp, int64_t n, int bits_per_pass, void* ws, size_t ws_bytes,
+                   void* stream) {
+    if (n < 0 || (bits_per_pass != 1 && bits_per_pass != 4)) return LIBSCAN_EINVAL;
+    if (n > INT32_MAX) return LIBSCAN_ERANGE;
+    if (n == 0) return LIBSCAN_OK;
+    if (!keys || !keys_out || !keys_tmp || (perm_out && !perm_tmp)) return LIBSCAN_EINVAL;
+    const size_t b = (size_t)n * 4;
+    const void* bufs[5] = {keys, keys_out, perm_out, keys_tmp, perm_out ? perm_tmp : nullptr};
+    for (int i = 0; i < 5; ++i)
+        for (int j = i + 1; j < 5; ++j)
+            if (overlaps(bufs[i], bufs[i] ? b : 0, bufs[j], bufs[j] ? b : 0)) return LIBSCAN_EINVAL;
+    const int w = check_ws(ws, ws_bytes, ls::radix_ws_bytes(n, bits_per_pass));
+    if (w != LIBSCAN_OK) return w;
+    return hip_status(ls::launch_radix_sort(keys, keys_out, perm_out, keys_tmp, perm_tmp, n,
+                                            bits_per_pass, ws, ws_bytes, (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -1,0 +1,329 @@
+// compact.hip -- scan-based data movement: Compress and Split (Section 5).
+//
+// Compress (torch.masked_select): keep x_i where mask_i != 0, in index order.
+// The exclusive count of kept elements before i is their output position; it
+// is a scan of 0/1 flags, computed tile-locally (lane serial + DPP wavefront
+// + LDS) and carried between tiles by decoupled look-back on the counts --
+// one kernel, one pass: mask and values read once, kept values written once.
+//
+// Split (SplitInd): stable two-way partition with source indices.  Flagged
+// element i goes to e_i (exclusive count of flagged before it), unflagged to
+// n_true + (i - e_i).  n_true must be known before any tile stores, so a
+// small counting kernel runs first (reading only the flags, or only the keys
+// when the flag is a key bit, as in the radix-sort pass of Section 5); its
+// total lands in an epoch-tagged workspace word that the split kernel reads.
+#include <limits.h>
+
+#include "launch.hpp"
+#include "tile.hpp"
+
+namespace ls {
+
+constexpr int kCWaves = 4;
+constexpr int kCChunks = 4;
+constexpr int kCVec = 4;
+constexpr int64_t kCTile = kCWaves * kCChunks * kWave * kCVec;  // 4096
+
+static inline int64_t c_tiles(int64_t n) { return (n + kCTile - 1) / kCTile; }
+
+using FlagTile = Tile<uint8_t, uint32_t, kCVec, kCChunks, kCWaves>;
+using KeyTile = Tile<uint32_t, uint32_t, kCVec, kCChunks, kCWaves>;
+using ValTile = Tile<float, float, kCVec, kCChunks, kCWaves>;
+using IdxTile = Tile<int32_t, int32_t, kCVec, kCChunks, kCWaves>;
+
+// Header accumulator used by split for the number of flagged elements.
+constexpr int kTagNTrue = 0;
+
+// Flags of one tile as 0/1 values (any non-zero byte is true, or for the
+// radix pass: key bit `bit` is 0).
+template <bool FROM_BITS, bool VEC>
+__device__ __forceinline__ void load_flags(const uint8_t* flags, const uint32_t* keys, int bit,
+                                           int64_t n, int64_t base, uint32_t (&f)[kCChunks][kCVec],
+                                           uint32_t (&k)[kCChunks][kCVec]) {
+    if constexpr (FROM_BITS) {
+        KeyTile::template load<VEC>(keys, n, base, k);
+#pragma unroll
+        for (int j = 0; j < kCChunks; ++j)
+#pragma unroll
+            for (int e = 0; e < kCVec; ++e) f[j][e] = ((k[j][e] >> bit) & 1u) ^ 1u;
+    } else {
+        FlagTile::template load<VEC>(flags, n, base, f);
+#pragma unroll
+        for (int j = 0; j < kCChunks; ++j)
+#pragma unroll
+            for (int e = 0; e < kCVec; ++e) f[j][e] = f[j][e] != 0u;
+    }
+}
+
+// Elements past n have flag 0 after load_flags for u8 flags (loaded as 0);
+// for key bits the padding key 0 would read as flagged, so mask it.
+template <bool FROM_BITS>
+__device__ __forceinline__ void mask_tail(int64_t n, int64_t base, uint32_t (&f)[kCChunks][kCVec]) {
+    if (!FROM_BITS || base + kCTile <= n) return;
+#pragma unroll
+    for (int j = 0; j < kCChunks; ++j) {
+        const int64_t off = KeyTile::offset(base, j);
+#pragma unroll
+        for (int e = 0; e < kCVec; ++e)
+            if (off + e >= n) f[j][e] = 0;
+    }
+}
+
+// ---------------------------------------------------------------- compress
+
+template <bool VEC, bool WITH_IDX>
+__global__ __launch_bounds__(FlagTile::kThreads) void k_compact(
+    const float* x, const uint8_t* mask, float* out, int32_t* idx, int32_t* count, int64_t n,
+    WsHeader* hdr, uint64_t* status, int64_t status_words, uint32_t ntiles) {
+    __shared__ Ticket s_ticket;
+    __shared__ uint32_t s_wtot[kCWaves];
+    __shared__ uint32_t s_carry;
+
+    if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
+    __syncthreads();
+    const uint32_t tile32 = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.tile);
+    const uint32_t epoch = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.epoch);
+    if (tile32 >= ntiles) {
+        if (threadIdx.x == 0)
+            __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
+    const int64_t tile = tile32;
+    const int64_t base = tile * kCTile;
+
+    uint32_t f[kCChunks][kCVec], unused[kCChunks][kCVec];
+    float xv[kCChunks][kCVec];
+    load_flags<false, VEC>(mask, nullptr, 0, n, base, f, unused);
+    ValTile::template load<VEC>(x, n, base, xv);
+    uint32_t lane_off[kCChunks];
+    const uint32_t wtot = FlagTile::wave_scan(f, lane_off);  // f becomes in-lane inclusive counts
+    uint32_t wofs;
+    const uint32_t agg = FlagTile::combine_waves(wtot, s_wtot, &wofs);
+    if (threadIdx.x < kWave) {
+        const uint32_t excl = lookback<uint32_t>(status, tile, 0, agg, 0u, epoch, hdr);
+        if (threadIdx.x == 0) {
+            s_carry = excl;
+            if (tile == ntiles - 1) *count = (int32_t)(excl + agg);
+            finish_epoch(hdr, epoch, ntiles, status, status_words);
+        }
+    }
+    __syncthreads();
+    const uint32_t c = s_carry + wofs;
+#pragma unroll
+    for (int j = 0; j < kCChunks; ++j) {
+        const int64_t off = FlagTile::offset(base, j);
+        const uint32_t lb = c + lane_off[j];
+        uint32_t prev = 0;
+#pragma unroll
+        for (int e = 0; e < kCVec; ++e) {
+            if (f[j][e] != prev) {  // this element is kept; its rank is the count before it
+                const uint32_t pos = lb + prev;
+                if (pos < (uint64_t)n) {  // always true; guards the write against a bad count
+                    out[pos] = xv[j][e];
+                    if (WITH_IDX) idx[pos] = (int32_t)(off + e);
+                }
+            }
+            prev = f[j][e];
+        }
+    }
+}
+
+// ---------------------------------------------------------------- split
+
+// Count the flagged elements into the header accumulator (grid-stride).
+template <bool FROM_BITS, bool VEC>
+__global__ __launch_bounds__(256) void k_count_flags(const uint8_t* flags, const uint32_t* keys,
+                                                     int bit, int64_t n, WsHeader* hdr) {
+    __shared__ uint32_t s_part[4];
+    const uint32_t epoch = current_epoch(hdr);
+    uint32_t cnt = 0;
+    const int64_t per_block = kCTile;
+    for (int64_t base = (int64_t)blockIdx.x * per_block; base < n;
+         base += (int64_t)gridDim.x * per_block) {
+        uint32_t f[kCChunks][kCVec], k[kCChunks][kCVec];
+        load_flags<FROM_BITS, VEC>(flags, keys, bit, n, base, f, k);
+        mask_tail<FROM_BITS>(n, base, f);
+#pragma unroll
+        for (int j = 0; j < kCChunks; ++j)
+#pragma unroll
+            for (int e = 0; e < kCVec; ++e) cnt += f[j][e];
+    }
+    const uint32_t wsum = wave_sum(cnt);
+    if (lane_id() == 0) s_part[threadIdx.x / kWave] = wsum;
+    __syncthreads();
+    if (threadIdx.x == 0)
+        tagged_add(&hdr->tagged[kTagNTrue], epoch, s_part[0] + s_part[1] + s_part[2] + s_part[3]);
+}
+
+// Number of keys whose bit `bit` is 0, from the 8 x 16 digit histogram of
+// the radix sort (tagged words, digit position bit / 4).
+__device__ __forceinline__ uint32_t zeros_of_bit(const uint64_t* hist, int bit) {
+    uint32_t z = 0;
+    for (int v = 0; v < 16; ++v)
+        if (((v >> (bit & 3)) & 1) == 0) z += (uint32_t)hist[(bit >> 2) * 16 + v];
+    return z;
+}
+
+// hist == nullptr: n_true comes from the counting kernel's header word;
+// otherwise (radix-sort pass) it is derived from the digit histogram.
+template <bool FROM_BITS, bool VEC, bool HAS_IDX_IN, bool WITH_IDX>
+__global__ __launch_bounds__(FlagTile::kThreads) void k_split(
+    const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags, int bit, uint32_t* keys_out,
+    int32_t* idx_out, int32_t* n_true_out, int64_t n, WsHeader* hdr, uint64_t* status,
+    int64_t status_words, uint32_t ntiles, const uint64_t* hist) {
+    __shared__ Ticket s_ticket;
+    __shared__ uint32_t s_wtot[kCWaves];
+    __shared__ uint32_t s_carry;
+
+    if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
+    __syncthreads();
+    const uint32_t tile32 = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.tile);
+    const uint32_t epoch = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.epoch);
+    if (tile32 >= ntiles) {
+        if (threadIdx.x == 0)
+            __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
+    const int64_t tile = tile32;
+    const int64_t base = tile * kCTile;
+    const uint32_t n_true = hist ? zeros_of_bit(hist, bit) : tagged_value(&hdr->tagged[kTagNTrue]);
+
+    uint32_t f[kCChunks][kCVec], k[kCChunks][kCVec];
+    if constexpr (FROM_BITS) {
+        load_flags<true, VEC>(nullptr, keys, bit, n, base, f, k);
+        mask_tail<true>(n, base, f);
+    } else {
+        load_flags<false, VEC>(flags, nullptr, 0, n, base, f, k);
+        KeyTile::template load<VEC>(keys, n, base, k);
+    }
+    int32_t iv[kCChunks][kCVec];
+    if constexpr (HAS_IDX_IN) IdxTile::template load<VEC>(idx_in, n, base, iv);
+    uint32_t lane_off[kCChunks];
+    const uint32_t wtot = FlagTile::wave_scan(f, lane_off);
+    uint32_t wofs;
+    const uint32_t agg = FlagTile::combine_waves(wtot, s_wtot, &wofs);
+    if (threadIdx.x < kWave) {
+        const uint32_t excl = lookback<uint32_t>(status, tile, 0, agg, 0u, epoch, hdr);
+        if (threadIdx.x == 0) {
+            s_carry = excl;
+            if (tile == 0 && n_true_out) *n_true_out = (int32_t)n_true;
+            finish_epoch(hdr, epoch, ntiles, status, status_words);
+        }
+    }
+    __syncthreads();
+    const uint32_t c = s_carry + wofs;
+#pragma unroll
+    for (int j = 0; j < kCChunks; ++j) {
+        const int64_t off = FlagTile::offset(base, j);
+        const uint32_t lb = c + lane_off[j];
+        uint32_t prev = 0;
+#pragma unroll
+        for (int e = 0; e < kCVec; ++e) {
+            const int64_t i = off + e;
+            if (i < n) {
+                const uint32_t before = lb + prev;  // flagged elements before i
+                const uint32_t pos = (f[j][e] != prev) ? before : n_true + (uint32_t)i - before;
+                if (pos < (uint64_t)n) {  // always true; guards the write against a bad count
+                    keys_out[pos] = k[j][e];
+                    if (WITH_IDX) idx_out[pos] = HAS_IDX_IN ? iv[j][e] : (int32_t)i;
+                }
+            }
+            prev = f[j][e];
+        }
+    }
+}
+
+// ---------------------------------------------------------------- launchers
+
+size_t compact_ws_bytes(int64_t n) { return kWsHeader + (size_t)c_tiles(n) * sizeof(uint64_t); }
+
+static bool al(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+__global__ void k_zero_count(int32_t* count) {
+    if (threadIdx.x == 0) *count = 0;
+}
+
+hipError_t launch_compact(const float* x, const uint8_t* mask, float* out, int32_t* idx,
+                          int32_t* count, int64_t n, void* ws, size_t ws_bytes,
+                          hipStream_t stream) {
+    if (n == 0) {
+        hipLaunchKernelGGL(k_zero_count, dim3(1), dim3(64), 0, stream, count);
+        return hipGetLastError();
+    }
+    const uint32_t nt = (uint32_t)c_tiles(n);
+    WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
+    uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
+    const int64_t sw = (int64_t)((ws_bytes - kWsHeader) / sizeof(uint64_t));
+    const bool vec = al(x, 16) && al(mask, 4);
+    auto k = vec ? (idx ? k_compact<true, true> : k_compact<true, false>)
+                 : (idx ? k_compact<false, true> : k_compact<false, false>);
+    hipLaunchKernelGGL(k, dim3(nt), dim3(FlagTile::kThreads), 0, stream, x, mask, out, idx, count,
+                       n, hdr, status, sw, nt);
+    return hipGetLastError();
+}
+
+template <bool FROM_BITS, bool VEC>
+static void launch_split_typed(const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags,
+                               int bit, uint32_t* keys_out, int32_t* idx_out, int32_t* n_true_out,
+                               int64_t n, WsHeader* hdr, uint64_t* status, int64_t sw,
+                               uint32_t nt, hipStream_t stream) {
+    const int64_t cblocks = (n + kCTile - 1) / kCTile;
+    hipLaunchKernelGGL((k_count_flags<FROM_BITS, VEC>), dim3((unsigned)(cblocks < 2048 ? cblocks : 2048)),
+                       dim3(256), 0, stream, flags, keys, bit, n, hdr);
+    auto k = idx_in ? (idx_out ? k_split<FROM_BITS, VEC, true, true> : k_split<FROM_BITS, VEC, true, false>)
+                    : (idx_out ? k_split<FROM_BITS, VEC, false, true> : k_split<FROM_BITS, VEC, false, false>);
+    hipLaunchKernelGGL(k, dim3(nt), dim3(FlagTile::kThreads), 0, stream, keys, idx_in, flags, bit,
+                       keys_out, idx_out, n_true_out, n, hdr, status, sw, nt, (const uint64_t*)nullptr);
+}
+
+// One LSB radix-sort pass on key bit `bit` (flag = bit is 0), with the count
+// of zero bits taken from the digit histogram `hist`.
+hipError_t launch_radix1_pass(const uint32_t* keys, const int32_t* idx_in, int bit,
+                              uint32_t* keys_out, int32_t* idx_out, int64_t n, const uint64_t* hist,
+                              void* ws, size_t ws_bytes, size_t status_offset, hipStream_t stream) {
+    const uint32_t nt = (uint32_t)c_tiles(n);
+    WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
+    uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + status_offset);
+    const int64_t sw = (int64_t)((ws_bytes - status_offset) / sizeof(uint64_t));
+    const bool vec = al(keys, 16) && (!idx_in || al(idx_in, 16));
+    auto k = vec ? (idx_in ? (idx_out ? k_split<true, true, true, true> : k_split<true, true, true, false>)
+                           : (idx_out ? k_split<true, true, false, true> : k_split<true, true, false, false>))
+                 : (idx_in ? (idx_out ? k_split<true, false, true, true> : k_split<true, false, true, false>)
+                           : (idx_out ? k_split<true, false, false, true> : k_split<true, false, false, false>));
+    hipLaunchKernelGGL(k, dim3(nt), dim3(FlagTile::kThreads), 0, stream, keys, idx_in,
+                       (const uint8_t*)nullptr, bit, keys_out, idx_out, (int32_t*)nullptr, n, hdr,
+                       status, sw, nt, hist);
+    return hipGetLastError();
+}
+
+hipError_t launch_split(const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags, int bit,
+                        uint32_t* keys_out, int32_t* idx_out, int32_t* n_true_out, int64_t n,
+                        void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (n == 0) {
+        if (n_true_out) hipLaunchKernelGGL(k_zero_count, dim3(1), dim3(64), 0, stream, n_true_out);
+        return hipGetLastError();
+    }
+    const uint32_t nt = (uint32_t)c_tiles(n);
+    WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
+    uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
+    const int64_t sw = (int64_t)((ws_bytes - kWsHeader) / sizeof(uint64_t));
+    const bool vec = al(keys, 16) && (!idx_in || al(idx_in, 16)) && (flags == nullptr || al(flags, 4));
+    if (flags == nullptr) {
+        if (vec)
+            launch_split_typed<true, true>(keys, idx_in, flags, bit, keys_out, idx_out, n_true_out,
+                                           n, hdr, status, sw, nt, stream);
+        else
+            launch_split_typed<true, false>(keys, idx_in, flags, bit, keys_out, idx_out,
+                                            n_true_out, n, hdr, status, sw, nt, stream);
+    } else {
+        if (vec)
+            launch_split_typed<false, true>(keys, idx_in, flags, bit, keys_out, idx_out,
+                                            n_true_out, n, hdr, status, sw, nt, stream);
+        else
+            launch_split_typed<false, false>(keys, idx_in, flags, bit, keys_out, idx_out,
+                                             n_true_out, n, hdr, status, sw, nt, stream);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace ls

@@ -82,7 +82,7 @@ __device__ __forceinline__ int lane_id() { return (int)__lane_id(); }
 //   [8, 12)   done counter, used only by the call that wraps the epoch
 //   [12, 16)  error flag: set to 1 if a look-back gave up waiting (the
 //             workspace was not zero-filled before first use)
-//   [16, 256) op-specific counters
+//   [16, 256) 30 epoch-tagged 64-bit accumulators (see tagged_add)
 // A zero-filled workspace is ready; after that every look-back kernel leaves
 // it ready for the next call: the workgroup that takes the last ticket resets
 // the ticket count and advances the epoch, and status words are tagged with
@@ -96,7 +96,7 @@ struct WsHeader {
     uint64_t ticket;
     uint32_t done;
     uint32_t error;
-    uint32_t op[60];
+    uint64_t tagged[30];
 };
 static_assert(sizeof(WsHeader) == 256, "workspace header is 256 bytes");
 
@@ -116,6 +116,32 @@ __device__ __forceinline__ Ticket take_ticket(WsHeader* h, uint32_t nwg) {
         __hip_atomic_store(&h->ticket, (uint64_t)(t.epoch + 1) << 32, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
     return t;
+}
+
+__device__ __forceinline__ uint32_t current_epoch(WsHeader* h) {
+    return (uint32_t)(__hip_atomic_load(&h->ticket, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >> 32);
+}
+
+// Epoch-tagged accumulator [epoch:32 | value:32]: the first add of a call
+// (the word still carries an older epoch) replaces the value, later adds of
+// the same call accumulate.  A kernel that adds must run (and finish) before
+// the look-back kernel of the same call, which reads the value and advances
+// the epoch; so a word never needs clearing.
+__device__ __forceinline__ void tagged_add(uint64_t* w, uint32_t epoch, uint32_t v) {
+    uint64_t old = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    while (true) {
+        if ((uint32_t)(old >> 32) == epoch) {
+            __hip_atomic_fetch_add(w, (uint64_t)v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return;
+        }
+        const uint64_t fresh = ((uint64_t)epoch << 32) | v;
+        if (__hip_atomic_compare_exchange_strong(w, &old, fresh, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT))
+            return;
+    }
+}
+__device__ __forceinline__ uint32_t tagged_value(uint64_t* w) {
+    return (uint32_t)__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // ---------------------------------------------------------------- tile status
@@ -151,7 +177,7 @@ __device__ __forceinline__ void status_store(uint64_t* p, uint64_t v) {
 // published yet; they hold earlier tickets, so they are running and the wait
 // ends.  The spin is bounded all the same: after kSpinLimit rounds it raises
 // the workspace error flag and carries on with a wrong value rather than hang.
-template <class T>
+template <class T, int K = 1>
 __device__ T lookback(uint64_t* status, int64_t tile, int64_t first, T agg, T base,
                       uint32_t epoch, WsHeader* h) {
     const int lane = lane_id();
@@ -161,31 +187,49 @@ __device__ T lookback(uint64_t* status, int64_t tile, int64_t first, T agg, T ba
     }
     if (lane == 0) status_store(status + tile, status_word(kStateA, epoch, Bits<T>::to(agg)));
     T excl = T(0);
-    int64_t end = tile - 1;
+    int64_t end = tile - 1;  // nearest predecessor not summed yet
     uint32_t spins = 0;
     while (true) {
-        const int64_t idx = end - lane;
-        // Lanes past the segment start read an empty inclusive prefix; the
-        // walk never sums them because `first` (always P) comes before them.
-        uint64_t s = 0, st = kStateP;
-        if (idx >= first) {
-            s = status_load(status + idx);
-            st = status_state(s, epoch);
+        // K windows of 64 predecessors each, all loads in flight at once.
+        uint64_t s[K], st[K];
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const int64_t idx = end - lane - (int64_t)k * kWave;
+            // Lanes past the segment start read an empty inclusive prefix; the
+            // walk never sums them because `first` (always P) comes before them.
+            s[k] = 0;
+            st[k] = kStateP;
+            if (idx >= first) {
+                s[k] = status_load(status + idx);
+                st[k] = status_state(s[k], epoch);
+            }
         }
-        const uint64_t pmask = __ballot(st == kStateP);
-        const uint64_t xmask = __ballot(st == kStateX);
-        // lanes 0..p where p is the nearest predecessor with an inclusive prefix
-        const uint64_t upto = pmask ? (((pmask & (~pmask + 1)) << 1) - 1) : ~0ull;
-        if ((xmask & upto) && ++spins < kSpinLimit) {
+        bool done = false, retry = false;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            if (done || retry) break;
+            const uint64_t pmask = __ballot(st[k] == kStateP);
+            const uint64_t xmask = __ballot(st[k] == kStateX);
+            // lanes 0..p where p is the nearest predecessor with an inclusive prefix
+            const uint64_t upto = pmask ? (((pmask & (~pmask + 1)) << 1) - 1) : ~0ull;
+            if (xmask & upto) {  // a predecessor has not published: read again from here
+                retry = true;
+                break;
+            }
+            const T v = ((upto >> lane) & 1) ? Bits<T>::from((uint32_t)s[k]) : T(0);
+            excl = excl + wave_sum(v);
+            end -= kWave;
+            done = pmask != 0;
+        }
+        if (done) break;
+        if (retry) {
+            if (++spins >= kSpinLimit) {
+                if (lane == 0)
+                    __hip_atomic_store(&h->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                break;
+            }
             __builtin_amdgcn_s_sleep(1);
-            continue;
         }
-        if (spins >= kSpinLimit && lane == 0)
-            __hip_atomic_store(&h->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const T v = ((upto >> lane) & 1) ? Bits<T>::from((uint32_t)s) : T(0);
-        excl = excl + wave_sum(v);
-        if (pmask || spins >= kSpinLimit) break;
-        end -= kWave;
     }
     if (lane == 0) status_store(status + tile, status_word(kStateP, epoch, Bits<T>::to(excl + agg)));
     return excl;

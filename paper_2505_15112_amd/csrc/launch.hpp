@@ -30,4 +30,28 @@ size_t scan1d_rss_ws_bytes(int64_t n);
 hipError_t launch_scan1d_rss(Kind kind, const void* x, void* y, int64_t n, void* ws,
                              hipStream_t stream);
 
+// Batched row scans (rows x len, row-major) and the top-p cutoff on them.
+size_t scan_rows_ws_bytes(int64_t rows, int64_t len);
+hipError_t launch_scan_rows(Kind kind, bool exclusive, const void* x, void* y, int64_t rows,
+                            int64_t len, void* ws, size_t ws_bytes, hipStream_t stream);
+hipError_t launch_topp_cutoff(const float* probs, int32_t* cutoff, int64_t rows, int64_t len,
+                              float p, void* ws, size_t ws_bytes, hipStream_t stream);
+constexpr int64_t kMaxGridTiles = int64_t(1) << 24;
+
+// Compress and split (Section 5).  flags == nullptr in launch_split means
+// "flag = key bit `bit` is 0" (the LSB radix-sort pass).
+size_t compact_ws_bytes(int64_t n);
+hipError_t launch_compact(const float* x, const uint8_t* mask, float* out, int32_t* idx,
+                          int32_t* count, int64_t n, void* ws, size_t ws_bytes,
+                          hipStream_t stream);
+hipError_t launch_split(const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags, int bit,
+                        uint32_t* keys_out, int32_t* idx_out, int32_t* n_true_out, int64_t n,
+                        void* ws, size_t ws_bytes, hipStream_t stream);
+
+// LSD radix sort (1 or 4 bits per pass), caller-provided ping-pong buffers.
+size_t radix_ws_bytes(int64_t n, int bits);
+hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out,
+                             uint32_t* keys_tmp, int32_t* perm_tmp, int64_t n, int bits, void* ws,
+                             size_t ws_bytes, hipStream_t stream);
+
 }  // namespace ls

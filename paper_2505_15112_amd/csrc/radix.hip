@@ -1,0 +1,265 @@
+// radix.hip -- least-significant-digit radix sort of uint32 keys with a
+// stable permutation (Section 5 "Radix Sort": a loop over the bits from the
+// least significant one, each step a stable split; Section 6 returns the
+// indices as PyTorch's sort() does).
+//
+//  * One pre-pass reads the keys once and builds the 8 x 16 histogram of all
+//    4-bit digits into epoch-tagged workspace words.
+//  * 1 bit per pass: 32 split passes (compact.hip's split kernel with the
+//    flag "bit b is 0"), the number of zero bits of pass b read off the
+//    histogram, so no pass needs its own counting kernel.
+//  * 4 bits per pass: 8 passes.  A tile ranks its keys per digit with a
+//    wavefront multi-split (one ballot per digit bit; the lanes holding the
+//    same digit are the AND of the matching ballots, the rank is the count of
+//    them below the lane), carries the 16 per-digit counts between tiles with
+//    a 16-chain decoupled look-back, and scatters each key to
+//    (keys with a smaller digit) + (same digit in earlier tiles) + rank.
+// The two variants give identical output: a stable sort is unique.
+#include "launch.hpp"
+#include "tile.hpp"
+
+namespace ls {
+
+constexpr int kHistWords = 8 * 16;  // tagged [epoch | count] words after the header
+constexpr size_t kRadixStatusOffset = kWsHeader + kHistWords * sizeof(uint64_t);
+
+constexpr int kR4Waves = 4;
+constexpr int kR4Chunks = 16;  // 64 keys (one per lane) per chunk
+constexpr int64_t kR4Tile = kR4Waves * kR4Chunks * kWave;  // 4096 keys
+constexpr int64_t kR1Tile = 4096;                          // compact.hip's split tile
+
+static inline int64_t r4_tiles(int64_t n) { return (n + kR4Tile - 1) / kR4Tile; }
+
+// ---------------------------------------------------------------- histogram
+
+__global__ __launch_bounds__(256) void k_digit_hist(const uint32_t* keys, int64_t n,
+                                                    uint64_t* hist, WsHeader* hdr) {
+    __shared__ uint32_t s_hist[4][kHistWords];  // one copy per wavefront
+    const uint32_t epoch = current_epoch(hdr);
+    const int w = threadIdx.x / kWave;
+    for (int i = threadIdx.x; i < 4 * kHistWords; i += blockDim.x) (&s_hist[0][0])[i] = 0;
+    __syncthreads();
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        const uint32_t k = keys[i];
+#pragma unroll
+        for (int p = 0; p < 8; ++p) atomicAdd(&s_hist[w][p * 16 + ((k >> (4 * p)) & 15)], 1u);
+    }
+    __syncthreads();
+    if (threadIdx.x < kHistWords) {
+        const uint32_t c = s_hist[0][threadIdx.x] + s_hist[1][threadIdx.x] +
+                           s_hist[2][threadIdx.x] + s_hist[3][threadIdx.x];
+        tagged_add(hist + threadIdx.x, epoch, c);
+    }
+}
+
+// ---------------------------------------------------------------- 4-bit pass
+
+// Lanes whose digit equals `d`, from the four digit-bit ballots and the
+// ballot of valid lanes.
+__device__ __forceinline__ uint64_t digit_lanes(uint32_t d, uint64_t valid, uint64_t b0,
+                                                uint64_t b1, uint64_t b2, uint64_t b3) {
+    return valid & ((d & 1) ? b0 : ~b0) & ((d & 2) ? b1 : ~b1) & ((d & 4) ? b2 : ~b2) &
+           ((d & 8) ? b3 : ~b3);
+}
+
+__device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+}
+
+__device__ __forceinline__ uint32_t lane_shfl(uint32_t v, int src_lane) {
+    return (uint32_t)__builtin_amdgcn_ds_bpermute(src_lane << 2, (int)v);
+}
+
+// 16-chain look-back by one wavefront: lane l watches digit l & 15 of the
+// predecessor tile (l >> 4) steps back, so each round reads 4 tiles x 16
+// digits.  tot: this tile's count of digit (lane & 15).  Returns, in every
+// lane, the count of digit (lane & 15) in all earlier tiles.
+__device__ uint32_t lookback16(uint64_t* status, int64_t tile, uint32_t tot, uint32_t epoch,
+                               WsHeader* h) {
+    const int lane = lane_id();
+    const int d = lane & 15, q = lane >> 4;
+    if (tile == 0) {
+        if (q == 0) status_store(status + d, status_word(kStateP, epoch, tot));
+        return 0;
+    }
+    if (q == 0) status_store(status + tile * 16 + d, status_word(kStateA, epoch, tot));
+    uint32_t excl = 0;
+    int64_t end = tile - 1;  // per digit: nearest predecessor tile not summed yet
+    bool done = false;
+    uint32_t spins = 0;
+    while (true) {
+        const int64_t t = end - q;
+        uint64_t s = 0, st = kStateP;
+        if (!done && t >= 0) {
+            s = status_load(status + t * 16 + d);
+            st = status_state(s, epoch);
+        }
+        const uint64_t P = __ballot(st == kStateP);
+        const uint64_t X = __ballot(st == kStateX);
+        // this digit's four lanes: bits d, d+16, d+32, d+48 (nearest first)
+        uint32_t pq = 0, xq = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            pq |= (uint32_t)((P >> (d + 16 * k)) & 1) << k;
+            xq |= (uint32_t)((X >> (d + 16 * k)) & 1) << k;
+        }
+        const uint32_t upto = pq ? (((pq & (~pq + 1)) << 1) - 1) : 0xfu;  // tiles 0..nearest P
+        const bool wait = !done && (xq & upto);
+        uint32_t v = (!done && !wait && ((upto >> q) & 1)) ? (uint32_t)s : 0u;
+        v += lane_shfl(v, lane ^ 16);
+        v += lane_shfl(v, lane ^ 32);
+        if (!done && !wait) {
+            excl += v;
+            end -= 4;
+            done = pq != 0;
+        }
+        if (__ballot(!done) == 0) break;
+        if (__ballot(wait) != 0) {
+            if (++spins >= kSpinLimit) {
+                if (lane == 0)
+                    __hip_atomic_store(&h->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+    }
+    if (q == 0) status_store(status + tile * 16 + d, status_word(kStateP, epoch, excl + tot));
+    return excl;
+}
+
+template <bool HAS_PERM_IN, bool WITH_PERM>
+__global__ __launch_bounds__(kR4Waves* kWave) void k_radix4_pass(
+    const uint32_t* keys_in, const int32_t* perm_in, uint32_t* keys_out, int32_t* perm_out,
+    int64_t n, int shift, const uint64_t* hist, WsHeader* hdr, uint64_t* status,
+    int64_t status_words, uint32_t ntiles) {
+    __shared__ Ticket s_ticket;
+    __shared__ uint32_t s_cnt[kR4Waves][16];
+    __shared__ uint32_t s_base[16];
+
+    if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
+    __syncthreads();
+    const uint32_t tile32 = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.tile);
+    const uint32_t epoch = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.epoch);
+    if (tile32 >= ntiles) {
+        if (threadIdx.x == 0)
+            __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
+    const int64_t tile = tile32;
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    const int64_t wbase = tile * kR4Tile + (int64_t)w * kR4Chunks * kWave;
+
+    uint32_t key[kR4Chunks];
+    int32_t perm[kR4Chunks];
+    const bool full = tile * kR4Tile + kR4Tile <= n;
+#pragma unroll
+    for (int j = 0; j < kR4Chunks; ++j) {
+        const int64_t i = wbase + j * kWave + lane;
+        const bool ok = full || i < n;
+        key[j] = ok ? keys_in[i] : 0u;
+        if (WITH_PERM) perm[j] = HAS_PERM_IN ? (ok ? perm_in[i] : 0) : (int32_t)i;
+    }
+
+    // Stable rank of every key among the wave's keys of the same digit, and
+    // the wave's per-digit totals (lane L < 16 holds digit L's running count).
+    uint32_t rank[kR4Chunks];
+    uint32_t run = 0;
+#pragma unroll
+    for (int j = 0; j < kR4Chunks; ++j) {
+        const int64_t i = wbase + j * kWave + lane;
+        const bool ok = full || i < n;
+        const uint32_t d = (key[j] >> shift) & 15u;
+        const uint64_t valid = __ballot(ok);
+        const uint64_t b0 = __ballot(ok && (d & 1));
+        const uint64_t b1 = __ballot(ok && (d & 2));
+        const uint64_t b2 = __ballot(ok && (d & 4));
+        const uint64_t b3 = __ballot(ok && (d & 8));
+        const uint64_t mine = digit_lanes(d, valid, b0, b1, b2, b3);
+        rank[j] = lane_shfl(run, (int)d) + lanes_below(mine);
+        run += (uint32_t)__builtin_popcountll(digit_lanes((uint32_t)(lane & 15), valid, b0, b1, b2, b3));
+    }
+    if (lane < 16) s_cnt[w][lane] = run;
+    __syncthreads();
+
+    // lanes 0..15 of every wave: count of digit `lane` in earlier waves, and
+    // (wave 0) the tile total that goes into the look-back.
+    uint32_t wofs = 0, tot = 0;
+#pragma unroll
+    for (int k = 0; k < kR4Waves; ++k) {
+        const uint32_t c = s_cnt[k][lane & 15];
+        if (k < w) wofs += c;
+        tot += c;
+    }
+    if (w == 0) {
+        const uint32_t before = lookback16(status, tile, tot, epoch, hdr);
+        // keys with a smaller digit, over the whole array (exclusive scan of
+        // the 16 histogram bins of this digit position)
+        const uint32_t h = lane < 16 ? (uint32_t)hist[(shift >> 2) * 16 + lane] : 0u;
+        const uint32_t smaller = wave_incl_scan(h) - h;
+        if (lane < 16) s_base[lane] = smaller + before;
+        if (lane == 0) finish_epoch(hdr, epoch, ntiles, status, status_words);
+    }
+    __syncthreads();
+    const uint32_t dest = (lane < 16 ? s_base[lane] : 0u) + wofs;  // lane d: start of digit d
+#pragma unroll
+    for (int j = 0; j < kR4Chunks; ++j) {
+        const int64_t i = wbase + j * kWave + lane;
+        const uint32_t d = (key[j] >> shift) & 15u;
+        const uint32_t pos = lane_shfl(dest, (int)d) + rank[j];
+        if ((full || i < n) && pos < (uint64_t)n) {  // pos < n always; guards a bad count
+            keys_out[pos] = key[j];
+            if (WITH_PERM) perm_out[pos] = perm[j];
+        }
+    }
+}
+
+// ---------------------------------------------------------------- driver
+
+hipError_t launch_radix1_pass(const uint32_t* keys, const int32_t* idx_in, int bit,
+                              uint32_t* keys_out, int32_t* idx_out, int64_t n, const uint64_t* hist,
+                              void* ws, size_t ws_bytes, size_t status_offset, hipStream_t stream);
+
+size_t radix_ws_bytes(int64_t n, int bits) {
+    const int64_t words = bits == 4 ? r4_tiles(n) * 16 : (n + kR1Tile - 1) / kR1Tile;
+    return kRadixStatusOffset + (size_t)words * sizeof(uint64_t);
+}
+
+hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out,
+                             uint32_t* keys_tmp, int32_t* perm_tmp, int64_t n, int bits, void* ws,
+                             size_t ws_bytes, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
+    uint64_t* hist = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
+    const int64_t hb = (n + 255) / 256;
+    hipLaunchKernelGGL(k_digit_hist, dim3((unsigned)(hb < 1024 ? hb : 1024)), dim3(256), 0, stream,
+                       keys, n, hist, hdr);
+    const int passes = bits == 4 ? 8 : 32;
+    const uint32_t* src_k = keys;
+    const int32_t* src_p = nullptr;
+    for (int p = 0; p < passes; ++p) {
+        uint32_t* dk = (p % 2 == 0) ? keys_tmp : keys_out;
+        int32_t* dp = perm_out ? ((p % 2 == 0) ? perm_tmp : perm_out) : nullptr;
+        if (bits == 1) {
+            const hipError_t e = launch_radix1_pass(src_k, src_p, p, dk, dp, n, hist, ws, ws_bytes,
+                                                    kRadixStatusOffset, stream);
+            if (e != hipSuccess) return e;
+        } else {
+            const uint32_t nt = (uint32_t)r4_tiles(n);
+            uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kRadixStatusOffset);
+            const int64_t sw = (int64_t)((ws_bytes - kRadixStatusOffset) / sizeof(uint64_t));
+            auto k = dp ? (src_p ? k_radix4_pass<true, true> : k_radix4_pass<false, true>)
+                        : k_radix4_pass<false, false>;
+            hipLaunchKernelGGL(k, dim3(nt), dim3(kR4Waves * kWave), 0, stream, src_k, src_p, dk, dp,
+                               n, 4 * p, (const uint64_t*)hist, hdr, status, sw, nt);
+            const hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
+        src_k = dk;
+        src_p = dp;
+    }
+    return hipSuccess;
+}
+
+}  // namespace ls

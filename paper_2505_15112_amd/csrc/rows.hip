@@ -1,0 +1,245 @@
+// rows.hip -- batched scans over the rows of a row-major rows x len matrix
+// (appendix "Multiple (Batched) Scans") and the top-p cutoff built on them
+// (Section 5 "Top-p or Nucleus Sampling").
+//
+// Two schedules, after the paper's observation that many short rows and a
+// few long rows want different mappings (its batched-scan crossover):
+//  * len <= one tile: one wavefront owns a whole row and walks it in chunks
+//    of 64 lanes x 4 elements with a running carry -- many rows per
+//    workgroup, no inter-workgroup communication;
+//  * longer rows: each row is cut into tile-sized segments, tiles are handed
+//    out row-major by ticket, and the decoupled look-back runs inside a row
+//    (it stops at the row's first segment), so 128 rows of 2^17 still give
+//    4096 workgroups to fill 256 CUs.
+// The top-p variant replaces the store of the prefix sums by a search for
+// the first index whose running sum reaches p.
+#include <limits.h>
+
+#include "launch.hpp"
+#include "tile.hpp"
+
+namespace ls {
+
+constexpr int kRWaves = 4;
+constexpr int kRChunks = 4;
+constexpr int kRVec = 4;
+constexpr int64_t kRowTile = kRWaves * kRChunks * kWave * kRVec;  // 4096
+
+static inline int64_t row_segments(int64_t len) { return (len + kRowTile - 1) / kRowTile; }
+static inline bool long_rows(int64_t len) { return len > kRowTile; }
+
+// Wavefront minimum with DPP (lanes outside the row / disabled read INT_MAX).
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int32_t dpp_min(int32_t v) {
+    const int32_t o = __builtin_amdgcn_update_dpp(INT_MAX, v, CTRL, ROW_MASK, 0xf, false);
+    return o < v ? o : v;
+}
+__device__ __forceinline__ int32_t wave_min(int32_t v) {
+    v = dpp_min<0x111, 0xf>(v);
+    v = dpp_min<0x112, 0xf>(v);
+    v = dpp_min<0x114, 0xf>(v);
+    v = dpp_min<0x118, 0xf>(v);
+    v = dpp_min<0x142, 0xa>(v);
+    v = dpp_min<0x143, 0xc>(v);
+    return __builtin_amdgcn_readlane(v, kWave - 1);
+}
+
+// ---------------------------------------------------------------- long rows
+
+template <class TileT, bool EXCL, bool VEC, bool TOPP>
+__global__ __launch_bounds__(TileT::kThreads) void k_rows_lookback(
+    const typename TileT::T* x, typename TileT::T* y, int64_t len, uint32_t segs,
+    uint32_t ntiles, WsHeader* hdr, uint64_t* status, int64_t status_words, float p,
+    int32_t* cutoff) {
+    using T = typename TileT::T;
+    __shared__ Ticket s_ticket;
+    __shared__ T s_wtot[TileT::WAVES];
+    __shared__ T s_carry;
+    __shared__ int32_t s_min[TileT::WAVES];
+
+    if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
+    __syncthreads();
+    const uint32_t tile32 = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.tile);
+    const uint32_t epoch = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.epoch);
+    if (tile32 >= ntiles) {  // only with a workspace that was never zero-filled
+        if (threadIdx.x == 0)
+            __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
+    const int64_t tile = tile32;
+    const int64_t row = tile / segs;
+    const int64_t seg = tile - row * segs;
+    const int64_t base = seg * TileT::kElems;
+    const T* xr = x + row * len;
+
+    T v[TileT::J][TileT::V];
+    T lane_off[TileT::J];
+    TileT::template load<VEC>(xr, len, base, v);
+    const T wtot = TileT::wave_scan(v, lane_off);
+    T wofs;
+    const T agg = TileT::combine_waves(wtot, s_wtot, &wofs);
+
+    if (threadIdx.x < kWave) {
+        const T excl = lookback<T>(status, tile, row * (int64_t)segs, agg, T(0), epoch, hdr);
+        if (threadIdx.x == 0) {
+            s_carry = excl;
+            finish_epoch(hdr, epoch, ntiles, status, status_words);
+        }
+    }
+    __syncthreads();
+    const T carry = s_carry + wofs;
+    if constexpr (!TOPP) {
+        TileT::template store<EXCL, VEC>(y + row * len, len, base, v, lane_off, carry);
+    } else {
+        // first element (in index order) whose inclusive running sum is >= p
+        int32_t cand = INT_MAX;
+#pragma unroll
+        for (int j = TileT::J - 1; j >= 0; --j) {
+            const int64_t off = TileT::offset(base, j);
+            const T lb = carry + lane_off[j];
+#pragma unroll
+            for (int e = TileT::V - 1; e >= 0; --e)
+                if (off + e < len && lb + v[j][e] >= p) cand = (int32_t)(off + e);
+        }
+        const int32_t wm = wave_min(cand);
+        const int w = threadIdx.x / kWave;
+        if (lane_id() == 0) s_min[w] = wm;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            int32_t m = INT_MAX;
+            for (int k = 0; k < TileT::WAVES; ++k) m = s_min[k] < m ? s_min[k] : m;
+            if (m != INT_MAX) atomicMin(cutoff + row, m);
+        }
+    }
+}
+
+__global__ void k_fill_i32(int32_t* p, int64_t count, int32_t value) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) p[i] = value;
+}
+
+// ---------------------------------------------------------------- short rows
+
+template <class T, bool EXCL, bool VEC, bool TOPP>
+__global__ __launch_bounds__(256) void k_rows_wave(const T* x, T* y, int64_t rows, int64_t len,
+                                                   float p, int32_t* cutoff) {
+    constexpr int V = 4;
+    const int lane = lane_id();
+    const int64_t nw = (int64_t)gridDim.x * (blockDim.x / kWave);
+    for (int64_t r = (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave; r < rows;
+         r += nw) {
+        const T* xr = x + r * len;
+        T carry = T(0);
+        int32_t found = -1;
+        for (int64_t c = 0; c < len; c += kWave * V) {
+            const int64_t off = c + (int64_t)lane * V;
+            T v[V];
+            if (VEC && c + kWave * V <= len) {
+                load_vec<T, T, V>(xr + off, v);
+            } else {
+#pragma unroll
+                for (int e = 0; e < V; ++e) v[e] = off + e < len ? xr[off + e] : T(0);
+            }
+#pragma unroll
+            for (int e = 1; e < V; ++e) v[e] = v[e - 1] + v[e];
+            const T inc = wave_incl_scan(v[V - 1]);
+            const T lb = carry + wave_shr1(inc);
+            if constexpr (!TOPP) {
+                T o[V];
+#pragma unroll
+                for (int e = 0; e < V; ++e) o[e] = EXCL ? (e == 0 ? lb : lb + v[e - 1]) : lb + v[e];
+                T* yr = y + r * len;
+                if (VEC && c + kWave * V <= len) {
+                    store_vec<T, V>(yr + off, o);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < V; ++e)
+                        if (off + e < len) yr[off + e] = o[e];
+                }
+            } else {
+                int32_t hit = INT_MAX;
+#pragma unroll
+                for (int e = V - 1; e >= 0; --e)
+                    if (off + e < len && lb + v[e] >= p) hit = (int32_t)(off + e);
+                const uint64_t m = __ballot(hit != INT_MAX);
+                if (m) {  // lanes are in index order: the lowest hitting lane has the first hit
+                    found = __builtin_amdgcn_readlane(hit, __builtin_ctzll(m));
+                    break;
+                }
+            }
+            carry = carry + lane_read(inc, kWave - 1);
+        }
+        if (TOPP && lane == 0) cutoff[r] = found >= 0 ? found : (int32_t)(len - 1);
+    }
+}
+
+// ---------------------------------------------------------------- launchers
+
+size_t scan_rows_ws_bytes(int64_t rows, int64_t len) {
+    if (!long_rows(len)) return kWsHeader;
+    return kWsHeader + (size_t)rows * (size_t)row_segments(len) * sizeof(uint64_t);
+}
+
+static bool aligned16(const void* p) { return ((uintptr_t)p % 16) == 0; }
+
+static unsigned wave_grid(int64_t rows) {
+    const int64_t blocks = (rows + 3) / 4;
+    return (unsigned)(blocks < 65536 ? blocks : 65536);
+}
+
+template <class T, bool TOPP>
+static hipError_t rows_typed(bool exclusive, const T* x, T* y, int64_t rows, int64_t len, float p,
+                             int32_t* cutoff, void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (rows == 0) return hipSuccess;
+    if (len == 0) {
+        if (TOPP)
+            hipLaunchKernelGGL(k_fill_i32, dim3(wave_grid(rows)), dim3(256), 0, stream, cutoff,
+                               rows, (int32_t)-1);
+        return hipGetLastError();
+    }
+    const bool vec = (len % 4 == 0) && aligned16(x) && (TOPP || aligned16(y));
+    if (!long_rows(len)) {
+        const dim3 grid(wave_grid(rows)), block(256);
+        auto k = exclusive ? (vec ? k_rows_wave<T, true, true, TOPP> : k_rows_wave<T, true, false, TOPP>)
+                           : (vec ? k_rows_wave<T, false, true, TOPP> : k_rows_wave<T, false, false, TOPP>);
+        hipLaunchKernelGGL(k, grid, block, 0, stream, x, y, rows, len, p, cutoff);
+        return hipGetLastError();
+    }
+    using TileT = Tile<T, T, kRVec, kRChunks, kRWaves>;
+    static_assert(TileT::kElems == kRowTile, "row tile size");
+    const uint32_t segs = (uint32_t)row_segments(len);
+    const uint32_t nt = (uint32_t)(rows * segs);
+    WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
+    uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
+    const int64_t status_words = (int64_t)((ws_bytes - kWsHeader) / sizeof(uint64_t));
+    if (TOPP)  // every row starts at "never reached": len - 1
+        hipLaunchKernelGGL(k_fill_i32, dim3(wave_grid(rows)), dim3(256), 0, stream, cutoff, rows,
+                           (int32_t)(len - 1));
+    auto k = exclusive ? (vec ? k_rows_lookback<TileT, true, true, TOPP> : k_rows_lookback<TileT, true, false, TOPP>)
+                       : (vec ? k_rows_lookback<TileT, false, true, TOPP> : k_rows_lookback<TileT, false, false, TOPP>);
+    hipLaunchKernelGGL(k, dim3(nt), dim3(TileT::kThreads), 0, stream, x, y, len, segs, nt, hdr,
+                       status, status_words, p, cutoff);
+    return hipGetLastError();
+}
+
+hipError_t launch_scan_rows(Kind kind, bool exclusive, const void* x, void* y, int64_t rows,
+                            int64_t len, void* ws, size_t ws_bytes, hipStream_t stream) {
+    switch (kind) {
+        case Kind::I32:
+            return rows_typed<uint32_t, false>(exclusive, (const uint32_t*)x, (uint32_t*)y, rows,
+                                               len, 0.f, nullptr, ws, ws_bytes, stream);
+        case Kind::F32:
+            return rows_typed<float, false>(exclusive, (const float*)x, (float*)y, rows, len, 0.f,
+                                            nullptr, ws, ws_bytes, stream);
+        default:
+            return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_topp_cutoff(const float* probs, int32_t* cutoff, int64_t rows, int64_t len,
+                              float p, void* ws, size_t ws_bytes, hipStream_t stream) {
+    return rows_typed<float, true>(false, probs, nullptr, rows, len, p, cutoff, ws, ws_bytes,
+                                   stream);
+}
+
+}  // namespace ls

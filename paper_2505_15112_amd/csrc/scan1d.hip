@@ -15,10 +15,21 @@
 
 namespace ls {
 
-// Tile geometry: 4 waves x 4 chunks x 64 lanes x 4 elements = 4096 elements.
-constexpr int kWaves = 4;
-constexpr int kChunks = 4;
+// Tile geometry: waves x chunks x 64 lanes x 4 elements, and the number of
+// 64-tile windows the look-back reads per round trip.
+#ifndef LIBSCAN_SCAN_WAVES
+#define LIBSCAN_SCAN_WAVES 4
+#endif
+#ifndef LIBSCAN_SCAN_CHUNKS
+#define LIBSCAN_SCAN_CHUNKS 4
+#endif
+#ifndef LIBSCAN_LOOKBACK_WINDOWS
+#define LIBSCAN_LOOKBACK_WINDOWS 1
+#endif
+constexpr int kWaves = LIBSCAN_SCAN_WAVES;
+constexpr int kChunks = LIBSCAN_SCAN_CHUNKS;
 constexpr int kVec = 4;
+constexpr int kLookbackWindows = LIBSCAN_LOOKBACK_WINDOWS;
 constexpr int64_t kTileElems = kWaves * kChunks * kWave * kVec;
 
 static inline int64_t num_tiles(int64_t n) { return (n + kTileElems - 1) / kTileElems; }
@@ -62,7 +73,7 @@ __global__ __launch_bounds__(TileT::kThreads) void k_scan_lookback(
 
     if (threadIdx.x < kWave) {
         const T c0 = (tile == 0 && carry_in) ? *carry_in : T(0);
-        const T excl = lookback<T>(status, tile, 0, agg, c0, epoch, hdr);
+        const T excl = lookback<T, kLookbackWindows>(status, tile, 0, agg, c0, epoch, hdr);
         if (threadIdx.x == 0) {
             s_carry = excl;
             if (total_out && tile == ntiles - 1) *total_out = excl + agg;

@@ -27,6 +27,10 @@ struct Conv<uint32_t, uint32_t> {
     __device__ static uint32_t f(uint32_t v) { return v; }
 };
 template <>
+struct Conv<int32_t, int32_t> {  // moved as-is (indices)
+    __device__ static int32_t f(int32_t v) { return v; }
+};
+template <>
 struct Conv<float, float> {
     __device__ static float f(float v) { return v; }
 };

@@ -139,3 +139,113 @@ def scan_inclusive_rss_i32(x, out=None, ws=None):
 
 def scan_inclusive_rss_f32(x, out=None, ws=None):
     return _scan1d("scan_inclusive_rss_f32", x, torch.float32, torch.float32, out, ws)
+
+
+def _rows(cname, x, dtype, exclusive, out, ws):
+    _check(x, dtype, "x", dims=(2,))
+    rows, length = x.shape
+    y = _out(x, out, dtype)
+    if ws is None:
+        ws = workspace(_lib.OP_SCAN_ROWS, x.device, rows=rows, length=length)
+    with torch.cuda.device(x.device):
+        _lib.call(cname, _ptr(x), _ptr(y), rows, length, int(bool(exclusive)), _ptr(ws),
+                  ws.numel(), _stream(x.device))
+    return y
+
+
+def scan_rows_i32(x, exclusive=False, out=None, ws=None):
+    """Independent scan of every row of a 2-D int32 tensor."""
+    return _rows("scan_rows_i32", x, torch.int32, exclusive, out, ws)
+
+
+def scan_rows_f32(x, exclusive=False, out=None, ws=None):
+    """Independent scan of every row of a 2-D fp32 tensor."""
+    return _rows("scan_rows_f32", x, torch.float32, exclusive, out, ws)
+
+
+def topp_cutoff_f32(probs, p, out=None, ws=None):
+    """Per row of descending-sorted probabilities: first index whose running
+    sum reaches p (int32 tensor of shape [rows])."""
+    _check(probs, torch.float32, "probs", dims=(2,))
+    rows, length = probs.shape
+    cut = _out(probs, out, torch.int32, shape=(rows,))
+    if ws is None:
+        ws = workspace(_lib.OP_SCAN_ROWS, probs.device, rows=rows, length=length)
+    with torch.cuda.device(probs.device):
+        _lib.call("topp_cutoff_f32", _ptr(probs), _ptr(cut), rows, length, float(p), _ptr(ws),
+                  ws.numel(), _stream(probs.device))
+    return cut
+
+
+def compact_by_mask_f32(x, mask, with_idx=False, out=None, idx_out=None, count=None, ws=None):
+    """torch.masked_select order.  Returns (out, idx_out or None, count) with
+    out/idx_out sized n (the first count entries are valid) and count a
+    1-element int32 device tensor."""
+    _check(x, torch.float32, "x")
+    if mask.dtype == torch.bool:
+        mask = mask.view(torch.uint8)
+    _check(mask, torch.uint8, "mask")
+    if mask.numel() != x.numel():
+        raise ValueError("mask and x differ in size")
+    n = x.numel()
+    out = _out(x, out, torch.float32, shape=(n,))
+    if with_idx and idx_out is None:
+        idx_out = torch.empty(n, dtype=torch.int32, device=x.device)
+    if count is None:
+        count = torch.empty(1, dtype=torch.int32, device=x.device)
+    if ws is None:
+        ws = workspace(_lib.OP_COMPACT, x.device, n)
+    with torch.cuda.device(x.device):
+        _lib.call("compact_by_mask_f32", _ptr(x), _ptr(mask), _ptr(out), _ptr(idx_out),
+                  ctypes.c_void_p(count.data_ptr()), n, _ptr(ws), ws.numel(), _stream(x.device))
+    return out, idx_out, count
+
+
+def split_by_flags_u32(keys, flags, idx_in=None, with_idx=True, keys_out=None, idx_out=None,
+                       n_true=None, ws=None):
+    """Stable split: flagged keys first.  keys are uint32 values held in an
+    int32 tensor (torch has no uint32 arithmetic); returns
+    (keys_out, idx_out or None, n_true)."""
+    _check(keys, torch.int32, "keys")
+    if flags.dtype == torch.bool:
+        flags = flags.view(torch.uint8)
+    _check(flags, torch.uint8, "flags")
+    n = keys.numel()
+    if flags.numel() != n:
+        raise ValueError("flags and keys differ in size")
+    if idx_in is not None:
+        _check(idx_in, torch.int32, "idx_in")
+    keys_out = _out(keys, keys_out, torch.int32, shape=(n,))
+    if with_idx and idx_out is None:
+        idx_out = torch.empty(n, dtype=torch.int32, device=keys.device)
+    if n_true is None:
+        n_true = torch.empty(1, dtype=torch.int32, device=keys.device)
+    if ws is None:
+        ws = workspace(_lib.OP_COMPACT, keys.device, n)
+    with torch.cuda.device(keys.device):
+        _lib.call("split_by_flags_u32", _ptr(keys), _ptr(idx_in), _ptr(flags), _ptr(keys_out),
+                  _ptr(idx_out), ctypes.c_void_p(n_true.data_ptr()), n, _ptr(ws), ws.numel(),
+                  _stream(keys.device))
+    return keys_out, idx_out, n_true
+
+
+def radix_sort_u32(keys, bits_per_pass=4, with_perm=True, keys_out=None, perm_out=None,
+                   keys_tmp=None, perm_tmp=None, ws=None):
+    """Stable ascending sort of uint32 keys (held in an int32 tensor; compare
+    them as unsigned).  Returns (keys_out, perm_out or None)."""
+    _check(keys, torch.int32, "keys")
+    n = keys.numel()
+    dev = keys.device
+    keys_out = _out(keys, keys_out, torch.int32, shape=(n,))
+    keys_tmp = torch.empty(n, dtype=torch.int32, device=dev) if keys_tmp is None else keys_tmp
+    if with_perm:
+        perm_out = torch.empty(n, dtype=torch.int32, device=dev) if perm_out is None else perm_out
+        perm_tmp = torch.empty(n, dtype=torch.int32, device=dev) if perm_tmp is None else perm_tmp
+    else:
+        perm_out = perm_tmp = None
+    if ws is None:
+        ws = workspace(_lib.OP_RADIX_SORT, dev, n, bits=bits_per_pass)
+    with torch.cuda.device(dev):
+        _lib.call("radix_sort_u32", _ptr(keys), _ptr(keys_out), _ptr(perm_out), _ptr(keys_tmp),
+                  _ptr(perm_tmp), n, int(bits_per_pass), _ptr(ws), ws.numel(), _stream(dev))
+    return keys_out, perm_out

@@ -52,3 +52,23 @@ def assert_equal_first_diff(got: np.ndarray, want: np.ndarray, what=""):
 
 
 FULL = os.environ.get("LIBSCAN_FULL_SIZE_TESTS", "1") == "1"
+
+
+def topp_accept(g: int, k: int, csum: np.ndarray, p: float) -> bool:
+    """GPU cutoff g against the oracle's k on one row.  csum is the float64
+    inclusive prefix of the row (non-negative entries, so it is also the
+    prefix of |x|).  g is accepted if it equals k, or if the fp64 prefix at g
+    is within tolerance of reaching p and the one before is within tolerance
+    of not reaching it (tol_i = 1e-5 * csum_i + 1e-6)."""
+    if g == k:
+        return True
+    n = csum.size
+    if not (0 <= g < n):
+        return False
+    tol = FLOAT_REL * csum + FLOAT_ABS
+    pd = float(np.float32(p))
+    if g == n - 1 and csum[g] < pd + tol[g] and (g == 0 or csum[g - 1] < pd + tol[g - 1]):
+        return True  # never reached within tolerance
+    ok_here = csum[g] >= pd - tol[g]
+    ok_before = g == 0 or csum[g - 1] < pd + tol[g - 1]
+    return bool(ok_here and ok_before)

@@ -19,6 +19,8 @@ P = ctypes.c_void_p
 X = P(0x100000)      # fake, never dereferenced
 Y = P(0x900000)
 WS = P(0x4000000)
+XB = P(1 << 40)      # far apart, for large fake sizes
+YB = P(1 << 41)
 BIG = 1 << 30
 
 
@@ -48,7 +50,7 @@ def test_workspace_bytes(lib):
     assert lib.libscan_workspace_bytes(_lib.OP_SCAN, 0, 0, 0, 0, ctypes.byref(out)) == 0
     small = out.value
     assert lib.libscan_workspace_bytes(_lib.OP_SCAN, 1 << 28, 0, 0, 0, ctypes.byref(out)) == 0
-    assert out.value >= small + 8 * ((1 << 28) // 8192)
+    assert out.value >= small + 8 * ((1 << 28) // 16384)
     assert lib.libscan_workspace_bytes(_lib.OP_SCAN_RSS, 1 << 20, 0, 0, 0, ctypes.byref(out)) == 0
     assert lib.libscan_workspace_bytes(99, 10, 0, 0, 0, ctypes.byref(out)) == _lib.EINVAL
     assert lib.libscan_workspace_bytes(_lib.OP_SCAN, -1, 0, 0, 0, ctypes.byref(out)) == _lib.EINVAL
@@ -99,3 +101,81 @@ def test_python_binding_needs_gpu_tensors():
         ops.scan_inclusive_i32(torch.zeros(10, dtype=torch.int32))
     with pytest.raises(TypeError):
         ops.scan_inclusive_i32(torch.zeros(10, dtype=torch.int64))
+
+
+def test_rows_validation(lib):
+    for name in ("scan_rows_i32", "scan_rows_f32"):
+        fn = getattr(lib, name)
+        assert fn(X, Y, -1, 10, 0, WS, BIG, None) == _lib.EINVAL
+        assert fn(X, Y, 10, -1, 0, WS, BIG, None) == _lib.EINVAL
+        assert fn(None, Y, 10, 10, 0, WS, BIG, None) == _lib.EINVAL
+        assert fn(X, P(0x100010), 10, 10, 0, WS, BIG, None) == _lib.EINVAL  # overlap
+        assert fn(X, Y, 1 << 20, 1 << 20, 0, WS, BIG, None) == _lib.ERANGE
+        assert fn(X, Y, 1 << 24, 8192, 0, WS, BIG, None) == _lib.ERANGE      # grid too large
+        assert fn(XB, YB, 100, 100_000, 0, WS, 64, None) == _lib.ENOSPACE
+        assert fn(None, None, 0, 10, 0, None, 0, None) == _lib.OK
+
+
+def test_topp_validation(lib):
+    fn = lib.topp_cutoff_f32
+    assert fn(X, Y, 4, 10, float("nan"), WS, BIG, None) == _lib.EINVAL
+    assert fn(X, None, 4, 10, 0.9, WS, BIG, None) == _lib.EINVAL
+    assert fn(None, Y, 4, 10, 0.9, WS, BIG, None) == _lib.EINVAL
+    assert fn(X, P(0x100008), 4, 10, 0.9, WS, BIG, None) == _lib.EINVAL  # cutoff inside probs
+    assert fn(X, Y, 1, 1 << 31, 0.9, WS, BIG, None) == _lib.ERANGE
+    assert fn(XB, YB, 128, 131072, 0.9, WS, 256, None) == _lib.ENOSPACE
+    assert fn(None, None, 0, 10, 0.9, None, 0, None) == _lib.OK
+
+
+def test_rows_workspace_bytes(lib):
+    out = ctypes.c_size_t(0)
+    assert lib.libscan_workspace_bytes(_lib.OP_SCAN_ROWS, 0, 128, 131072, 0,
+                                       ctypes.byref(out)) == 0
+    assert out.value >= 256 + 128 * 32 * 8
+    assert lib.libscan_workspace_bytes(_lib.OP_SCAN_ROWS, 0, 1000, 100, 0, ctypes.byref(out)) == 0
+    assert out.value == 256  # one wavefront per row needs no status words
+
+
+def test_compact_validation(lib):
+    fn = lib.compact_by_mask_f32
+    C = P(0x7000000)
+    assert fn(X, Y, WS, None, C, -1, WS, BIG, None) == _lib.EINVAL
+    assert fn(X, Y, P(0x2000000), None, None, 10, WS, BIG, None) == _lib.EINVAL   # no count
+    assert fn(None, Y, P(0x2000000), None, C, 10, WS, BIG, None) == _lib.EINVAL
+    assert fn(X, Y, P(0x100010), None, C, 10, WS, BIG, None) == _lib.EINVAL     # out over x
+    assert fn(X, Y, P(0x2000000), P(0x2000010), C, 10, WS, BIG, None) == _lib.EINVAL  # idx/out
+    assert fn(XB, YB, P(1 << 42), None, C, 1 << 31, WS, BIG, None) == _lib.ERANGE
+    assert fn(XB, YB, P(1 << 42), None, C, 1 << 20, WS, 64, None) == _lib.ENOSPACE
+
+
+def test_split_validation(lib):
+    fn = lib.split_by_flags_u32
+    KO, IO, NT = P(0x2000000), P(0x3000000), P(0x7000000)
+    assert fn(X, None, Y, KO, IO, NT, -1, WS, BIG, None) == _lib.EINVAL
+    assert fn(None, None, Y, KO, IO, NT, 10, WS, BIG, None) == _lib.EINVAL
+    assert fn(X, None, None, KO, IO, NT, 10, WS, BIG, None) == _lib.EINVAL      # no flags
+    assert fn(X, None, Y, X, IO, NT, 10, WS, BIG, None) == _lib.EINVAL         # in place
+    assert fn(X, None, Y, KO, P(0x2000004), NT, 10, WS, BIG, None) == _lib.EINVAL
+    assert fn(X, IO, Y, KO, IO, NT, 10, WS, BIG, None) == _lib.EINVAL          # idx_out == idx_in
+    assert fn(XB, None, YB, P(1 << 42), None, None, 1 << 31, WS, BIG, None) == _lib.ERANGE
+    assert fn(XB, None, YB, P(1 << 42), None, None, 1 << 20, WS, 64, None) == _lib.ENOSPACE
+    assert fn(None, None, None, None, None, None, 0, None, 0, None) == _lib.OK
+
+
+def test_radix_validation(lib):
+    fn = lib.radix_sort_u32
+    KO, PO, KT, PT = P(0x2000000), P(0x3000000), P(0x4000000), P(0x5000000)
+    W2 = P(0x60000000)
+    assert fn(X, KO, PO, KT, PT, -1, 4, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, KO, PO, KT, PT, 10, 2, W2, BIG, None) == _lib.EINVAL        # bits not 1/4
+    assert fn(X, KO, PO, None, PT, 10, 4, W2, BIG, None) == _lib.EINVAL      # no keys_tmp
+    assert fn(X, KO, PO, KT, None, 10, 4, W2, BIG, None) == _lib.EINVAL      # perm without tmp
+    assert fn(X, X, PO, KT, PT, 10, 4, W2, BIG, None) == _lib.EINVAL         # in place
+    assert fn(X, KO, PO, P(0x2000008), PT, 10, 4, W2, BIG, None) == _lib.EINVAL
+    assert fn(XB, YB, None, P(1 << 42), None, 1 << 31, 4, W2, BIG, None) == _lib.ERANGE
+    assert fn(X, KO, PO, KT, PT, 1000, 4, W2, 64, None) == _lib.ENOSPACE
+    assert fn(None, None, None, None, None, 0, 4, None, 0, None) == _lib.OK
+    out = ctypes.c_size_t(0)
+    assert lib.libscan_workspace_bytes(_lib.OP_RADIX_SORT, 1 << 26, 0, 0, 4, ctypes.byref(out)) == 0
+    assert out.value >= 256 + 1024 + 16 * 8 * ((1 << 26) // 4096)
+    assert lib.libscan_workspace_bytes(_lib.OP_RADIX_SORT, 100, 0, 0, 3, ctypes.byref(out)) == _lib.EINVAL
