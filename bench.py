@@ -2,14 +2,21 @@
 """libscan benchmark on one MI355X.
 
 One step = one 1-D inclusive prefix sum over n = 2^28 int32 elements (inputs
-resident in HBM), i.e. the hot path's single kernel: tile load, lane / wave /
-workgroup scan, decoupled look-back, carry + store.  Printed value = achieved
-GB/s counting the algorithmic bytes n*(4+4) (read x once, write y once).  The
-same run also measures the fp32 scan and a device-to-device memcpy of the
-same byte count, and reports the scans as a fraction of that memcpy.
+resident in HBM): the hot path's single kernel -- tile load, lane / wave /
+workgroup scan, decoupled look-back, carry + store.  The printed value is the
+achieved GB/s on the algorithmic bytes n*(4+4) (x read once, y written once),
+beside a device-to-device memcpy of the same bytes timed in the same run.
 
-Output: ONE JSON line on stdout (rank 0).  --gpus N > 1 is refused: this
-library runs on one GPU.
+The same run measures every other operation of the library on its workload
+("ops"): the fp32 metric scan, the reduce-then-scan check variant, the
+fp16->fp32 scan (n = 2^24), the latency-bound int32 scan (n = 2^16), mask
+compaction (n = 2^28), batched rows and the top-p cutoff (128 x 131072),
+stable split and both radix sorts (n = 2^26).  Workloads that fit in the
+256 MB Infinity Cache are timed one call at a time after a 512 MiB flush.
+The CPU-baseline leg times the serial oracle on each workload (or a stated
+sample) and checks the GPU outputs against it.
+
+Output: ONE JSON line on stdout.  --gpus N > 1 is refused: one GPU only.
 """
 import argparse
 import ctypes
@@ -38,7 +45,7 @@ def kernel_source_hash() -> str:
     return h.hexdigest()
 
 
-def measured_traffic(bytes_per_launch):
+def measured_traffic():
     """HBM bytes per launch from the committed rocprofv3 PMC summary, or None
     when it is absent or was taken on different kernel sources."""
     try:
@@ -51,44 +58,55 @@ def measured_traffic(bytes_per_launch):
     return pmc.get("hbm_bytes_per_launch")
 
 
-def time_calls(torch, fn, steps, warmup, stream):
-    for _ in range(warmup):
-        fn()
-    torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for _ in range(steps):
-        fn()
-    end.record(stream)
-    torch.cuda.synchronize()
-    return start.elapsed_time(end) / steps  # ms per call
+class Timer:
+    def __init__(self, torch, stream, dev):
+        self.torch = torch
+        self.stream = stream
+        self.flush_buf = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+
+    def back_to_back(self, fn, steps, warmup):
+        torch = self.torch
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(self.stream)
+        for _ in range(steps):
+            fn()
+        b.record(self.stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / steps  # ms per call
+
+    def flushed(self, fn, steps, warmup):
+        """Each call timed alone after overwriting 512 MiB (evicts L2 and MALL)."""
+        torch = self.torch
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        evs = []
+        for _ in range(steps):
+            self.flush_buf.zero_()
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(self.stream)
+            fn()
+            b.record(self.stream)
+            evs.append((a, b))
+        torch.cuda.synchronize()
+        return sum(a.elapsed_time(b) for a, b in evs) / steps
 
 
-def cpu_baseline(x_host, y_dev, torch, reps=3):
-    """The CPU oracle (serial C, one thread) timed on the same input; its
-    output is also compared with the GPU result."""
-    import numpy as np
-    import oracle
-
-    times = []
-    ref = None
-    for _ in range(reps):
-        t0 = time.perf_counter()
-        ref = oracle.scan_i32(x_host)
-        times.append(time.perf_counter() - t0)
-    t = sorted(times)[len(times) // 2]
-    ok = bool(np.array_equal(ref, y_dev.cpu().numpy()))
-    nbytes = x_host.size * 8
-    return {
-        "value": round(nbytes / t / 1e9, 3),
-        "unit": "GB/s",
-        "cores": 1,
-        "kind": "oracle",
-        "sample": f"the full workload: 1-D inclusive int32 scan of n={x_host.size} "
-                  f"(serial C oracle, median of {reps} runs, {t:.3f} s each)",
-        "matches_gpu": ok,
-    }
+def entry(name, ms, nbytes, memcpy_ms, unit_note, extra=None):
+    gbps = nbytes / (ms * 1e-3) / 1e9
+    e = {"ms": round(ms, 5), "gbps": round(gbps, 2), "bytes": nbytes,
+         "pct_of_memcpy": round(100.0 * memcpy_ms / ms, 2),
+         "roofline": {"bound": "hbm", "achieved": round(gbps, 2), "peak": PEAK_HBM_GBPS,
+                      "unit": "GB/s", "frac": round(gbps / PEAK_HBM_GBPS, 4)},
+         "bytes_counted": unit_note}
+    if extra:
+        e.update(extra)
+    return e
 
 
 def main():
@@ -98,12 +116,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--n", type=int, default=1 << 28)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--metric-only", action="store_true", help="skip the per-op measurements")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py: libscan is a single-GPU library; only --gpus 1 is supported "
-              "(a sharded scan would exchange one carry per GPU; see DESIGN.md).",
-              file=sys.stderr)
+              "(a sharded scan would exchange one carry per GPU).", file=sys.stderr)
         return 2
 
     import numpy as np
@@ -112,51 +130,64 @@ def main():
     from paper_2505_15112_amd import _lib, ops
     from paper_2505_15112_amd import workloads as W
 
+    def log(*a):
+        print("[bench]", *a, file=sys.stderr, flush=True)
+
     n = args.n
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream(dev)
     lib = _lib.load()
     sp = ctypes.c_void_p(stream.cuda_stream)
+    T = Timer(torch, stream, dev)
+    K, Wm = args.steps, args.warmup
+    P = lambda t: ctypes.c_void_p(t.data_ptr()) if t is not None else None  # noqa: E731
 
+    def check(st, name):
+        if st != 0:
+            raise RuntimeError(f"{name}: status {st}")
+
+    def memcpy_ms(nbytes, flushed=False):
+        """D2D copy moving nbytes in total (nbytes/2 read + nbytes/2 written)."""
+        m = max(1, nbytes // 2)
+        src = torch.empty(m, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        f = lambda: dst.copy_(src)  # noqa: E731
+        return (T.flushed(f, K, Wm) if flushed else T.back_to_back(f, K, Wm))
+
+    # ---------------------------------------------------------------- metric
+    log("metric inputs")
     x_i32_host = W.scan_i32(n, seed=0)
     x_i32 = torch.from_numpy(x_i32_host).to(dev)
     y_i32 = torch.empty_like(x_i32)
-    x_f32 = torch.from_numpy(W.scan_f32(n, seed=0)).to(dev)
+    x_f32_host = W.scan_f32(n, seed=0)
+    x_f32 = torch.from_numpy(x_f32_host).to(dev)
     y_f32 = torch.empty_like(x_f32)
     ws = ops.workspace(_lib.OP_SCAN, dev, n)
-    wsp, wsb = ctypes.c_void_p(ws.data_ptr()), ws.numel()
+    wsp, wsb = P(ws), ws.numel()
     torch.cuda.synchronize()
 
-    def call(name, x, y):
+    def scan_call(name, x, y, nn, w=None):
         fn = getattr(lib, name)
-        xp, yp = ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(y.data_ptr())
-
-        def run():
-            st = fn(xp, yp, n, wsp, wsb, sp)
-            if st != 0:
-                raise RuntimeError(f"{name}: status {st}")
-        return run
+        wp, wb = (wsp, wsb) if w is None else (P(w), w.numel())
+        a = (P(x), P(y), nn, wp, wb, sp)
+        return lambda: check(fn(*a), name)
 
     nbytes = n * 8
-    ms_i32 = time_calls(torch, call("scan_inclusive_i32", x_i32, y_i32), args.steps, args.warmup,
-                        stream)
-    ms_f32 = time_calls(torch, call("scan_inclusive_f32", x_f32, y_f32), args.steps, args.warmup,
-                        stream)
-    # same-run device memcpy moving the same bytes (n*4 read + n*4 written)
-    cp_dst = torch.empty_like(x_i32)
-    ms_cp = time_calls(torch, lambda: cp_dst.copy_(x_i32), args.steps, args.warmup, stream)
-
-    gbps = lambda ms: nbytes / (ms * 1e-3) / 1e9  # noqa: E731
-    g_i32, g_f32, g_cp = gbps(ms_i32), gbps(ms_f32), gbps(ms_cp)
+    log("metric timing")
+    ms_i32 = T.back_to_back(scan_call("scan_inclusive_i32", x_i32, y_i32, n), K, Wm)
+    ms_f32 = T.back_to_back(scan_call("scan_inclusive_f32", x_f32, y_f32, n), K, Wm)
+    ms_cp = memcpy_ms(nbytes)
+    g = lambda ms, b=nbytes: b / (ms * 1e-3) / 1e9  # noqa: E731
+    g_i32, g_f32, g_cp = g(ms_i32), g(ms_f32), g(ms_cp)
 
     line = {
         "metric": METRIC,
         "value": round(g_i32, 2),
         "unit": "GB/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": K,
+        "warmup": Wm,
         "ms_per_step": round(ms_i32, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -176,20 +207,208 @@ def main():
             "pct_of_memcpy": round(100.0 * g_f32 / g_cp, 2),
         },
         "roofline": {
-            "kernel": "k_scan_lookback (int32, inclusive, 16-byte vector path)",
+            "kernel": "k_scan_lookback<Tile<u32,u32,4,16,8>> (int32 inclusive, 32768-element "
+                      "tiles, 16-byte vector path)",
             "bound": "hbm",
             "achieved": round(g_i32, 2),
             "peak": PEAK_HBM_GBPS,
             "unit": "GB/s",
             "frac": round(g_i32 / PEAK_HBM_GBPS, 4),
-            "traffic": measured_traffic(nbytes),
+            "traffic": measured_traffic(),
             "algorithmic_bytes_per_launch": nbytes,
         },
     }
+
+    # ---------------------------------------------------------------- other rows
+    outputs = {}
+    if not args.metric_only:
+        opsd = {}
+        # reduce-then-scan check variant (3 kernels, x read twice)
+        wsr = ops.workspace(_lib.OP_SCAN_RSS, dev, n)
+        y_rss = torch.empty_like(x_i32)
+        ms = T.back_to_back(scan_call("scan_inclusive_rss_i32", x_i32, y_rss, n, wsr), K, Wm)
+        opsd["scan_rss_i32_n2^28"] = entry("rss", ms, nbytes, ms_cp, "n*(4+4); x is read twice",
+                                          {"traffic_ratio_vs_lookback": 1.5})
+        outputs["rss_equal"] = bool(torch.equal(y_rss, y_i32))
+        del y_rss, wsr
+
+        # config: fp16 -> fp32, n = 2^24 (fits in MALL: flushed timing)
+        n2 = 1 << 24
+        x16_host = W.scan_f16(n2, seed=0)
+        x16 = torch.from_numpy(x16_host).to(dev)
+        y16 = torch.empty(n2, dtype=torch.float32, device=dev)
+        b2 = n2 * 6
+        ms = T.flushed(scan_call("scan_inclusive_f16f32", x16, y16, n2), K, Wm)
+        opsd["scan_f16f32_n2^24"] = entry("f16", ms, b2, memcpy_ms(b2, True),
+                                          "n*(2+4), cache-flushed")
+        outputs["f16"] = (x16_host, y16)
+
+        # config: int32, n = 2^16 (latency-bound)
+        n1 = 1 << 16
+        x1_host = W.scan_i32(n1, seed=0)
+        x1 = torch.from_numpy(x1_host).to(dev)
+        y1 = torch.empty_like(x1)
+        ms_f = T.flushed(scan_call("scan_inclusive_i32", x1, y1, n1), K, Wm)
+        ms_b = T.back_to_back(scan_call("scan_inclusive_i32", x1, y1, n1), K, Wm)
+        opsd["scan_i32_n2^16"] = entry("c1", ms_f, n1 * 8, memcpy_ms(n1 * 8, True),
+                                       "n*(4+4), cache-flushed; latency-bound",
+                                       {"us_flushed": round(ms_f * 1e3, 2),
+                                        "us_back_to_back": round(ms_b * 1e3, 2)})
+        outputs["c1"] = (x1_host, y1)
+
+        # config: compaction n = 2^28, Bernoulli(1/2) mask, N(0,1) values
+        log("compaction")
+        vals_host = W.values_f32(n, seed=0)
+        mask_host = W.mask_u8(n, seed=0)
+        vals = torch.from_numpy(vals_host).to(dev)
+        mask = torch.from_numpy(mask_host).to(dev)
+        out = torch.empty_like(vals)
+        idx = torch.empty(n, dtype=torch.int32, device=dev)
+        cnt = torch.empty(1, dtype=torch.int32, device=dev)
+        wsc = ops.workspace(_lib.OP_COMPACT, dev, n)
+        fnc = lib.compact_by_mask_f32
+        for with_idx in (False, True):
+            a = (P(vals), P(mask), P(out), P(idx) if with_idx else None, P(cnt), n, P(wsc),
+                 wsc.numel(), sp)
+            ms = T.back_to_back(lambda: check(fnc(*a), "compact"), K, Wm)
+            c = int(cnt.item())
+            bb = n * 5 + c * 4 + (c * 4 if with_idx else 0)
+            opsd["compact_n2^28" + ("_idx" if with_idx else "")] = entry(
+                "compact", ms, bb, memcpy_ms(bb), "n*(1+4) + count*4 (+count*4 indices)",
+                {"count": c})
+        outputs["compact"] = (vals_host, mask_host, out, idx, cnt)
+        del x_f32, y_f32
+
+        # config: rows + top-p, 128 x 131072 sorted softmax rows (64 MiB: flushed)
+        log("rows/top-p")
+        rows, length = 128, 131072
+        probs_host = W.topp_probs(rows, length, seed=0)
+        probs = torch.from_numpy(probs_host).to(dev)
+        cut = torch.empty(rows, dtype=torch.int32, device=dev)
+        wst = ops.workspace(_lib.OP_SCAN_ROWS, dev, rows=rows, length=length)
+        a = (P(probs), P(cut), rows, length, ctypes.c_float(0.9), P(wst), wst.numel(), sp)
+        ms = T.flushed(lambda: check(lib.topp_cutoff_f32(*a), "topp"), K, Wm)
+        bt = rows * length * 4
+        opsd["topp_128x131072"] = entry("topp", ms, bt, memcpy_ms(bt, True),
+                                        "full rows read once (rows*len*4), cache-flushed",
+                                        {"p": 0.9})
+        yr = torch.empty_like(probs)
+        a2 = (P(probs), P(yr), rows, length, 0, P(wst), wst.numel(), sp)
+        ms = T.flushed(lambda: check(lib.scan_rows_f32(*a2), "rows"), K, Wm)
+        opsd["scan_rows_f32_128x131072"] = entry("rows", ms, 2 * bt, memcpy_ms(2 * bt, True),
+                                                 "rows*len*(4+4), cache-flushed")
+        outputs["topp"] = (probs_host, cut, yr)
+
+        # config: radix sort, n = 2^26 uint32 keys (+ int32 permutation)
+        log("radix")
+        n5 = 1 << 26
+        keys_host = W.keys_u32(n5, seed=0)
+        keys = torch.from_numpy(keys_host.view(np.int32)).to(dev)
+        ko = torch.empty_like(keys)
+        po = torch.empty_like(keys)
+        kt = torch.empty_like(keys)
+        pt = torch.empty_like(keys)
+        for bits, passes in ((4, 8), (1, 32)):
+            wsx = ops.workspace(_lib.OP_RADIX_SORT, dev, n5, bits=bits)
+            a = (P(keys), P(ko), P(po), P(kt), P(pt), n5, bits, P(wsx), wsx.numel(), sp)
+            ms = T.back_to_back(lambda: check(lib.radix_sort_u32(*a), "radix"), max(3, K // 4),
+                                2)
+            bb = n5 * (4 + 12 + 16 * (passes - 1))  # histogram read + passes
+            opsd[f"radix{bits}_n2^26"] = entry(
+                "radix", ms, bb, memcpy_ms(bb), f"keys read once for the histogram + pass 0 "
+                f"4+4+4 + {passes - 1} passes x 16 bytes per key",
+                {"mkeys_per_s": round(n5 / (ms * 1e-3) / 1e6, 1), "passes": passes})
+            outputs[f"radix{bits}"] = (ko.clone(), po.clone())
+        # stable split on its own (flags Bernoulli(1/2)), n = 2^26
+        flags = torch.from_numpy(W.mask_u8(n5, seed=1)).to(dev)
+        nt = torch.empty(1, dtype=torch.int32, device=dev)
+        wss = ops.workspace(_lib.OP_COMPACT, dev, n5)
+        a = (P(keys), None, P(flags), P(ko), P(po), P(nt), n5, P(wss), wss.numel(), sp)
+        ms = T.back_to_back(lambda: check(lib.split_by_flags_u32(*a), "split"), K, Wm)
+        bb = n5 * (1 + 1 + 4 + 4 + 4)  # count kernel reads flags; split reads flags+keys, writes
+        opsd["split_n2^26"] = entry("split", ms, bb, memcpy_ms(bb), "n*(1 count + 1+4 read + "
+                                    "4+4 written), no input indices")
+        outputs["radix_keys"] = keys_host
+        line["ops"] = opsd
+
+    # ---------------------------------------------------------------- CPU leg
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(x_i32_host, y_i32, torch)
+        log("cpu baseline")
+        line["cpu_baseline"], line["cpu_baseline_ops"] = cpu_baseline_leg(
+            x_i32_host, y_i32, outputs, np, torch)
     print(json.dumps(line), flush=True)
     return 0
+
+
+def cpu_baseline_leg(x_host, y_dev, outputs, np, torch):
+    """The serial CPU oracle timed on the machine's host (one thread), and every
+    GPU output of this run checked against it."""
+    import oracle
+
+    def timed(fn, reps=3):
+        ts, r = [], None
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            r = fn()
+            ts.append(time.perf_counter() - t0)
+        return sorted(ts)[len(ts) // 2], r
+
+    t, ref = timed(lambda: oracle.scan_i32(x_host))
+    metric = {
+        "value": round(x_host.size * 8 / t / 1e9, 3), "unit": "GB/s", "cores": 1,
+        "kind": "oracle",
+        "sample": f"the full workload: 1-D inclusive int32 scan of n={x_host.size} "
+                  f"(serial C oracle, median of 3 runs, {t:.3f} s each)",
+        "matches_gpu": bool(np.array_equal(ref, y_dev.cpu().numpy())),
+    }
+    res = {}
+    if "f16" in outputs:
+        xh, y = outputs["f16"]
+        t, (r, a) = timed(lambda: oracle.scan_f16(xh))
+        ok = bool(np.all(np.abs(y.cpu().numpy() - r) <= 1e-5 * a + 1e-6))
+        res["scan_f16f32_n2^24"] = {"gbps": round(xh.size * 6 / t / 1e9, 3), "s": round(t, 4),
+                                    "matches_gpu": ok}
+        xh, y = outputs["c1"]
+        t, r = timed(lambda: oracle.scan_i32(xh))
+        res["scan_i32_n2^16"] = {"us": round(t * 1e6, 1),
+                                 "matches_gpu": bool(np.array_equal(r, y.cpu().numpy()))}
+        res["scan_rss_i32_n2^28"] = {"matches_lookback_bitwise": outputs["rss_equal"]}
+        vh, mh, out, idx, cnt = outputs["compact"]
+        t, (ro, ri) = timed(lambda: oracle.compact_f32(vh, mh), reps=1)
+        c = int(cnt.item())
+        ok = c == ro.size and np.array_equal(out[:c].cpu().numpy().view(np.uint32),
+                                             ro.view(np.uint32)) and np.array_equal(
+            idx[:c].cpu().numpy(), ri)
+        res["compact_n2^28"] = {"gbps": round((vh.size * 5 + c * 8) / t / 1e9, 3),
+                                "s": round(t, 3), "matches_gpu": bool(ok)}
+        ph, cut, yr = outputs["topp"]
+        t, rc = timed(lambda: oracle.topp_cutoff_f32(ph, 0.9))
+        g = cut.cpu().numpy()
+        csum = np.cumsum(ph.astype(np.float64), axis=1)
+        tol = 1e-5 * csum + 1e-6
+        pd = float(np.float32(0.9))
+        band = [g[r] == rc[r] or (csum[r, g[r]] >= pd - tol[r, g[r]] and
+                                  (g[r] == 0 or csum[r, g[r] - 1] < pd + tol[r, g[r] - 1]))
+                for r in range(ph.shape[0])]
+        res["topp_128x131072"] = {"gbps": round(ph.size * 4 / t / 1e9, 3), "s": round(t, 4),
+                                  "matches_gpu_within_band": bool(all(band)),
+                                  "exact_rows": int(np.sum(g == rc))}
+        t, (ry, ra) = timed(lambda: oracle.scan_rows_f32(ph), reps=1)
+        ok = bool(np.all(np.abs(yr.cpu().numpy() - ry) <= 1e-5 * ra + 1e-6))
+        res["scan_rows_f32_128x131072"] = {"gbps": round(ph.size * 8 / t / 1e9, 3),
+                                           "s": round(t, 4), "matches_gpu": ok}
+        kh = outputs["radix_keys"]
+        sample = kh[: 1 << 22]
+        t, _ = timed(lambda: oracle.sort_u32(sample), reps=1)
+        rk, rp = oracle.sort_u32(kh)
+        for bits in (4, 1):
+            ko, po = outputs[f"radix{bits}"]
+            res[f"radix{bits}_n2^26"] = {
+                "mkeys_per_s": round(sample.size / t / 1e6, 2),
+                "sample": "first 2^22 keys of the workload (qsort of (key, index) pairs)",
+                "matches_gpu": bool(np.array_equal(ko.cpu().numpy().view(np.uint32), rk) and
+                                    np.array_equal(po.cpu().numpy(), rp))}
+    return metric, res
 
 
 if __name__ == "__main__":

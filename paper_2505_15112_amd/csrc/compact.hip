@@ -25,6 +25,7 @@ constexpr int kCVec = 4;
 constexpr int64_t kCTile = kCWaves * kCChunks * kWave * kCVec;  // 4096
 
 static inline int64_t c_tiles(int64_t n) { return (n + kCTile - 1) / kCTile; }
+static inline int64_t s_tiles(int64_t n);
 
 using FlagTile = Tile<uint8_t, uint32_t, kCVec, kCChunks, kCWaves>;
 using KeyTile = Tile<uint32_t, uint32_t, kCVec, kCChunks, kCWaves>;
@@ -71,12 +72,28 @@ __device__ __forceinline__ void mask_tail(int64_t n, int64_t base, uint32_t (&f)
 
 // ---------------------------------------------------------------- compress
 
+// Compress tile: 8 waves x 16 chunks x 64 lanes x 4 elements = 32768.  A
+// lane keeps the 4 mask bytes of a chunk packed in one register (bit 8e set
+// when element e is kept) next to its 4 values, so a large tile fits in
+// registers and the per-tile look-back is paid rarely.
+constexpr int kPWaves = 8;
+constexpr int kPChunks = 16;
+constexpr int64_t kPTile = kPWaves * kPChunks * kWave * 4;
+
+// Per byte: 1 if the byte is non-zero, else 0 (bits 0, 8, 16, 24).
+__device__ __forceinline__ uint32_t nonzero_bytes(uint32_t m) {
+    uint32_t t = m | ((m >> 4) & 0x0f0f0f0fu);
+    t |= (t >> 2) & 0x33333333u;
+    t |= (t >> 1) & 0x55555555u;
+    return t & 0x01010101u;
+}
+
 template <bool VEC, bool WITH_IDX>
-__global__ __launch_bounds__(FlagTile::kThreads) void k_compact(
+__global__ __launch_bounds__(kPWaves* kWave) void k_compact(
     const float* x, const uint8_t* mask, float* out, int32_t* idx, int32_t* count, int64_t n,
     WsHeader* hdr, uint64_t* status, int64_t status_words, uint32_t ntiles) {
     __shared__ Ticket s_ticket;
-    __shared__ uint32_t s_wtot[kCWaves];
+    __shared__ uint32_t s_wtot[kPWaves];
     __shared__ uint32_t s_carry;
 
     if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
@@ -89,16 +106,54 @@ __global__ __launch_bounds__(FlagTile::kThreads) void k_compact(
         return;
     }
     const int64_t tile = tile32;
-    const int64_t base = tile * kCTile;
+    const int64_t base = tile * kPTile;
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    auto offset = [&](int j) { return base + ((int64_t)(w * kPChunks + j) * kWave + lane) * 4; };
 
-    uint32_t f[kCChunks][kCVec], unused[kCChunks][kCVec];
-    float xv[kCChunks][kCVec];
-    load_flags<false, VEC>(mask, nullptr, 0, n, base, f, unused);
-    ValTile::template load<VEC>(x, n, base, xv);
-    uint32_t lane_off[kCChunks];
-    const uint32_t wtot = FlagTile::wave_scan(f, lane_off);  // f becomes in-lane inclusive counts
-    uint32_t wofs;
-    const uint32_t agg = FlagTile::combine_waves(wtot, s_wtot, &wofs);
+    uint32_t kept[kPChunks];
+    float xv[kPChunks][4];
+    if (VEC && base + kPTile <= n) {
+#pragma unroll
+        for (int j = 0; j < kPChunks; ++j) {
+            const int64_t off = offset(j);
+            kept[j] = nonzero_bytes(*reinterpret_cast<const uint32_t*>(mask + off));
+            load_vec<float, float, 4>(x + off, xv[j]);
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < kPChunks; ++j) {
+            const int64_t off = offset(j);
+            kept[j] = 0;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                xv[j][e] = 0.f;
+                if (off + e < n) {
+                    kept[j] |= (uint32_t)(mask[off + e] != 0) << (8 * e);
+                    xv[j][e] = x[off + e];
+                }
+            }
+        }
+    }
+    // lane counts -> wavefront scans -> tile total
+    uint32_t lane_off[kPChunks];
+    uint32_t run = 0;
+#pragma unroll
+    for (int j = 0; j < kPChunks; ++j) {
+        const uint32_t c = (uint32_t)__builtin_popcount(kept[j]);
+        const uint32_t inc = wave_incl_scan(c);
+        lane_off[j] = run + inc - c;
+        run += lane_read(inc, kWave - 1);
+    }
+    if (lane == 0) s_wtot[w] = run;
+    __syncthreads();
+    uint32_t wofs = 0, agg = 0;
+#pragma unroll
+    for (int k = 0; k < kPWaves; ++k) {
+        const uint32_t t = s_wtot[k];
+        if (k < w) wofs += t;
+        agg += t;
+    }
     if (threadIdx.x < kWave) {
         const uint32_t excl = lookback<uint32_t>(status, tile, 0, agg, 0u, epoch, hdr);
         if (threadIdx.x == 0) {
@@ -108,22 +163,20 @@ __global__ __launch_bounds__(FlagTile::kThreads) void k_compact(
         }
     }
     __syncthreads();
-    const uint32_t c = s_carry + wofs;
+    const uint32_t c0 = s_carry + wofs;
 #pragma unroll
-    for (int j = 0; j < kCChunks; ++j) {
-        const int64_t off = FlagTile::offset(base, j);
-        const uint32_t lb = c + lane_off[j];
-        uint32_t prev = 0;
+    for (int j = 0; j < kPChunks; ++j) {
+        const int64_t off = offset(j);
+        uint32_t pos = c0 + lane_off[j];
 #pragma unroll
-        for (int e = 0; e < kCVec; ++e) {
-            if (f[j][e] != prev) {  // this element is kept; its rank is the count before it
-                const uint32_t pos = lb + prev;
+        for (int e = 0; e < 4; ++e) {
+            if ((kept[j] >> (8 * e)) & 1u) {
                 if (pos < (uint64_t)n) {  // always true; guards the write against a bad count
                     out[pos] = xv[j][e];
                     if (WITH_IDX) idx[pos] = (int32_t)(off + e);
                 }
+                ++pos;
             }
-            prev = f[j][e];
         }
     }
 }
@@ -164,15 +217,21 @@ __device__ __forceinline__ uint32_t zeros_of_bit(const uint64_t* hist, int bit) 
     return z;
 }
 
-// hist == nullptr: n_true comes from the counting kernel's header word;
-// otherwise (radix-sort pass) it is derived from the digit histogram.
+// Split tile: 8 waves x 8 chunks x 64 lanes x 4 elements = 16384.  Flags are
+// kept packed (bit 8e of one register per chunk), keys and source indices in
+// registers.  hist == nullptr: n_true comes from the counting kernel's header
+// word; otherwise (radix-sort pass) it is derived from the digit histogram.
+constexpr int kSWaves = 8;
+constexpr int kSChunks = 8;
+constexpr int64_t kSTile = kSWaves * kSChunks * kWave * 4;
+
 template <bool FROM_BITS, bool VEC, bool HAS_IDX_IN, bool WITH_IDX>
-__global__ __launch_bounds__(FlagTile::kThreads) void k_split(
+__global__ __launch_bounds__(kSWaves* kWave) void k_split(
     const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags, int bit, uint32_t* keys_out,
     int32_t* idx_out, int32_t* n_true_out, int64_t n, WsHeader* hdr, uint64_t* status,
     int64_t status_words, uint32_t ntiles, const uint64_t* hist) {
     __shared__ Ticket s_ticket;
-    __shared__ uint32_t s_wtot[kCWaves];
+    __shared__ uint32_t s_wtot[kSWaves];
     __shared__ uint32_t s_carry;
 
     if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
@@ -185,23 +244,66 @@ __global__ __launch_bounds__(FlagTile::kThreads) void k_split(
         return;
     }
     const int64_t tile = tile32;
-    const int64_t base = tile * kCTile;
+    const int64_t base = tile * kSTile;
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    auto offset = [&](int j) { return base + ((int64_t)(w * kSChunks + j) * kWave + lane) * 4; };
     const uint32_t n_true = hist ? zeros_of_bit(hist, bit) : tagged_value(&hdr->tagged[kTagNTrue]);
 
-    uint32_t f[kCChunks][kCVec], k[kCChunks][kCVec];
-    if constexpr (FROM_BITS) {
-        load_flags<true, VEC>(nullptr, keys, bit, n, base, f, k);
-        mask_tail<true>(n, base, f);
+    uint32_t k[kSChunks][4];
+    int32_t iv[kSChunks][4];
+    uint32_t fl[kSChunks];  // bit 8e: element e is flagged
+    const bool full = base + kSTile <= n;
+    if (VEC && full) {
+#pragma unroll
+        for (int j = 0; j < kSChunks; ++j) {
+            const int64_t off = offset(j);
+            load_vec<uint32_t, uint32_t, 4>(keys + off, k[j]);
+            if (HAS_IDX_IN) load_vec<int32_t, int32_t, 4>(idx_in + off, iv[j]);
+            if (!FROM_BITS) fl[j] = nonzero_bytes(*reinterpret_cast<const uint32_t*>(flags + off));
+        }
     } else {
-        load_flags<false, VEC>(flags, nullptr, 0, n, base, f, k);
-        KeyTile::template load<VEC>(keys, n, base, k);
+#pragma unroll
+        for (int j = 0; j < kSChunks; ++j) {
+            const int64_t off = offset(j);
+            fl[j] = 0;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const bool ok = off + e < n;
+                k[j][e] = ok ? keys[off + e] : 0u;
+                if (HAS_IDX_IN) iv[j][e] = ok ? idx_in[off + e] : 0;
+                if (!FROM_BITS && ok) fl[j] |= (uint32_t)(flags[off + e] != 0) << (8 * e);
+            }
+        }
     }
-    int32_t iv[kCChunks][kCVec];
-    if constexpr (HAS_IDX_IN) IdxTile::template load<VEC>(idx_in, n, base, iv);
-    uint32_t lane_off[kCChunks];
-    const uint32_t wtot = FlagTile::wave_scan(f, lane_off);
-    uint32_t wofs;
-    const uint32_t agg = FlagTile::combine_waves(wtot, s_wtot, &wofs);
+    if (FROM_BITS) {
+#pragma unroll
+        for (int j = 0; j < kSChunks; ++j) {
+            const int64_t off = offset(j);
+            fl[j] = 0;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (full || off + e < n) fl[j] |= (((k[j][e] >> bit) & 1u) ^ 1u) << (8 * e);
+        }
+    }
+    uint32_t lane_off[kSChunks];
+    uint32_t run = 0;
+#pragma unroll
+    for (int j = 0; j < kSChunks; ++j) {
+        const uint32_t c = (uint32_t)__builtin_popcount(fl[j]);
+        const uint32_t inc = wave_incl_scan(c);
+        lane_off[j] = run + inc - c;
+        run += lane_read(inc, kWave - 1);
+    }
+    if (lane == 0) s_wtot[w] = run;
+    __syncthreads();
+    uint32_t wofs = 0, agg = 0;
+#pragma unroll
+    for (int q = 0; q < kSWaves; ++q) {
+        const uint32_t t = s_wtot[q];
+        if (q < w) wofs += t;
+        agg += t;
+    }
     if (threadIdx.x < kWave) {
         const uint32_t excl = lookback<uint32_t>(status, tile, 0, agg, 0u, epoch, hdr);
         if (threadIdx.x == 0) {
@@ -211,31 +313,33 @@ __global__ __launch_bounds__(FlagTile::kThreads) void k_split(
         }
     }
     __syncthreads();
-    const uint32_t c = s_carry + wofs;
+    const uint32_t c0 = s_carry + wofs;
 #pragma unroll
-    for (int j = 0; j < kCChunks; ++j) {
-        const int64_t off = FlagTile::offset(base, j);
-        const uint32_t lb = c + lane_off[j];
-        uint32_t prev = 0;
+    for (int j = 0; j < kSChunks; ++j) {
+        const int64_t off = offset(j);
+        uint32_t before = c0 + lane_off[j];  // flagged elements before this one
 #pragma unroll
-        for (int e = 0; e < kCVec; ++e) {
+        for (int e = 0; e < 4; ++e) {
             const int64_t i = off + e;
-            if (i < n) {
-                const uint32_t before = lb + prev;  // flagged elements before i
-                const uint32_t pos = (f[j][e] != prev) ? before : n_true + (uint32_t)i - before;
+            const bool flagged = (fl[j] >> (8 * e)) & 1u;
+            if (full || i < n) {
+                const uint32_t pos = flagged ? before : n_true + (uint32_t)i - before;
                 if (pos < (uint64_t)n) {  // always true; guards the write against a bad count
                     keys_out[pos] = k[j][e];
                     if (WITH_IDX) idx_out[pos] = HAS_IDX_IN ? iv[j][e] : (int32_t)i;
                 }
             }
-            prev = f[j][e];
+            before += flagged;
         }
     }
 }
 
+static inline int64_t s_tiles(int64_t n) { return (n + kSTile - 1) / kSTile; }
+
 // ---------------------------------------------------------------- launchers
 
-size_t compact_ws_bytes(int64_t n) { return kWsHeader + (size_t)c_tiles(n) * sizeof(uint64_t); }
+// Sized for the split tile (the smaller one); compress uses fewer words.
+size_t compact_ws_bytes(int64_t n) { return kWsHeader + (size_t)s_tiles(n) * sizeof(uint64_t); }
 
 static bool al(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
@@ -250,14 +354,14 @@ hipError_t launch_compact(const float* x, const uint8_t* mask, float* out, int32
         hipLaunchKernelGGL(k_zero_count, dim3(1), dim3(64), 0, stream, count);
         return hipGetLastError();
     }
-    const uint32_t nt = (uint32_t)c_tiles(n);
+    const uint32_t nt = (uint32_t)((n + kPTile - 1) / kPTile);
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
     uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
     const int64_t sw = (int64_t)((ws_bytes - kWsHeader) / sizeof(uint64_t));
     const bool vec = al(x, 16) && al(mask, 4);
     auto k = vec ? (idx ? k_compact<true, true> : k_compact<true, false>)
                  : (idx ? k_compact<false, true> : k_compact<false, false>);
-    hipLaunchKernelGGL(k, dim3(nt), dim3(FlagTile::kThreads), 0, stream, x, mask, out, idx, count,
+    hipLaunchKernelGGL(k, dim3(nt), dim3(kPWaves * kWave), 0, stream, x, mask, out, idx, count,
                        n, hdr, status, sw, nt);
     return hipGetLastError();
 }
@@ -272,7 +376,7 @@ static void launch_split_typed(const uint32_t* keys, const int32_t* idx_in, cons
                        dim3(256), 0, stream, flags, keys, bit, n, hdr);
     auto k = idx_in ? (idx_out ? k_split<FROM_BITS, VEC, true, true> : k_split<FROM_BITS, VEC, true, false>)
                     : (idx_out ? k_split<FROM_BITS, VEC, false, true> : k_split<FROM_BITS, VEC, false, false>);
-    hipLaunchKernelGGL(k, dim3(nt), dim3(FlagTile::kThreads), 0, stream, keys, idx_in, flags, bit,
+    hipLaunchKernelGGL(k, dim3(nt), dim3(kSWaves * kWave), 0, stream, keys, idx_in, flags, bit,
                        keys_out, idx_out, n_true_out, n, hdr, status, sw, nt, (const uint64_t*)nullptr);
 }
 
@@ -281,7 +385,7 @@ static void launch_split_typed(const uint32_t* keys, const int32_t* idx_in, cons
 hipError_t launch_radix1_pass(const uint32_t* keys, const int32_t* idx_in, int bit,
                               uint32_t* keys_out, int32_t* idx_out, int64_t n, const uint64_t* hist,
                               void* ws, size_t ws_bytes, size_t status_offset, hipStream_t stream) {
-    const uint32_t nt = (uint32_t)c_tiles(n);
+    const uint32_t nt = (uint32_t)s_tiles(n);
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
     uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + status_offset);
     const int64_t sw = (int64_t)((ws_bytes - status_offset) / sizeof(uint64_t));
@@ -290,7 +394,7 @@ hipError_t launch_radix1_pass(const uint32_t* keys, const int32_t* idx_in, int b
                            : (idx_out ? k_split<true, true, false, true> : k_split<true, true, false, false>))
                  : (idx_in ? (idx_out ? k_split<true, false, true, true> : k_split<true, false, true, false>)
                            : (idx_out ? k_split<true, false, false, true> : k_split<true, false, false, false>));
-    hipLaunchKernelGGL(k, dim3(nt), dim3(FlagTile::kThreads), 0, stream, keys, idx_in,
+    hipLaunchKernelGGL(k, dim3(nt), dim3(kSWaves * kWave), 0, stream, keys, idx_in,
                        (const uint8_t*)nullptr, bit, keys_out, idx_out, (int32_t*)nullptr, n, hdr,
                        status, sw, nt, hist);
     return hipGetLastError();
@@ -303,7 +407,7 @@ hipError_t launch_split(const uint32_t* keys, const int32_t* idx_in, const uint8
         if (n_true_out) hipLaunchKernelGGL(k_zero_count, dim3(1), dim3(64), 0, stream, n_true_out);
         return hipGetLastError();
     }
-    const uint32_t nt = (uint32_t)c_tiles(n);
+    const uint32_t nt = (uint32_t)s_tiles(n);
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
     uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
     const int64_t sw = (int64_t)((ws_bytes - kWsHeader) / sizeof(uint64_t));

@@ -23,9 +23,9 @@ namespace ls {
 constexpr int kHistWords = 8 * 16;  // tagged [epoch | count] words after the header
 constexpr size_t kRadixStatusOffset = kWsHeader + kHistWords * sizeof(uint64_t);
 
-constexpr int kR4Waves = 4;
+constexpr int kR4Waves = 8;
 constexpr int kR4Chunks = 16;  // 64 keys (one per lane) per chunk
-constexpr int64_t kR4Tile = kR4Waves * kR4Chunks * kWave;  // 4096 keys
+constexpr int64_t kR4Tile = kR4Waves * kR4Chunks * kWave;  // 8192 keys
 constexpr int64_t kR1Tile = 4096;                          // compact.hip's split tile
 
 static inline int64_t r4_tiles(int64_t n) { return (n + kR4Tile - 1) / kR4Tile; }

@@ -11,8 +11,13 @@
 //    out row-major by ticket, and the decoupled look-back runs inside a row
 //    (it stops at the row's first segment), so 128 rows of 2^17 still give
 //    4096 workgroups to fill 256 CUs.
-// The top-p variant replaces the store of the prefix sums by a search for
-// the first index whose running sum reaches p.
+// The top-p cutoff needs only one index per row, so it does not use the
+// look-back: a first kernel sums every tile of every row (reading all the
+// probabilities once, no inter-workgroup waiting), and a second kernel, one
+// workgroup per tile again, scans the tile sums of its row to find the first
+// tile whose inclusive sum reaches p; only that tile re-reads its data to
+// locate the index (the two phases of the paper's Algorithm 3, MCScan, with
+// the down-sweep cut to the one tile that matters).
 #include <limits.h>
 
 #include "launch.hpp"
@@ -20,12 +25,19 @@
 
 namespace ls {
 
-constexpr int kRWaves = 4;
-constexpr int kRChunks = 4;
 constexpr int kRVec = 4;
-constexpr int64_t kRowTile = kRWaves * kRChunks * kWave * kRVec;  // 4096
+constexpr int64_t kRowTile = 4096;  // rows up to this length: one wavefront per row
 
-static inline int64_t row_segments(int64_t len) { return (len + kRowTile - 1) / kRowTile; }
+// Long-row tile geometries (waves x chunks x 64 x 4): long rows take big
+// tiles (each tile costs one ticket, about 11 ns serialised on MI355X), rows
+// of a few tiles take smaller ones so that a row still spans several tiles.
+struct RGeomS { static constexpr int W = 4, J = 4; };   //  4096
+struct RGeomM { static constexpr int W = 4, J = 8; };   //  8192
+struct RGeomL { static constexpr int W = 8, J = 16; };  // 32768
+static inline int64_t row_tile(int64_t len) {
+    return len > 65536 ? 32768 : (len > 16384 ? 8192 : 4096);
+}
+static inline int64_t row_segments(int64_t len) { return (len + row_tile(len) - 1) / row_tile(len); }
 static inline bool long_rows(int64_t len) { return len > kRowTile; }
 
 // Wavefront minimum with DPP (lanes outside the row / disabled read INT_MAX).
@@ -46,16 +58,14 @@ __device__ __forceinline__ int32_t wave_min(int32_t v) {
 
 // ---------------------------------------------------------------- long rows
 
-template <class TileT, bool EXCL, bool VEC, bool TOPP>
+template <class TileT, bool EXCL, bool VEC>
 __global__ __launch_bounds__(TileT::kThreads) void k_rows_lookback(
     const typename TileT::T* x, typename TileT::T* y, int64_t len, uint32_t segs,
-    uint32_t ntiles, WsHeader* hdr, uint64_t* status, int64_t status_words, float p,
-    int32_t* cutoff) {
+    uint32_t ntiles, WsHeader* hdr, uint64_t* status, int64_t status_words) {
     using T = typename TileT::T;
     __shared__ Ticket s_ticket;
     __shared__ T s_wtot[TileT::WAVES];
     __shared__ T s_carry;
-    __shared__ int32_t s_min[TileT::WAVES];
 
     if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
     __syncthreads();
@@ -70,11 +80,10 @@ __global__ __launch_bounds__(TileT::kThreads) void k_rows_lookback(
     const int64_t row = tile / segs;
     const int64_t seg = tile - row * segs;
     const int64_t base = seg * TileT::kElems;
-    const T* xr = x + row * len;
 
     T v[TileT::J][TileT::V];
     T lane_off[TileT::J];
-    TileT::template load<VEC>(xr, len, base, v);
+    TileT::template load<VEC>(x + row * len, len, base, v);
     const T wtot = TileT::wave_scan(v, lane_off);
     T wofs;
     const T agg = TileT::combine_waves(wtot, s_wtot, &wofs);
@@ -87,29 +96,97 @@ __global__ __launch_bounds__(TileT::kThreads) void k_rows_lookback(
         }
     }
     __syncthreads();
-    const T carry = s_carry + wofs;
-    if constexpr (!TOPP) {
-        TileT::template store<EXCL, VEC>(y + row * len, len, base, v, lane_off, carry);
-    } else {
-        // first element (in index order) whose inclusive running sum is >= p
-        int32_t cand = INT_MAX;
-#pragma unroll
-        for (int j = TileT::J - 1; j >= 0; --j) {
-            const int64_t off = TileT::offset(base, j);
-            const T lb = carry + lane_off[j];
-#pragma unroll
-            for (int e = TileT::V - 1; e >= 0; --e)
-                if (off + e < len && lb + v[j][e] >= p) cand = (int32_t)(off + e);
+    TileT::template store<EXCL, VEC>(y + row * len, len, base, v, lane_off, s_carry + wofs);
+}
+
+// ---------------------------------------------------------------- top-p
+
+// Phase 1: the fp32 sum of every tile, stored with its two top bits clear
+// (so the workspace word reads as "nothing published" to any look-back).
+template <class TileT, bool VEC>
+__global__ __launch_bounds__(TileT::kThreads) void k_topp_sums(const float* probs, int64_t len,
+                                                               uint32_t segs, uint64_t* partial) {
+    __shared__ float s_wtot[TileT::WAVES];
+    const int64_t row = blockIdx.x / segs;
+    const int64_t seg = blockIdx.x - row * segs;
+    float v[TileT::J][TileT::V];
+    TileT::template load<VEC>(probs + row * len, len, seg * TileT::kElems, v);
+    float wofs;
+    const float agg = TileT::combine_waves(wave_sum(TileT::lane_sum(v)), s_wtot, &wofs);
+    if (threadIdx.x == 0) partial[blockIdx.x] = (uint64_t)Bits<float>::to(agg);
+}
+
+// Phase 2: every workgroup recomputes its row's inclusive tile sums up to its
+// own tile with one fixed formula (64 at a time, DPP scan, carried in order),
+// so all workgroups of a row agree bit for bit on which tile is the first to
+// reach p.  That tile rescans its data for the first element whose running
+// sum reaches p (its last element if rounding kept them all below p); the
+// row's last tile writes len - 1 if no tile reaches p.
+template <class TileT, bool VEC>
+__global__ __launch_bounds__(TileT::kThreads) void k_topp_owner(const float* probs,
+                                                                int32_t* cutoff, int64_t len,
+                                                                uint32_t segs,
+                                                                const uint64_t* partial, float p) {
+    __shared__ int s_role;  // 0: not involved, 1: owns the crossing, 2: writes len - 1
+    __shared__ float s_excl;
+    __shared__ float s_wtot[TileT::WAVES];
+    __shared__ int32_t s_min[TileT::WAVES];
+    const int64_t row = blockIdx.x / segs;
+    const int64_t seg = blockIdx.x - row * segs;
+    const int lane = lane_id();
+    if (threadIdx.x < kWave) {
+        const uint64_t* pr = partial + row * segs;
+        float carry = 0.f, excl = 0.f;
+        int64_t first = -1;
+        for (int64_t b = 0; b <= seg && first < 0; b += kWave) {
+            const int64_t s = b + lane;
+            const float a = s <= seg ? Bits<float>::from((uint32_t)pr[s]) : 0.f;
+            const float inc = carry + wave_incl_scan(a);
+            const uint64_t hit = __ballot(s <= seg && inc >= p);
+            if (hit) {
+                const int l = __builtin_ctzll(hit);
+                first = b + l;
+                if (first == seg) excl = l ? lane_read(inc, l - 1) : carry;
+            }
+            carry = lane_read(inc, kWave - 1);
         }
-        const int32_t wm = wave_min(cand);
-        const int w = threadIdx.x / kWave;
-        if (lane_id() == 0) s_min[w] = wm;
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            int32_t m = INT_MAX;
-            for (int k = 0; k < TileT::WAVES; ++k) m = s_min[k] < m ? s_min[k] : m;
-            if (m != INT_MAX) atomicMin(cutoff + row, m);
+        if (lane == 0) {
+            s_role = first == seg ? 1 : (first < 0 && seg == (int64_t)segs - 1 ? 2 : 0);
+            s_excl = excl;
         }
+    }
+    __syncthreads();
+    const int role = s_role;
+    if (role == 0) return;
+    if (role == 2) {
+        if (threadIdx.x == 0) cutoff[row] = (int32_t)(len - 1);
+        return;
+    }
+    const int64_t base = seg * TileT::kElems;
+    float v[TileT::J][TileT::V];
+    float lane_off[TileT::J];
+    TileT::template load<VEC>(probs + row * len, len, base, v);
+    const float wtot = TileT::wave_scan(v, lane_off);
+    float wofs;
+    TileT::combine_waves(wtot, s_wtot, &wofs);
+    const float c = s_excl + wofs;
+    int32_t cand = INT_MAX;
+#pragma unroll
+    for (int j = TileT::J - 1; j >= 0; --j) {
+        const int64_t off = TileT::offset(base, j);
+        const float lb = c + lane_off[j];
+#pragma unroll
+        for (int e = TileT::V - 1; e >= 0; --e)
+            if (off + e < len && lb + v[j][e] >= p) cand = (int32_t)(off + e);
+    }
+    const int32_t wm = wave_min(cand);
+    if (lane == 0) s_min[threadIdx.x / kWave] = wm;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int32_t m = INT_MAX;
+        for (int k = 0; k < TileT::WAVES; ++k) m = s_min[k] < m ? s_min[k] : m;
+        const int64_t last = (base + TileT::kElems < len ? base + TileT::kElems : len) - 1;
+        cutoff[row] = m != INT_MAX ? m : (int32_t)last;
     }
 }
 
@@ -187,6 +264,35 @@ static unsigned wave_grid(int64_t rows) {
     return (unsigned)(blocks < 65536 ? blocks : 65536);
 }
 
+template <class T, class G>
+static void rows_long(bool exclusive, bool vec, const T* x, T* y, int64_t rows, int64_t len,
+                      void* ws, size_t ws_bytes, hipStream_t stream) {
+    using TileT = Tile<T, T, kRVec, G::J, G::W>;
+    const uint32_t segs = (uint32_t)((len + TileT::kElems - 1) / TileT::kElems);
+    const uint32_t nt = (uint32_t)(rows * segs);
+    WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
+    uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
+    const int64_t status_words = (int64_t)((ws_bytes - kWsHeader) / sizeof(uint64_t));
+    auto k = exclusive ? (vec ? k_rows_lookback<TileT, true, true> : k_rows_lookback<TileT, true, false>)
+                       : (vec ? k_rows_lookback<TileT, false, true> : k_rows_lookback<TileT, false, false>);
+    hipLaunchKernelGGL(k, dim3(nt), dim3(TileT::kThreads), 0, stream, x, y, len, segs, nt, hdr,
+                       status, status_words);
+}
+
+template <class G>
+static void topp_long(bool vec, const float* probs, int32_t* cutoff, int64_t rows, int64_t len,
+                      float p, void* ws, hipStream_t stream) {
+    using TileT = Tile<float, float, kRVec, G::J, G::W>;
+    const uint32_t segs = (uint32_t)((len + TileT::kElems - 1) / TileT::kElems);
+    const uint32_t nt = (uint32_t)(rows * segs);
+    uint64_t* partial = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
+    auto ks = vec ? k_topp_sums<TileT, true> : k_topp_sums<TileT, false>;
+    auto ko = vec ? k_topp_owner<TileT, true> : k_topp_owner<TileT, false>;
+    hipLaunchKernelGGL(ks, dim3(nt), dim3(TileT::kThreads), 0, stream, probs, len, segs, partial);
+    hipLaunchKernelGGL(ko, dim3(nt), dim3(TileT::kThreads), 0, stream, probs, cutoff, len, segs,
+                       (const uint64_t*)partial, p);
+}
+
 template <class T, bool TOPP>
 static hipError_t rows_typed(bool exclusive, const T* x, T* y, int64_t rows, int64_t len, float p,
                              int32_t* cutoff, void* ws, size_t ws_bytes, hipStream_t stream) {
@@ -205,20 +311,16 @@ static hipError_t rows_typed(bool exclusive, const T* x, T* y, int64_t rows, int
         hipLaunchKernelGGL(k, grid, block, 0, stream, x, y, rows, len, p, cutoff);
         return hipGetLastError();
     }
-    using TileT = Tile<T, T, kRVec, kRChunks, kRWaves>;
-    static_assert(TileT::kElems == kRowTile, "row tile size");
-    const uint32_t segs = (uint32_t)row_segments(len);
-    const uint32_t nt = (uint32_t)(rows * segs);
-    WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
-    uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
-    const int64_t status_words = (int64_t)((ws_bytes - kWsHeader) / sizeof(uint64_t));
-    if (TOPP)  // every row starts at "never reached": len - 1
-        hipLaunchKernelGGL(k_fill_i32, dim3(wave_grid(rows)), dim3(256), 0, stream, cutoff, rows,
-                           (int32_t)(len - 1));
-    auto k = exclusive ? (vec ? k_rows_lookback<TileT, true, true, TOPP> : k_rows_lookback<TileT, true, false, TOPP>)
-                       : (vec ? k_rows_lookback<TileT, false, true, TOPP> : k_rows_lookback<TileT, false, false, TOPP>);
-    hipLaunchKernelGGL(k, dim3(nt), dim3(TileT::kThreads), 0, stream, x, y, len, segs, nt, hdr,
-                       status, status_words, p, cutoff);
+    const int64_t t = row_tile(len);
+    if constexpr (TOPP) {
+        if (t == 32768) topp_long<RGeomL>(vec, x, cutoff, rows, len, p, ws, stream);
+        else if (t == 8192) topp_long<RGeomM>(vec, x, cutoff, rows, len, p, ws, stream);
+        else topp_long<RGeomS>(vec, x, cutoff, rows, len, p, ws, stream);
+    } else {
+        if (t == 32768) rows_long<T, RGeomL>(exclusive, vec, x, y, rows, len, ws, ws_bytes, stream);
+        else if (t == 8192) rows_long<T, RGeomM>(exclusive, vec, x, y, rows, len, ws, ws_bytes, stream);
+        else rows_long<T, RGeomS>(exclusive, vec, x, y, rows, len, ws, ws_bytes, stream);
+    }
     return hipGetLastError();
 }
 

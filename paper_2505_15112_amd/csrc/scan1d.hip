@@ -15,24 +15,20 @@
 
 namespace ls {
 
-// Tile geometry: waves x chunks x 64 lanes x 4 elements, and the number of
-// 64-tile windows the look-back reads per round trip.
-#ifndef LIBSCAN_SCAN_WAVES
-#define LIBSCAN_SCAN_WAVES 4
-#endif
-#ifndef LIBSCAN_SCAN_CHUNKS
-#define LIBSCAN_SCAN_CHUNKS 4
-#endif
-#ifndef LIBSCAN_LOOKBACK_WINDOWS
-#define LIBSCAN_LOOKBACK_WINDOWS 1
-#endif
-constexpr int kWaves = LIBSCAN_SCAN_WAVES;
-constexpr int kChunks = LIBSCAN_SCAN_CHUNKS;
+// Tile geometries (waves x chunks x 64 lanes x 4 elements).  Every tile costs
+// one ticket and one look-back, so big arrays want big tiles: measured on
+// MI355X at n = 2^28, 4096-element tiles reach half the device memcpy rate
+// and 32768-element tiles match it.  Small arrays want more, smaller tiles
+// to occupy the 256 CUs.
+struct GeomSmall { static constexpr int W = 4, J = 4; };   //  4096 elements
+struct GeomMid { static constexpr int W = 4, J = 16; };    // 16384 elements
+struct GeomLarge { static constexpr int W = 8, J = 16; };  // 32768 elements
 constexpr int kVec = 4;
-constexpr int kLookbackWindows = LIBSCAN_LOOKBACK_WINDOWS;
-constexpr int64_t kTileElems = kWaves * kChunks * kWave * kVec;
+constexpr int64_t kMinTileElems = GeomSmall::W * GeomSmall::J * kWave * kVec;
+constexpr int64_t kRssTileElems = GeomMid::W * GeomMid::J * kWave * kVec;
 
-static inline int64_t num_tiles(int64_t n) { return (n + kTileElems - 1) / kTileElems; }
+// Workspaces are sized for the smallest tile, so any geometry fits.
+static inline int64_t num_tiles(int64_t n, int64_t tile) { return (n + tile - 1) / tile; }
 
 // ---------------------------------------------------------------- kernels
 
@@ -73,7 +69,7 @@ __global__ __launch_bounds__(TileT::kThreads) void k_scan_lookback(
 
     if (threadIdx.x < kWave) {
         const T c0 = (tile == 0 && carry_in) ? *carry_in : T(0);
-        const T excl = lookback<T, kLookbackWindows>(status, tile, 0, agg, c0, epoch, hdr);
+        const T excl = lookback<T>(status, tile, 0, agg, c0, epoch, hdr);
         if (threadIdx.x == 0) {
             s_carry = excl;
             if (total_out && tile == ntiles - 1) *total_out = excl + agg;
@@ -161,31 +157,48 @@ __global__ __launch_bounds__(TileT::kThreads) void k_rss_rescan(const typename T
 
 // ---------------------------------------------------------------- launchers
 
-size_t scan1d_ws_bytes(int64_t n) { return kWsHeader + (size_t)num_tiles(n) * sizeof(uint64_t); }
+size_t scan1d_ws_bytes(int64_t n) {
+    return kWsHeader + (size_t)num_tiles(n, kMinTileElems) * sizeof(uint64_t);
+}
 
-size_t scan1d_rss_ws_bytes(int64_t n) { return kWsHeader + (size_t)num_tiles(n) * sizeof(uint32_t); }
+size_t scan1d_rss_ws_bytes(int64_t n) {
+    return kWsHeader + (size_t)num_tiles(n, kRssTileElems) * sizeof(uint32_t);
+}
 
 static bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+template <class In, class T, class G>
+static void scan1d_geom(bool exclusive, bool vec, const In* x, T* y, int64_t n, const T* carry_in,
+                        T* total_out, WsHeader* hdr, uint64_t* status, int64_t status_words,
+                        hipStream_t stream) {
+    using TileT = Tile<In, T, kVec, G::J, G::W>;
+    const uint32_t nt = (uint32_t)num_tiles(n, TileT::kElems);
+    auto k = exclusive ? (vec ? k_scan_lookback<TileT, true, true> : k_scan_lookback<TileT, true, false>)
+                       : (vec ? k_scan_lookback<TileT, false, true> : k_scan_lookback<TileT, false, false>);
+    hipLaunchKernelGGL(k, dim3(nt), dim3(TileT::kThreads), 0, stream, x, y, n, hdr, status,
+                       status_words, nt, carry_in, total_out);
+}
 
 template <class In, class T>
 static hipError_t scan1d_typed(bool exclusive, const In* x, T* y, int64_t n, const T* carry_in,
                                T* total_out, void* ws, size_t ws_bytes, hipStream_t stream) {
-    using TileT = Tile<In, T, kVec, kChunks, kWaves>;
-    static_assert(TileT::kElems == kTileElems, "tile size mismatch");
     if (n == 0) {
         if (total_out) hipLaunchKernelGGL(k_write_total<T>, dim3(1), dim3(64), 0, stream, total_out, carry_in);
         return hipGetLastError();
     }
-    const uint32_t nt = (uint32_t)num_tiles(n);
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
     uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
     const int64_t status_words = (int64_t)((ws_bytes - kWsHeader) / sizeof(uint64_t));
     const bool vec = aligned(x, kVec * sizeof(In)) && aligned(y, kVec * sizeof(T));
-    const dim3 grid(nt), block(TileT::kThreads);
-    auto k = exclusive ? (vec ? k_scan_lookback<TileT, true, true> : k_scan_lookback<TileT, true, false>)
-                       : (vec ? k_scan_lookback<TileT, false, true> : k_scan_lookback<TileT, false, false>);
-    hipLaunchKernelGGL(k, grid, block, 0, stream, x, y, n, hdr, status, status_words, nt, carry_in,
-                       total_out);
+    if (n >= (int64_t(1) << 22))
+        scan1d_geom<In, T, GeomLarge>(exclusive, vec, x, y, n, carry_in, total_out, hdr, status,
+                                      status_words, stream);
+    else if (n >= (int64_t(1) << 18))
+        scan1d_geom<In, T, GeomMid>(exclusive, vec, x, y, n, carry_in, total_out, hdr, status,
+                                    status_words, stream);
+    else
+        scan1d_geom<In, T, GeomSmall>(exclusive, vec, x, y, n, carry_in, total_out, hdr, status,
+                                      status_words, stream);
     return hipGetLastError();
 }
 
@@ -215,9 +228,10 @@ hipError_t launch_scan1d(Kind kind, bool exclusive, const void* x, void* y, int6
 
 template <class In, class T>
 static hipError_t rss_typed(const In* x, T* y, int64_t n, void* ws, hipStream_t stream) {
-    using TileT = Tile<In, T, kVec, kChunks, kWaves>;
+    using TileT = Tile<In, T, kVec, GeomMid::J, GeomMid::W>;
+    static_assert(TileT::kElems == kRssTileElems, "rss tile");
     if (n == 0) return hipSuccess;
-    const int64_t nt = num_tiles(n);
+    const int64_t nt = num_tiles(n, TileT::kElems);
     T* partial = reinterpret_cast<T*>(reinterpret_cast<char*>(ws) + kWsHeader);
     const bool vec = aligned(x, kVec * sizeof(In)) && aligned(y, kVec * sizeof(T));
     const dim3 grid((unsigned)nt), block(TileT::kThreads);
