@@ -34,14 +34,17 @@ PEAK_HBM_GBPS = 8000.0  # MI355X published HBM3E bandwidth
 PMC_FILE = os.path.join(ROOT, "profiles", "scan_lookback_i32_n2^28_pmc.json")
 
 
+METRIC_KERNEL_SOURCES = ("device.hpp", "tile.hpp", "scan1d.hip")
+
+
 def kernel_source_hash() -> str:
-    """sha256 over the HIP sources; ties counter measurements to a kernel version."""
+    """sha256 over the sources of the metric kernel; ties counter measurements
+    to the kernel version they were taken on."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2505_15112_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".hpp")):
-            with open(os.path.join(csrc, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
+    for name in METRIC_KERNEL_SOURCES:
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()
 
 

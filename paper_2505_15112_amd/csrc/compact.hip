@@ -9,9 +9,14 @@
 // Split (SplitInd): stable two-way partition with source indices.  Flagged
 // element i goes to e_i (exclusive count of flagged before it), unflagged to
 // n_true + (i - e_i).  n_true must be known before any tile stores, so a
-// small counting kernel runs first (reading only the flags, or only the keys
-// when the flag is a key bit, as in the radix-sort pass of Section 5); its
-// total lands in an epoch-tagged workspace word that the split kernel reads.
+// small counting kernel runs first (reading only the flag bytes); its total
+// lands in an epoch-tagged workspace word that the split kernel reads.  As
+// the pass of the one-bit radix sort (Section 5), the flag is "key bit b is
+// 0" and n_true comes from the sort's digit histogram instead.
+//
+// Both kernels store through LDS: the elements of one wavefront chunk that go
+// to one contiguous output run are gathered first, then written by
+// consecutive lanes, so the stores are dense rather than scattered dwords.
 #include <limits.h>
 
 #include "launch.hpp"
@@ -19,56 +24,18 @@
 
 namespace ls {
 
-constexpr int kCWaves = 4;
-constexpr int kCChunks = 4;
-constexpr int kCVec = 4;
-constexpr int64_t kCTile = kCWaves * kCChunks * kWave * kCVec;  // 4096
-
-static inline int64_t c_tiles(int64_t n) { return (n + kCTile - 1) / kCTile; }
 static inline int64_t s_tiles(int64_t n);
 
-using FlagTile = Tile<uint8_t, uint32_t, kCVec, kCChunks, kCWaves>;
-using KeyTile = Tile<uint32_t, uint32_t, kCVec, kCChunks, kCWaves>;
-using ValTile = Tile<float, float, kCVec, kCChunks, kCWaves>;
-using IdxTile = Tile<int32_t, int32_t, kCVec, kCChunks, kCWaves>;
+// Per byte: 1 if the byte is non-zero, else 0 (bits 0, 8, 16, 24).
+__device__ __forceinline__ uint32_t nonzero_bytes(uint32_t m) {
+    uint32_t t = m | ((m >> 4) & 0x0f0f0f0fu);
+    t |= (t >> 2) & 0x33333333u;
+    t |= (t >> 1) & 0x55555555u;
+    return t & 0x01010101u;
+}
 
 // Header accumulator used by split for the number of flagged elements.
 constexpr int kTagNTrue = 0;
-
-// Flags of one tile as 0/1 values (any non-zero byte is true, or for the
-// radix pass: key bit `bit` is 0).
-template <bool FROM_BITS, bool VEC>
-__device__ __forceinline__ void load_flags(const uint8_t* flags, const uint32_t* keys, int bit,
-                                           int64_t n, int64_t base, uint32_t (&f)[kCChunks][kCVec],
-                                           uint32_t (&k)[kCChunks][kCVec]) {
-    if constexpr (FROM_BITS) {
-        KeyTile::template load<VEC>(keys, n, base, k);
-#pragma unroll
-        for (int j = 0; j < kCChunks; ++j)
-#pragma unroll
-            for (int e = 0; e < kCVec; ++e) f[j][e] = ((k[j][e] >> bit) & 1u) ^ 1u;
-    } else {
-        FlagTile::template load<VEC>(flags, n, base, f);
-#pragma unroll
-        for (int j = 0; j < kCChunks; ++j)
-#pragma unroll
-            for (int e = 0; e < kCVec; ++e) f[j][e] = f[j][e] != 0u;
-    }
-}
-
-// Elements past n have flag 0 after load_flags for u8 flags (loaded as 0);
-// for key bits the padding key 0 would read as flagged, so mask it.
-template <bool FROM_BITS>
-__device__ __forceinline__ void mask_tail(int64_t n, int64_t base, uint32_t (&f)[kCChunks][kCVec]) {
-    if (!FROM_BITS || base + kCTile <= n) return;
-#pragma unroll
-    for (int j = 0; j < kCChunks; ++j) {
-        const int64_t off = KeyTile::offset(base, j);
-#pragma unroll
-        for (int e = 0; e < kCVec; ++e)
-            if (off + e >= n) f[j][e] = 0;
-    }
-}
 
 // ---------------------------------------------------------------- compress
 
@@ -80,14 +47,6 @@ constexpr int kPWaves = 8;
 constexpr int kPChunks = 16;
 constexpr int64_t kPTile = kPWaves * kPChunks * kWave * 4;
 
-// Per byte: 1 if the byte is non-zero, else 0 (bits 0, 8, 16, 24).
-__device__ __forceinline__ uint32_t nonzero_bytes(uint32_t m) {
-    uint32_t t = m | ((m >> 4) & 0x0f0f0f0fu);
-    t |= (t >> 2) & 0x33333333u;
-    t |= (t >> 1) & 0x55555555u;
-    return t & 0x01010101u;
-}
-
 template <bool VEC, bool WITH_IDX>
 __global__ __launch_bounds__(kPWaves* kWave) void k_compact(
     const float* x, const uint8_t* mask, float* out, int32_t* idx, int32_t* count, int64_t n,
@@ -95,6 +54,8 @@ __global__ __launch_bounds__(kPWaves* kWave) void k_compact(
     __shared__ Ticket s_ticket;
     __shared__ uint32_t s_wtot[kPWaves];
     __shared__ uint32_t s_carry;
+    __shared__ float s_val[kPWaves][kWave * 4];
+    __shared__ int32_t s_idx[WITH_IDX ? kPWaves : 1][kWave * 4];
 
     if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
     __syncthreads();
@@ -163,44 +124,67 @@ __global__ __launch_bounds__(kPWaves* kWave) void k_compact(
         }
     }
     __syncthreads();
+    // The kept elements of one chunk form one contiguous output run: gather
+    // them in this wave's LDS slot, then write the run with consecutive lanes.
     const uint32_t c0 = s_carry + wofs;
+    float* st = s_val[w];
+    int32_t* si = s_idx[WITH_IDX ? w : 0];
 #pragma unroll
     for (int j = 0; j < kPChunks; ++j) {
         const int64_t off = offset(j);
-        uint32_t pos = c0 + lane_off[j];
+        const uint32_t run0 = lane_read(lane_off[j], 0);  // kept before this chunk, in the wave
+        uint32_t r = lane_off[j] - run0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             if ((kept[j] >> (8 * e)) & 1u) {
-                if (pos < (uint64_t)n) {  // always true; guards the write against a bad count
-                    out[pos] = xv[j][e];
-                    if (WITH_IDX) idx[pos] = (int32_t)(off + e);
-                }
-                ++pos;
+                st[r] = xv[j][e];
+                if (WITH_IDX) si[r] = (int32_t)(off + e);
+                ++r;
             }
         }
+        const uint32_t cnt = (j + 1 < kPChunks ? lane_read(lane_off[j + 1], 0) : run) - run0;
+        wave_lds_sync();
+        const uint32_t dst = c0 + run0;
+        for (uint32_t t = lane; t < cnt; t += kWave) {
+            if (dst + t < (uint64_t)n) {  // always true; guards the write against a bad count
+                out[dst + t] = st[t];
+                if (WITH_IDX) idx[dst + t] = si[t];
+            }
+        }
+        wave_lds_sync();
     }
 }
 
 // ---------------------------------------------------------------- split
 
-// Count the flagged elements into the header accumulator (grid-stride).
-template <bool FROM_BITS, bool VEC>
-__global__ __launch_bounds__(256) void k_count_flags(const uint8_t* flags, const uint32_t* keys,
-                                                     int bit, int64_t n, WsHeader* hdr) {
+// Count the non-zero flag bytes into the header accumulator: grid-stride,
+// 16 flags per 16-byte load, 4 loads in flight per thread.
+__global__ __launch_bounds__(256) void k_count_flags(const uint8_t* flags, int64_t n, bool vec,
+                                                     WsHeader* hdr) {
     __shared__ uint32_t s_part[4];
     const uint32_t epoch = current_epoch(hdr);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     uint32_t cnt = 0;
-    const int64_t per_block = kCTile;
-    for (int64_t base = (int64_t)blockIdx.x * per_block; base < n;
-         base += (int64_t)gridDim.x * per_block) {
-        uint32_t f[kCChunks][kCVec], k[kCChunks][kCVec];
-        load_flags<FROM_BITS, VEC>(flags, keys, bit, n, base, f, k);
-        mask_tail<FROM_BITS>(n, base, f);
+    int64_t done = 0;
+    if (vec) {
+        const u32x4* f4 = reinterpret_cast<const u32x4*>(flags);
+        const int64_t n16 = n / 16;
+        for (int64_t i = t0; i < n16; i += 4 * stride) {
+            u32x4 v[4];
 #pragma unroll
-        for (int j = 0; j < kCChunks; ++j)
+            for (int u = 0; u < 4; ++u) {
+                const int64_t q = i + u * stride;
+                v[u] = q < n16 ? f4[q] : u32x4{0, 0, 0, 0};
+            }
 #pragma unroll
-            for (int e = 0; e < kCVec; ++e) cnt += f[j][e];
+            for (int u = 0; u < 4; ++u)
+                cnt += __builtin_popcount(nonzero_bytes(v[u].x)) + __builtin_popcount(nonzero_bytes(v[u].y)) +
+                       __builtin_popcount(nonzero_bytes(v[u].z)) + __builtin_popcount(nonzero_bytes(v[u].w));
+        }
+        done = n16 * 16;
     }
+    for (int64_t i = done + t0; i < n; i += stride) cnt += flags[i] != 0;
     const uint32_t wsum = wave_sum(cnt);
     if (lane_id() == 0) s_part[threadIdx.x / kWave] = wsum;
     __syncthreads();
@@ -233,6 +217,8 @@ __global__ __launch_bounds__(kSWaves* kWave) void k_split(
     __shared__ Ticket s_ticket;
     __shared__ uint32_t s_wtot[kSWaves];
     __shared__ uint32_t s_carry;
+    __shared__ uint32_t s_key[kSWaves][kWave * 4];
+    __shared__ int32_t s_idx[WITH_IDX ? kSWaves : 1][kWave * 4];
 
     if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
     __syncthreads();
@@ -313,24 +299,43 @@ __global__ __launch_bounds__(kSWaves* kWave) void k_split(
         }
     }
     __syncthreads();
+    // A chunk's flagged keys form one contiguous output run and its other
+    // keys another: gather both in this wave's LDS slot (flagged first), then
+    // write the two runs with consecutive lanes.
     const uint32_t c0 = s_carry + wofs;
+    uint32_t* sk = s_key[w];
+    int32_t* si = s_idx[WITH_IDX ? w : 0];
 #pragma unroll
     for (int j = 0; j < kSChunks; ++j) {
         const int64_t off = offset(j);
-        uint32_t before = c0 + lane_off[j];  // flagged elements before this one
+        const int64_t g0 = base + (int64_t)(w * kSChunks + j) * kWave * 4;  // chunk start
+        const uint32_t run0 = lane_read(lane_off[j], 0);
+        const uint32_t cnt = (j + 1 < kSChunks ? lane_read(lane_off[j + 1], 0) : run) - run0;
+        const int64_t valid64 = n - g0 < kWave * 4 ? n - g0 : kWave * 4;
+        const uint32_t valid = valid64 > 0 ? (uint32_t)valid64 : 0u;
+        uint32_t r = lane_off[j] - run0;  // flagged before this element, in the chunk
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const int64_t i = off + e;
-            const bool flagged = (fl[j] >> (8 * e)) & 1u;
-            if (full || i < n) {
-                const uint32_t pos = flagged ? before : n_true + (uint32_t)i - before;
-                if (pos < (uint64_t)n) {  // always true; guards the write against a bad count
-                    keys_out[pos] = k[j][e];
-                    if (WITH_IDX) idx_out[pos] = HAS_IDX_IN ? iv[j][e] : (int32_t)i;
-                }
+            const uint32_t le = (uint32_t)lane * 4 + e;  // element index in the chunk
+            if (le < valid) {
+                const bool flagged = (fl[j] >> (8 * e)) & 1u;
+                const uint32_t slot = flagged ? r : cnt + (le - r);
+                sk[slot] = k[j][e];
+                if (WITH_IDX) si[slot] = HAS_IDX_IN ? iv[j][e] : (int32_t)(off + e);
+                r += flagged;
             }
-            before += flagged;
         }
+        wave_lds_sync();
+        const uint32_t true_dst = c0 + run0;                        // flagged before the chunk
+        const uint32_t false_dst = n_true + (uint32_t)g0 - true_dst;  // unflagged before it
+        for (uint32_t t = lane; t < valid; t += kWave) {
+            const uint32_t pos = t < cnt ? true_dst + t : false_dst + (t - cnt);
+            if (pos < (uint64_t)n) {  // always true; guards the write against a bad count
+                keys_out[pos] = sk[t];
+                if (WITH_IDX) idx_out[pos] = si[t];
+            }
+        }
+        wave_lds_sync();
     }
 }
 
@@ -366,17 +371,17 @@ hipError_t launch_compact(const float* x, const uint8_t* mask, float* out, int32
     return hipGetLastError();
 }
 
-template <bool FROM_BITS, bool VEC>
+template <bool VEC>
 static void launch_split_typed(const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags,
-                               int bit, uint32_t* keys_out, int32_t* idx_out, int32_t* n_true_out,
+                               uint32_t* keys_out, int32_t* idx_out, int32_t* n_true_out,
                                int64_t n, WsHeader* hdr, uint64_t* status, int64_t sw,
                                uint32_t nt, hipStream_t stream) {
-    const int64_t cblocks = (n + kCTile - 1) / kCTile;
-    hipLaunchKernelGGL((k_count_flags<FROM_BITS, VEC>), dim3((unsigned)(cblocks < 2048 ? cblocks : 2048)),
-                       dim3(256), 0, stream, flags, keys, bit, n, hdr);
-    auto k = idx_in ? (idx_out ? k_split<FROM_BITS, VEC, true, true> : k_split<FROM_BITS, VEC, true, false>)
-                    : (idx_out ? k_split<FROM_BITS, VEC, false, true> : k_split<FROM_BITS, VEC, false, false>);
-    hipLaunchKernelGGL(k, dim3(nt), dim3(kSWaves * kWave), 0, stream, keys, idx_in, flags, bit,
+    const int64_t cblocks = (n + 16 * 256 * 4 - 1) / (16 * 256 * 4);
+    hipLaunchKernelGGL(k_count_flags, dim3((unsigned)(cblocks < 2048 ? cblocks : 2048)), dim3(256),
+                       0, stream, flags, n, ((uintptr_t)flags % 16) == 0, hdr);
+    auto k = idx_in ? (idx_out ? k_split<false, VEC, true, true> : k_split<false, VEC, true, false>)
+                    : (idx_out ? k_split<false, VEC, false, true> : k_split<false, VEC, false, false>);
+    hipLaunchKernelGGL(k, dim3(nt), dim3(kSWaves * kWave), 0, stream, keys, idx_in, flags, 0,
                        keys_out, idx_out, n_true_out, n, hdr, status, sw, nt, (const uint64_t*)nullptr);
 }
 
@@ -403,6 +408,7 @@ hipError_t launch_radix1_pass(const uint32_t* keys, const int32_t* idx_in, int b
 hipError_t launch_split(const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags, int bit,
                         uint32_t* keys_out, int32_t* idx_out, int32_t* n_true_out, int64_t n,
                         void* ws, size_t ws_bytes, hipStream_t stream) {
+    (void)bit;
     if (n == 0) {
         if (n_true_out) hipLaunchKernelGGL(k_zero_count, dim3(1), dim3(64), 0, stream, n_true_out);
         return hipGetLastError();
@@ -411,22 +417,13 @@ hipError_t launch_split(const uint32_t* keys, const int32_t* idx_in, const uint8
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
     uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
     const int64_t sw = (int64_t)((ws_bytes - kWsHeader) / sizeof(uint64_t));
-    const bool vec = al(keys, 16) && (!idx_in || al(idx_in, 16)) && (flags == nullptr || al(flags, 4));
-    if (flags == nullptr) {
-        if (vec)
-            launch_split_typed<true, true>(keys, idx_in, flags, bit, keys_out, idx_out, n_true_out,
-                                           n, hdr, status, sw, nt, stream);
-        else
-            launch_split_typed<true, false>(keys, idx_in, flags, bit, keys_out, idx_out,
-                                            n_true_out, n, hdr, status, sw, nt, stream);
-    } else {
-        if (vec)
-            launch_split_typed<false, true>(keys, idx_in, flags, bit, keys_out, idx_out,
-                                            n_true_out, n, hdr, status, sw, nt, stream);
-        else
-            launch_split_typed<false, false>(keys, idx_in, flags, bit, keys_out, idx_out,
-                                             n_true_out, n, hdr, status, sw, nt, stream);
-    }
+    const bool vec = al(keys, 16) && (!idx_in || al(idx_in, 16)) && al(flags, 4);
+    if (vec)
+        launch_split_typed<true>(keys, idx_in, flags, keys_out, idx_out, n_true_out, n, hdr, status,
+                                 sw, nt, stream);
+    else
+        launch_split_typed<false>(keys, idx_in, flags, keys_out, idx_out, n_true_out, n, hdr, status,
+                                  sw, nt, stream);
     return hipGetLastError();
 }
 

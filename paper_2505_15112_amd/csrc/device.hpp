@@ -75,6 +75,15 @@ __device__ __forceinline__ T wave_sum(T v) {
 
 __device__ __forceinline__ int lane_id() { return (int)__lane_id(); }
 
+// Orders one wavefront's LDS writes before its later LDS reads of other
+// lanes' data (the LDS executes a wave's instructions in order; this keeps
+// the compiler from moving the accesses across).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // ---------------------------------------------------------------- workspace
 
 // Every workspace starts with a 256-byte header:

@@ -32,23 +32,55 @@ static inline int64_t r4_tiles(int64_t n) { return (n + kR4Tile - 1) / kR4Tile; 
 
 // ---------------------------------------------------------------- histogram
 
-__global__ __launch_bounds__(256) void k_digit_hist(const uint32_t* keys, int64_t n,
-                                                    uint64_t* hist, WsHeader* hdr) {
-    __shared__ uint32_t s_hist[4][kHistWords];  // one copy per wavefront
-    const uint32_t epoch = current_epoch(hdr);
-    const int w = threadIdx.x / kWave;
-    for (int i = threadIdx.x; i < 4 * kHistWords; i += blockDim.x) (&s_hist[0][0])[i] = 0;
-    __syncthreads();
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
-        const uint32_t k = keys[i];
+// 16 copies of the 8 x 16 histogram in LDS, the copy picked by lane & 15 and
+// held in the low address bits: the lanes of one atomic instruction rarely
+// hit the same word, and spread over the banks.
+constexpr int kHistCopies = 16;
+
+__device__ __forceinline__ void hist_add(uint32_t* s_h, uint32_t k, uint32_t copy) {
 #pragma unroll
-        for (int p = 0; p < 8; ++p) atomicAdd(&s_hist[w][p * 16 + ((k >> (4 * p)) & 15)], 1u);
+    for (int p = 0; p < 8; ++p)
+        atomicAdd(&s_h[(p * 16 + ((k >> (4 * p)) & 15u)) * kHistCopies + copy], 1u);
+}
+
+__global__ __launch_bounds__(256) void k_digit_hist(const uint32_t* keys, int64_t n, bool vec,
+                                                    uint64_t* hist, WsHeader* hdr) {
+    __shared__ uint32_t s_h[kHistWords * kHistCopies];
+    const uint32_t epoch = current_epoch(hdr);
+    for (int i = threadIdx.x; i < kHistWords * kHistCopies; i += blockDim.x) s_h[i] = 0;
+    __syncthreads();
+    const uint32_t copy = threadIdx.x & (kHistCopies - 1);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int64_t done = 0;
+    if (vec) {  // 4 keys per 16-byte load, 4 loads in flight per thread
+        const u32x4* k4 = reinterpret_cast<const u32x4*>(keys);
+        const int64_t n4 = n / 4;
+        for (int64_t i = t0; i < n4; i += 4 * stride) {
+            u32x4 v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int64_t q = i + u * stride;
+                v[u] = q < n4 ? k4[q] : u32x4{0, 0, 0, 0};
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (i + u * stride < n4) {
+                    hist_add(s_h, v[u].x, copy);
+                    hist_add(s_h, v[u].y, copy);
+                    hist_add(s_h, v[u].z, copy);
+                    hist_add(s_h, v[u].w, copy);
+                }
+            }
+        }
+        done = n4 * 4;
     }
+    for (int64_t i = done + t0; i < n; i += stride) hist_add(s_h, keys[i], copy);
     __syncthreads();
     if (threadIdx.x < kHistWords) {
-        const uint32_t c = s_hist[0][threadIdx.x] + s_hist[1][threadIdx.x] +
-                           s_hist[2][threadIdx.x] + s_hist[3][threadIdx.x];
+        uint32_t c = 0;
+#pragma unroll
+        for (int k = 0; k < kHistCopies; ++k) c += s_h[threadIdx.x * kHistCopies + k];
         tagged_add(hist + threadIdx.x, epoch, c);
     }
 }
@@ -135,7 +167,9 @@ __global__ __launch_bounds__(kR4Waves* kWave) void k_radix4_pass(
     int64_t status_words, uint32_t ntiles) {
     __shared__ Ticket s_ticket;
     __shared__ uint32_t s_cnt[kR4Waves][16];
-    __shared__ uint32_t s_base[16];
+    __shared__ uint32_t s_tstart[16];  // first slot of digit d in the tile's digit order
+    __shared__ uint32_t s_gbase[16];   // global position of that slot
+    __shared__ uint32_t s_stage[kR4Tile];
 
     if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
     __syncthreads();
@@ -149,11 +183,13 @@ __global__ __launch_bounds__(kR4Waves* kWave) void k_radix4_pass(
     const int64_t tile = tile32;
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
-    const int64_t wbase = tile * kR4Tile + (int64_t)w * kR4Chunks * kWave;
+    const int64_t tbase = tile * kR4Tile;
+    const int64_t wbase = tbase + (int64_t)w * kR4Chunks * kWave;
+    const bool full = tbase + kR4Tile <= n;
+    const uint32_t valid = full ? (uint32_t)kR4Tile : (uint32_t)(n - tbase);
 
     uint32_t key[kR4Chunks];
     int32_t perm[kR4Chunks];
-    const bool full = tile * kR4Tile + kR4Tile <= n;
 #pragma unroll
     for (int j = 0; j < kR4Chunks; ++j) {
         const int64_t i = wbase + j * kWave + lane;
@@ -171,20 +207,20 @@ __global__ __launch_bounds__(kR4Waves* kWave) void k_radix4_pass(
         const int64_t i = wbase + j * kWave + lane;
         const bool ok = full || i < n;
         const uint32_t d = (key[j] >> shift) & 15u;
-        const uint64_t valid = __ballot(ok);
+        const uint64_t valid_l = __ballot(ok);
         const uint64_t b0 = __ballot(ok && (d & 1));
         const uint64_t b1 = __ballot(ok && (d & 2));
         const uint64_t b2 = __ballot(ok && (d & 4));
         const uint64_t b3 = __ballot(ok && (d & 8));
-        const uint64_t mine = digit_lanes(d, valid, b0, b1, b2, b3);
+        const uint64_t mine = digit_lanes(d, valid_l, b0, b1, b2, b3);
         rank[j] = lane_shfl(run, (int)d) + lanes_below(mine);
-        run += (uint32_t)__builtin_popcountll(digit_lanes((uint32_t)(lane & 15), valid, b0, b1, b2, b3));
+        run += (uint32_t)__builtin_popcountll(digit_lanes((uint32_t)(lane & 15), valid_l, b0, b1, b2, b3));
     }
     if (lane < 16) s_cnt[w][lane] = run;
     __syncthreads();
 
     // lanes 0..15 of every wave: count of digit `lane` in earlier waves, and
-    // (wave 0) the tile total that goes into the look-back.
+    // the tile total of that digit.
     uint32_t wofs = 0, tot = 0;
 #pragma unroll
     for (int k = 0; k < kR4Waves; ++k) {
@@ -194,23 +230,59 @@ __global__ __launch_bounds__(kR4Waves* kWave) void k_radix4_pass(
     }
     if (w == 0) {
         const uint32_t before = lookback16(status, tile, tot, epoch, hdr);
-        // keys with a smaller digit, over the whole array (exclusive scan of
-        // the 16 histogram bins of this digit position)
+        // keys with a smaller digit over the whole array (exclusive scan of
+        // this digit position's 16 histogram bins) and within the tile
         const uint32_t h = lane < 16 ? (uint32_t)hist[(shift >> 2) * 16 + lane] : 0u;
+        const uint32_t t16 = lane < 16 ? tot : 0u;
         const uint32_t smaller = wave_incl_scan(h) - h;
-        if (lane < 16) s_base[lane] = smaller + before;
+        const uint32_t tstart = wave_incl_scan(t16) - t16;
+        if (lane < 16) {
+            s_tstart[lane] = tstart;
+            s_gbase[lane] = smaller + before;
+        }
         if (lane == 0) finish_epoch(hdr, epoch, ntiles, status, status_words);
     }
     __syncthreads();
-    const uint32_t dest = (lane < 16 ? s_base[lane] : 0u) + wofs;  // lane d: start of digit d
+
+    // Sort the tile by digit in LDS (slot = digit start + earlier waves +
+    // rank), then write each digit's run with consecutive threads.
+    const uint32_t wstart = (lane < 16 ? s_tstart[lane] : 0u) + wofs;  // lane d: this wave's slot 0 for d
+    uint32_t slot[kR4Chunks];
 #pragma unroll
     for (int j = 0; j < kR4Chunks; ++j) {
-        const int64_t i = wbase + j * kWave + lane;
         const uint32_t d = (key[j] >> shift) & 15u;
-        const uint32_t pos = lane_shfl(dest, (int)d) + rank[j];
-        if ((full || i < n) && pos < (uint64_t)n) {  // pos < n always; guards a bad count
-            keys_out[pos] = key[j];
-            if (WITH_PERM) perm_out[pos] = perm[j];
+        slot[j] = lane_shfl(wstart, (int)d) + rank[j];
+        const int64_t i = wbase + j * kWave + lane;
+        if ((full || i < n) && slot[j] < kR4Tile) s_stage[slot[j]] = key[j];
+    }
+    __syncthreads();
+    uint32_t skey[kR4Chunks];
+#pragma unroll
+    for (int j = 0; j < kR4Chunks; ++j) {
+        const uint32_t t = (uint32_t)threadIdx.x + j * kR4Waves * kWave;
+        skey[j] = s_stage[t];
+        if (t < valid) {
+            const uint32_t d = (skey[j] >> shift) & 15u;
+            const uint32_t pos = s_gbase[d] + (t - s_tstart[d]);
+            if (pos < (uint64_t)n) keys_out[pos] = skey[j];  // pos < n always; guards a bad count
+        }
+    }
+    if (WITH_PERM) {
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kR4Chunks; ++j) {
+            const int64_t i = wbase + j * kWave + lane;
+            if ((full || i < n) && slot[j] < kR4Tile) s_stage[slot[j]] = (uint32_t)perm[j];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kR4Chunks; ++j) {
+            const uint32_t t = (uint32_t)threadIdx.x + j * kR4Waves * kWave;
+            if (t < valid) {
+                const uint32_t d = (skey[j] >> shift) & 15u;
+                const uint32_t pos = s_gbase[d] + (t - s_tstart[d]);
+                if (pos < (uint64_t)n) perm_out[pos] = (int32_t)s_stage[t];
+            }
         }
     }
 }
@@ -232,9 +304,10 @@ hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* 
     if (n == 0) return hipSuccess;
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
     uint64_t* hist = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
-    const int64_t hb = (n + 255) / 256;
+    const int64_t hb = (n + 1023) / 1024;
+    const bool vec = ((uintptr_t)keys % 16) == 0;
     hipLaunchKernelGGL(k_digit_hist, dim3((unsigned)(hb < 1024 ? hb : 1024)), dim3(256), 0, stream,
-                       keys, n, hist, hdr);
+                       keys, n, vec, hist, hdr);
     const int passes = bits == 4 ? 8 : 32;
     const uint32_t* src_k = keys;
     const int32_t* src_p = nullptr;

@@ -14,10 +14,10 @@
 // The top-p cutoff needs only one index per row, so it does not use the
 // look-back: a first kernel sums every tile of every row (reading all the
 // probabilities once, no inter-workgroup waiting), and a second kernel, one
-// workgroup per tile again, scans the tile sums of its row to find the first
-// tile whose inclusive sum reaches p; only that tile re-reads its data to
-// locate the index (the two phases of the paper's Algorithm 3, MCScan, with
-// the down-sweep cut to the one tile that matters).
+// workgroup per row, scans the row's tile sums to find the first tile whose
+// inclusive sum reaches p and re-reads only that tile to locate the index
+// (the two phases of the paper's Algorithm 3, MCScan, with the down-sweep cut
+// to the one tile that matters).
 #include <limits.h>
 
 #include "launch.hpp"
@@ -116,49 +116,46 @@ __global__ __launch_bounds__(TileT::kThreads) void k_topp_sums(const float* prob
     if (threadIdx.x == 0) partial[blockIdx.x] = (uint64_t)Bits<float>::to(agg);
 }
 
-// Phase 2: every workgroup recomputes its row's inclusive tile sums up to its
-// own tile with one fixed formula (64 at a time, DPP scan, carried in order),
-// so all workgroups of a row agree bit for bit on which tile is the first to
-// reach p.  That tile rescans its data for the first element whose running
-// sum reaches p (its last element if rounding kept them all below p); the
-// row's last tile writes len - 1 if no tile reaches p.
+// Phase 2, one workgroup per row: scan the row's tile sums (64 at a time,
+// DPP scan, carried in order) for the first tile whose inclusive sum reaches
+// p, rescan only that tile for the first element whose running sum reaches p
+// (its last element if rounding kept them all below p), or write len - 1 if
+// no tile reaches p.
 template <class TileT, bool VEC>
 __global__ __launch_bounds__(TileT::kThreads) void k_topp_owner(const float* probs,
                                                                 int32_t* cutoff, int64_t len,
                                                                 uint32_t segs,
                                                                 const uint64_t* partial, float p) {
-    __shared__ int s_role;  // 0: not involved, 1: owns the crossing, 2: writes len - 1
+    __shared__ int64_t s_first;
     __shared__ float s_excl;
     __shared__ float s_wtot[TileT::WAVES];
     __shared__ int32_t s_min[TileT::WAVES];
-    const int64_t row = blockIdx.x / segs;
-    const int64_t seg = blockIdx.x - row * segs;
+    const int64_t row = blockIdx.x;
     const int lane = lane_id();
     if (threadIdx.x < kWave) {
         const uint64_t* pr = partial + row * segs;
         float carry = 0.f, excl = 0.f;
         int64_t first = -1;
-        for (int64_t b = 0; b <= seg && first < 0; b += kWave) {
+        for (int64_t b = 0; b < segs && first < 0; b += kWave) {
             const int64_t s = b + lane;
-            const float a = s <= seg ? Bits<float>::from((uint32_t)pr[s]) : 0.f;
+            const float a = s < segs ? Bits<float>::from((uint32_t)pr[s]) : 0.f;
             const float inc = carry + wave_incl_scan(a);
-            const uint64_t hit = __ballot(s <= seg && inc >= p);
+            const uint64_t hit = __ballot(s < segs && inc >= p);
             if (hit) {
                 const int l = __builtin_ctzll(hit);
                 first = b + l;
-                if (first == seg) excl = l ? lane_read(inc, l - 1) : carry;
+                excl = l ? lane_read(inc, l - 1) : carry;
             }
             carry = lane_read(inc, kWave - 1);
         }
         if (lane == 0) {
-            s_role = first == seg ? 1 : (first < 0 && seg == (int64_t)segs - 1 ? 2 : 0);
+            s_first = first;
             s_excl = excl;
         }
     }
     __syncthreads();
-    const int role = s_role;
-    if (role == 0) return;
-    if (role == 2) {
+    const int64_t seg = s_first;
+    if (seg < 0) {
         if (threadIdx.x == 0) cutoff[row] = (int32_t)(len - 1);
         return;
     }
@@ -289,8 +286,8 @@ static void topp_long(bool vec, const float* probs, int32_t* cutoff, int64_t row
     auto ks = vec ? k_topp_sums<TileT, true> : k_topp_sums<TileT, false>;
     auto ko = vec ? k_topp_owner<TileT, true> : k_topp_owner<TileT, false>;
     hipLaunchKernelGGL(ks, dim3(nt), dim3(TileT::kThreads), 0, stream, probs, len, segs, partial);
-    hipLaunchKernelGGL(ko, dim3(nt), dim3(TileT::kThreads), 0, stream, probs, cutoff, len, segs,
-                       (const uint64_t*)partial, p);
+    hipLaunchKernelGGL(ko, dim3((unsigned)rows), dim3(TileT::kThreads), 0, stream, probs, cutoff,
+                       len, segs, (const uint64_t*)partial, p);
 }
 
 template <class T, bool TOPP>

@@ -1,0 +1,105 @@
+"""The workspace contract on the GPU: zero-filled once, then shared by any
+sequence of calls of any op, never cleared again -- including across the
+once-in-2^30-calls wrap of the 30-bit status epoch, which is forced here by
+writing the header's epoch from the host.  A header that was never
+initialised must make the kernel raise the error word and finish (no hang).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import announce, assert_equal_first_diff, assert_float_close, to_dev, to_host
+from paper_2505_15112_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ops():
+    from paper_2505_15112_amd import ops
+    return ops
+
+
+def _big_ws(ops, n):
+    import torch
+    from paper_2505_15112_amd import _lib
+    sizes = [_lib.workspace_bytes(_lib.OP_SCAN, n), _lib.workspace_bytes(_lib.OP_SCAN_RSS, n),
+             _lib.workspace_bytes(_lib.OP_COMPACT, n),
+             _lib.workspace_bytes(_lib.OP_RADIX_SORT, n, bits=4),
+             _lib.workspace_bytes(_lib.OP_RADIX_SORT, n, bits=1),
+             _lib.workspace_bytes(_lib.OP_SCAN_ROWS, rows=16, length=n // 16)]
+    return ops.workspace(_lib.OP_SCAN, torch.device("cuda", 0), (max(sizes) // 8) * 8 * 8)
+
+
+def _run_all(ops, ws, n, seed):
+    """Every op on one workspace, each checked against the oracle."""
+    x = W.scan_i32_full_range(n, seed=seed)
+    xd = to_dev(x)
+    assert_equal_first_diff(to_host(ops.scan_inclusive_i32(xd, ws=ws)), oracle.scan_i32(x), "scan")
+    assert_equal_first_diff(to_host(ops.scan_inclusive_rss_i32(xd, ws=ws)), oracle.scan_i32(x), "rss")
+    xf = W.scan_f32(n, seed=seed)
+    ref, a = oracle.scan_f32(xf, exclusive=True)
+    assert_float_close(to_host(ops.scan_exclusive_f32(to_dev(xf), ws=ws)), ref, a, "scan f32")
+    m = W.mask_u8(n, seed=seed)
+    out, idx, cnt = ops.compact_by_mask_f32(to_dev(xf), to_dev(m), with_idx=True, ws=ws)
+    ro, ri = oracle.compact_f32(xf, m)
+    assert int(cnt.item()) == ro.size
+    assert_equal_first_diff(to_host(idx)[: ro.size], ri, "compact idx")
+    k = W.keys_u32(n, seed=seed)
+    ko, io, nt = ops.split_by_flags_u32(to_dev(k.view(np.int32)), to_dev(m), ws=ws)
+    rk, rio, rn = oracle.split_u32(k, m)
+    assert int(nt.item()) == rn
+    assert_equal_first_diff(to_host(io), rio, "split idx")
+    rk, rp = oracle.sort_u32(k)
+    for bits in (4, 1):
+        so, sp = ops.radix_sort_u32(to_dev(k.view(np.int32)), bits_per_pass=bits, ws=ws)
+        assert_equal_first_diff(to_host(sp), rp, f"radix{bits}")
+    xr = x.reshape(16, n // 16)
+    assert_equal_first_diff(to_host(ops.scan_rows_i32(to_dev(xr), ws=ws)), oracle.scan_rows_i32(xr),
+                            "rows")
+
+
+def test_one_workspace_for_every_op(ops):
+    announce("shared workspace, all ops")
+    n = 16 * 40_000
+    ws = _big_ws(ops, n)
+    for seed in range(3):
+        _run_all(ops, ws, n, seed)
+    assert int(ws[12:16].cpu().numpy().view(np.int32)[0]) == 0
+
+
+def test_epoch_wrap(ops):
+    """Set the header epoch to the last value before the 30-bit status tag
+    wraps: that call must clear the workspace, and every later call of every
+    op must still be right."""
+    import torch
+    announce("epoch wrap")
+    n = 16 * 40_000
+    ws = _big_ws(ops, n)
+    _run_all(ops, ws, n, 7)  # leaves live-looking status words of low epochs
+    hdr = ws[:8].view(torch.int64)
+    hdr.copy_(torch.tensor([((1 << 30) - 1) << 32], dtype=torch.int64, device=ws.device))
+    torch.cuda.synchronize()
+    x = W.scan_i32_full_range(n, seed=8)
+    assert_equal_first_diff(to_host(ops.scan_inclusive_i32(to_dev(x), ws=ws)), oracle.scan_i32(x),
+                            "wrap call")
+    epoch = int(ws[:8].view(torch.int64).cpu()[0]) >> 32
+    assert epoch == 1 << 30
+    for seed in (9, 10):
+        _run_all(ops, ws, n, seed)
+    assert int(ws[12:16].cpu().numpy().view(np.int32)[0]) == 0
+
+
+def test_uninitialised_header_raises_error_word(ops):
+    """Tickets that start past the grid: the workgroup sets the error word and
+    finishes instead of waiting for tiles nobody will process."""
+    import torch
+    from paper_2505_15112_amd import _lib
+    announce("uninitialised header")
+    n = 1000  # one tile
+    ws = ops.workspace(_lib.OP_SCAN, torch.device("cuda", 0), n)
+    ws[:8].view(torch.int64).fill_(5)  # ticket count 5: the only workgroup draws ticket 5
+    x = to_dev(W.scan_i32(n, seed=1))
+    ops.scan_inclusive_i32(x, ws=ws)
+    torch.cuda.synchronize()
+    assert int(ws[12:16].cpu().numpy().view(np.int32)[0]) == 1
