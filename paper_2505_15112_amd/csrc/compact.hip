@@ -9,8 +9,8 @@
 // Split (SplitInd): stable two-way partition with source indices.  Flagged
 // element i goes to e_i (exclusive count of flagged before it), unflagged to
 // n_true + (i - e_i).  n_true must be known before any tile stores, so a
-// small counting kernel runs first (reading only the flag bytes); its total
-// lands in an epoch-tagged workspace word that the split kernel reads.  As
+// small counting kernel runs first (reading only the flag bytes, each block
+// storing its own partial count), and every split tile adds the partials.  As
 // the pass of the one-bit radix sort (Section 5), the flag is "key bit b is
 // 0" and n_true comes from the sort's digit histogram instead.
 //
@@ -34,8 +34,9 @@ __device__ __forceinline__ uint32_t nonzero_bytes(uint32_t m) {
     return t & 0x01010101u;
 }
 
-// Header accumulator used by split for the number of flagged elements.
-constexpr int kTagNTrue = 0;
+// The flag-counting kernel runs this many blocks; each writes its count to
+// one 64-bit workspace word after the split's status words.
+constexpr int kCountBlocks = 256;
 
 // ---------------------------------------------------------------- compress
 
@@ -157,12 +158,13 @@ __global__ __launch_bounds__(kPWaves* kWave) void k_compact(
 
 // ---------------------------------------------------------------- split
 
-// Count the non-zero flag bytes into the header accumulator: grid-stride,
-// 16 flags per 16-byte load, 4 loads in flight per thread.
-__global__ __launch_bounds__(256) void k_count_flags(const uint8_t* flags, int64_t n, bool vec,
-                                                     WsHeader* hdr) {
-    __shared__ uint32_t s_part[4];
-    const uint32_t epoch = current_epoch(hdr);
+// Count the non-zero flag bytes: kCountBlocks blocks of 1024 threads,
+// grid-stride, 16 flags per 16-byte load, 4 loads in flight per thread; every
+// block stores its count in part[blockIdx.x] (no atomics: the split kernel
+// sums the partials).
+__global__ __launch_bounds__(1024) void k_count_flags(const uint8_t* flags, int64_t n, bool vec,
+                                                      uint64_t* part) {
+    __shared__ uint32_t s_part[16];
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     uint32_t cnt = 0;
@@ -188,12 +190,22 @@ __global__ __launch_bounds__(256) void k_count_flags(const uint8_t* flags, int64
     const uint32_t wsum = wave_sum(cnt);
     if (lane_id() == 0) s_part[threadIdx.x / kWave] = wsum;
     __syncthreads();
-    if (threadIdx.x == 0)
-        tagged_add(&hdr->tagged[kTagNTrue], epoch, s_part[0] + s_part[1] + s_part[2] + s_part[3]);
+    if (threadIdx.x == 0) {
+        uint32_t t = 0;
+        for (int k = 0; k < 16; ++k) t += s_part[k];
+        part[blockIdx.x] = t;
+    }
+}
+
+// Sum of the kCountBlocks partial counts, by one full wavefront.
+__device__ __forceinline__ uint32_t sum_partials(const uint64_t* part) {
+    uint32_t v = 0;
+    for (int i = lane_id(); i < kCountBlocks; i += kWave) v += (uint32_t)part[i];
+    return wave_sum(v);
 }
 
 // Number of keys whose bit `bit` is 0, from the 8 x 16 digit histogram of
-// the radix sort (tagged words, digit position bit / 4).
+// the radix sort (digit position bit / 4).
 __device__ __forceinline__ uint32_t zeros_of_bit(const uint64_t* hist, int bit) {
     uint32_t z = 0;
     for (int v = 0; v < 16; ++v)
@@ -213,10 +225,11 @@ template <bool FROM_BITS, bool VEC, bool HAS_IDX_IN, bool WITH_IDX>
 __global__ __launch_bounds__(kSWaves* kWave) void k_split(
     const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags, int bit, uint32_t* keys_out,
     int32_t* idx_out, int32_t* n_true_out, int64_t n, WsHeader* hdr, uint64_t* status,
-    int64_t status_words, uint32_t ntiles, const uint64_t* hist) {
+    int64_t status_words, uint32_t ntiles, const uint64_t* hist, const uint64_t* part) {
     __shared__ Ticket s_ticket;
     __shared__ uint32_t s_wtot[kSWaves];
     __shared__ uint32_t s_carry;
+    __shared__ uint32_t s_ntrue;
     __shared__ uint32_t s_key[kSWaves][kWave * 4];
     __shared__ int32_t s_idx[WITH_IDX ? kSWaves : 1][kWave * 4];
 
@@ -234,7 +247,10 @@ __global__ __launch_bounds__(kSWaves* kWave) void k_split(
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
     auto offset = [&](int j) { return base + ((int64_t)(w * kSChunks + j) * kWave + lane) * 4; };
-    const uint32_t n_true = hist ? zeros_of_bit(hist, bit) : tagged_value(&hdr->tagged[kTagNTrue]);
+    if (threadIdx.x < kWave) {
+        const uint32_t nt = hist ? zeros_of_bit(hist, bit) : sum_partials(part);
+        if (threadIdx.x == 0) s_ntrue = nt;
+    }
 
     uint32_t k[kSChunks][4];
     int32_t iv[kSChunks][4];
@@ -276,7 +292,7 @@ __global__ __launch_bounds__(kSWaves* kWave) void k_split(
     uint32_t run = 0;
 #pragma unroll
     for (int j = 0; j < kSChunks; ++j) {
-        const uint32_t c = (uint32_t)__builtin_popcount(fl[j]);
+        const uint32_t c = (uint32_t)__builtin_popcount(fl[j]);  // (split: s_ntrue set before the barrier below)
         const uint32_t inc = wave_incl_scan(c);
         lane_off[j] = run + inc - c;
         run += lane_read(inc, kWave - 1);
@@ -294,7 +310,7 @@ __global__ __launch_bounds__(kSWaves* kWave) void k_split(
         const uint32_t excl = lookback<uint32_t>(status, tile, 0, agg, 0u, epoch, hdr);
         if (threadIdx.x == 0) {
             s_carry = excl;
-            if (tile == 0 && n_true_out) *n_true_out = (int32_t)n_true;
+            if (tile == 0 && n_true_out) *n_true_out = (int32_t)s_ntrue;
             finish_epoch(hdr, epoch, ntiles, status, status_words);
         }
     }
@@ -303,6 +319,7 @@ __global__ __launch_bounds__(kSWaves* kWave) void k_split(
     // keys another: gather both in this wave's LDS slot (flagged first), then
     // write the two runs with consecutive lanes.
     const uint32_t c0 = s_carry + wofs;
+    const uint32_t n_true = s_ntrue;
     uint32_t* sk = s_key[w];
     int32_t* si = s_idx[WITH_IDX ? w : 0];
 #pragma unroll
@@ -343,8 +360,10 @@ static inline int64_t s_tiles(int64_t n) { return (n + kSTile - 1) / kSTile; }
 
 // ---------------------------------------------------------------- launchers
 
-// Sized for the split tile (the smaller one); compress uses fewer words.
-size_t compact_ws_bytes(int64_t n) { return kWsHeader + (size_t)s_tiles(n) * sizeof(uint64_t); }
+// Sized for the split tile (the smaller one; compress uses fewer words), then
+// the flag counter's per-block partials.
+static size_t split_part_offset(int64_t n) { return kWsHeader + (size_t)s_tiles(n) * sizeof(uint64_t); }
+size_t compact_ws_bytes(int64_t n) { return split_part_offset(n) + kCountBlocks * sizeof(uint64_t); }
 
 static bool al(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
@@ -375,14 +394,14 @@ template <bool VEC>
 static void launch_split_typed(const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags,
                                uint32_t* keys_out, int32_t* idx_out, int32_t* n_true_out,
                                int64_t n, WsHeader* hdr, uint64_t* status, int64_t sw,
-                               uint32_t nt, hipStream_t stream) {
-    const int64_t cblocks = (n + 16 * 256 * 4 - 1) / (16 * 256 * 4);
-    hipLaunchKernelGGL(k_count_flags, dim3((unsigned)(cblocks < 2048 ? cblocks : 2048)), dim3(256),
-                       0, stream, flags, n, ((uintptr_t)flags % 16) == 0, hdr);
+                               uint32_t nt, uint64_t* part, hipStream_t stream) {
+    hipLaunchKernelGGL(k_count_flags, dim3(kCountBlocks), dim3(1024), 0, stream, flags, n,
+                       ((uintptr_t)flags % 16) == 0, part);
     auto k = idx_in ? (idx_out ? k_split<false, VEC, true, true> : k_split<false, VEC, true, false>)
                     : (idx_out ? k_split<false, VEC, false, true> : k_split<false, VEC, false, false>);
     hipLaunchKernelGGL(k, dim3(nt), dim3(kSWaves * kWave), 0, stream, keys, idx_in, flags, 0,
-                       keys_out, idx_out, n_true_out, n, hdr, status, sw, nt, (const uint64_t*)nullptr);
+                       keys_out, idx_out, n_true_out, n, hdr, status, sw, nt, (const uint64_t*)nullptr,
+                       (const uint64_t*)part);
 }
 
 // One LSB radix-sort pass on key bit `bit` (flag = bit is 0), with the count
@@ -401,7 +420,7 @@ hipError_t launch_radix1_pass(const uint32_t* keys, const int32_t* idx_in, int b
                            : (idx_out ? k_split<true, false, false, true> : k_split<true, false, false, false>));
     hipLaunchKernelGGL(k, dim3(nt), dim3(kSWaves * kWave), 0, stream, keys, idx_in,
                        (const uint8_t*)nullptr, bit, keys_out, idx_out, (int32_t*)nullptr, n, hdr,
-                       status, sw, nt, hist);
+                       status, sw, nt, hist, (const uint64_t*)nullptr);
     return hipGetLastError();
 }
 
@@ -416,14 +435,17 @@ hipError_t launch_split(const uint32_t* keys, const int32_t* idx_in, const uint8
     const uint32_t nt = (uint32_t)s_tiles(n);
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
     uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
+    // (the epoch-wrap clear may zero the partial counts too: they are read
+    // before any workgroup finishes)
     const int64_t sw = (int64_t)((ws_bytes - kWsHeader) / sizeof(uint64_t));
+    uint64_t* part = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + split_part_offset(n));
     const bool vec = al(keys, 16) && (!idx_in || al(idx_in, 16)) && al(flags, 4);
     if (vec)
         launch_split_typed<true>(keys, idx_in, flags, keys_out, idx_out, n_true_out, n, hdr, status,
-                                 sw, nt, stream);
+                                 sw, nt, part, stream);
     else
         launch_split_typed<false>(keys, idx_in, flags, keys_out, idx_out, n_true_out, n, hdr, status,
-                                  sw, nt, stream);
+                                  sw, nt, part, stream);
     return hipGetLastError();
 }
 

@@ -91,21 +91,22 @@ __device__ __forceinline__ void wave_lds_sync() {
 //   [8, 12)   done counter, used only by the call that wraps the epoch
 //   [12, 16)  error flag: set to 1 if a look-back gave up waiting (the
 //             workspace was not zero-filled before first use)
-//   [16, 256) 30 epoch-tagged 64-bit accumulators (see tagged_add)
+//   [16, 256) reserved
 // A zero-filled workspace is ready; after that every look-back kernel leaves
 // it ready for the next call: the workgroup that takes the last ticket resets
 // the ticket count and advances the epoch, and status words are tagged with
 // the epoch of the call that wrote them, so words left by earlier calls read
 // as "nothing published yet".  No per-call clearing is needed.
 // Invariant kept by every op: outside the header, every 64-bit workspace word
-// either has its two top bits 0 (state "nothing published": zero, scratch
-// values, tagged accumulators) or is a status word of an epoch no later than
-// the current one.  So any workspace can serve any sequence of calls.
+// either has its two top bits 0 (state "nothing published": zero, or scratch
+// such as per-block partial counts and sums, which are always below 2^30) or
+// is a status word of an epoch no later than the current one.  So any
+// workspace can serve any sequence of calls.
 struct WsHeader {
     uint64_t ticket;
     uint32_t done;
     uint32_t error;
-    uint64_t tagged[30];
+    uint64_t reserved[30];
 };
 static_assert(sizeof(WsHeader) == 256, "workspace header is 256 bytes");
 
@@ -125,34 +126,6 @@ __device__ __forceinline__ Ticket take_ticket(WsHeader* h, uint32_t nwg) {
         __hip_atomic_store(&h->ticket, (uint64_t)(t.epoch + 1) << 32, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
     return t;
-}
-
-__device__ __forceinline__ uint32_t current_epoch(WsHeader* h) {
-    return (uint32_t)(__hip_atomic_load(&h->ticket, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >> 32);
-}
-
-// Epoch-tagged accumulator [0:2 | epoch:30 | value:32]: the first add of a
-// call (the word still carries an older epoch) replaces the value, later adds
-// of the same call accumulate.  A kernel that adds must run (and finish)
-// before the look-back kernel of the same call, which reads the value and
-// advances the epoch; so a word never needs clearing.  The two top bits stay
-// 0, so read as a tile status word it is "nothing published yet".
-__device__ __forceinline__ void tagged_add(uint64_t* w, uint32_t epoch, uint32_t v) {
-    const uint32_t tag = epoch & ((1u << 30) - 1);
-    uint64_t old = __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    while (true) {
-        if ((uint32_t)(old >> 32) == tag) {
-            __hip_atomic_fetch_add(w, (uint64_t)v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            return;
-        }
-        const uint64_t fresh = ((uint64_t)tag << 32) | v;
-        if (__hip_atomic_compare_exchange_strong(w, &old, fresh, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_AGENT))
-            return;
-    }
-}
-__device__ __forceinline__ uint32_t tagged_value(uint64_t* w) {
-    return (uint32_t)__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // ---------------------------------------------------------------- tile status
@@ -257,7 +230,6 @@ __device__ __forceinline__ void finish_epoch(WsHeader* h, uint32_t epoch, uint32
     const uint32_t d = __hip_atomic_fetch_add(&h->done, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
     if (d != nwg - 1) return;
     for (int64_t i = 0; i < status_words; ++i) status[i] = 0;
-    for (int i = 0; i < 30; ++i) h->tagged[i] = 0;
     __hip_atomic_store(&h->done, 0u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
 

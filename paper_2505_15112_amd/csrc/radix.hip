@@ -4,7 +4,7 @@
 // indices as PyTorch's sort() does).
 //
 //  * One pre-pass reads the keys once and builds the 8 x 16 histogram of all
-//    4-bit digits into epoch-tagged workspace words.
+//    4-bit digits (per-block partial histograms, then one block adds them).
 //  * 1 bit per pass: 32 split passes (compact.hip's split kernel with the
 //    flag "bit b is 0"), the number of zero bits of pass b read off the
 //    histogram, so no pass needs its own counting kernel.
@@ -20,13 +20,14 @@
 
 namespace ls {
 
-constexpr int kHistWords = 8 * 16;  // tagged [epoch | count] words after the header
+constexpr int kHistWords = 8 * 16;  // final counts, one 64-bit word each, after the header
 constexpr size_t kRadixStatusOffset = kWsHeader + kHistWords * sizeof(uint64_t);
+constexpr int kHistBlocks = 512;  // blocks of the histogram pre-pass (one partial each)
 
 constexpr int kR4Waves = 8;
 constexpr int kR4Chunks = 16;  // 64 keys (one per lane) per chunk
 constexpr int64_t kR4Tile = kR4Waves * kR4Chunks * kWave;  // 8192 keys
-constexpr int64_t kR1Tile = 4096;                          // compact.hip's split tile
+constexpr int64_t kR1Tile = 4096;  // at most compact.hip's split tile: enough status words
 
 static inline int64_t r4_tiles(int64_t n) { return (n + kR4Tile - 1) / kR4Tile; }
 
@@ -44,9 +45,8 @@ __device__ __forceinline__ void hist_add(uint32_t* s_h, uint32_t k, uint32_t cop
 }
 
 __global__ __launch_bounds__(256) void k_digit_hist(const uint32_t* keys, int64_t n, bool vec,
-                                                    uint64_t* hist, WsHeader* hdr) {
+                                                    uint32_t* part) {
     __shared__ uint32_t s_h[kHistWords * kHistCopies];
-    const uint32_t epoch = current_epoch(hdr);
     for (int i = threadIdx.x; i < kHistWords * kHistCopies; i += blockDim.x) s_h[i] = 0;
     __syncthreads();
     const uint32_t copy = threadIdx.x & (kHistCopies - 1);
@@ -81,7 +81,24 @@ __global__ __launch_bounds__(256) void k_digit_hist(const uint32_t* keys, int64_
         uint32_t c = 0;
 #pragma unroll
         for (int k = 0; k < kHistCopies; ++k) c += s_h[threadIdx.x * kHistCopies + k];
-        tagged_add(hist + threadIdx.x, epoch, c);
+        part[blockIdx.x * kHistWords + threadIdx.x] = c;
+    }
+}
+
+// One block adds the per-block histograms into the final 128 counts.
+__global__ __launch_bounds__(1024) void k_hist_reduce(const uint32_t* part, int nblocks,
+                                                      uint64_t* hist) {
+    __shared__ uint32_t s_sum[8][kHistWords];
+    const int word = threadIdx.x % kHistWords, slice = threadIdx.x / kHistWords;  // 8 slices
+    uint32_t c = 0;
+    for (int b = slice; b < nblocks; b += 8) c += part[b * kHistWords + word];
+    s_sum[slice][word] = c;
+    __syncthreads();
+    if (threadIdx.x < kHistWords) {
+        uint32_t t = 0;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) t += s_sum[k][threadIdx.x];
+        hist[threadIdx.x] = t;
     }
 }
 
@@ -103,10 +120,14 @@ __device__ __forceinline__ uint32_t lane_shfl(uint32_t v, int src_lane) {
     return (uint32_t)__builtin_amdgcn_ds_bpermute(src_lane << 2, (int)v);
 }
 
-// 16-chain look-back by one wavefront: lane l watches digit l & 15 of the
-// predecessor tile (l >> 4) steps back, so each round reads 4 tiles x 16
-// digits.  tot: this tile's count of digit (lane & 15).  Returns, in every
-// lane, the count of digit (lane & 15) in all earlier tiles.
+// 16-chain look-back by one wavefront.  Lane l watches digit l & 15; in one
+// round it loads the status words of 4 predecessor tiles, at offsets
+// (l >> 4) + 4k for k = 0..3, so a round covers 16 tiles x 16 digits with
+// every load in flight at once.  tot: this tile's count of digit (lane & 15).
+// Returns, in every lane, the count of digit (lane & 15) in all earlier tiles.
+constexpr int kLb16Loads = 4;
+constexpr int kLb16Span = 4 * kLb16Loads;  // tiles per round
+
 __device__ uint32_t lookback16(uint64_t* status, int64_t tile, uint32_t tot, uint32_t epoch,
                                WsHeader* h) {
     const int lane = lane_id();
@@ -121,29 +142,42 @@ __device__ uint32_t lookback16(uint64_t* status, int64_t tile, uint32_t tot, uin
     bool done = false;
     uint32_t spins = 0;
     while (true) {
-        const int64_t t = end - q;
-        uint64_t s = 0, st = kStateP;
-        if (!done && t >= 0) {
-            s = status_load(status + t * 16 + d);
-            st = status_state(s, epoch);
+        uint64_t s[kLb16Loads], st[kLb16Loads];
+#pragma unroll
+        for (int k = 0; k < kLb16Loads; ++k) {
+            const int64_t t = end - (q + 4 * k);
+            s[k] = 0;
+            st[k] = kStateP;  // tiles before tile 0 read as an empty prefix
+            if (!done && t >= 0) {
+                s[k] = status_load(status + t * 16 + d);
+                st[k] = status_state(s[k], epoch);
+            }
         }
-        const uint64_t P = __ballot(st == kStateP);
-        const uint64_t X = __ballot(st == kStateX);
-        // this digit's four lanes: bits d, d+16, d+32, d+48 (nearest first)
+        // this digit's states at tile offsets 0..15 (bit o: tile end - o)
         uint32_t pq = 0, xq = 0;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            pq |= (uint32_t)((P >> (d + 16 * k)) & 1) << k;
-            xq |= (uint32_t)((X >> (d + 16 * k)) & 1) << k;
+        for (int k = 0; k < kLb16Loads; ++k) {
+            const uint64_t P = __ballot(st[k] == kStateP);
+            const uint64_t X = __ballot(st[k] == kStateX);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                pq |= (uint32_t)((P >> (d + 16 * r)) & 1) << (r + 4 * k);
+                xq |= (uint32_t)((X >> (d + 16 * r)) & 1) << (r + 4 * k);
+            }
         }
-        const uint32_t upto = pq ? (((pq & (~pq + 1)) << 1) - 1) : 0xfu;  // tiles 0..nearest P
+        const uint32_t upto = pq ? (((pq & (~pq + 1)) << 1) - 1) : 0xffffu;  // up to nearest P
         const bool wait = !done && (xq & upto);
-        uint32_t v = (!done && !wait && ((upto >> q) & 1)) ? (uint32_t)s : 0u;
+        uint32_t v = 0;
+        if (!done && !wait) {
+#pragma unroll
+            for (int k = 0; k < kLb16Loads; ++k)
+                if ((upto >> (q + 4 * k)) & 1) v += (uint32_t)s[k];
+        }
         v += lane_shfl(v, lane ^ 16);
         v += lane_shfl(v, lane ^ 32);
         if (!done && !wait) {
             excl += v;
-            end -= 4;
+            end -= kLb16Span;
             done = pq != 0;
         }
         if (__ballot(!done) == 0) break;
@@ -293,9 +327,14 @@ hipError_t launch_radix1_pass(const uint32_t* keys, const int32_t* idx_in, int b
                               uint32_t* keys_out, int32_t* idx_out, int64_t n, const uint64_t* hist,
                               void* ws, size_t ws_bytes, size_t status_offset, hipStream_t stream);
 
+static int64_t radix_status_words(int64_t n, int bits) {
+    return bits == 4 ? r4_tiles(n) * 16 : (n + kR1Tile - 1) / kR1Tile;
+}
+
+// header | final histogram | status words | per-block partial histograms
 size_t radix_ws_bytes(int64_t n, int bits) {
-    const int64_t words = bits == 4 ? r4_tiles(n) * 16 : (n + kR1Tile - 1) / kR1Tile;
-    return kRadixStatusOffset + (size_t)words * sizeof(uint64_t);
+    return kRadixStatusOffset + (size_t)radix_status_words(n, bits) * sizeof(uint64_t) +
+           (size_t)kHistBlocks * kHistWords * sizeof(uint32_t);
 }
 
 hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out,
@@ -304,10 +343,13 @@ hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* 
     if (n == 0) return hipSuccess;
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
     uint64_t* hist = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
-    const int64_t hb = (n + 1023) / 1024;
+    uint32_t* part = reinterpret_cast<uint32_t*>(
+        reinterpret_cast<char*>(ws) + kRadixStatusOffset + radix_status_words(n, bits) * sizeof(uint64_t));
+    const int64_t hb64 = (n + 1023) / 1024;
+    const int hb = (int)(hb64 < kHistBlocks ? hb64 : kHistBlocks);
     const bool vec = ((uintptr_t)keys % 16) == 0;
-    hipLaunchKernelGGL(k_digit_hist, dim3((unsigned)(hb < 1024 ? hb : 1024)), dim3(256), 0, stream,
-                       keys, n, vec, hist, hdr);
+    hipLaunchKernelGGL(k_digit_hist, dim3(hb), dim3(256), 0, stream, keys, n, vec, part);
+    hipLaunchKernelGGL(k_hist_reduce, dim3(1), dim3(1024), 0, stream, (const uint32_t*)part, hb, hist);
     const int passes = bits == 4 ? 8 : 32;
     const uint32_t* src_k = keys;
     const int32_t* src_p = nullptr;

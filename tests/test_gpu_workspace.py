@@ -28,7 +28,8 @@ def _big_ws(ops, n):
              _lib.workspace_bytes(_lib.OP_RADIX_SORT, n, bits=4),
              _lib.workspace_bytes(_lib.OP_RADIX_SORT, n, bits=1),
              _lib.workspace_bytes(_lib.OP_SCAN_ROWS, rows=16, length=n // 16)]
-    return ops.workspace(_lib.OP_SCAN, torch.device("cuda", 0), (max(sizes) // 8) * 8 * 8)
+    nbytes = (max(sizes) + 15) // 16 * 16
+    return torch.zeros(nbytes, dtype=torch.uint8, device="cuda")  # zero-filled = ready
 
 
 def _run_all(ops, ws, n, seed):
