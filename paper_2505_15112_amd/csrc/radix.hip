@@ -3,17 +3,24 @@
 // least significant one, each step a stable split; Section 6 returns the
 // indices as PyTorch's sort() does).
 //
-//  * One pre-pass reads the keys once and builds the 8 x 16 histogram of all
-//    4-bit digits (per-block partial histograms, then one block adds them).
-//  * 1 bit per pass: 32 split passes (compact.hip's split kernel with the
-//    flag "bit b is 0"), the number of zero bits of pass b read off the
+//  * 1 bit per pass: one pre-pass reads the keys once and builds the 8 x 16
+//    histogram of all 4-bit digits (per-block partial histograms, then one
+//    block adds them); then 32 split passes (compact.hip's split kernel with
+//    the flag "bit b is 0"), the number of zero bits of pass b read off the
 //    histogram, so no pass needs its own counting kernel.
-//  * 4 bits per pass: 8 passes.  A tile ranks its keys per digit with a
-//    wavefront multi-split (one ballot per digit bit; the lanes holding the
-//    same digit are the AND of the matching ballots, the rank is the count of
-//    them below the lane), carries the 16 per-digit counts between tiles with
-//    a 16-chain decoupled look-back, and scatters each key to
-//    (keys with a smaller digit) + (same digit in earlier tiles) + rank.
+//  * 4 bits per pass: 8 passes, each three kernels with no inter-workgroup
+//    waiting: every tile counts its 16 digits (keys read once more), the
+//    digit-major count table (16 x tiles) is turned into output offsets by
+//    one exclusive 1-D scan (scan1d's look-back kernel: the offset of digit d
+//    in tile t is the number of keys with a smaller digit, plus those with
+//    digit d in earlier tiles), and
+//    every tile ranks its keys per digit with a wavefront multi-split (one
+//    ballot per digit bit; the lanes holding the same digit are the AND of
+//    the matching ballots, the rank is the count of them below the lane),
+//    sorts them by digit in LDS and writes each digit's run contiguously.
+//    (A single-pass version carrying the 16 counts by a 16-chain decoupled
+//    look-back measured 2x slower per pass on MI355X: every tile's walk
+//    waited on its predecessors' 16 words.)
 // The two variants give identical output: a stable sort is unique.
 #include "launch.hpp"
 #include "tile.hpp"
@@ -120,101 +127,71 @@ __device__ __forceinline__ uint32_t lane_shfl(uint32_t v, int src_lane) {
     return (uint32_t)__builtin_amdgcn_ds_bpermute(src_lane << 2, (int)v);
 }
 
-// 16-chain look-back by one wavefront.  Lane l watches digit l & 15; in one
-// round it loads the status words of 4 predecessor tiles, at offsets
-// (l >> 4) + 4k for k = 0..3, so a round covers 16 tiles x 16 digits with
-// every load in flight at once.  tot: this tile's count of digit (lane & 15).
-// Returns, in every lane, the count of digit (lane & 15) in all earlier tiles.
-constexpr int kLb16Loads = 4;
-constexpr int kLb16Span = 4 * kLb16Loads;  // tiles per round
-
-__device__ uint32_t lookback16(uint64_t* status, int64_t tile, uint32_t tot, uint32_t epoch,
-                               WsHeader* h) {
+// Per-tile digit counts: counts[d * ntiles + tile] (digit-major, so the
+// spine kernel scans contiguous columns).  Order does not matter here, so the
+// keys are read with 16-byte loads when aligned.
+__global__ __launch_bounds__(kR4Waves* kWave) void k_radix4_count(const uint32_t* keys, int64_t n,
+                                                                  int shift, bool vec,
+                                                                  uint32_t* counts,
+                                                                  uint32_t ntiles) {
+    __shared__ uint32_t s_cnt[kR4Waves][16];
     const int lane = lane_id();
-    const int d = lane & 15, q = lane >> 4;
-    if (tile == 0) {
-        if (q == 0) status_store(status + d, status_word(kStateP, epoch, tot));
-        return 0;
-    }
-    if (q == 0) status_store(status + tile * 16 + d, status_word(kStateA, epoch, tot));
-    uint32_t excl = 0;
-    int64_t end = tile - 1;  // per digit: nearest predecessor tile not summed yet
-    bool done = false;
-    uint32_t spins = 0;
-    while (true) {
-        uint64_t s[kLb16Loads], st[kLb16Loads];
+    const int w = threadIdx.x / kWave;
+    const int64_t tbase = (int64_t)blockIdx.x * kR4Tile;
+    const bool full = tbase + kR4Tile <= n;
+    uint32_t run = 0;  // lane L < 16: this wave's count of digit L
+    auto count64 = [&](uint32_t key, bool ok) {
+        const uint32_t d = (key >> shift) & 15u;
+        const uint64_t valid = __ballot(ok);
+        const uint64_t b0 = __ballot(ok && (d & 1));
+        const uint64_t b1 = __ballot(ok && (d & 2));
+        const uint64_t b2 = __ballot(ok && (d & 4));
+        const uint64_t b3 = __ballot(ok && (d & 8));
+        run += (uint32_t)__builtin_popcountll(digit_lanes((uint32_t)(lane & 15), valid, b0, b1, b2, b3));
+    };
+    if (vec && full) {  // this wave's 1024 keys as 4 x 16-byte loads per lane
+        const u32x4* k4 = reinterpret_cast<const u32x4*>(keys + tbase + (int64_t)w * kR4Chunks * kWave);
+        u32x4 v[kR4Chunks / 4];
 #pragma unroll
-        for (int k = 0; k < kLb16Loads; ++k) {
-            const int64_t t = end - (q + 4 * k);
-            s[k] = 0;
-            st[k] = kStateP;  // tiles before tile 0 read as an empty prefix
-            if (!done && t >= 0) {
-                s[k] = status_load(status + t * 16 + d);
-                st[k] = status_state(s[k], epoch);
-            }
-        }
-        // this digit's states at tile offsets 0..15 (bit o: tile end - o)
-        uint32_t pq = 0, xq = 0;
+        for (int j = 0; j < kR4Chunks / 4; ++j) v[j] = k4[j * kWave + lane];
 #pragma unroll
-        for (int k = 0; k < kLb16Loads; ++k) {
-            const uint64_t P = __ballot(st[k] == kStateP);
-            const uint64_t X = __ballot(st[k] == kStateX);
+        for (int j = 0; j < kR4Chunks / 4; ++j) {
+            count64(v[j].x, true);
+            count64(v[j].y, true);
+            count64(v[j].z, true);
+            count64(v[j].w, true);
+        }
+    } else {
+        const int64_t wbase = tbase + (int64_t)w * kR4Chunks * kWave;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                pq |= (uint32_t)((P >> (d + 16 * r)) & 1) << (r + 4 * k);
-                xq |= (uint32_t)((X >> (d + 16 * r)) & 1) << (r + 4 * k);
-            }
-        }
-        const uint32_t upto = pq ? (((pq & (~pq + 1)) << 1) - 1) : 0xffffu;  // up to nearest P
-        const bool wait = !done && (xq & upto);
-        uint32_t v = 0;
-        if (!done && !wait) {
-#pragma unroll
-            for (int k = 0; k < kLb16Loads; ++k)
-                if ((upto >> (q + 4 * k)) & 1) v += (uint32_t)s[k];
-        }
-        v += lane_shfl(v, lane ^ 16);
-        v += lane_shfl(v, lane ^ 32);
-        if (!done && !wait) {
-            excl += v;
-            end -= kLb16Span;
-            done = pq != 0;
-        }
-        if (__ballot(!done) == 0) break;
-        if (__ballot(wait) != 0) {
-            if (++spins >= kSpinLimit) {
-                if (lane == 0)
-                    __hip_atomic_store(&h->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                break;
-            }
-            __builtin_amdgcn_s_sleep(1);
+        for (int j = 0; j < kR4Chunks; ++j) {
+            const int64_t i = wbase + j * kWave + lane;
+            const bool ok = i < n;
+            count64(ok ? keys[i] : 0u, ok);
         }
     }
-    if (q == 0) status_store(status + tile * 16 + d, status_word(kStateP, epoch, excl + tot));
-    return excl;
+    if (lane < 16) s_cnt[w][lane] = run;
+    __syncthreads();
+    if (threadIdx.x < 16) {
+        uint32_t t = 0;
+#pragma unroll
+        for (int k = 0; k < kR4Waves; ++k) t += s_cnt[k][threadIdx.x];
+        counts[(int64_t)threadIdx.x * ntiles + blockIdx.x] = t;
+    }
 }
 
+// Rank and scatter one tile of 8192 keys (one key per lane per chunk, so the
+// chunk's index order is the lane order) with the offsets from the spine.
 template <bool HAS_PERM_IN, bool WITH_PERM>
-__global__ __launch_bounds__(kR4Waves* kWave) void k_radix4_pass(
+__global__ __launch_bounds__(kR4Waves* kWave) void k_radix4_scatter(
     const uint32_t* keys_in, const int32_t* perm_in, uint32_t* keys_out, int32_t* perm_out,
-    int64_t n, int shift, const uint64_t* hist, WsHeader* hdr, uint64_t* status,
-    int64_t status_words, uint32_t ntiles) {
-    __shared__ Ticket s_ticket;
+    int64_t n, int shift, uint32_t* offsets, uint32_t ntiles) {
     __shared__ uint32_t s_cnt[kR4Waves][16];
     __shared__ uint32_t s_tstart[16];  // first slot of digit d in the tile's digit order
     __shared__ uint32_t s_gbase[16];   // global position of that slot
     __shared__ uint32_t s_stage[kR4Tile];
 
-    if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
-    __syncthreads();
-    const uint32_t tile32 = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.tile);
-    const uint32_t epoch = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.epoch);
-    if (tile32 >= ntiles) {
-        if (threadIdx.x == 0)
-            __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        return;
-    }
-    const int64_t tile = tile32;
+    const int64_t tile = blockIdx.x;
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
     const int64_t tbase = tile * kR4Tile;
@@ -231,11 +208,17 @@ __global__ __launch_bounds__(kR4Waves* kWave) void k_radix4_pass(
         key[j] = ok ? keys_in[i] : 0u;
         if (WITH_PERM) perm[j] = HAS_PERM_IN ? (ok ? perm_in[i] : 0) : (int32_t)i;
     }
+    if (threadIdx.x < 16) {
+        uint32_t* o = offsets + (int64_t)threadIdx.x * ntiles + tile;
+        s_gbase[threadIdx.x] = *o;
+        *o = 0;  // offsets can reach 2^30 and more: leave the workspace word zero
+    }
 
-    // Stable rank of every key among the wave's keys of the same digit, and
-    // the wave's per-digit totals (lane L < 16 holds digit L's running count).
+    // Per-chunk digit counts first (independent), then the stable rank of
+    // each key: its digit's count in the wave's earlier chunks plus the lanes
+    // below it holding the same digit.
+    uint32_t cnt[kR4Chunks];
     uint32_t rank[kR4Chunks];
-    uint32_t run = 0;
 #pragma unroll
     for (int j = 0; j < kR4Chunks; ++j) {
         const int64_t i = wbase + j * kWave + lane;
@@ -246,15 +229,20 @@ __global__ __launch_bounds__(kR4Waves* kWave) void k_radix4_pass(
         const uint64_t b1 = __ballot(ok && (d & 2));
         const uint64_t b2 = __ballot(ok && (d & 4));
         const uint64_t b3 = __ballot(ok && (d & 8));
-        const uint64_t mine = digit_lanes(d, valid_l, b0, b1, b2, b3);
-        rank[j] = lane_shfl(run, (int)d) + lanes_below(mine);
-        run += (uint32_t)__builtin_popcountll(digit_lanes((uint32_t)(lane & 15), valid_l, b0, b1, b2, b3));
+        rank[j] = lanes_below(digit_lanes(d, valid_l, b0, b1, b2, b3));
+        cnt[j] = (uint32_t)__builtin_popcountll(digit_lanes((uint32_t)(lane & 15), valid_l, b0, b1, b2, b3));
+    }
+    uint32_t run = 0;
+#pragma unroll
+    for (int j = 0; j < kR4Chunks; ++j) {
+        const uint32_t d = (key[j] >> shift) & 15u;
+        rank[j] += lane_shfl(run, (int)d);
+        run += cnt[j];
     }
     if (lane < 16) s_cnt[w][lane] = run;
     __syncthreads();
 
-    // lanes 0..15 of every wave: count of digit `lane` in earlier waves, and
-    // the tile total of that digit.
+    // lanes 0..15: count of digit `lane` in earlier waves, and the tile total
     uint32_t wofs = 0, tot = 0;
 #pragma unroll
     for (int k = 0; k < kR4Waves; ++k) {
@@ -263,18 +251,9 @@ __global__ __launch_bounds__(kR4Waves* kWave) void k_radix4_pass(
         tot += c;
     }
     if (w == 0) {
-        const uint32_t before = lookback16(status, tile, tot, epoch, hdr);
-        // keys with a smaller digit over the whole array (exclusive scan of
-        // this digit position's 16 histogram bins) and within the tile
-        const uint32_t h = lane < 16 ? (uint32_t)hist[(shift >> 2) * 16 + lane] : 0u;
         const uint32_t t16 = lane < 16 ? tot : 0u;
-        const uint32_t smaller = wave_incl_scan(h) - h;
         const uint32_t tstart = wave_incl_scan(t16) - t16;
-        if (lane < 16) {
-            s_tstart[lane] = tstart;
-            s_gbase[lane] = smaller + before;
-        }
-        if (lane == 0) finish_epoch(hdr, epoch, ntiles, status, status_words);
+        if (lane < 16) s_tstart[lane] = tstart;
     }
     __syncthreads();
 
@@ -327,13 +306,18 @@ hipError_t launch_radix1_pass(const uint32_t* keys, const int32_t* idx_in, int b
                               uint32_t* keys_out, int32_t* idx_out, int64_t n, const uint64_t* hist,
                               void* ws, size_t ws_bytes, size_t status_offset, hipStream_t stream);
 
-static int64_t radix_status_words(int64_t n, int bits) {
-    return bits == 4 ? r4_tiles(n) * 16 : (n + kR1Tile - 1) / kR1Tile;
+// 1-bit: header | final histogram | one status word per split tile |
+//        per-block histograms.
+// 4-bit: header | the count-table scan's workspace body | count table
+//        (16 x tiles 32-bit counts, 16-byte aligned).
+static int64_t radix1_status_words(int64_t n) { return (n + kR1Tile - 1) / kR1Tile; }
+static size_t radix4_table_offset(int64_t n) {
+    return (scan1d_ws_bytes(r4_tiles(n) * 16) + 15) / 16 * 16;
 }
 
-// header | final histogram | status words | per-block partial histograms
 size_t radix_ws_bytes(int64_t n, int bits) {
-    return kRadixStatusOffset + (size_t)radix_status_words(n, bits) * sizeof(uint64_t) +
+    if (bits == 4) return radix4_table_offset(n) + (size_t)r4_tiles(n) * 16 * sizeof(uint32_t);
+    return kRadixStatusOffset + (size_t)radix1_status_words(n) * sizeof(uint64_t) +
            (size_t)kHistBlocks * kHistWords * sizeof(uint32_t);
 }
 
@@ -341,16 +325,17 @@ hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* 
                              uint32_t* keys_tmp, int32_t* perm_tmp, int64_t n, int bits, void* ws,
                              size_t ws_bytes, hipStream_t stream) {
     if (n == 0) return hipSuccess;
-    WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
-    uint64_t* hist = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
-    uint32_t* part = reinterpret_cast<uint32_t*>(
-        reinterpret_cast<char*>(ws) + kRadixStatusOffset + radix_status_words(n, bits) * sizeof(uint64_t));
-    const int64_t hb64 = (n + 1023) / 1024;
-    const int hb = (int)(hb64 < kHistBlocks ? hb64 : kHistBlocks);
-    const bool vec = ((uintptr_t)keys % 16) == 0;
-    hipLaunchKernelGGL(k_digit_hist, dim3(hb), dim3(256), 0, stream, keys, n, vec, part);
-    hipLaunchKernelGGL(k_hist_reduce, dim3(1), dim3(1024), 0, stream, (const uint32_t*)part, hb, hist);
     const int passes = bits == 4 ? 8 : 32;
+    uint64_t* hist = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
+    if (bits == 1) {
+        uint32_t* part = reinterpret_cast<uint32_t*>(
+            reinterpret_cast<char*>(ws) + kRadixStatusOffset + radix1_status_words(n) * sizeof(uint64_t));
+        const int64_t hb64 = (n + 1023) / 1024;
+        const int hb = (int)(hb64 < kHistBlocks ? hb64 : kHistBlocks);
+        const bool vec = ((uintptr_t)keys % 16) == 0;
+        hipLaunchKernelGGL(k_digit_hist, dim3(hb), dim3(256), 0, stream, keys, n, vec, part);
+        hipLaunchKernelGGL(k_hist_reduce, dim3(1), dim3(1024), 0, stream, (const uint32_t*)part, hb, hist);
+    }
     const uint32_t* src_k = keys;
     const int32_t* src_p = nullptr;
     for (int p = 0; p < passes; ++p) {
@@ -362,13 +347,20 @@ hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* 
             if (e != hipSuccess) return e;
         } else {
             const uint32_t nt = (uint32_t)r4_tiles(n);
-            uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kRadixStatusOffset);
-            const int64_t sw = (int64_t)((ws_bytes - kRadixStatusOffset) / sizeof(uint64_t));
-            auto k = dp ? (src_p ? k_radix4_pass<true, true> : k_radix4_pass<false, true>)
-                        : k_radix4_pass<false, false>;
+            const int64_t ncount = (int64_t)nt * 16;
+            const size_t toff = radix4_table_offset(n);
+            uint32_t* counts = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + toff);
+            const bool vec = ((uintptr_t)src_k % 16) == 0;
+            hipLaunchKernelGGL(k_radix4_count, dim3(nt), dim3(kR4Waves * kWave), 0, stream, src_k, n,
+                               4 * p, vec, counts, nt);
+            hipError_t e = launch_scan1d(Kind::I32, true, counts, counts, ncount, nullptr, nullptr,
+                                         ws, toff, stream);
+            if (e != hipSuccess) return e;
+            auto k = dp ? (src_p ? k_radix4_scatter<true, true> : k_radix4_scatter<false, true>)
+                        : k_radix4_scatter<false, false>;
             hipLaunchKernelGGL(k, dim3(nt), dim3(kR4Waves * kWave), 0, stream, src_k, src_p, dk, dp,
-                               n, 4 * p, (const uint64_t*)hist, hdr, status, sw, nt);
-            const hipError_t e = hipGetLastError();
+                               n, 4 * p, counts, nt);
+            e = hipGetLastError();
             if (e != hipSuccess) return e;
         }
         src_k = dk;

@@ -177,5 +177,5 @@ def test_radix_validation(lib):
     assert fn(None, None, None, None, None, 0, 4, None, 0, None) == _lib.OK
     out = ctypes.c_size_t(0)
     assert lib.libscan_workspace_bytes(_lib.OP_RADIX_SORT, 1 << 26, 0, 0, 4, ctypes.byref(out)) == 0
-    assert out.value >= 256 + 1024 + 16 * 8 * ((1 << 26) // 8192)
+    assert out.value >= 256 + 16 * 4 * ((1 << 26) // 8192)
     assert lib.libscan_workspace_bytes(_lib.OP_RADIX_SORT, 100, 0, 0, 3, ctypes.byref(out)) == _lib.EINVAL
