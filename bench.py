@@ -210,7 +210,7 @@ def main():
             "pct_of_memcpy": round(100.0 * g_f32 / g_cp, 2),
         },
         "roofline": {
-            "kernel": "k_scan_lookback<Tile<u32,u32,4,16,8>> (int32 inclusive, 32768-element "
+            "kernel": "k_scan_lookback<Tile<u32,u32,4,20,8>> (int32 inclusive, 40960-element "
                       "tiles, 16-byte vector path)",
             "bound": "hbm",
             "achieved": round(g_i32, 2),

@@ -48,15 +48,16 @@ constexpr int kPWaves = 8;
 constexpr int kPChunks = 16;
 constexpr int64_t kPTile = kPWaves * kPChunks * kWave * 4;
 
-template <bool VEC, bool WITH_IDX>
-__global__ __launch_bounds__(kPWaves* kWave) void k_compact(
+template <bool VEC, bool WITH_IDX, int WAVES, int CHUNKS>
+__global__ __launch_bounds__(WAVES* kWave) LS_OCCUPANCY4 void k_compact(
     const float* x, const uint8_t* mask, float* out, int32_t* idx, int32_t* count, int64_t n,
     WsHeader* hdr, uint64_t* status, int64_t status_words, uint32_t ntiles) {
+    static_assert(WAVES * CHUNKS * kWave * 4 == kPTile, "one compaction tile size");
     __shared__ Ticket s_ticket;
-    __shared__ uint32_t s_wtot[kPWaves];
+    __shared__ uint32_t s_wtot[WAVES];
     __shared__ uint32_t s_carry;
-    __shared__ float s_val[kPWaves][kWave * 4];
-    __shared__ int32_t s_idx[WITH_IDX ? kPWaves : 1][kWave * 4];
+    __shared__ float s_val[WAVES][kWave * 4];
+    __shared__ int32_t s_idx[WITH_IDX ? WAVES : 1][kWave * 4];
 
     if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
     __syncthreads();
@@ -71,20 +72,21 @@ __global__ __launch_bounds__(kPWaves* kWave) void k_compact(
     const int64_t base = tile * kPTile;
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
-    auto offset = [&](int j) { return base + ((int64_t)(w * kPChunks + j) * kWave + lane) * 4; };
+    auto offset = [&](int j) { return base + ((int64_t)(w * CHUNKS + j) * kWave + lane) * 4; };
 
-    uint32_t kept[kPChunks];
-    float xv[kPChunks][4];
+    uint32_t kept[CHUNKS];
+    float xv[CHUNKS][4];
     if (VEC && base + kPTile <= n) {
+        // All mask loads first: the tile's count (and so its look-back) needs
+        // only them, and the value loads stay in flight meanwhile.
 #pragma unroll
-        for (int j = 0; j < kPChunks; ++j) {
-            const int64_t off = offset(j);
-            kept[j] = nonzero_bytes(*reinterpret_cast<const uint32_t*>(mask + off));
-            load_vec<float, float, 4>(x + off, xv[j]);
-        }
+        for (int j = 0; j < CHUNKS; ++j)
+            kept[j] = nonzero_bytes(*reinterpret_cast<const uint32_t*>(mask + offset(j)));
+#pragma unroll
+        for (int j = 0; j < CHUNKS; ++j) load_vec<float, float, 4>(x + offset(j), xv[j]);
     } else {
 #pragma unroll
-        for (int j = 0; j < kPChunks; ++j) {
+        for (int j = 0; j < CHUNKS; ++j) {
             const int64_t off = offset(j);
             kept[j] = 0;
 #pragma unroll
@@ -98,10 +100,10 @@ __global__ __launch_bounds__(kPWaves* kWave) void k_compact(
         }
     }
     // lane counts -> wavefront scans -> tile total
-    uint32_t lane_off[kPChunks];
+    uint32_t lane_off[CHUNKS];
     uint32_t run = 0;
 #pragma unroll
-    for (int j = 0; j < kPChunks; ++j) {
+    for (int j = 0; j < CHUNKS; ++j) {
         const uint32_t c = (uint32_t)__builtin_popcount(kept[j]);
         const uint32_t inc = wave_incl_scan(c);
         lane_off[j] = run + inc - c;
@@ -111,13 +113,13 @@ __global__ __launch_bounds__(kPWaves* kWave) void k_compact(
     __syncthreads();
     uint32_t wofs = 0, agg = 0;
 #pragma unroll
-    for (int k = 0; k < kPWaves; ++k) {
+    for (int k = 0; k < WAVES; ++k) {
         const uint32_t t = s_wtot[k];
         if (k < w) wofs += t;
         agg += t;
     }
     if (threadIdx.x < kWave) {
-        const uint32_t excl = lookback<uint32_t>(status, tile, 0, agg, 0u, epoch, hdr);
+        const uint32_t excl = lookback<uint32_t>(status, tile32, 0u, agg, 0u, epoch, hdr);
         if (threadIdx.x == 0) {
             s_carry = excl;
             if (tile == ntiles - 1) *count = (int32_t)(excl + agg);
@@ -131,7 +133,7 @@ __global__ __launch_bounds__(kPWaves* kWave) void k_compact(
     float* st = s_val[w];
     int32_t* si = s_idx[WITH_IDX ? w : 0];
 #pragma unroll
-    for (int j = 0; j < kPChunks; ++j) {
+    for (int j = 0; j < CHUNKS; ++j) {
         const int64_t off = offset(j);
         const uint32_t run0 = lane_read(lane_off[j], 0);  // kept before this chunk, in the wave
         uint32_t r = lane_off[j] - run0;
@@ -143,7 +145,7 @@ __global__ __launch_bounds__(kPWaves* kWave) void k_compact(
                 ++r;
             }
         }
-        const uint32_t cnt = (j + 1 < kPChunks ? lane_read(lane_off[j + 1], 0) : run) - run0;
+        const uint32_t cnt = (j + 1 < CHUNKS ? lane_read(lane_off[j + 1], 0) : run) - run0;
         wave_lds_sync();
         const uint32_t dst = c0 + run0;
         for (uint32_t t = lane; t < cnt; t += kWave) {
@@ -222,7 +224,7 @@ constexpr int kSChunks = 8;
 constexpr int64_t kSTile = kSWaves * kSChunks * kWave * 4;
 
 template <bool FROM_BITS, bool VEC, bool HAS_IDX_IN, bool WITH_IDX>
-__global__ __launch_bounds__(kSWaves* kWave) void k_split(
+__global__ __launch_bounds__(kSWaves* kWave) LS_OCCUPANCY4 void k_split(
     const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags, int bit, uint32_t* keys_out,
     int32_t* idx_out, int32_t* n_true_out, int64_t n, WsHeader* hdr, uint64_t* status,
     int64_t status_words, uint32_t ntiles, const uint64_t* hist, const uint64_t* part) {
@@ -257,12 +259,18 @@ __global__ __launch_bounds__(kSWaves* kWave) void k_split(
     uint32_t fl[kSChunks];  // bit 8e: element e is flagged
     const bool full = base + kSTile <= n;
     if (VEC && full) {
+        // Loads in the order the tile's count needs them (flags, or the keys
+        // whose bit is the flag), source indices last.
+        if (!FROM_BITS) {
 #pragma unroll
-        for (int j = 0; j < kSChunks; ++j) {
-            const int64_t off = offset(j);
-            load_vec<uint32_t, uint32_t, 4>(keys + off, k[j]);
-            if (HAS_IDX_IN) load_vec<int32_t, int32_t, 4>(idx_in + off, iv[j]);
-            if (!FROM_BITS) fl[j] = nonzero_bytes(*reinterpret_cast<const uint32_t*>(flags + off));
+            for (int j = 0; j < kSChunks; ++j)
+                fl[j] = nonzero_bytes(*reinterpret_cast<const uint32_t*>(flags + offset(j)));
+        }
+#pragma unroll
+        for (int j = 0; j < kSChunks; ++j) load_vec<uint32_t, uint32_t, 4>(keys + offset(j), k[j]);
+        if (HAS_IDX_IN) {
+#pragma unroll
+            for (int j = 0; j < kSChunks; ++j) load_vec<int32_t, int32_t, 4>(idx_in + offset(j), iv[j]);
         }
     } else {
 #pragma unroll
@@ -307,7 +315,7 @@ __global__ __launch_bounds__(kSWaves* kWave) void k_split(
         agg += t;
     }
     if (threadIdx.x < kWave) {
-        const uint32_t excl = lookback<uint32_t>(status, tile, 0, agg, 0u, epoch, hdr);
+        const uint32_t excl = lookback<uint32_t>(status, tile32, 0u, agg, 0u, epoch, hdr);
         if (threadIdx.x == 0) {
             s_carry = excl;
             if (tile == 0 && n_true_out) *n_true_out = (int32_t)s_ntrue;
@@ -383,10 +391,14 @@ hipError_t launch_compact(const float* x, const uint8_t* mask, float* out, int32
     uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
     const int64_t sw = (int64_t)((ws_bytes - kWsHeader) / sizeof(uint64_t));
     const bool vec = al(x, 16) && al(mask, 4);
-    auto k = vec ? (idx ? k_compact<true, true> : k_compact<true, false>)
-                 : (idx ? k_compact<false, true> : k_compact<false, false>);
-    hipLaunchKernelGGL(k, dim3(nt), dim3(kPWaves * kWave), 0, stream, x, mask, out, idx, count,
-                       n, hdr, status, sw, nt);
+    // Misaligned data is loaded element by element, which needs more
+    // registers per element: the same tile as 16 waves x 8 chunks.
+    auto k = vec ? (idx ? k_compact<true, true, kPWaves, kPChunks> : k_compact<true, false, kPWaves, kPChunks>)
+                 : (idx ? k_compact<false, true, 2 * kPWaves, kPChunks / 2>
+                        : k_compact<false, false, 2 * kPWaves, kPChunks / 2>);
+    const unsigned threads = (vec ? kPWaves : 2 * kPWaves) * kWave;
+    hipLaunchKernelGGL(k, dim3(nt), dim3(threads), 0, stream, x, mask, out, idx, count, n, hdr,
+                       status, sw, nt);
     return hipGetLastError();
 }
 

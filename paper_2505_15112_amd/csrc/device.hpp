@@ -14,6 +14,12 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+// Register budget of the tile kernels: at least 4 waves per SIMD, i.e. at
+// most 128 VGPRs, so two 8-wave (or four 4-wave) workgroups share a CU.  A
+// tile's data lives in registers from its loads to its stores, so this is
+// what bounds the bytes in flight per CU.
+#define LS_OCCUPANCY4 __attribute__((amdgpu_waves_per_eu(4)))
+
 namespace ls {
 
 constexpr int kWave = 64;
@@ -162,7 +168,7 @@ __device__ __forceinline__ void status_store(uint64_t* p, uint64_t v) {
 // ends.  The spin is bounded all the same: after kSpinLimit rounds it raises
 // the workspace error flag and carries on with a wrong value rather than hang.
 template <class T, int K = 1>
-__device__ T lookback(uint64_t* status, int64_t tile, int64_t first, T agg, T base,
+__device__ T lookback(uint64_t* status, uint32_t tile, uint32_t first, T agg, T base,
                       uint32_t epoch, WsHeader* h) {
     const int lane = lane_id();
     if (tile == first) {
@@ -171,19 +177,21 @@ __device__ T lookback(uint64_t* status, int64_t tile, int64_t first, T agg, T ba
     }
     if (lane == 0) status_store(status + tile, status_word(kStateA, epoch, Bits<T>::to(agg)));
     T excl = T(0);
-    int64_t end = tile - 1;  // nearest predecessor not summed yet
+    // Tile indices are below 2^24 (the launchers cap the grid), so 32-bit
+    // signed arithmetic holds them and the walk past `first`.
+    int32_t end = (int32_t)tile - 1;  // nearest predecessor not summed yet
     uint32_t spins = 0;
     while (true) {
         // K windows of 64 predecessors each, all loads in flight at once.
         uint64_t s[K], st[K];
 #pragma unroll
         for (int k = 0; k < K; ++k) {
-            const int64_t idx = end - lane - (int64_t)k * kWave;
+            const int32_t idx = end - lane - k * kWave;
             // Lanes past the segment start read an empty inclusive prefix; the
             // walk never sums them because `first` (always P) comes before them.
             s[k] = 0;
             st[k] = kStateP;
-            if (idx >= first) {
+            if (idx >= (int32_t)first) {
                 s[k] = status_load(status + idx);
                 st[k] = status_state(s[k], epoch);
             }

@@ -130,7 +130,7 @@ __device__ __forceinline__ uint32_t lane_shfl(uint32_t v, int src_lane) {
 // Per-tile digit counts: counts[d * ntiles + tile] (digit-major, so the
 // spine kernel scans contiguous columns).  Order does not matter here, so the
 // keys are read with 16-byte loads when aligned.
-__global__ __launch_bounds__(kR4Waves* kWave) void k_radix4_count(const uint32_t* keys, int64_t n,
+__global__ __launch_bounds__(kR4Waves* kWave) LS_OCCUPANCY4 void k_radix4_count(const uint32_t* keys, int64_t n,
                                                                   int shift, bool vec,
                                                                   uint32_t* counts,
                                                                   uint32_t ntiles) {
@@ -183,7 +183,7 @@ __global__ __launch_bounds__(kR4Waves* kWave) void k_radix4_count(const uint32_t
 // Rank and scatter one tile of 8192 keys (one key per lane per chunk, so the
 // chunk's index order is the lane order) with the offsets from the spine.
 template <bool HAS_PERM_IN, bool WITH_PERM>
-__global__ __launch_bounds__(kR4Waves* kWave) void k_radix4_scatter(
+__global__ __launch_bounds__(kR4Waves* kWave) LS_OCCUPANCY4 void k_radix4_scatter(
     const uint32_t* keys_in, const int32_t* perm_in, uint32_t* keys_out, int32_t* perm_out,
     int64_t n, int shift, uint32_t* offsets, uint32_t ntiles) {
     __shared__ uint32_t s_cnt[kR4Waves][16];

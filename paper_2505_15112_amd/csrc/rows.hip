@@ -38,6 +38,10 @@ static inline int64_t row_tile(int64_t len) {
     return len > 65536 ? 32768 : (len > 16384 ? 8192 : 4096);
 }
 static inline int64_t row_segments(int64_t len) { return (len + row_tile(len) - 1) / row_tile(len); }
+// The same tile for misaligned rows (element-wise loads need more registers
+// per element): twice the waves, half the chunks.
+template <class T, class G, bool VEC>
+using RowTile = Tile<T, T, kRVec, VEC ? G::J : G::J / 2, VEC ? G::W : G::W * 2>;
 static inline bool long_rows(int64_t len) { return len > kRowTile; }
 
 // Wavefront minimum with DPP (lanes outside the row / disabled read INT_MAX).
@@ -59,7 +63,7 @@ __device__ __forceinline__ int32_t wave_min(int32_t v) {
 // ---------------------------------------------------------------- long rows
 
 template <class TileT, bool EXCL, bool VEC>
-__global__ __launch_bounds__(TileT::kThreads) void k_rows_lookback(
+__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_rows_lookback(
     const typename TileT::T* x, typename TileT::T* y, int64_t len, uint32_t segs,
     uint32_t ntiles, WsHeader* hdr, uint64_t* status, int64_t status_words) {
     using T = typename TileT::T;
@@ -77,26 +81,26 @@ __global__ __launch_bounds__(TileT::kThreads) void k_rows_lookback(
         return;
     }
     const int64_t tile = tile32;
-    const int64_t row = tile / segs;
-    const int64_t seg = tile - row * segs;
+    const uint32_t row32 = tile32 / segs;  // 32-bit: no 64-bit division code
+    const int64_t row = row32;
+    const int64_t seg = tile32 - row32 * segs;
     const int64_t base = seg * TileT::kElems;
 
     T v[TileT::J][TileT::V];
-    T lane_off[TileT::J];
     TileT::template load<VEC>(x + row * len, len, base, v);
-    const T wtot = TileT::wave_scan(v, lane_off);
+    const T wtot = TileT::template wave_scan<EXCL>(v);
     T wofs;
     const T agg = TileT::combine_waves(wtot, s_wtot, &wofs);
 
     if (threadIdx.x < kWave) {
-        const T excl = lookback<T>(status, tile, row * (int64_t)segs, agg, T(0), epoch, hdr);
+        const T excl = lookback<T>(status, tile32, row32 * segs, agg, T(0), epoch, hdr);
         if (threadIdx.x == 0) {
             s_carry = excl;
             finish_epoch(hdr, epoch, ntiles, status, status_words);
         }
     }
     __syncthreads();
-    TileT::template store<EXCL, VEC>(y + row * len, len, base, v, lane_off, s_carry + wofs);
+    TileT::template store<VEC>(y + row * len, len, base, v, s_carry + wofs);
 }
 
 // ---------------------------------------------------------------- top-p
@@ -104,7 +108,7 @@ __global__ __launch_bounds__(TileT::kThreads) void k_rows_lookback(
 // Phase 1: the fp32 sum of every tile, stored with its two top bits clear
 // (so the workspace word reads as "nothing published" to any look-back).
 template <class TileT, bool VEC>
-__global__ __launch_bounds__(TileT::kThreads) void k_topp_sums(const float* probs, int64_t len,
+__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp_sums(const float* probs, int64_t len,
                                                                uint32_t segs, uint64_t* partial) {
     __shared__ float s_wtot[TileT::WAVES];
     const int64_t row = blockIdx.x / segs;
@@ -122,7 +126,7 @@ __global__ __launch_bounds__(TileT::kThreads) void k_topp_sums(const float* prob
 // (its last element if rounding kept them all below p), or write len - 1 if
 // no tile reaches p.
 template <class TileT, bool VEC>
-__global__ __launch_bounds__(TileT::kThreads) void k_topp_owner(const float* probs,
+__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp_owner(const float* probs,
                                                                 int32_t* cutoff, int64_t len,
                                                                 uint32_t segs,
                                                                 const uint64_t* partial, float p) {
@@ -161,9 +165,8 @@ __global__ __launch_bounds__(TileT::kThreads) void k_topp_owner(const float* pro
     }
     const int64_t base = seg * TileT::kElems;
     float v[TileT::J][TileT::V];
-    float lane_off[TileT::J];
     TileT::template load<VEC>(probs + row * len, len, base, v);
-    const float wtot = TileT::wave_scan(v, lane_off);
+    const float wtot = TileT::template wave_scan<false>(v);
     float wofs;
     TileT::combine_waves(wtot, s_wtot, &wofs);
     const float c = s_excl + wofs;
@@ -171,10 +174,9 @@ __global__ __launch_bounds__(TileT::kThreads) void k_topp_owner(const float* pro
 #pragma unroll
     for (int j = TileT::J - 1; j >= 0; --j) {
         const int64_t off = TileT::offset(base, j);
-        const float lb = c + lane_off[j];
 #pragma unroll
         for (int e = TileT::V - 1; e >= 0; --e)
-            if (off + e < len && lb + v[j][e] >= p) cand = (int32_t)(off + e);
+            if (off + e < len && c + v[j][e] >= p) cand = (int32_t)(off + e);
     }
     const int32_t wm = wave_min(cand);
     if (lane == 0) s_min[threadIdx.x / kWave] = wm;
@@ -264,30 +266,35 @@ static unsigned wave_grid(int64_t rows) {
 template <class T, class G>
 static void rows_long(bool exclusive, bool vec, const T* x, T* y, int64_t rows, int64_t len,
                       void* ws, size_t ws_bytes, hipStream_t stream) {
-    using TileT = Tile<T, T, kRVec, G::J, G::W>;
-    const uint32_t segs = (uint32_t)((len + TileT::kElems - 1) / TileT::kElems);
+    using TV = RowTile<T, G, true>;
+    using TU = RowTile<T, G, false>;
+    static_assert(TV::kElems == TU::kElems, "one tile size per geometry");
+    const uint32_t segs = (uint32_t)((len + TV::kElems - 1) / TV::kElems);
     const uint32_t nt = (uint32_t)(rows * segs);
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
     uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
     const int64_t status_words = (int64_t)((ws_bytes - kWsHeader) / sizeof(uint64_t));
-    auto k = exclusive ? (vec ? k_rows_lookback<TileT, true, true> : k_rows_lookback<TileT, true, false>)
-                       : (vec ? k_rows_lookback<TileT, false, true> : k_rows_lookback<TileT, false, false>);
-    hipLaunchKernelGGL(k, dim3(nt), dim3(TileT::kThreads), 0, stream, x, y, len, segs, nt, hdr,
-                       status, status_words);
+    auto k = exclusive ? (vec ? k_rows_lookback<TV, true, true> : k_rows_lookback<TU, true, false>)
+                       : (vec ? k_rows_lookback<TV, false, true> : k_rows_lookback<TU, false, false>);
+    const unsigned threads = vec ? TV::kThreads : TU::kThreads;
+    hipLaunchKernelGGL(k, dim3(nt), dim3(threads), 0, stream, x, y, len, segs, nt, hdr, status,
+                       status_words);
 }
 
 template <class G>
 static void topp_long(bool vec, const float* probs, int32_t* cutoff, int64_t rows, int64_t len,
                       float p, void* ws, hipStream_t stream) {
-    using TileT = Tile<float, float, kRVec, G::J, G::W>;
-    const uint32_t segs = (uint32_t)((len + TileT::kElems - 1) / TileT::kElems);
+    using TV = RowTile<float, G, true>;
+    using TU = RowTile<float, G, false>;
+    const uint32_t segs = (uint32_t)((len + TV::kElems - 1) / TV::kElems);
     const uint32_t nt = (uint32_t)(rows * segs);
     uint64_t* partial = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
-    auto ks = vec ? k_topp_sums<TileT, true> : k_topp_sums<TileT, false>;
-    auto ko = vec ? k_topp_owner<TileT, true> : k_topp_owner<TileT, false>;
-    hipLaunchKernelGGL(ks, dim3(nt), dim3(TileT::kThreads), 0, stream, probs, len, segs, partial);
-    hipLaunchKernelGGL(ko, dim3((unsigned)rows), dim3(TileT::kThreads), 0, stream, probs, cutoff,
-                       len, segs, (const uint64_t*)partial, p);
+    auto ks = vec ? k_topp_sums<TV, true> : k_topp_sums<TU, false>;
+    auto ko = vec ? k_topp_owner<TV, true> : k_topp_owner<TU, false>;
+    const unsigned threads = vec ? TV::kThreads : TU::kThreads;
+    hipLaunchKernelGGL(ks, dim3(nt), dim3(threads), 0, stream, probs, len, segs, partial);
+    hipLaunchKernelGGL(ko, dim3((unsigned)rows), dim3(threads), 0, stream, probs, cutoff, len, segs,
+                       (const uint64_t*)partial, p);
 }
 
 template <class T, bool TOPP>

@@ -10,6 +10,8 @@
 // of Algorithm 3): per-tile sums, one workgroup scanning the tile sums, then
 // every tile rescanned with its carry -- 3N transfers, no inter-workgroup
 // waiting at all.
+#include <type_traits>
+
 #include "launch.hpp"
 #include "tile.hpp"
 
@@ -18,11 +20,21 @@ namespace ls {
 // Tile geometries (waves x chunks x 64 lanes x 4 elements).  Every tile costs
 // one ticket and one look-back, so big arrays want big tiles: measured on
 // MI355X at n = 2^28, 4096-element tiles reach half the device memcpy rate
-// and 32768-element tiles match it.  Small arrays want more, smaller tiles
-// to occupy the 256 CUs.
+// and 32768-element tiles match it.  A tile's data stays in registers from
+// its loads until its stores, so the bytes in flight per CU are set by how
+// much of the register file holds data: the large integer tile keeps 80 of
+// at most 128 VGPRs per lane as data (two 8-wave workgroups per CU); the
+// float scans need more scratch registers and keep 64.  Small arrays want
+// more, smaller tiles to occupy the 256 CUs.
 struct GeomSmall { static constexpr int W = 4, J = 4; };   //  4096 elements
 struct GeomMid { static constexpr int W = 4, J = 16; };    // 16384 elements
-struct GeomLarge { static constexpr int W = 8, J = 16; };  // 32768 elements
+template <class T>
+struct GeomLarge {  // 40960 (integer) / 32768 (float) elements
+    static constexpr int W = 8, J = std::is_same<T, float>::value ? 16 : 20;
+};
+// Misaligned data is loaded element by element: more registers per element,
+// so fewer elements per lane.
+struct GeomUnaligned { static constexpr int W = 8, J = 8; };  // 16384 elements
 constexpr int kVec = 4;
 constexpr int64_t kMinTileElems = GeomSmall::W * GeomSmall::J * kWave * kVec;
 constexpr int64_t kRssTileElems = GeomMid::W * GeomMid::J * kWave * kVec;
@@ -38,7 +50,7 @@ __global__ void k_write_total(T* total_out, const T* carry_in) {
 }
 
 template <class TileT, bool EXCL, bool VEC>
-__global__ __launch_bounds__(TileT::kThreads) void k_scan_lookback(
+__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_scan_lookback(
     const typename TileT::In* x, typename TileT::T* y, int64_t n, WsHeader* hdr,
     uint64_t* status, int64_t status_words, uint32_t ntiles, const typename TileT::T* carry_in,
     typename TileT::T* total_out) {
@@ -61,15 +73,14 @@ __global__ __launch_bounds__(TileT::kThreads) void k_scan_lookback(
     const int64_t base = tile * TileT::kElems;
 
     T v[TileT::J][TileT::V];
-    T lane_off[TileT::J];
     TileT::template load<VEC>(x, n, base, v);
-    const T wtot = TileT::wave_scan(v, lane_off);
+    const T wtot = TileT::template wave_scan<EXCL>(v);
     T wofs;
     const T agg = TileT::combine_waves(wtot, s_wtot, &wofs);
 
     if (threadIdx.x < kWave) {
         const T c0 = (tile == 0 && carry_in) ? *carry_in : T(0);
-        const T excl = lookback<T>(status, tile, 0, agg, c0, epoch, hdr);
+        const T excl = lookback<T>(status, tile32, 0u, agg, c0, epoch, hdr);
         if (threadIdx.x == 0) {
             s_carry = excl;
             if (total_out && tile == ntiles - 1) *total_out = excl + agg;
@@ -77,13 +88,13 @@ __global__ __launch_bounds__(TileT::kThreads) void k_scan_lookback(
         }
     }
     __syncthreads();
-    TileT::template store<EXCL, VEC>(y, n, base, v, lane_off, s_carry + wofs);
+    TileT::template store<VEC>(y, n, base, v, s_carry + wofs);
 }
 
 // --- reduce-then-scan
 
 template <class TileT, bool VEC>
-__global__ __launch_bounds__(TileT::kThreads) void k_rss_reduce(const typename TileT::In* x,
+__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_rss_reduce(const typename TileT::In* x,
                                                                 int64_t n,
                                                                 typename TileT::T* partial) {
     using T = typename TileT::T;
@@ -136,7 +147,7 @@ __global__ __launch_bounds__(1024) void k_rss_spine(T* partial, int64_t ntiles) 
 }
 
 template <class TileT, bool VEC>
-__global__ __launch_bounds__(TileT::kThreads) void k_rss_rescan(const typename TileT::In* x,
+__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_rss_rescan(const typename TileT::In* x,
                                                                 typename TileT::T* y, int64_t n,
                                                                 typename TileT::T* partial) {
     using T = typename TileT::T;
@@ -144,15 +155,14 @@ __global__ __launch_bounds__(TileT::kThreads) void k_rss_rescan(const typename T
     const int64_t base = (int64_t)blockIdx.x * TileT::kElems;
     const T carry = partial[blockIdx.x];
     T v[TileT::J][TileT::V];
-    T lane_off[TileT::J];
     TileT::template load<VEC>(x, n, base, v);
-    const T wtot = TileT::wave_scan(v, lane_off);
+    const T wtot = TileT::template wave_scan<false>(v);
     T wofs;
     TileT::combine_waves(wtot, s_wtot, &wofs);  // barrier: every thread has read `carry`
     // Leave the workspace zero where no status word is live, so that any
     // later look-back call can use it without clearing.
     if (threadIdx.x == 0) partial[blockIdx.x] = T(0);
-    TileT::template store<false, VEC>(y, n, base, v, lane_off, carry + wofs);
+    TileT::template store<VEC>(y, n, base, v, carry + wofs);
 }
 
 // ---------------------------------------------------------------- launchers
@@ -167,14 +177,13 @@ size_t scan1d_rss_ws_bytes(int64_t n) {
 
 static bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
-template <class In, class T, class G>
-static void scan1d_geom(bool exclusive, bool vec, const In* x, T* y, int64_t n, const T* carry_in,
+template <class In, class T, class G, bool VEC>
+static void scan1d_geom(bool exclusive, const In* x, T* y, int64_t n, const T* carry_in,
                         T* total_out, WsHeader* hdr, uint64_t* status, int64_t status_words,
                         hipStream_t stream) {
     using TileT = Tile<In, T, kVec, G::J, G::W>;
     const uint32_t nt = (uint32_t)num_tiles(n, TileT::kElems);
-    auto k = exclusive ? (vec ? k_scan_lookback<TileT, true, true> : k_scan_lookback<TileT, true, false>)
-                       : (vec ? k_scan_lookback<TileT, false, true> : k_scan_lookback<TileT, false, false>);
+    auto k = exclusive ? k_scan_lookback<TileT, true, VEC> : k_scan_lookback<TileT, false, VEC>;
     hipLaunchKernelGGL(k, dim3(nt), dim3(TileT::kThreads), 0, stream, x, y, n, hdr, status,
                        status_words, nt, carry_in, total_out);
 }
@@ -189,16 +198,23 @@ static hipError_t scan1d_typed(bool exclusive, const In* x, T* y, int64_t n, con
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
     uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
     const int64_t status_words = (int64_t)((ws_bytes - kWsHeader) / sizeof(uint64_t));
+    // 16-byte vector loads and stores need both arrays 16-byte aligned.
     const bool vec = aligned(x, kVec * sizeof(In)) && aligned(y, kVec * sizeof(T));
-    if (n >= (int64_t(1) << 22))
-        scan1d_geom<In, T, GeomLarge>(exclusive, vec, x, y, n, carry_in, total_out, hdr, status,
-                                      status_words, stream);
+    if (!vec && n >= (int64_t(1) << 18))
+        scan1d_geom<In, T, GeomUnaligned, false>(exclusive, x, y, n, carry_in, total_out, hdr,
+                                                 status, status_words, stream);
+    else if (!vec)
+        scan1d_geom<In, T, GeomSmall, false>(exclusive, x, y, n, carry_in, total_out, hdr, status,
+                                             status_words, stream);
+    else if (n >= (int64_t(1) << 22))
+        scan1d_geom<In, T, GeomLarge<T>, true>(exclusive, x, y, n, carry_in, total_out, hdr,
+                                               status, status_words, stream);
     else if (n >= (int64_t(1) << 18))
-        scan1d_geom<In, T, GeomMid>(exclusive, vec, x, y, n, carry_in, total_out, hdr, status,
-                                    status_words, stream);
+        scan1d_geom<In, T, GeomMid, true>(exclusive, x, y, n, carry_in, total_out, hdr, status,
+                                          status_words, stream);
     else
-        scan1d_geom<In, T, GeomSmall>(exclusive, vec, x, y, n, carry_in, total_out, hdr, status,
-                                      status_words, stream);
+        scan1d_geom<In, T, GeomSmall, true>(exclusive, x, y, n, carry_in, total_out, hdr, status,
+                                            status_words, stream);
     return hipGetLastError();
 }
 
@@ -228,22 +244,23 @@ hipError_t launch_scan1d(Kind kind, bool exclusive, const void* x, void* y, int6
 
 template <class In, class T>
 static hipError_t rss_typed(const In* x, T* y, int64_t n, void* ws, hipStream_t stream) {
-    using TileT = Tile<In, T, kVec, GeomMid::J, GeomMid::W>;
-    static_assert(TileT::kElems == kRssTileElems, "rss tile");
+    using TV = Tile<In, T, kVec, GeomMid::J, GeomMid::W>;
+    using TU = Tile<In, T, kVec, GeomUnaligned::J, GeomUnaligned::W>;  // misaligned data
+    static_assert(TV::kElems == kRssTileElems && TU::kElems == kRssTileElems, "rss tile");
     if (n == 0) return hipSuccess;
-    const int64_t nt = num_tiles(n, TileT::kElems);
+    const int64_t nt = num_tiles(n, kRssTileElems);
     T* partial = reinterpret_cast<T*>(reinterpret_cast<char*>(ws) + kWsHeader);
     const bool vec = aligned(x, kVec * sizeof(In)) && aligned(y, kVec * sizeof(T));
-    const dim3 grid((unsigned)nt), block(TileT::kThreads);
+    const dim3 grid((unsigned)nt), bv(TV::kThreads), bu(TU::kThreads);
     if (vec)
-        hipLaunchKernelGGL((k_rss_reduce<TileT, true>), grid, block, 0, stream, x, n, partial);
+        hipLaunchKernelGGL((k_rss_reduce<TV, true>), grid, bv, 0, stream, x, n, partial);
     else
-        hipLaunchKernelGGL((k_rss_reduce<TileT, false>), grid, block, 0, stream, x, n, partial);
+        hipLaunchKernelGGL((k_rss_reduce<TU, false>), grid, bu, 0, stream, x, n, partial);
     hipLaunchKernelGGL(k_rss_spine<T>, dim3(1), dim3(1024), 0, stream, partial, nt);
     if (vec)
-        hipLaunchKernelGGL((k_rss_rescan<TileT, true>), grid, block, 0, stream, x, y, n, partial);
+        hipLaunchKernelGGL((k_rss_rescan<TV, true>), grid, bv, 0, stream, x, y, n, partial);
     else
-        hipLaunchKernelGGL((k_rss_rescan<TileT, false>), grid, block, 0, stream, x, y, n, partial);
+        hipLaunchKernelGGL((k_rss_rescan<TU, false>), grid, bu, 0, stream, x, y, n, partial);
     return hipGetLastError();
 }
 

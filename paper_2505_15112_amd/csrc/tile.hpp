@@ -85,40 +85,71 @@ struct Tile {
     static constexpr int kThreads = WAVES * kWave;
     static constexpr int kElems = WAVES * J * kWave * V;
 
-    __device__ static int64_t offset(int64_t base, int j) {
-        const int w = threadIdx.x / kWave;
-        return base + ((int64_t)(w * J + j) * kWave + lane_id()) * V;
+    // Offset of the lane's chunk-j elements from the tile base (< kElems, so
+    // 32 bits: with the tile base pointer wave-uniform, loads and stores take
+    // the scalar-base + 32-bit vector-offset form and no 64-bit addresses live
+    // in vector registers).
+    __device__ static uint32_t lane_offset(int j) {
+        const uint32_t w = threadIdx.x / kWave;
+        return ((w * J + (uint32_t)j) * kWave + (uint32_t)lane_id()) * V;
     }
+    __device__ static int64_t offset(int64_t base, int j) { return base + lane_offset(j); }
 
     // Load the tile starting at `base`; elements at or past n read as zero.
     template <bool VEC>
     __device__ static void load(const In* x, int64_t n, int64_t base, T (&v)[J][V]) {
+        const In* xt = x + base;  // wave-uniform
         if (VEC && base + kElems <= n) {  // uniform: all vector loads issued back to back
 #pragma unroll
-            for (int j = 0; j < J; ++j) load_vec<In, T, V>(x + offset(base, j), v[j]);
+            for (int j = 0; j < J; ++j) load_vec<In, T, V>(xt + lane_offset(j), v[j]);
         } else {
+            // Ragged last tile (or unaligned data): per chunk, a lane with all
+            // V elements in range loads them without per-element tests (one
+            // vector load when aligned), a lane straddling the end loads
+            // element by element.  Counts are 32-bit (valid <= kElems).
+            const int32_t valid = (int32_t)(n - base < kElems ? n - base : kElems);
 #pragma unroll
             for (int j = 0; j < J; ++j) {
-                const int64_t off = offset(base, j);
+                const int32_t off = (int32_t)lane_offset(j);
+                const int32_t rem = valid - off;
+                if (rem >= V) {  // one branch per chunk, not one predicate per element
+                    if (VEC) {
+                        load_vec<In, T, V>(xt + off, v[j]);
+                    } else {
 #pragma unroll
-                for (int e = 0; e < V; ++e)
-                    v[j][e] = (off + e < n) ? Conv<In, T>::f(x[off + e]) : T(0);
+                        for (int e = 0; e < V; ++e) v[j][e] = Conv<In, T>::f(xt[off + e]);
+                    }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < V; ++e) v[j][e] = e < rem ? Conv<In, T>::f(xt[off + e]) : T(0);
+                }
             }
         }
     }
 
-    // In-lane inclusive scans and wavefront scans.  Afterwards v[j][e] is the
-    // inclusive prefix of the lane's own elements and lane_off[j] the sum of
-    // everything in the wave before the lane's chunk-j elements.  Returns the
-    // wave's total (uniform).
-    __device__ static T wave_scan(T (&v)[J][V], T (&lane_off)[J]) {
+    // Tile-local scan up to the wave: afterwards v[j][e] is the sum of the
+    // wave's elements before (EXCL) or up to and including (inclusive) that
+    // element, so the only thing left to add is one wave-uniform carry.
+    // Lane-serial scan of the V elements, DPP wavefront scan of the lane
+    // totals per chunk, running total over the J chunks.  Returns the wave's
+    // total (uniform).
+    template <bool EXCL>
+    __device__ static T wave_scan(T (&v)[J][V]) {
         T run = T(0);
 #pragma unroll
         for (int j = 0; j < J; ++j) {
 #pragma unroll
             for (int e = 1; e < V; ++e) v[j][e] = v[j][e - 1] + v[j][e];
             const T inc = wave_incl_scan(v[j][V - 1]);
-            lane_off[j] = run + wave_shr1(inc);
+            const T lb = run + wave_shr1(inc);  // everything in the wave before this lane's chunk-j elements
+            if (EXCL) {
+#pragma unroll
+                for (int e = V - 1; e > 0; --e) v[j][e] = lb + v[j][e - 1];
+                v[j][0] = lb;
+            } else {
+#pragma unroll
+                for (int e = 0; e < V; ++e) v[j][e] = lb + v[j][e];
+            }
             run = run + lane_read(inc, kWave - 1);
         }
         return run;
@@ -151,24 +182,39 @@ struct Tile {
         return agg;
     }
 
-    // Store carry + scanned values (inclusive or exclusive); only i < n.
-    template <bool EXCL, bool VEC>
-    __device__ static void store(T* y, int64_t n, int64_t base, const T (&v)[J][V],
-                                 const T (&lane_off)[J], T carry) {
-        const bool full = VEC && base + kElems <= n;
+    // Store carry + v (v from wave_scan; carry uniform per wave); only i < n.
+    template <bool VEC>
+    __device__ static void store(T* y, int64_t n, int64_t base, const T (&v)[J][V], T carry) {
+        T* yt = y + base;  // wave-uniform
+        if (VEC && base + kElems <= n) {
 #pragma unroll
-        for (int j = 0; j < J; ++j) {
-            const int64_t off = offset(base, j);
-            const T lb = carry + lane_off[j];
-            T o[V];
+            for (int j = 0; j < J; ++j) {
+                T o[V];
 #pragma unroll
-            for (int e = 0; e < V; ++e) o[e] = EXCL ? (e == 0 ? lb : lb + v[j][e - 1]) : lb + v[j][e];
-            if (full) {
-                store_vec<T, V>(y + off, o);
-            } else {
+                for (int e = 0; e < V; ++e) o[e] = carry + v[j][e];
+                store_vec<T, V>(yt + lane_offset(j), o);
+            }
+        } else {
+            const int32_t valid = (int32_t)(n - base < kElems ? n - base : kElems);
 #pragma unroll
-                for (int e = 0; e < V; ++e)
-                    if (off + e < n) y[off + e] = o[e];
+            for (int j = 0; j < J; ++j) {
+                const int32_t off = (int32_t)lane_offset(j);
+                const int32_t rem = valid - off;
+                T o[V];
+#pragma unroll
+                for (int e = 0; e < V; ++e) o[e] = carry + v[j][e];
+                if (rem >= V) {
+                    if (VEC) {
+                        store_vec<T, V>(yt + off, o);
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < V; ++e) yt[off + e] = o[e];
+                    }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < V; ++e)
+                        if (e < rem) yt[off + e] = o[e];
+                }
             }
         }
     }

@@ -148,6 +148,47 @@ def test_rss_matches_lookback(ops, n):
     assert_float_close(yf, ref, ab, "rss f32")
 
 
+@pytest.mark.parametrize("kind", ["i32", "f32", "f16", "u8"])
+@pytest.mark.parametrize("excl", [False, True])
+@pytest.mark.parametrize("shift", [0, 1])
+def test_large_tiles_ragged(ops, kind, excl, shift):
+    """Large-tile schedule (n >= 2^22) with a ragged last tile whose end falls
+    inside a lane's 4 elements; shift = 1 runs it on views one element off
+    16-byte alignment (the element-wise load/store path)."""
+    import torch
+    n = (1 << 22) + 3 * 40960 + 12345
+    announce("large ragged", kind, excl, shift)
+    if kind == "i32":
+        x = W.scan_i32_full_range(n + shift, seed=21)
+        xd = to_dev(x)[shift:]
+        fn = ops.scan_exclusive_i32 if excl else ops.scan_inclusive_i32
+        y = torch.empty(n + shift, dtype=torch.int32, device="cuda")
+        fn(xd, out=y[shift:])
+        assert_equal_first_diff(to_host(y[shift:]), oracle.scan_i32(x[shift:], exclusive=excl), "i32")
+    elif kind == "f32":
+        x = W.scan_f32(n + shift, seed=22)
+        fn = ops.scan_exclusive_f32 if excl else ops.scan_inclusive_f32
+        y = torch.empty(n + shift, dtype=torch.float32, device="cuda")
+        fn(to_dev(x)[shift:], out=y[shift:])
+        ref, a = oracle.scan_f32(x[shift:], exclusive=excl)
+        assert_float_close(to_host(y[shift:]), ref, a, "f32")
+    elif kind == "f16":
+        x = W.exact_pm1(n + shift, seed=23, dtype=np.float16)
+        fn = ops.scan_exclusive_f16f32 if excl else ops.scan_inclusive_f16f32
+        y = torch.empty(n + shift, dtype=torch.float32, device="cuda")
+        fn(to_dev(x)[shift:], out=y[shift:])
+        assert_equal_first_diff(to_host(y[shift:]).astype(np.float64),
+                                oracle.scan_f16(x[shift:], exclusive=excl)[0], "f16 exact")
+    else:
+        if not excl:
+            pytest.skip("the byte scan is exclusive only")
+        x = W.bytes_u8(n + shift, seed=24)
+        y, total = ops.scan_exclusive_u8i32(to_dev(x)[shift:])
+        ref, rtot = oracle.scan_u8(x[shift:])
+        assert_equal_first_diff(to_host(y), ref, "u8")
+        assert int(to_host(total)[0]) == rtot
+
+
 def test_repeat_no_race(ops):
     """The same input 100 times: the look-back must give one result every time."""
     import torch
