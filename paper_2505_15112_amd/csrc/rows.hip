@@ -11,13 +11,14 @@
 //    out row-major by ticket, and the decoupled look-back runs inside a row
 //    (it stops at the row's first segment), so 128 rows of 2^17 still give
 //    4096 workgroups to fill 256 CUs.
-// The top-p cutoff needs only one index per row, so it does not use the
-// look-back: a first kernel sums every tile of every row (reading all the
-// probabilities once, no inter-workgroup waiting), and a second kernel, one
-// workgroup per row, scans the row's tile sums to find the first tile whose
-// inclusive sum reaches p and re-reads only that tile to locate the index
-// (the two phases of the paper's Algorithm 3, MCScan, with the down-sweep cut
-// to the one tile that matters).
+// The top-p cutoff needs only one index per row.  Rows of up to 64 tiles take
+// one pass: every tile publishes its sum, adds the sums of the row's earlier
+// tiles in a fixed order, and the tile whose range holds the crossing finds
+// the index in the probabilities it already holds (k_topp_onepass).  Longer
+// rows take two phases (the two phases of the paper's Algorithm 3, MCScan,
+// with the down-sweep cut to the one tile that matters): a first kernel sums
+// every tile, a second, one workgroup per row, finds the first tile whose
+// inclusive sum reaches p and re-reads only that tile.
 #include <limits.h>
 
 #include "launch.hpp"
@@ -189,6 +190,102 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp_owner(co
     }
 }
 
+// One pass for rows of at most kToppMaxSegs tiles.  Every tile publishes its
+// sum (state A, epoch-tagged) as soon as it has loaded, waits only for the
+// sums of the row's earlier tiles, and adds them left to right in fp32.  All
+// tiles of a row add the same numbers in the same order, so the boundary sum
+// S_{k-1} that tile k compares with p is bit for bit the S_{k-1} that tile
+// k-1 compared, and for non-negative probabilities S is non-decreasing: the
+// one tile with S_{k-1} < p <= S_k (or the row's last tile, if p is never
+// reached) owns the cutoff and finds it in the data it already holds -- no
+// tile is read twice and no workgroup waits for another one's decision.
+constexpr uint32_t kToppMaxSegs = kWave;
+
+template <class TileT, bool VEC>
+__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp_onepass(
+    const float* probs, int32_t* cutoff, int64_t len, uint32_t segs, uint32_t ntiles, float p,
+    WsHeader* hdr, uint64_t* status, int64_t status_words) {
+    __shared__ Ticket s_ticket;
+    __shared__ float s_wtot[TileT::WAVES];
+    __shared__ float s_excl;
+    __shared__ uint32_t s_own;
+    __shared__ int32_t s_min[TileT::WAVES];
+
+    if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
+    __syncthreads();
+    const uint32_t tile32 = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.tile);
+    const uint32_t epoch = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.epoch);
+    if (tile32 >= ntiles) {  // only with a workspace that was never zero-filled
+        if (threadIdx.x == 0)
+            __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
+    const uint32_t row32 = tile32 / segs;
+    const uint32_t seg = tile32 - row32 * segs;
+    const int64_t row = row32;
+    const int64_t base = (int64_t)seg * TileT::kElems;
+
+    float v[TileT::J][TileT::V];
+    TileT::template load<VEC>(probs + row * len, len, base, v);
+    const float wtot = TileT::template wave_scan<false>(v);
+    float wofs;
+    const float agg = TileT::combine_waves(wtot, s_wtot, &wofs);
+
+    if (threadIdx.x < kWave) {
+        const int lane = lane_id();
+        const uint32_t first = row32 * segs;
+        if (lane == 0) status_store(status + tile32, status_word(kStateA, epoch, Bits<float>::to(agg)));
+        // The sums of tiles first .. tile-1 (seg < kToppMaxSegs, one per lane).
+        uint32_t bits = 0;
+        for (uint32_t spins = 0;; ++spins) {
+            uint64_t w = 0;
+            bool ready = true;
+            if ((uint32_t)lane < seg) {
+                w = status_load(status + first + lane);
+                ready = status_state(w, epoch) != kStateX;
+            }
+            if (__ballot(!ready) == 0) {
+                bits = (uint32_t)w;
+                break;
+            }
+            if (spins >= kSpinLimit) {
+                if (lane == 0)
+                    __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        float sum = 0.f;  // left to right, the same on every tile of the row
+        for (uint32_t l = 0; l < seg; ++l) sum = sum + Bits<float>::from(lane_read(bits, (int)l));
+        if (lane == 0) {
+            const float incl = sum + agg;
+            s_excl = sum;
+            s_own = (seg == 0 || !(sum >= p)) && (seg == segs - 1 || incl >= p);
+            finish_epoch(hdr, epoch, ntiles, status, status_words);
+        }
+    }
+    __syncthreads();
+    if (!s_own) return;  // uniform over the workgroup
+    const float c = s_excl + wofs;
+    int32_t cand = INT_MAX;
+#pragma unroll
+    for (int j = TileT::J - 1; j >= 0; --j) {
+        const int64_t off = TileT::offset(base, j);
+#pragma unroll
+        for (int e = TileT::V - 1; e >= 0; --e)
+            if (off + e < len && c + v[j][e] >= p) cand = (int32_t)(off + e);
+    }
+    const int32_t wm = wave_min(cand);
+    if (lane_id() == 0) s_min[threadIdx.x / kWave] = wm;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int32_t m = INT_MAX;
+        for (int k = 0; k < TileT::WAVES; ++k) m = s_min[k] < m ? s_min[k] : m;
+        const int64_t last = (base + TileT::kElems < len ? base + TileT::kElems : len) - 1;
+        cutoff[row] = m != INT_MAX ? m : (int32_t)last;  // rounding kept every prefix below p
+    }
+}
+
 __global__ void k_fill_i32(int32_t* p, int64_t count, int32_t value) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) p[i] = value;
@@ -283,15 +380,24 @@ static void rows_long(bool exclusive, bool vec, const T* x, T* y, int64_t rows, 
 
 template <class G>
 static void topp_long(bool vec, const float* probs, int32_t* cutoff, int64_t rows, int64_t len,
-                      float p, void* ws, hipStream_t stream) {
+                      float p, void* ws, size_t ws_bytes, hipStream_t stream) {
     using TV = RowTile<float, G, true>;
     using TU = RowTile<float, G, false>;
     const uint32_t segs = (uint32_t)((len + TV::kElems - 1) / TV::kElems);
     const uint32_t nt = (uint32_t)(rows * segs);
+    const unsigned threads = vec ? TV::kThreads : TU::kThreads;
+    if (segs <= kToppMaxSegs) {
+        WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
+        uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
+        const int64_t status_words = (int64_t)((ws_bytes - kWsHeader) / sizeof(uint64_t));
+        auto k = vec ? k_topp_onepass<TV, true> : k_topp_onepass<TU, false>;
+        hipLaunchKernelGGL(k, dim3(nt), dim3(threads), 0, stream, probs, cutoff, len, segs, nt, p,
+                           hdr, status, status_words);
+        return;
+    }
     uint64_t* partial = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
     auto ks = vec ? k_topp_sums<TV, true> : k_topp_sums<TU, false>;
     auto ko = vec ? k_topp_owner<TV, true> : k_topp_owner<TU, false>;
-    const unsigned threads = vec ? TV::kThreads : TU::kThreads;
     hipLaunchKernelGGL(ks, dim3(nt), dim3(threads), 0, stream, probs, len, segs, partial);
     hipLaunchKernelGGL(ko, dim3((unsigned)rows), dim3(threads), 0, stream, probs, cutoff, len, segs,
                        (const uint64_t*)partial, p);
@@ -317,9 +423,9 @@ static hipError_t rows_typed(bool exclusive, const T* x, T* y, int64_t rows, int
     }
     const int64_t t = row_tile(len);
     if constexpr (TOPP) {
-        if (t == 32768) topp_long<RGeomL>(vec, x, cutoff, rows, len, p, ws, stream);
-        else if (t == 8192) topp_long<RGeomM>(vec, x, cutoff, rows, len, p, ws, stream);
-        else topp_long<RGeomS>(vec, x, cutoff, rows, len, p, ws, stream);
+        if (t == 32768) topp_long<RGeomL>(vec, x, cutoff, rows, len, p, ws, ws_bytes, stream);
+        else if (t == 8192) topp_long<RGeomM>(vec, x, cutoff, rows, len, p, ws, ws_bytes, stream);
+        else topp_long<RGeomS>(vec, x, cutoff, rows, len, p, ws, ws_bytes, stream);
     } else {
         if (t == 32768) rows_long<T, RGeomL>(exclusive, vec, x, y, rows, len, ws, ws_bytes, stream);
         else if (t == 8192) rows_long<T, RGeomM>(exclusive, vec, x, y, rows, len, ws, ws_bytes, stream);

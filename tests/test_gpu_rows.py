@@ -80,6 +80,27 @@ def test_topp_shapes(ops, length, p):
     _check_topp(ops, probs, p, f"topp len={length} p={p}")
 
 
+@pytest.mark.parametrize("length", [64 * 32768, 64 * 32768 + 1, 65 * 32768 + 7])
+@pytest.mark.parametrize("p", [0.5, 0.9, 1.5])
+def test_topp_one_pass_limit(ops, length, p):
+    """Rows of exactly 64 tiles (the last one-pass shape) and longer rows (the
+    two-phase schedule)."""
+    announce("topp long rows", length, p)
+    probs = W.topp_probs(2, length, seed=length % 1000)
+    _check_topp(ops, probs, p, f"topp len={length} p={p}")
+
+
+def test_topp_misaligned_view(ops):
+    announce("topp misaligned")
+    probs = W.topp_probs(3, 131_072 + 1, seed=5)
+    d = to_dev(probs.reshape(-1))[1:1 + 3 * 131_072].reshape(3, 131_072)
+    g = to_host(ops.topp_cutoff_f32(d, 0.9))
+    host = probs.reshape(-1)[1:1 + 3 * 131_072].reshape(3, 131_072)
+    k = oracle.topp_cutoff_f32(host, 0.9)
+    csum, _ = oracle.scan_rows_f32(host)
+    assert all(topp_accept(int(g[r]), int(k[r]), csum[r], 0.9) for r in range(3)), (g, k)
+
+
 @pytest.mark.parametrize("m", [2, 7, 12, 13, 17])
 def test_topp_dyadic_exact(ops, m):
     """2^m equal probabilities 2^-m: every fp32 running sum is exact."""
