@@ -12,7 +12,8 @@ The same run measures every other operation of the library on its workload
 fp16->fp32 scan (n = 2^24), the latency-bound int32 scan (n = 2^16), mask
 compaction (n = 2^28), batched rows and the top-p cutoff (128 x 131072),
 stable split and both radix sorts (n = 2^26).  Workloads that fit in the
-256 MB Infinity Cache are timed one call at a time after a 512 MiB flush.
+256 MB Infinity Cache are timed cold: rounds of (512 MiB overwrite, call)
+enqueued back to back, minus the overwrites alone.
 The CPU-baseline leg times the serial oracle on each workload (or a stated
 sample) and checks the GPU outputs against it.
 
@@ -81,23 +82,37 @@ class Timer:
         torch.cuda.synchronize()
         return a.elapsed_time(b) / steps  # ms per call
 
-    def flushed(self, fn, steps, warmup):
-        """Each call timed alone after overwriting 512 MiB (evicts L2 and MALL)."""
+    def flushed(self, fn, steps, warmup, reps=3):
+        """Cost of one call on data that is not in any cache: `steps` rounds of
+        (overwrite 512 MiB, which evicts L2 and MALL; call) enqueued back to
+        back, minus the same number of overwrites alone, per call; median of
+        `reps`.  Timing each call alone between two events would add the
+        event-to-kernel launch latency (about 6 us on MI355X) to every call."""
         torch = self.torch
+        flush = self.flush_buf.zero_
         for _ in range(warmup):
+            flush()
             fn()
         torch.cuda.synchronize()
-        evs = []
-        for _ in range(steps):
-            self.flush_buf.zero_()
+
+        def timed(body):
             a = torch.cuda.Event(enable_timing=True)
             b = torch.cuda.Event(enable_timing=True)
             a.record(self.stream)
-            fn()
+            for _ in range(steps):
+                body()
             b.record(self.stream)
-            evs.append((a, b))
-        torch.cuda.synchronize()
-        return sum(a.elapsed_time(b) for a, b in evs) / steps
+            torch.cuda.synchronize()
+            return a.elapsed_time(b)
+
+        def both():
+            flush()
+            fn()
+
+        out = []
+        for _ in range(reps):
+            out.append((timed(both) - timed(flush)) / steps)
+        return sorted(out)[len(out) // 2]
 
 
 def entry(name, ms, nbytes, memcpy_ms, unit_note, extra=None):

@@ -223,7 +223,7 @@ constexpr int kSWaves = 8;
 constexpr int kSChunks = 8;
 constexpr int64_t kSTile = kSWaves * kSChunks * kWave * 4;
 
-template <bool FROM_BITS, bool VEC, bool HAS_IDX_IN, bool WITH_IDX>
+template <bool FROM_BITS, bool VEC, bool HAS_IDX_IN, bool WITH_IDX, int CHUNKS>
 __global__ __launch_bounds__(kSWaves* kWave) LS_OCCUPANCY4 void k_split(
     const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags, int bit, uint32_t* keys_out,
     int32_t* idx_out, int32_t* n_true_out, int64_t n, WsHeader* hdr, uint64_t* status,
@@ -245,36 +245,37 @@ __global__ __launch_bounds__(kSWaves* kWave) LS_OCCUPANCY4 void k_split(
         return;
     }
     const int64_t tile = tile32;
-    const int64_t base = tile * kSTile;
+    constexpr int64_t kTile = (int64_t)kSWaves * CHUNKS * kWave * 4;
+    const int64_t base = tile * kTile;
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
-    auto offset = [&](int j) { return base + ((int64_t)(w * kSChunks + j) * kWave + lane) * 4; };
+    auto offset = [&](int j) { return base + ((int64_t)(w * CHUNKS + j) * kWave + lane) * 4; };
     if (threadIdx.x < kWave) {
         const uint32_t nt = hist ? zeros_of_bit(hist, bit) : sum_partials(part);
         if (threadIdx.x == 0) s_ntrue = nt;
     }
 
-    uint32_t k[kSChunks][4];
-    int32_t iv[kSChunks][4];
-    uint32_t fl[kSChunks];  // bit 8e: element e is flagged
-    const bool full = base + kSTile <= n;
+    uint32_t k[CHUNKS][4];
+    int32_t iv[CHUNKS][4];
+    uint32_t fl[CHUNKS];  // bit 8e: element e is flagged
+    const bool full = base + kTile <= n;
     if (VEC && full) {
         // Loads in the order the tile's count needs them (flags, or the keys
         // whose bit is the flag), source indices last.
         if (!FROM_BITS) {
 #pragma unroll
-            for (int j = 0; j < kSChunks; ++j)
+            for (int j = 0; j < CHUNKS; ++j)
                 fl[j] = nonzero_bytes(*reinterpret_cast<const uint32_t*>(flags + offset(j)));
         }
 #pragma unroll
-        for (int j = 0; j < kSChunks; ++j) load_vec<uint32_t, uint32_t, 4>(keys + offset(j), k[j]);
+        for (int j = 0; j < CHUNKS; ++j) load_vec<uint32_t, uint32_t, 4>(keys + offset(j), k[j]);
         if (HAS_IDX_IN) {
 #pragma unroll
-            for (int j = 0; j < kSChunks; ++j) load_vec<int32_t, int32_t, 4>(idx_in + offset(j), iv[j]);
+            for (int j = 0; j < CHUNKS; ++j) load_vec<int32_t, int32_t, 4>(idx_in + offset(j), iv[j]);
         }
     } else {
 #pragma unroll
-        for (int j = 0; j < kSChunks; ++j) {
+        for (int j = 0; j < CHUNKS; ++j) {
             const int64_t off = offset(j);
             fl[j] = 0;
 #pragma unroll
@@ -288,7 +289,7 @@ __global__ __launch_bounds__(kSWaves* kWave) LS_OCCUPANCY4 void k_split(
     }
     if (FROM_BITS) {
 #pragma unroll
-        for (int j = 0; j < kSChunks; ++j) {
+        for (int j = 0; j < CHUNKS; ++j) {
             const int64_t off = offset(j);
             fl[j] = 0;
 #pragma unroll
@@ -296,10 +297,10 @@ __global__ __launch_bounds__(kSWaves* kWave) LS_OCCUPANCY4 void k_split(
                 if (full || off + e < n) fl[j] |= (((k[j][e] >> bit) & 1u) ^ 1u) << (8 * e);
         }
     }
-    uint32_t lane_off[kSChunks];
+    uint32_t lane_off[CHUNKS];
     uint32_t run = 0;
 #pragma unroll
-    for (int j = 0; j < kSChunks; ++j) {
+    for (int j = 0; j < CHUNKS; ++j) {
         const uint32_t c = (uint32_t)__builtin_popcount(fl[j]);  // (split: s_ntrue set before the barrier below)
         const uint32_t inc = wave_incl_scan(c);
         lane_off[j] = run + inc - c;
@@ -331,11 +332,11 @@ __global__ __launch_bounds__(kSWaves* kWave) LS_OCCUPANCY4 void k_split(
     uint32_t* sk = s_key[w];
     int32_t* si = s_idx[WITH_IDX ? w : 0];
 #pragma unroll
-    for (int j = 0; j < kSChunks; ++j) {
+    for (int j = 0; j < CHUNKS; ++j) {
         const int64_t off = offset(j);
-        const int64_t g0 = base + (int64_t)(w * kSChunks + j) * kWave * 4;  // chunk start
+        const int64_t g0 = base + (int64_t)(w * CHUNKS + j) * kWave * 4;  // chunk start
         const uint32_t run0 = lane_read(lane_off[j], 0);
-        const uint32_t cnt = (j + 1 < kSChunks ? lane_read(lane_off[j + 1], 0) : run) - run0;
+        const uint32_t cnt = (j + 1 < CHUNKS ? lane_read(lane_off[j + 1], 0) : run) - run0;
         const int64_t valid64 = n - g0 < kWave * 4 ? n - g0 : kWave * 4;
         const uint32_t valid = valid64 > 0 ? (uint32_t)valid64 : 0u;
         uint32_t r = lane_off[j] - run0;  // flagged before this element, in the chunk
@@ -402,18 +403,35 @@ hipError_t launch_compact(const float* x, const uint8_t* mask, float* out, int32
     return hipGetLastError();
 }
 
-template <bool VEC>
-static void launch_split_typed(const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags,
-                               uint32_t* keys_out, int32_t* idx_out, int32_t* n_true_out,
-                               int64_t n, WsHeader* hdr, uint64_t* status, int64_t sw,
-                               uint32_t nt, uint64_t* part, hipStream_t stream) {
-    hipLaunchKernelGGL(k_count_flags, dim3(kCountBlocks), dim3(1024), 0, stream, flags, n,
-                       ((uintptr_t)flags % 16) == 0, part);
-    auto k = idx_in ? (idx_out ? k_split<false, VEC, true, true> : k_split<false, VEC, true, false>)
-                    : (idx_out ? k_split<false, VEC, false, true> : k_split<false, VEC, false, false>);
-    hipLaunchKernelGGL(k, dim3(nt), dim3(kSWaves * kWave), 0, stream, keys, idx_in, flags, 0,
-                       keys_out, idx_out, n_true_out, n, hdr, status, sw, nt, (const uint64_t*)nullptr,
-                       (const uint64_t*)part);
+// Tiles of kSWaves x CHUNKS x 64 x 4 elements.  With aligned data, flags from
+// a mask and no input indices a lane holds 4 keys and a packed flag word per
+// chunk, so 16 chunks fit the register budget (32768-element tiles); the
+// other forms need more registers per element and take 8 (16384).
+template <bool FROM_BITS, bool VEC, bool HAS_IDX_IN>
+static void split_launch(const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags, int bit,
+                         uint32_t* keys_out, int32_t* idx_out, int32_t* n_true_out, int64_t n,
+                         WsHeader* hdr, uint64_t* status, int64_t sw, const uint64_t* hist,
+                         const uint64_t* part, hipStream_t stream) {
+    constexpr int CHUNKS = (VEC && !HAS_IDX_IN && !FROM_BITS) ? 2 * kSChunks : kSChunks;
+    constexpr int64_t tile = (int64_t)kSWaves * CHUNKS * kWave * 4;
+    const uint32_t nt = (uint32_t)((n + tile - 1) / tile);
+    auto k = idx_out ? k_split<FROM_BITS, VEC, HAS_IDX_IN, true, CHUNKS>
+                     : k_split<FROM_BITS, VEC, HAS_IDX_IN, false, CHUNKS>;
+    hipLaunchKernelGGL(k, dim3(nt), dim3(kSWaves * kWave), 0, stream, keys, idx_in, flags, bit,
+                       keys_out, idx_out, n_true_out, n, hdr, status, sw, nt, hist, part);
+}
+
+template <bool FROM_BITS, bool VEC>
+static void split_launch_any(const uint32_t* keys, const int32_t* idx_in, const uint8_t* flags,
+                             int bit, uint32_t* keys_out, int32_t* idx_out, int32_t* n_true_out,
+                             int64_t n, WsHeader* hdr, uint64_t* status, int64_t sw,
+                             const uint64_t* hist, const uint64_t* part, hipStream_t stream) {
+    if (idx_in)
+        split_launch<FROM_BITS, VEC, true>(keys, idx_in, flags, bit, keys_out, idx_out, n_true_out,
+                                           n, hdr, status, sw, hist, part, stream);
+    else
+        split_launch<FROM_BITS, VEC, false>(keys, idx_in, flags, bit, keys_out, idx_out, n_true_out,
+                                            n, hdr, status, sw, hist, part, stream);
 }
 
 // One LSB radix-sort pass on key bit `bit` (flag = bit is 0), with the count
@@ -421,18 +439,16 @@ static void launch_split_typed(const uint32_t* keys, const int32_t* idx_in, cons
 hipError_t launch_radix1_pass(const uint32_t* keys, const int32_t* idx_in, int bit,
                               uint32_t* keys_out, int32_t* idx_out, int64_t n, const uint64_t* hist,
                               void* ws, size_t ws_bytes, size_t status_offset, hipStream_t stream) {
-    const uint32_t nt = (uint32_t)s_tiles(n);
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
     uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + status_offset);
     const int64_t sw = (int64_t)((ws_bytes - status_offset) / sizeof(uint64_t));
     const bool vec = al(keys, 16) && (!idx_in || al(idx_in, 16));
-    auto k = vec ? (idx_in ? (idx_out ? k_split<true, true, true, true> : k_split<true, true, true, false>)
-                           : (idx_out ? k_split<true, true, false, true> : k_split<true, true, false, false>))
-                 : (idx_in ? (idx_out ? k_split<true, false, true, true> : k_split<true, false, true, false>)
-                           : (idx_out ? k_split<true, false, false, true> : k_split<true, false, false, false>));
-    hipLaunchKernelGGL(k, dim3(nt), dim3(kSWaves * kWave), 0, stream, keys, idx_in,
-                       (const uint8_t*)nullptr, bit, keys_out, idx_out, (int32_t*)nullptr, n, hdr,
-                       status, sw, nt, hist, (const uint64_t*)nullptr);
+    if (vec)
+        split_launch_any<true, true>(keys, idx_in, nullptr, bit, keys_out, idx_out, nullptr, n, hdr,
+                                     status, sw, hist, nullptr, stream);
+    else
+        split_launch_any<true, false>(keys, idx_in, nullptr, bit, keys_out, idx_out, nullptr, n,
+                                      hdr, status, sw, hist, nullptr, stream);
     return hipGetLastError();
 }
 
@@ -444,20 +460,21 @@ hipError_t launch_split(const uint32_t* keys, const int32_t* idx_in, const uint8
         if (n_true_out) hipLaunchKernelGGL(k_zero_count, dim3(1), dim3(64), 0, stream, n_true_out);
         return hipGetLastError();
     }
-    const uint32_t nt = (uint32_t)s_tiles(n);
     WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
     uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
     // (the epoch-wrap clear may zero the partial counts too: they are read
     // before any workgroup finishes)
     const int64_t sw = (int64_t)((ws_bytes - kWsHeader) / sizeof(uint64_t));
     uint64_t* part = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + split_part_offset(n));
+    hipLaunchKernelGGL(k_count_flags, dim3(kCountBlocks), dim3(1024), 0, stream, flags, n,
+                       ((uintptr_t)flags % 16) == 0, part);
     const bool vec = al(keys, 16) && (!idx_in || al(idx_in, 16)) && al(flags, 4);
     if (vec)
-        launch_split_typed<true>(keys, idx_in, flags, keys_out, idx_out, n_true_out, n, hdr, status,
-                                 sw, nt, part, stream);
+        split_launch_any<false, true>(keys, idx_in, flags, 0, keys_out, idx_out, n_true_out, n, hdr,
+                                      status, sw, nullptr, part, stream);
     else
-        launch_split_typed<false>(keys, idx_in, flags, keys_out, idx_out, n_true_out, n, hdr, status,
-                                  sw, nt, part, stream);
+        split_launch_any<false, false>(keys, idx_in, flags, 0, keys_out, idx_out, n_true_out, n,
+                                       hdr, status, sw, nullptr, part, stream);
     return hipGetLastError();
 }
 

@@ -13,7 +13,8 @@ from paper_2505_15112_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
 
-SIZES = [1, 5, 63, 64, 65, 255, 4095, 4096, 4097, 3 * 4096 + 5, 65_536, (1 << 20) + 17]
+SIZES = [1, 5, 63, 64, 65, 255, 4095, 4096, 4097, 3 * 4096 + 5, 65_536, 3 * 32768 + 5,
+         (1 << 20) + 17]
 
 
 @pytest.fixture(scope="module")
@@ -93,6 +94,20 @@ def test_split(ops, n):
         _check_split(ops, k, f, None, f"split n={n} {name}")
     perm = np.random.default_rng(n).permutation(n).astype(np.int32)
     _check_split(ops, k, W.mask_u8(n, seed=2), perm, f"split n={n} idx_in")
+
+
+def test_split_misaligned(ops):
+    """Keys and flags one element off alignment: the element-wise tile path."""
+    n = 3 * 32768 + 5
+    announce("split misaligned", n)
+    k = W.keys_u32(n + 1, seed=31)
+    f = W.mask_u8(n + 1, seed=32)
+    kd, fd = to_dev(k.view(np.int32)), to_dev(f)
+    ko, io, nt = ops.split_by_flags_u32(kd[1:], fd[1:])
+    rk, ri, rn = oracle.split_u32(k[1:], f[1:])
+    assert int(nt.item()) == rn
+    assert_equal_first_diff(to_host(ko).view(np.uint32), rk, "split misaligned keys")
+    assert_equal_first_diff(to_host(io), ri, "split misaligned idx")
 
 
 def test_split_repeated_calls_share_workspace(ops):
