@@ -11,9 +11,9 @@ The same run measures every other operation of the library on its workload
 ("ops"): the fp32 metric scan, the reduce-then-scan check variant, the
 fp16->fp32 scan (n = 2^24), the latency-bound int32 scan (n = 2^16), mask
 compaction (n = 2^28), batched rows and the top-p cutoff (128 x 131072),
-stable split and both radix sorts (n = 2^26).  Workloads that fit in the
-256 MB Infinity Cache are timed cold: rounds of (512 MiB overwrite, call)
-enqueued back to back, minus the overwrites alone.
+stable split and the 1-, 4- and 8-bit radix sorts (n = 2^26).  Workloads
+that fit in the 256 MB Infinity Cache are timed cold: rounds of (512 MiB
+overwrite, call) enqueued back to back, minus the overwrites alone.
 The CPU-baseline leg times the serial oracle on each workload (or a stated
 sample) and checks the GPU outputs against it.
 
@@ -326,19 +326,19 @@ def main():
         po = torch.empty_like(keys)
         kt = torch.empty_like(keys)
         pt = torch.empty_like(keys)
-        for bits, passes in ((4, 8), (1, 32)):
+        for bits, passes in ((8, 4), (4, 8), (1, 32)):
             wsx = ops.workspace(_lib.OP_RADIX_SORT, dev, n5, bits=bits)
             a = (P(keys), P(ko), P(po), P(kt), P(pt), n5, bits, P(wsx), wsx.numel(), sp)
             ms = T.back_to_back(lambda: check(lib.radix_sort_u32(*a), "radix"), max(3, K // 4),
                                 2)
             # algorithmic bytes: pass 0 reads keys and writes keys + indices (12 B),
-            # later passes read and write both (16 B); the 4-bit sort also needs one
-            # histogram read (4 B).  Reads this implementation adds (the 1-bit
-            # histogram, the 4-bit per-pass count kernel) are not credited.
-            bb = n5 * (12 + 16 * (passes - 1) + (4 if bits == 4 else 0))
+            # later passes read and write both (16 B); the 4- and 8-bit sorts also
+            # need one histogram read (4 B).  Reads this implementation adds (the
+            # 1-bit histogram, the per-pass count kernels) are not credited.
+            bb = n5 * (12 + 16 * (passes - 1) + (4 if bits > 1 else 0))
             opsd[f"radix{bits}_n2^26"] = entry(
                 "radix", ms, bb, memcpy_ms(bb), "12 + 16 x (passes-1) bytes per key"
-                + (" + 4 (histogram)" if bits == 4 else ""),
+                + (" + 4 (histogram)" if bits > 1 else ""),
                 {"mkeys_per_s": round(n5 / (ms * 1e-3) / 1e6, 1), "passes": passes})
             outputs[f"radix{bits}"] = (ko.clone(), po.clone())
         # stable split on its own (flags Bernoulli(1/2)), n = 2^26
@@ -423,7 +423,7 @@ def cpu_baseline_leg(x_host, y_dev, outputs, np, torch):
         sample = kh[: 1 << 22]
         t, _ = timed(lambda: oracle.sort_u32(sample), reps=1)
         rk, rp = oracle.sort_u32(kh)
-        for bits in (4, 1):
+        for bits in (8, 4, 1):
             ko, po = outputs[f"radix{bits}"]
             res[f"radix{bits}_n2^26"] = {
                 "mkeys_per_s": round(sample.size / t / 1e6, 2),

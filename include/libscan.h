@@ -182,8 +182,9 @@ int split_by_flags_u32(const uint32_t* keys, const int32_t* idx_in, const uint8_
  * least significant one, each step a stable split; Section 6 returns source
  * indices like PyTorch's sort()).  keys_out receives the n keys in ascending
  * order, stably; perm_out (nullable) the source index of each, so that
- * keys_out[i] == keys[perm_out[i]].  bits_per_pass: 1 (32 split passes) or 4
- * (8 passes of 16-way stable splits); both give the same output.  keys_tmp
+ * keys_out[i] == keys[perm_out[i]].  bits_per_pass: 1 (32 split passes), 4
+ * (8 passes of 16-way stable splits) or 8 (4 passes of 256-way stable
+ * splits); all give the same output.  keys_tmp
  * (and perm_tmp when perm_out is given) are caller-provided n-element
  * ping-pong buffers whose contents are clobbered.  No two of keys, keys_out,
  * perm_out, keys_tmp, perm_tmp may overlap.  n <= INT32_MAX.  Workspace:

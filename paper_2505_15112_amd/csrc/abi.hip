@@ -142,7 +142,7 @@ int libscan_workspace_bytes(int op, int64_t n, int64_t rows, int64_t len, int bi
             return LIBSCAN_OK;
         case LIBSCAN_OP_RADIX_SORT:
             if (n > INT32_MAX) return LIBSCAN_ERANGE;
-            if (bits != 1 && bits != 4) return LIBSCAN_EINVAL;
+            if (bits != 1 && bits != 4 && bits != 8) return LIBSCAN_EINVAL;
             *bytes = ls::radix_ws_bytes(n, bits);
             return LIBSCAN_OK;
         case LIBSCAN_OP_SCAN_ROWS: {
@@ -284,7 +284,8 @@ int split_by_flags_u32(const uint32_t* keys, const int32_t* idx_in, const uint8_
 int radix_sort_u32(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out, uint32_t* keys_tmp,
                    int32_t* perm_tmp, int64_t n, int bits_per_pass, void* ws, size_t ws_bytes,
                    void* stream) {
-    if (n < 0 || (bits_per_pass != 1 && bits_per_pass != 4)) return LIBSCAN_EINVAL;
+    if (n < 0 || (bits_per_pass != 1 && bits_per_pass != 4 && bits_per_pass != 8))
+        return LIBSCAN_EINVAL;
     if (n > INT32_MAX) return LIBSCAN_ERANGE;
     if (n == 0) return LIBSCAN_OK;
     if (!keys || !keys_out || !keys_tmp || (perm_out && !perm_tmp)) return LIBSCAN_EINVAL;

@@ -21,7 +21,10 @@
 //    (A single-pass version carrying the 16 counts by a 16-chain decoupled
 //    look-back measured 2x slower per pass on MI355X: every tile's walk
 //    waited on its predecessors' 16 words.)
-// The two variants give identical output: a stable sort is unique.
+//  * 8 bits per pass: 4 passes of the same three kernels with 256 digits;
+//    ranking goes through per-wave digit counts in LDS (see below).  Half the
+//    passes of the 4-bit sort, so half its key and index traffic.
+// All variants give identical output: a stable sort is unique.
 #include "launch.hpp"
 #include "tile.hpp"
 
@@ -300,6 +303,193 @@ __global__ __launch_bounds__(kR4Waves* kWave) LS_OCCUPANCY4 void k_radix4_scatte
     }
 }
 
+// ---------------------------------------------------------------- 8-bit pass
+
+// 4 passes of 8-bit digits: the same count -> scan -> scatter structure as the
+// 4-bit pass, with 256 digits.  Ranking cannot give every digit a lane, so
+// each wave keeps its digit counts in LDS: per chunk of 64 keys, the lanes
+// holding one digit (found with 8 ballots) are a peer group, the group's
+// lowest lane adds the group size to the wave's count of that digit and
+// reads the previous count (one LDS atomic per group, never two lanes on one
+// word), and a key's rank is that count plus its peers in lower lanes.  The
+// wave's atomics execute in order, so ranks follow the index order.
+constexpr int kR8Waves = 8;
+constexpr int kR8Chunks = 16;
+constexpr int64_t kR8Tile = kR8Waves * kR8Chunks * kWave;  // 8192 keys
+constexpr int kR8Digits = 256;
+
+static inline int64_t r8_tiles(int64_t n) { return (n + kR8Tile - 1) / kR8Tile; }
+
+// Lanes holding the same 8-bit digit as this lane, among the `ok` lanes.
+__device__ __forceinline__ uint64_t peers8(uint32_t d, bool ok) {
+    uint64_t m = __ballot(ok);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+        const uint64_t bb = __ballot(ok && ((d >> b) & 1u));
+        m &= ((d >> b) & 1u) ? bb : ~bb;
+    }
+    return m;
+}
+
+// Per-tile counts of the 256 digits: counts[d * ntiles + tile].  Order does
+// not matter here, so the keys are read with 16-byte loads when aligned.
+__global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_count(
+    const uint32_t* keys, int64_t n, int shift, bool vec, uint32_t* counts, uint32_t ntiles) {
+    __shared__ uint32_t s_h[kR8Waves][kR8Digits];
+    for (int i = threadIdx.x; i < kR8Waves * kR8Digits; i += kR8Waves * kWave) (&s_h[0][0])[i] = 0;
+    __syncthreads();
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    const int64_t tbase = (int64_t)blockIdx.x * kR8Tile;
+    const int64_t wbase = tbase + (int64_t)w * kR8Chunks * kWave;
+    auto add = [&](uint32_t key, bool ok) {
+        const uint32_t d = (key >> shift) & 255u;
+        const uint64_t peers = peers8(d, ok);
+        if (ok && lane == __builtin_ctzll(peers))
+            atomicAdd(&s_h[w][d], (uint32_t)__builtin_popcountll(peers));
+    };
+    if (vec && tbase + kR8Tile <= n) {  // this wave's 1024 keys as 4 x 16-byte loads per lane
+        const u32x4* k4 = reinterpret_cast<const u32x4*>(keys + wbase);
+        u32x4 v[kR8Chunks / 4];
+#pragma unroll
+        for (int j = 0; j < kR8Chunks / 4; ++j) v[j] = k4[j * kWave + lane];
+#pragma unroll
+        for (int j = 0; j < kR8Chunks / 4; ++j) {
+            add(v[j].x, true);
+            add(v[j].y, true);
+            add(v[j].z, true);
+            add(v[j].w, true);
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < kR8Chunks; ++j) {
+            const int64_t i = wbase + j * kWave + lane;
+            const bool ok = i < n;
+            add(ok ? keys[i] : 0u, ok);
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < kR8Digits) {
+        uint32_t t = 0;
+#pragma unroll
+        for (int k = 0; k < kR8Waves; ++k) t += s_h[k][threadIdx.x];
+        counts[(int64_t)threadIdx.x * ntiles + blockIdx.x] = t;
+    }
+}
+
+// Rank and scatter one tile of 8192 keys (one key per lane per chunk, so the
+// chunk's index order is the lane order) with the offsets from the spine.
+template <bool HAS_PERM_IN, bool WITH_PERM>
+__global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatter(
+    const uint32_t* keys_in, const int32_t* perm_in, uint32_t* keys_out, int32_t* perm_out,
+    int64_t n, int shift, uint32_t* offsets, uint32_t ntiles) {
+    __shared__ uint32_t s_wh[kR8Waves][kR8Digits];  // wave counts, then each wave's first slot
+    __shared__ uint32_t s_tstart[kR8Digits];         // first slot of digit d in the tile
+    __shared__ uint32_t s_gbase[kR8Digits];          // global position of that slot
+    __shared__ uint32_t s_part[kR8Digits / kWave];
+    __shared__ uint32_t s_stage[kR8Tile];
+
+    const int64_t tile = blockIdx.x;
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    const int64_t tbase = tile * kR8Tile;
+    const int64_t wbase = tbase + (int64_t)w * kR8Chunks * kWave;
+    const bool full = tbase + kR8Tile <= n;
+    const uint32_t valid = full ? (uint32_t)kR8Tile : (uint32_t)(n - tbase);
+
+    for (int i = threadIdx.x; i < kR8Waves * kR8Digits; i += kR8Waves * kWave) (&s_wh[0][0])[i] = 0;
+    if (threadIdx.x < kR8Digits) {
+        uint32_t* o = offsets + (int64_t)threadIdx.x * ntiles + tile;
+        s_gbase[threadIdx.x] = *o;
+        *o = 0;  // offsets can reach 2^30 and more: leave the workspace word zero
+    }
+    uint32_t key[kR8Chunks];
+    int32_t perm[kR8Chunks];
+#pragma unroll
+    for (int j = 0; j < kR8Chunks; ++j) {
+        const int64_t i = wbase + j * kWave + lane;
+        const bool ok = full || i < n;
+        key[j] = ok ? keys_in[i] : 0u;
+        if (WITH_PERM) perm[j] = HAS_PERM_IN ? (ok ? perm_in[i] : 0) : (int32_t)i;
+    }
+    __syncthreads();
+
+    uint32_t rank[kR8Chunks];
+#pragma unroll
+    for (int j = 0; j < kR8Chunks; ++j) {
+        const int64_t i = wbase + j * kWave + lane;
+        const bool ok = full || i < n;
+        const uint32_t d = (key[j] >> shift) & 255u;
+        const uint64_t peers = peers8(d, ok);
+        const int leader = ok ? __builtin_ctzll(peers) : lane;
+        uint32_t before = 0;
+        if (ok && lane == leader) before = atomicAdd(&s_wh[w][d], (uint32_t)__builtin_popcountll(peers));
+        rank[j] = lane_shfl(before, leader) + lanes_below(peers);
+    }
+    __syncthreads();
+
+    // Digit d (thread d): the waves' first slots within the digit, the tile
+    // total, and the exclusive scan of the totals over the 256 digits.
+    uint32_t tot = 0, inc = 0;
+    if (threadIdx.x < kR8Digits) {
+#pragma unroll
+        for (int k = 0; k < kR8Waves; ++k) {
+            const uint32_t c = s_wh[k][threadIdx.x];
+            s_wh[k][threadIdx.x] = tot;
+            tot += c;
+        }
+        inc = wave_incl_scan(tot);
+        if (lane == kWave - 1) s_part[w] = inc;
+    }
+    __syncthreads();
+    if (threadIdx.x < kR8Digits) {
+        uint32_t before = 0;
+        for (int k = 0; k < w; ++k) before += s_part[k];
+        s_tstart[threadIdx.x] = before + inc - tot;
+    }
+    __syncthreads();
+
+    // Sort the tile by digit in LDS, then write it out with consecutive threads
+    // (each digit's keys form one contiguous output run).
+#pragma unroll
+    for (int j = 0; j < kR8Chunks; ++j) {
+        const int64_t i = wbase + j * kWave + lane;
+        const uint32_t d = (key[j] >> shift) & 255u;
+        rank[j] += s_tstart[d] + s_wh[w][d];  // now the slot
+        if ((full || i < n) && rank[j] < kR8Tile) s_stage[rank[j]] = key[j];
+    }
+    __syncthreads();
+    uint32_t skey[kR8Chunks];
+#pragma unroll
+    for (int j = 0; j < kR8Chunks; ++j) {
+        const uint32_t t = (uint32_t)threadIdx.x + j * kR8Waves * kWave;
+        skey[j] = s_stage[t];
+        if (t < valid) {
+            const uint32_t d = (skey[j] >> shift) & 255u;
+            const uint32_t pos = s_gbase[d] + (t - s_tstart[d]);
+            if (pos < (uint64_t)n) keys_out[pos] = skey[j];  // pos < n always; guards a bad count
+        }
+    }
+    if (WITH_PERM) {
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kR8Chunks; ++j) {
+            const int64_t i = wbase + j * kWave + lane;
+            if ((full || i < n) && rank[j] < kR8Tile) s_stage[rank[j]] = (uint32_t)perm[j];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kR8Chunks; ++j) {
+            const uint32_t t = (uint32_t)threadIdx.x + j * kR8Waves * kWave;
+            if (t < valid) {
+                const uint32_t d = (skey[j] >> shift) & 255u;
+                const uint32_t pos = s_gbase[d] + (t - s_tstart[d]);
+                if (pos < (uint64_t)n) perm_out[pos] = (int32_t)s_stage[t];
+            }
+        }
+    }
+}
+
 // ---------------------------------------------------------------- driver
 
 hipError_t launch_radix1_pass(const uint32_t* keys, const int32_t* idx_in, int bit,
@@ -308,15 +498,19 @@ hipError_t launch_radix1_pass(const uint32_t* keys, const int32_t* idx_in, int b
 
 // 1-bit: header | final histogram | one status word per split tile |
 //        per-block histograms.
-// 4-bit: header | the count-table scan's workspace body | count table
-//        (16 x tiles 32-bit counts, 16-byte aligned).
+// 4- and 8-bit: header | the count-table scan's workspace body | count table
+//        (digits x tiles 32-bit counts, 16-byte aligned).
 static int64_t radix1_status_words(int64_t n) { return (n + kR1Tile - 1) / kR1Tile; }
-static size_t radix4_table_offset(int64_t n) {
-    return (scan1d_ws_bytes(r4_tiles(n) * 16) + 15) / 16 * 16;
+static int64_t digit_table_entries(int64_t n, int bits) {
+    return bits == 8 ? r8_tiles(n) * kR8Digits : r4_tiles(n) * 16;
+}
+static size_t digit_table_offset(int64_t n, int bits) {
+    return (scan1d_ws_bytes(digit_table_entries(n, bits)) + 15) / 16 * 16;
 }
 
 size_t radix_ws_bytes(int64_t n, int bits) {
-    if (bits == 4) return radix4_table_offset(n) + (size_t)r4_tiles(n) * 16 * sizeof(uint32_t);
+    if (bits == 4 || bits == 8)
+        return digit_table_offset(n, bits) + (size_t)digit_table_entries(n, bits) * sizeof(uint32_t);
     return kRadixStatusOffset + (size_t)radix1_status_words(n) * sizeof(uint64_t) +
            (size_t)kHistBlocks * kHistWords * sizeof(uint32_t);
 }
@@ -325,7 +519,7 @@ hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* 
                              uint32_t* keys_tmp, int32_t* perm_tmp, int64_t n, int bits, void* ws,
                              size_t ws_bytes, hipStream_t stream) {
     if (n == 0) return hipSuccess;
-    const int passes = bits == 4 ? 8 : 32;
+    const int passes = 32 / bits;
     uint64_t* hist = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
     if (bits == 1) {
         uint32_t* part = reinterpret_cast<uint32_t*>(
@@ -345,21 +539,36 @@ hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* 
             const hipError_t e = launch_radix1_pass(src_k, src_p, p, dk, dp, n, hist, ws, ws_bytes,
                                                     kRadixStatusOffset, stream);
             if (e != hipSuccess) return e;
-        } else {
+        } else if (bits == 4) {
             const uint32_t nt = (uint32_t)r4_tiles(n);
-            const int64_t ncount = (int64_t)nt * 16;
-            const size_t toff = radix4_table_offset(n);
+            const size_t toff = digit_table_offset(n, 4);
             uint32_t* counts = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + toff);
             const bool vec = ((uintptr_t)src_k % 16) == 0;
             hipLaunchKernelGGL(k_radix4_count, dim3(nt), dim3(kR4Waves * kWave), 0, stream, src_k, n,
                                4 * p, vec, counts, nt);
-            hipError_t e = launch_scan1d(Kind::I32, true, counts, counts, ncount, nullptr, nullptr,
-                                         ws, toff, stream);
+            hipError_t e = launch_scan1d(Kind::I32, true, counts, counts, digit_table_entries(n, 4),
+                                         nullptr, nullptr, ws, toff, stream);
             if (e != hipSuccess) return e;
             auto k = dp ? (src_p ? k_radix4_scatter<true, true> : k_radix4_scatter<false, true>)
                         : k_radix4_scatter<false, false>;
             hipLaunchKernelGGL(k, dim3(nt), dim3(kR4Waves * kWave), 0, stream, src_k, src_p, dk, dp,
                                n, 4 * p, counts, nt);
+            e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        } else {
+            const uint32_t nt = (uint32_t)r8_tiles(n);
+            const size_t toff = digit_table_offset(n, 8);
+            uint32_t* counts = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + toff);
+            const bool vec = ((uintptr_t)src_k % 16) == 0;
+            hipLaunchKernelGGL(k_radix8_count, dim3(nt), dim3(kR8Waves * kWave), 0, stream, src_k, n,
+                               8 * p, vec, counts, nt);
+            hipError_t e = launch_scan1d(Kind::I32, true, counts, counts, digit_table_entries(n, 8),
+                                         nullptr, nullptr, ws, toff, stream);
+            if (e != hipSuccess) return e;
+            auto k = dp ? (src_p ? k_radix8_scatter<true, true> : k_radix8_scatter<false, true>)
+                        : k_radix8_scatter<false, false>;
+            hipLaunchKernelGGL(k, dim3(nt), dim3(kR8Waves * kWave), 0, stream, src_k, src_p, dk, dp,
+                               n, 8 * p, counts, nt);
             e = hipGetLastError();
             if (e != hipSuccess) return e;
         }

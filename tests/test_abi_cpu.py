@@ -167,7 +167,8 @@ def test_radix_validation(lib):
     KO, PO, KT, PT = P(0x2000000), P(0x3000000), P(0x4000000), P(0x5000000)
     W2 = P(0x60000000)
     assert fn(X, KO, PO, KT, PT, -1, 4, W2, BIG, None) == _lib.EINVAL
-    assert fn(X, KO, PO, KT, PT, 10, 2, W2, BIG, None) == _lib.EINVAL        # bits not 1/4
+    assert fn(X, KO, PO, KT, PT, 10, 2, W2, BIG, None) == _lib.EINVAL        # bits not 1/4/8
+    assert fn(X, KO, PO, KT, PT, 10, 16, W2, BIG, None) == _lib.EINVAL
     assert fn(X, KO, PO, None, PT, 10, 4, W2, BIG, None) == _lib.EINVAL      # no keys_tmp
     assert fn(X, KO, PO, KT, None, 10, 4, W2, BIG, None) == _lib.EINVAL      # perm without tmp
     assert fn(X, X, PO, KT, PT, 10, 4, W2, BIG, None) == _lib.EINVAL         # in place
@@ -178,4 +179,6 @@ def test_radix_validation(lib):
     out = ctypes.c_size_t(0)
     assert lib.libscan_workspace_bytes(_lib.OP_RADIX_SORT, 1 << 26, 0, 0, 4, ctypes.byref(out)) == 0
     assert out.value >= 256 + 16 * 4 * ((1 << 26) // 8192)
+    assert lib.libscan_workspace_bytes(_lib.OP_RADIX_SORT, 1 << 26, 0, 0, 8, ctypes.byref(out)) == 0
+    assert out.value >= 256 + 256 * 4 * ((1 << 26) // 8192)
     assert lib.libscan_workspace_bytes(_lib.OP_RADIX_SORT, 100, 0, 0, 3, ctypes.byref(out)) == _lib.EINVAL
