@@ -112,6 +112,20 @@ __global__ __launch_bounds__(1024) void k_hist_reduce(const uint32_t* part, int 
     }
 }
 
+// The scatter kernels have no inter-workgroup order, so their tile index is
+// free: workgroups are dealt to the 8 XCDs round-robin by block index, and
+// this gives each XCD one contiguous range of tiles.  Neighbouring tiles then
+// write the two halves of the cache lines at their shared run boundaries from
+// the same L2, where the partial lines merge before going to HBM.  (A
+// bijection on block indices whatever the placement; only speed depends on
+// the round-robin dealing.)
+constexpr uint32_t kXcds = 8;
+__device__ __forceinline__ uint32_t xcd_tile(uint32_t b, uint32_t nblocks) {
+    const uint32_t x = b % kXcds, k = b / kXcds;
+    const uint32_t per = nblocks / kXcds, extra = nblocks % kXcds;
+    return x * per + (x < extra ? x : extra) + k;
+}
+
 // ---------------------------------------------------------------- 4-bit pass
 
 // Lanes whose digit equals `d`, from the four digit-bit ballots and the
@@ -194,7 +208,7 @@ __global__ __launch_bounds__(kR4Waves* kWave) LS_OCCUPANCY4 void k_radix4_scatte
     __shared__ uint32_t s_gbase[16];   // global position of that slot
     __shared__ uint32_t s_stage[kR4Tile];
 
-    const int64_t tile = blockIdx.x;
+    const int64_t tile = xcd_tile(blockIdx.x, gridDim.x);
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
     const int64_t tbase = tile * kR4Tile;
@@ -332,22 +346,21 @@ __device__ __forceinline__ uint64_t peers8(uint32_t d, bool ok) {
 }
 
 // Per-tile counts of the 256 digits: counts[d * ntiles + tile].  Order does
-// not matter here, so the keys are read with 16-byte loads when aligned.
+// not matter here: keys are read with 16-byte loads when aligned and counted
+// with plain LDS atomics, into 4 histograms per wave (picked by lane & 3) so
+// that equal digits in one instruction collide at most 16 ways.
+constexpr int kR8Sub = 4;
 __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_count(
     const uint32_t* keys, int64_t n, int shift, bool vec, uint32_t* counts, uint32_t ntiles) {
-    __shared__ uint32_t s_h[kR8Waves][kR8Digits];
-    for (int i = threadIdx.x; i < kR8Waves * kR8Digits; i += kR8Waves * kWave) (&s_h[0][0])[i] = 0;
+    __shared__ uint32_t s_h[kR8Waves * kR8Sub][kR8Digits];
+    for (int i = threadIdx.x; i < kR8Waves * kR8Sub * kR8Digits; i += kR8Waves * kWave)
+        (&s_h[0][0])[i] = 0;
     __syncthreads();
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
+    uint32_t* h = s_h[w * kR8Sub + (lane & (kR8Sub - 1))];
     const int64_t tbase = (int64_t)blockIdx.x * kR8Tile;
     const int64_t wbase = tbase + (int64_t)w * kR8Chunks * kWave;
-    auto add = [&](uint32_t key, bool ok) {
-        const uint32_t d = (key >> shift) & 255u;
-        const uint64_t peers = peers8(d, ok);
-        if (ok && lane == __builtin_ctzll(peers))
-            atomicAdd(&s_h[w][d], (uint32_t)__builtin_popcountll(peers));
-    };
     if (vec && tbase + kR8Tile <= n) {  // this wave's 1024 keys as 4 x 16-byte loads per lane
         const u32x4* k4 = reinterpret_cast<const u32x4*>(keys + wbase);
         u32x4 v[kR8Chunks / 4];
@@ -355,24 +368,23 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_count(
         for (int j = 0; j < kR8Chunks / 4; ++j) v[j] = k4[j * kWave + lane];
 #pragma unroll
         for (int j = 0; j < kR8Chunks / 4; ++j) {
-            add(v[j].x, true);
-            add(v[j].y, true);
-            add(v[j].z, true);
-            add(v[j].w, true);
+            atomicAdd(&h[(v[j].x >> shift) & 255u], 1u);
+            atomicAdd(&h[(v[j].y >> shift) & 255u], 1u);
+            atomicAdd(&h[(v[j].z >> shift) & 255u], 1u);
+            atomicAdd(&h[(v[j].w >> shift) & 255u], 1u);
         }
     } else {
 #pragma unroll
         for (int j = 0; j < kR8Chunks; ++j) {
             const int64_t i = wbase + j * kWave + lane;
-            const bool ok = i < n;
-            add(ok ? keys[i] : 0u, ok);
+            if (i < n) atomicAdd(&h[(keys[i] >> shift) & 255u], 1u);
         }
     }
     __syncthreads();
     if (threadIdx.x < kR8Digits) {
         uint32_t t = 0;
 #pragma unroll
-        for (int k = 0; k < kR8Waves; ++k) t += s_h[k][threadIdx.x];
+        for (int k = 0; k < kR8Waves * kR8Sub; ++k) t += s_h[k][threadIdx.x];
         counts[(int64_t)threadIdx.x * ntiles + blockIdx.x] = t;
     }
 }
@@ -389,7 +401,7 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
     __shared__ uint32_t s_part[kR8Digits / kWave];
     __shared__ uint32_t s_stage[kR8Tile];
 
-    const int64_t tile = blockIdx.x;
+    const int64_t tile = xcd_tile(blockIdx.x, gridDim.x);
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
     const int64_t tbase = tile * kR8Tile;
