@@ -14,6 +14,8 @@ compaction (n = 2^28), batched rows and the top-p cutoff (128 x 131072),
 stable split and the 1-, 4- and 8-bit radix sorts (n = 2^26).  Workloads
 that fit in the 256 MB Infinity Cache are timed cold: rounds of (512 MiB
 overwrite, call) enqueued back to back, minus the overwrites alone.
+A sweep of the int32 scan over n = 2^20 .. 2^28 (and 2^k + 17) gives bandwidth
+against length beside a memcpy of the same bytes.
 The CPU-baseline leg times the serial oracle on each workload (or a stated
 sample) and checks the GPU outputs against it.
 
@@ -352,6 +354,24 @@ def main():
                                     "4+4 written), no input indices")
         outputs["radix_keys"] = keys_host
         line["ops"] = opsd
+
+        # bandwidth against length, int32 inclusive: powers of two and 2^k + 17
+        # (ragged last tile); totals under 512 MiB are timed cold
+        log("sweep")
+        sweep = []
+        for k in range(20, 29):
+            for m in (1 << k, (1 << k) + 17):
+                if m > n:
+                    continue
+                xs, ys = x_i32[:m], y_i32[:m]
+                cold = m * 8 < (512 << 20)
+                f = scan_call("scan_inclusive_i32", xs, ys, m)
+                ms = T.flushed(f, K, Wm) if cold else T.back_to_back(f, K, Wm)
+                mc = memcpy_ms(m * 8, cold)
+                sweep.append({"n": m, "us": round(ms * 1e3, 2),
+                              "gbps": round(m * 8 / (ms * 1e-3) / 1e9, 1),
+                              "pct_of_memcpy": round(100.0 * mc / ms, 1), "cold": cold})
+        line["sweep_i32"] = sweep
 
     # ---------------------------------------------------------------- CPU leg
     if not args.no_cpu_baseline:

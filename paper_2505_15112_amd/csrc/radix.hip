@@ -416,27 +416,51 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
         *o = 0;  // offsets can reach 2^30 and more: leave the workspace word zero
     }
     uint32_t key[kR8Chunks];
-    int32_t perm[kR8Chunks];
 #pragma unroll
     for (int j = 0; j < kR8Chunks; ++j) {
         const int64_t i = wbase + j * kWave + lane;
-        const bool ok = full || i < n;
-        key[j] = ok ? keys_in[i] : 0u;
-        if (WITH_PERM) perm[j] = HAS_PERM_IN ? (ok ? perm_in[i] : 0) : (int32_t)i;
+        key[j] = (full || i < n) ? keys_in[i] : 0u;
     }
     __syncthreads();
 
-    uint32_t rank[kR8Chunks];
+    // Chunks in groups of 4: the peer groups of the 4 chunks, their LDS
+    // atomics back to back (they execute in order, so a later chunk sees the
+    // earlier chunks' counts), then the broadcasts from the leaders -- the
+    // atomics' latencies overlap without holding 16 results at once.
+    constexpr int kG = 4;
+    uint32_t rank[kR8Chunks];  // peers in lower lanes, then the rank
 #pragma unroll
-    for (int j = 0; j < kR8Chunks; ++j) {
-        const int64_t i = wbase + j * kWave + lane;
-        const bool ok = full || i < n;
-        const uint32_t d = (key[j] >> shift) & 255u;
-        const uint64_t peers = peers8(d, ok);
-        const int leader = ok ? __builtin_ctzll(peers) : lane;
-        uint32_t before = 0;
-        if (ok && lane == leader) before = atomicAdd(&s_wh[w][d], (uint32_t)__builtin_popcountll(peers));
-        rank[j] = lane_shfl(before, leader) + lanes_below(peers);
+    for (int g = 0; g < kR8Chunks; g += kG) {
+        uint32_t leader[kG];  // leader lane | group size << 8 (size 0: invalid lane)
+#pragma unroll
+        for (int q = 0; q < kG; ++q) {
+            const int64_t i = wbase + (g + q) * kWave + lane;
+            const bool ok = full || i < n;
+            const uint64_t peers = peers8((key[g + q] >> shift) & 255u, ok);
+            rank[g + q] = lanes_below(peers);
+            leader[q] = ok ? ((uint32_t)__builtin_ctzll(peers) |
+                              ((uint32_t)__builtin_popcountll(peers) << 8))
+                           : (uint32_t)lane;
+        }
+        uint32_t before[kG];
+#pragma unroll
+        for (int q = 0; q < kG; ++q) {
+            before[q] = 0;
+            if ((leader[q] & 255u) == (uint32_t)lane && (leader[q] >> 8))
+                before[q] = atomicAdd(&s_wh[w][(key[g + q] >> shift) & 255u], leader[q] >> 8);
+        }
+#pragma unroll
+        for (int q = 0; q < kG; ++q) rank[g + q] += lane_shfl(before[q], (int)(leader[q] & 255u));
+    }
+    // The source indices are needed only when they are staged: load them now
+    // (ranking holds four registers per key), in flight while the keys move.
+    int32_t perm[kR8Chunks];
+    if (WITH_PERM) {
+#pragma unroll
+        for (int j = 0; j < kR8Chunks; ++j) {
+            const int64_t i = wbase + j * kWave + lane;
+            perm[j] = HAS_PERM_IN ? ((full || i < n) ? perm_in[i] : 0) : (int32_t)i;
+        }
     }
     __syncthreads();
 

@@ -11,14 +11,8 @@
 //    out row-major by ticket, and the decoupled look-back runs inside a row
 //    (it stops at the row's first segment), so 128 rows of 2^17 still give
 //    4096 workgroups to fill 256 CUs.
-// The top-p cutoff needs only one index per row.  Rows of up to 64 tiles take
-// one pass: every tile publishes its sum, adds the sums of the row's earlier
-// tiles in a fixed order, and the tile whose range holds the crossing finds
-// the index in the probabilities it already holds (k_topp_onepass).  Longer
-// rows take two phases (the two phases of the paper's Algorithm 3, MCScan,
-// with the down-sweep cut to the one tile that matters): a first kernel sums
-// every tile, a second, one workgroup per row, finds the first tile whose
-// inclusive sum reaches p and re-reads only that tile.
+// The top-p cutoff needs only one index per row: every tile sums its part of
+// the row and the row's last tile to finish locates the index (k_topp).
 #include <limits.h>
 
 #include "launch.hpp"
@@ -106,166 +100,123 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_rows_lookback
 
 // ---------------------------------------------------------------- top-p
 
-// Phase 1: the fp32 sum of every tile, stored with its two top bits clear
-// (so the workspace word reads as "nothing published" to any look-back).
-template <class TileT, bool VEC>
-__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp_sums(const float* probs, int64_t len,
-                                                               uint32_t segs, uint64_t* partial) {
-    __shared__ float s_wtot[TileT::WAVES];
-    const int64_t row = blockIdx.x / segs;
-    const int64_t seg = blockIdx.x - row * segs;
-    float v[TileT::J][TileT::V];
-    TileT::template load<VEC>(probs + row * len, len, seg * TileT::kElems, v);
-    float wofs;
-    const float agg = TileT::combine_waves(wave_sum(TileT::lane_sum(v)), s_wtot, &wofs);
-    if (threadIdx.x == 0) partial[blockIdx.x] = (uint64_t)Bits<float>::to(agg);
+// One kernel; no workgroup waits for another's work.  Every tile of a row
+// sums its probabilities, stores the sum (in a workspace word with its two
+// top bits clear, which any look-back reads as "nothing published", and a
+// "set" bit below them) and counts itself in the row's arrival counter.  The
+// row's last tile to arrive -- every other tile has stored its sum by then,
+// it waits only for the stores to become visible -- clears the sums again and
+// scans them in order for the first tile
+// whose inclusive sum reaches p, then re-reads that one tile (just read, so
+// still in the 256 MB Infinity Cache) to locate the index.  p never reached:
+// len - 1.
+// The last tile resets the counter and the sums, so the workspace needs no
+// clearing.
+// (The two phases of the paper's Algorithm 3, MCScan, with the down-sweep cut
+// to the one tile that matters and the second phase run by whichever
+// workgroup finishes a row last.)
+// Top-p's workspace words (a published tile sum, a row's arrival count) carry
+// the top three bits 001.  Other ops leave status words with a non-zero state
+// in the top two bits, or counts with the top three bits clear, and cleared
+// words are 0, so nothing else can pass for a top-p word.
+constexpr uint64_t kToppTag = 1ull << 61;
+__device__ __forceinline__ bool topp_word(uint64_t w) { return (w >> 61) == 1; }
+
+// Count one arrival in the row's counter; returns the arrivals before it.  A
+// word that is not a top-p word (left by another op sharing the workspace)
+// counts as zero, hence compare-and-swap rather than a plain add.
+__device__ __forceinline__ uint32_t topp_arrive(uint64_t* counter) {
+    uint64_t old = __hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    while (true) {
+        const uint32_t before = topp_word(old) ? (uint32_t)old : 0u;
+        uint64_t expected = old;
+        if (__hip_atomic_compare_exchange_strong(counter, &expected, kToppTag | (before + 1u),
+                                                 __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT))
+            return before;
+        old = expected;
+    }
 }
 
-// Phase 2, one workgroup per row: scan the row's tile sums (64 at a time,
-// DPP scan, carried in order) for the first tile whose inclusive sum reaches
-// p, rescan only that tile for the first element whose running sum reaches p
-// (its last element if rounding kept them all below p), or write len - 1 if
-// no tile reaches p.
 template <class TileT, bool VEC>
-__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp_owner(const float* probs,
-                                                                int32_t* cutoff, int64_t len,
-                                                                uint32_t segs,
-                                                                const uint64_t* partial, float p) {
-    __shared__ int64_t s_first;
-    __shared__ float s_excl;
+__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp(
+    const float* probs, int32_t* cutoff, int64_t len, uint32_t segs, float p, WsHeader* hdr,
+    uint64_t* sums, uint64_t* arrivals) {
     __shared__ float s_wtot[TileT::WAVES];
+    __shared__ uint32_t s_last;
+    __shared__ int32_t s_first;
+    __shared__ float s_excl;
     __shared__ int32_t s_min[TileT::WAVES];
-    const int64_t row = blockIdx.x;
-    const int lane = lane_id();
+
+    const uint32_t row32 = blockIdx.x / segs;
+    const uint32_t seg = blockIdx.x - row32 * segs;
+    const int64_t row = row32;
+    const float* xr = probs + row * len;
+    float v[TileT::J][TileT::V];
+    TileT::template load<VEC>(xr, len, (int64_t)seg * TileT::kElems, v);
+    float wofs;
+    const float agg = TileT::combine_waves(wave_sum(TileT::lane_sum(v)), s_wtot, &wofs);
+    if (threadIdx.x == 0) {
+        // Relaxed only (a release/acquire pair at device scope would write back
+        // and invalidate L2 in every workgroup): the sum word carries its own
+        // "published" bit, and the last arrival waits for those bits.
+        __hip_atomic_store(&sums[blockIdx.x], kToppTag | Bits<float>::to(agg), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+        s_last = topp_arrive(&arrivals[row]) == segs - 1;
+    }
+    __syncthreads();
+    if (!s_last) return;  // uniform over the workgroup
+
     if (threadIdx.x < kWave) {
-        const uint64_t* pr = partial + row * segs;
+        const int lane = lane_id();
+        uint64_t* rs = sums + (int64_t)row32 * segs;
         float carry = 0.f, excl = 0.f;
-        int64_t first = -1;
-        for (int64_t b = 0; b < segs && first < 0; b += kWave) {
-            const int64_t s = b + lane;
-            const float a = s < segs ? Bits<float>::from((uint32_t)pr[s]) : 0.f;
+        int32_t first = -1;
+        bool failed = false;
+        for (uint32_t b = 0; b < segs; b += kWave) {
+            const uint32_t s = b + lane;
+            uint64_t word = kToppTag;
+            if (s < segs) {
+                for (uint32_t spins = 0;; ++spins) {  // bounded: every tile has stored already
+                    word = __hip_atomic_load(&rs[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (topp_word(word) || spins >= kSpinLimit) break;
+                    __builtin_amdgcn_s_sleep(1);
+                }
+                failed |= !topp_word(word);
+                // leave the word clear for the next call
+                __hip_atomic_store(&rs[s], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            if (first >= 0) continue;  // keep clearing the rest of the row
+            const float a = s < segs ? Bits<float>::from((uint32_t)word) : 0.f;
             const float inc = carry + wave_incl_scan(a);
             const uint64_t hit = __ballot(s < segs && inc >= p);
             if (hit) {
                 const int l = __builtin_ctzll(hit);
-                first = b + l;
+                first = (int32_t)(b + l);
                 excl = l ? lane_read(inc, l - 1) : carry;
             }
             carry = lane_read(inc, kWave - 1);
         }
+        if (__ballot(failed) && lane == 0)
+            __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (lane == 0) {
             s_first = first;
             s_excl = excl;
+            __hip_atomic_store(&arrivals[row], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
     __syncthreads();
-    const int64_t seg = s_first;
-    if (seg < 0) {
+    const int32_t first = s_first;
+    if (first < 0) {
         if (threadIdx.x == 0) cutoff[row] = (int32_t)(len - 1);
         return;
     }
-    const int64_t base = seg * TileT::kElems;
-    float v[TileT::J][TileT::V];
-    TileT::template load<VEC>(probs + row * len, len, base, v);
-    const float wtot = TileT::template wave_scan<false>(v);
-    float wofs;
-    TileT::combine_waves(wtot, s_wtot, &wofs);
-    const float c = s_excl + wofs;
-    int32_t cand = INT_MAX;
-#pragma unroll
-    for (int j = TileT::J - 1; j >= 0; --j) {
-        const int64_t off = TileT::offset(base, j);
-#pragma unroll
-        for (int e = TileT::V - 1; e >= 0; --e)
-            if (off + e < len && c + v[j][e] >= p) cand = (int32_t)(off + e);
-    }
-    const int32_t wm = wave_min(cand);
-    if (lane == 0) s_min[threadIdx.x / kWave] = wm;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        int32_t m = INT_MAX;
-        for (int k = 0; k < TileT::WAVES; ++k) m = s_min[k] < m ? s_min[k] : m;
-        const int64_t last = (base + TileT::kElems < len ? base + TileT::kElems : len) - 1;
-        cutoff[row] = m != INT_MAX ? m : (int32_t)last;
-    }
-}
-
-// One pass for rows of at most kToppMaxSegs tiles.  Every tile publishes its
-// sum (state A, epoch-tagged) as soon as it has loaded, waits only for the
-// sums of the row's earlier tiles, and adds them left to right in fp32.  All
-// tiles of a row add the same numbers in the same order, so the boundary sum
-// S_{k-1} that tile k compares with p is bit for bit the S_{k-1} that tile
-// k-1 compared, and for non-negative probabilities S is non-decreasing: the
-// one tile with S_{k-1} < p <= S_k (or the row's last tile, if p is never
-// reached) owns the cutoff and finds it in the data it already holds -- no
-// tile is read twice and no workgroup waits for another one's decision.
-constexpr uint32_t kToppMaxSegs = kWave;
-
-template <class TileT, bool VEC>
-__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp_onepass(
-    const float* probs, int32_t* cutoff, int64_t len, uint32_t segs, uint32_t ntiles, float p,
-    WsHeader* hdr, uint64_t* status, int64_t status_words) {
-    __shared__ Ticket s_ticket;
-    __shared__ float s_wtot[TileT::WAVES];
-    __shared__ float s_excl;
-    __shared__ uint32_t s_own;
-    __shared__ int32_t s_min[TileT::WAVES];
-
-    if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
-    __syncthreads();
-    const uint32_t tile32 = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.tile);
-    const uint32_t epoch = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.epoch);
-    if (tile32 >= ntiles) {  // only with a workspace that was never zero-filled
-        if (threadIdx.x == 0)
-            __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        return;
-    }
-    const uint32_t row32 = tile32 / segs;
-    const uint32_t seg = tile32 - row32 * segs;
-    const int64_t row = row32;
-    const int64_t base = (int64_t)seg * TileT::kElems;
-
-    float v[TileT::J][TileT::V];
-    TileT::template load<VEC>(probs + row * len, len, base, v);
-    const float wtot = TileT::template wave_scan<false>(v);
-    float wofs;
-    const float agg = TileT::combine_waves(wtot, s_wtot, &wofs);
-
-    if (threadIdx.x < kWave) {
-        const int lane = lane_id();
-        const uint32_t first = row32 * segs;
-        if (lane == 0) status_store(status + tile32, status_word(kStateA, epoch, Bits<float>::to(agg)));
-        // The sums of tiles first .. tile-1 (seg < kToppMaxSegs, one per lane).
-        uint32_t bits = 0;
-        for (uint32_t spins = 0;; ++spins) {
-            uint64_t w = 0;
-            bool ready = true;
-            if ((uint32_t)lane < seg) {
-                w = status_load(status + first + lane);
-                ready = status_state(w, epoch) != kStateX;
-            }
-            if (__ballot(!ready) == 0) {
-                bits = (uint32_t)w;
-                break;
-            }
-            if (spins >= kSpinLimit) {
-                if (lane == 0)
-                    __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                break;
-            }
-            __builtin_amdgcn_s_sleep(1);
-        }
-        float sum = 0.f;  // left to right, the same on every tile of the row
-        for (uint32_t l = 0; l < seg; ++l) sum = sum + Bits<float>::from(lane_read(bits, (int)l));
-        if (lane == 0) {
-            const float incl = sum + agg;
-            s_excl = sum;
-            s_own = (seg == 0 || !(sum >= p)) && (seg == segs - 1 || incl >= p);
-            finish_epoch(hdr, epoch, ntiles, status, status_words);
-        }
-    }
-    __syncthreads();
-    if (!s_own) return;  // uniform over the workgroup
+    // Re-read the owning tile even when it is this one: keeping this tile's
+    // registers live across the scan of the sums would exceed the register
+    // budget (one tile per row, read moments ago by its own workgroup).
+    const int64_t base = (int64_t)first * TileT::kElems;
+    TileT::template load<VEC>(xr, len, base, v);
+    TileT::combine_waves(TileT::template wave_scan<false>(v), s_wtot, &wofs);
     const float c = s_excl + wofs;
     int32_t cand = INT_MAX;
 #pragma unroll
@@ -348,9 +299,14 @@ __global__ __launch_bounds__(256) void k_rows_wave(const T* x, T* y, int64_t row
 
 // ---------------------------------------------------------------- launchers
 
+// Long rows: header | one status word (row scan) or tile sum (top-p) per
+// smallest-geometry segment | one top-p arrival counter per row.
+static size_t topp_arrivals_offset(int64_t rows, int64_t len) {
+    return kWsHeader + (size_t)rows * (size_t)row_segments(len) * sizeof(uint64_t);
+}
 size_t scan_rows_ws_bytes(int64_t rows, int64_t len) {
     if (!long_rows(len)) return kWsHeader;
-    return kWsHeader + (size_t)rows * (size_t)row_segments(len) * sizeof(uint64_t);
+    return topp_arrivals_offset(rows, len) + (size_t)rows * sizeof(uint64_t);
 }
 
 static bool aligned16(const void* p) { return ((uintptr_t)p % 16) == 0; }
@@ -381,26 +337,18 @@ static void rows_long(bool exclusive, bool vec, const T* x, T* y, int64_t rows, 
 template <class G>
 static void topp_long(bool vec, const float* probs, int32_t* cutoff, int64_t rows, int64_t len,
                       float p, void* ws, size_t ws_bytes, hipStream_t stream) {
+    (void)ws_bytes;
     using TV = RowTile<float, G, true>;
     using TU = RowTile<float, G, false>;
     const uint32_t segs = (uint32_t)((len + TV::kElems - 1) / TV::kElems);
     const uint32_t nt = (uint32_t)(rows * segs);
     const unsigned threads = vec ? TV::kThreads : TU::kThreads;
-    if (segs <= kToppMaxSegs) {
-        WsHeader* hdr = reinterpret_cast<WsHeader*>(ws);
-        uint64_t* status = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
-        const int64_t status_words = (int64_t)((ws_bytes - kWsHeader) / sizeof(uint64_t));
-        auto k = vec ? k_topp_onepass<TV, true> : k_topp_onepass<TU, false>;
-        hipLaunchKernelGGL(k, dim3(nt), dim3(threads), 0, stream, probs, cutoff, len, segs, nt, p,
-                           hdr, status, status_words);
-        return;
-    }
-    uint64_t* partial = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
-    auto ks = vec ? k_topp_sums<TV, true> : k_topp_sums<TU, false>;
-    auto ko = vec ? k_topp_owner<TV, true> : k_topp_owner<TU, false>;
-    hipLaunchKernelGGL(ks, dim3(nt), dim3(threads), 0, stream, probs, len, segs, partial);
-    hipLaunchKernelGGL(ko, dim3((unsigned)rows), dim3(threads), 0, stream, probs, cutoff, len, segs,
-                       (const uint64_t*)partial, p);
+    uint64_t* sums = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
+    uint64_t* arrivals = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) +
+                                                     topp_arrivals_offset(rows, len));
+    auto k = vec ? k_topp<TV, true> : k_topp<TU, false>;
+    hipLaunchKernelGGL(k, dim3(nt), dim3(threads), 0, stream, probs, cutoff, len, segs, p,
+                       reinterpret_cast<WsHeader*>(ws), sums, arrivals);
 }
 
 template <class T, bool TOPP>

@@ -229,10 +229,11 @@ def split_by_flags_u32(keys, flags, idx_in=None, with_idx=True, keys_out=None, i
     return keys_out, idx_out, n_true
 
 
-def radix_sort_u32(keys, bits_per_pass=4, with_perm=True, keys_out=None, perm_out=None,
+def radix_sort_u32(keys, bits_per_pass=8, with_perm=True, keys_out=None, perm_out=None,
                    keys_tmp=None, perm_tmp=None, ws=None):
     """Stable ascending sort of uint32 keys (held in an int32 tensor; compare
-    them as unsigned).  Returns (keys_out, perm_out or None)."""
+    them as unsigned), 1, 4 or 8 key bits per pass (8, the fewest passes, by
+    default).  Returns (keys_out, perm_out or None)."""
     _check(keys, torch.int32, "keys")
     n = keys.numel()
     dev = keys.device

@@ -25,6 +25,7 @@ def _big_ws(ops, n):
     from paper_2505_15112_amd import _lib
     sizes = [_lib.workspace_bytes(_lib.OP_SCAN, n), _lib.workspace_bytes(_lib.OP_SCAN_RSS, n),
              _lib.workspace_bytes(_lib.OP_COMPACT, n),
+             _lib.workspace_bytes(_lib.OP_RADIX_SORT, n, bits=8),
              _lib.workspace_bytes(_lib.OP_RADIX_SORT, n, bits=4),
              _lib.workspace_bytes(_lib.OP_RADIX_SORT, n, bits=1),
              _lib.workspace_bytes(_lib.OP_SCAN_ROWS, rows=16, length=n // 16)]
@@ -52,12 +53,23 @@ def _run_all(ops, ws, n, seed):
     assert int(nt.item()) == rn
     assert_equal_first_diff(to_host(io), rio, "split idx")
     rk, rp = oracle.sort_u32(k)
-    for bits in (4, 1):
+    for bits in (8, 4, 1):
         so, sp = ops.radix_sort_u32(to_dev(k.view(np.int32)), bits_per_pass=bits, ws=ws)
         assert_equal_first_diff(to_host(sp), rp, f"radix{bits}")
     xr = x.reshape(16, n // 16)
     assert_equal_first_diff(to_host(ops.scan_rows_i32(to_dev(xr), ws=ws)), oracle.scan_rows_i32(xr),
                             "rows")
+    _check_topp(ops, ws, n, seed)
+
+
+def _check_topp(ops, ws, n, seed):
+    from gpu_util import topp_accept
+    probs = W.topp_probs(16, n // 16, seed=seed)
+    g = to_host(ops.topp_cutoff_f32(to_dev(probs), 0.9, ws=ws))
+    k = oracle.topp_cutoff_f32(probs, 0.9)
+    csum, _ = oracle.scan_rows_f32(probs)
+    bad = [r for r in range(16) if not topp_accept(int(g[r]), int(k[r]), csum[r], 0.9)]
+    assert not bad, ("topp", bad, g[bad], k[bad])
 
 
 def test_one_workspace_for_every_op(ops):
@@ -88,6 +100,24 @@ def test_epoch_wrap(ops):
     assert epoch == 1 << 30
     for seed in (9, 10):
         _run_all(ops, ws, n, seed)
+    assert int(ws[12:16].cpu().numpy().view(np.int32)[0]) == 0
+
+
+def test_topp_after_row_scan_at_high_epoch(ops):
+    """A row scan at an epoch >= 2^29 leaves status words whose bit 61 is set
+    where top-p keeps its tile sums; top-p on the same workspace must not take
+    them for sums."""
+    import torch
+    announce("topp after high-epoch row scan")
+    n = 16 * 40_000
+    ws = _big_ws(ops, n)
+    ws[:8].view(torch.int64).copy_(torch.tensor([((1 << 29) + 5) << 32], dtype=torch.int64,
+                                                device=ws.device))
+    for seed in (11, 12):
+        x = W.scan_i32_full_range(n, seed=seed).reshape(16, n // 16)
+        assert_equal_first_diff(to_host(ops.scan_rows_i32(to_dev(x), ws=ws)),
+                                oracle.scan_rows_i32(x), "rows at high epoch")
+        _check_topp(ops, ws, n, seed)
     assert int(ws[12:16].cpu().numpy().view(np.int32)[0]) == 0
 
 
