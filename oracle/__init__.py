@@ -35,6 +35,9 @@ _SIGNATURES = {
     "oracle_compact_f32": ([_p, _p, _p, _p, _i64], _i64),
     "oracle_split_u32": ([_p, _p, _p, _p, _p, _i64], _i64),
     "oracle_sort_u32": ([_p, _p, _p, _i64], ctypes.c_int),
+    "oracle_sort_i32": ([_p, _p, _p, _i64, ctypes.c_int], ctypes.c_int),
+    "oracle_sort_f32": ([_p, _p, _p, _i64, ctypes.c_int], ctypes.c_int),
+    "oracle_sort_f16": ([_p, _p, _p, _i64, ctypes.c_int], ctypes.c_int),
     "oracle_topp_cutoff_f32": ([_p, _p, _i64, _i64, ctypes.c_float], None),
     "oracle_half_to_double": ([ctypes.c_uint16], ctypes.c_double),
 }
@@ -153,6 +156,27 @@ class Oracle:
         if self.lib.oracle_sort_u32(_ptr(keys), _ptr(ko), _ptr(perm), keys.size) != 0:
             raise MemoryError("oracle_sort_u32: allocation failed")
         return ko, perm
+
+    def _sort_typed(self, name, keys, dtype, bits_dtype, descending):
+        keys = _c(keys, dtype).view(bits_dtype)
+        ko = np.empty(keys.size, bits_dtype)
+        perm = np.empty(keys.size, np.int32)
+        if getattr(self.lib, name)(_ptr(keys), _ptr(ko), _ptr(perm), keys.size,
+                                   int(bool(descending))) != 0:
+            raise MemoryError(f"{name}: allocation failed")
+        return ko.view(dtype), perm
+
+    def sort_i32(self, keys, descending=False):
+        """Stable sort of int32 keys, ascending or descending.  Returns (keys_out, perm)."""
+        return self._sort_typed("oracle_sort_i32", keys, np.int32, np.int32, descending)
+
+    def sort_f32(self, keys, descending=False):
+        """Stable sort of float32 keys in IEEE 754 totalOrder (bit copies)."""
+        return self._sort_typed("oracle_sort_f32", keys, np.float32, np.uint32, descending)
+
+    def sort_f16(self, keys, descending=False):
+        """Stable sort of float16 keys in IEEE 754 totalOrder (bit copies)."""
+        return self._sort_typed("oracle_sort_f16", keys, np.float16, np.uint16, descending)
 
     def topp_cutoff_f32(self, probs, p):
         """Section 5 "Top-p": per row, first index whose float64 running sum >= p."""

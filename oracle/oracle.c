@@ -13,6 +13,7 @@
 #include "oracle.h"
 
 #include <math.h>
+#include <string.h>
 #include <stdlib.h>
 
 /* ---- Section 2: inclusive prefix sum, y_i = x_1 + x_2 + ... + x_i -------- */
@@ -206,6 +207,107 @@ int oracle_sort_u32(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out,
     }
     free(p);
     return 0;
+}
+
+/* ---- Section 5 "Radix Sort" on signed and floating-point keys ---------- */
+
+/* Order of two keys of one type: -1, 0 or 1.  Floats follow IEEE 754
+ * totalOrder, written from its definition: numbers by value, the two zeros by
+ * sign, NaNs outside everything by sign and among themselves by payload. */
+static int oracle_cmp_i32(uint64_t a, uint64_t b) {
+    const int32_t x = (int32_t)(uint32_t)a, y = (int32_t)(uint32_t)b;
+    return x < y ? -1 : (x > y ? 1 : 0);
+}
+
+static int oracle_cmp_float(double x, double y, int sx, int sy, int nanx, int nany, uint32_t payx,
+                            uint32_t payy) {
+    if (!nanx && !nany) {
+        if (x < y) return -1;
+        if (x > y) return 1;
+        if (sx != sy) return sx ? -1 : 1; /* -0 before +0 */
+        return 0;
+    }
+    if (nanx && nany) {
+        if (sx != sy) return sx ? -1 : 1;
+        if (payx == payy) return 0;
+        /* larger payload farther from zero: later if positive, earlier if negative */
+        return ((payx < payy) != (sx != 0)) ? -1 : 1;
+    }
+    if (nanx) return sx ? -1 : 1;
+    return sy ? 1 : -1;
+}
+
+static int oracle_cmp_f32(uint64_t a, uint64_t b) {
+    float x, y;
+    const uint32_t ba = (uint32_t)a, bb = (uint32_t)b;
+    memcpy(&x, &ba, 4);
+    memcpy(&y, &bb, 4);
+    return oracle_cmp_float(x, y, (int)(ba >> 31), (int)(bb >> 31), isnan(x), isnan(y),
+                            ba & 0x7fffffu, bb & 0x7fffffu);
+}
+
+static int oracle_cmp_f16(uint64_t a, uint64_t b) {
+    const uint16_t ha = (uint16_t)a, hb = (uint16_t)b;
+    const double x = oracle_half_to_double(ha), y = oracle_half_to_double(hb);
+    return oracle_cmp_float(x, y, ha >> 15, hb >> 15, isnan(x), isnan(y), ha & 0x3ffu,
+                            hb & 0x3ffu);
+}
+
+typedef struct {
+    uint64_t key;
+    int32_t index;
+} oracle_kpair;
+
+/* qsort comparators take no context: the key order and direction are set
+ * here for the duration of one call (the oracle is single-threaded). */
+static int (*oracle_kcmp)(uint64_t, uint64_t);
+static int oracle_kdesc;
+
+static int oracle_kpair_less(const void* pa, const void* pb) {
+    const oracle_kpair* a = (const oracle_kpair*)pa;
+    const oracle_kpair* b = (const oracle_kpair*)pb;
+    int c = oracle_kcmp(a->key, b->key);
+    if (oracle_kdesc) c = -c;
+    if (c != 0) return c;
+    return (a->index > b->index) - (a->index < b->index); /* ties: index order */
+}
+
+static int oracle_sort_keys(const void* keys, void* keys_out, int32_t* perm_out, int64_t n,
+                            int bytes, int (*cmp)(uint64_t, uint64_t), int descending) {
+    if (n <= 0) return 0;
+    oracle_kpair* p = (oracle_kpair*)malloc((size_t)n * sizeof(oracle_kpair));
+    if (!p) return -1;
+    for (int64_t i = 0; i < n; ++i) {
+        p[i].key = bytes == 4 ? ((const uint32_t*)keys)[i] : ((const uint16_t*)keys)[i];
+        p[i].index = (int32_t)i;
+    }
+    oracle_kcmp = cmp;
+    oracle_kdesc = descending != 0;
+    qsort(p, (size_t)n, sizeof(oracle_kpair), oracle_kpair_less);
+    for (int64_t i = 0; i < n; ++i) {
+        if (bytes == 4)
+            ((uint32_t*)keys_out)[i] = (uint32_t)p[i].key;
+        else
+            ((uint16_t*)keys_out)[i] = (uint16_t)p[i].key;
+        perm_out[i] = p[i].index;
+    }
+    free(p);
+    return 0;
+}
+
+int oracle_sort_i32(const int32_t* keys, int32_t* keys_out, int32_t* perm_out, int64_t n,
+                    int descending) {
+    return oracle_sort_keys(keys, keys_out, perm_out, n, 4, oracle_cmp_i32, descending);
+}
+
+int oracle_sort_f32(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out, int64_t n,
+                    int descending) {
+    return oracle_sort_keys(keys, keys_out, perm_out, n, 4, oracle_cmp_f32, descending);
+}
+
+int oracle_sort_f16(const uint16_t* keys, uint16_t* keys_out, int32_t* perm_out, int64_t n,
+                    int descending) {
+    return oracle_sort_keys(keys, keys_out, perm_out, n, 2, oracle_cmp_f16, descending);
 }
 
 /* ---- Section 5 "Top-p": first index whose running probability mass

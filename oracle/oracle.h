@@ -12,7 +12,7 @@
  *   - floating-point sums are accumulated in double and returned in double,
  *     together with the running sum of |x| that the float tolerance uses.
  * All pointers are host pointers owned by the caller; nothing is allocated
- * except the temporary array of oracle_sort_u32.
+ * except the temporary arrays of the sorts.
  */
 #ifndef LIBSCAN_ORACLE_H
 #define LIBSCAN_ORACLE_H
@@ -67,6 +67,21 @@ int64_t oracle_split_u32(const uint32_t* keys, const int32_t* idx_in, const uint
  * keys_out[i].  Defined as the lexicographic order of (key, source index).
  * Returns 0, or -1 if the temporary array cannot be allocated. */
 int oracle_sort_u32(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out, int64_t n);
+
+/* Section 5 "Radix Sort" on signed integer and floating-point keys (the
+ * paper sorts fp16 and supports signed integers and floats): a stable sort,
+ * ascending or (descending != 0) descending, ties kept in index order.
+ * Integers compare as integers.  Floats compare in IEEE 754 totalOrder:
+ * numerical order, -0 before +0, NaNs with the sign bit set below everything
+ * and the others above, NaNs of one sign ordered by payload (larger payload
+ * farther from zero).  Keys are copied as bit patterns.  Return 0, or -1 if
+ * the temporary array cannot be allocated. */
+int oracle_sort_i32(const int32_t* keys, int32_t* keys_out, int32_t* perm_out, int64_t n,
+                    int descending);
+int oracle_sort_f32(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out, int64_t n,
+                    int descending);
+int oracle_sort_f16(const uint16_t* keys, uint16_t* keys_out, int32_t* perm_out, int64_t n,
+                    int descending);
 
 /* Section 5 "Top-p or Nucleus Sampling": per row of probabilities already
  * sorted in descending order, the first index whose inclusive running sum

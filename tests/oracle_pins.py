@@ -293,6 +293,48 @@ def check_sort_lsd_split(o):
     assert np.array_equal(k4, ko) and np.array_equal(idx4, perm)
 
 
+def check_sort_typed_golden(o):
+    g = _golden("sort_typed.json")
+    for c in g["i32"]:
+        k = np.array(c["keys"], np.int32)
+        for desc, key in ((False, "asc_perm"), (True, "desc_perm")):
+            ko, perm = o.sort_i32(k, descending=desc)
+            assert perm.tolist() == c[key] and np.array_equal(ko, k[perm]), (desc, perm)
+    for name, dt, bt in (("f32_bits", np.float32, np.uint32), ("f16_bits", np.float16, np.uint16)):
+        for c in g[name]:
+            bits = np.array([int(h, 16) for h in c["keys"]], bt)
+            fn = o.sort_f32 if dt is np.float32 else o.sort_f16
+            for desc, key in ((False, "asc_perm"), (True, "desc_perm")):
+                ko, perm = fn(bits.view(dt), descending=desc)
+                assert perm.tolist() == c[key], (name, desc, perm)
+                assert np.array_equal(ko.view(bt), bits[perm]), (name, desc)
+
+
+def check_sort_typed_numpy(o):
+    """Against numpy's stable argsort (ascending, and on the negated keys for
+    descending) where numpy's order is the same: integers, and floats with no
+    NaN and no -0 (numpy ranks -0 and +0 equal)."""
+    rng = np.random.default_rng(17)
+    ki = rng.integers(-2**31, 2**31, 50_000, dtype=np.int64).astype(np.int32)
+    ki[::7] = ki[::7] % 5  # ties
+    ki[:4] = [-2**31, 2**31 - 1, 0, -1]
+    for desc in (False, True):
+        ko, perm = o.sort_i32(ki, descending=desc)
+        ref = np.argsort(-ki.astype(np.int64) if desc else ki, kind="stable").astype(np.int32)
+        assert np.array_equal(perm, ref) and np.array_equal(ko, ki[perm]), desc
+    for dt in (np.float32, np.float16):
+        kf = (rng.standard_normal(40_000) * 100).astype(dt)
+        kf[::5] = np.round(kf[::5] / 10) * 10  # ties
+        kf[kf == 0] = dt(1)  # no zeros of either sign
+        kf[:3] = [np.inf, -np.inf, dt(-2.5)]
+        fn = o.sort_f32 if dt is np.float32 else o.sort_f16
+        for desc in (False, True):
+            ko, perm = fn(kf, descending=desc)
+            ref = np.argsort(-kf if desc else kf, kind="stable").astype(np.int32)
+            assert np.array_equal(perm, ref), (dt, desc)
+            assert np.array_equal(ko, kf[perm]), (dt, desc)
+
+
 # ---------------------------------------------------------------- top-p
 
 def check_topp(o):

@@ -53,6 +53,16 @@ MUTANTS = {
     "sort_descending": ("return a->key < b->key ? -1 : 1;", "return a->key < b->key ? 1 : -1;"),
     "sort_ties_reversed": ("return a->index < b->index ? -1 : (a->index > b->index ? 1 : 0);",
                            "return a->index < b->index ? 1 : (a->index > b->index ? -1 : 0);"),
+    "typed_sort_zeros_unordered": ("if (sx != sy) return sx ? -1 : 1; /* -0 before +0 */",
+                                   "if (sx != sy) return 0; /* -0 before +0 */"),
+    "typed_sort_nan_sign_flipped": ("    if (nanx) return sx ? -1 : 1;\n    return sy ? 1 : -1;",
+                                    "    if (nanx) return sx ? 1 : -1;\n    return sy ? -1 : 1;"),
+    "typed_sort_nan_payload_order": ("return ((payx < payy) != (sx != 0)) ? -1 : 1;",
+                                     "return ((payx < payy) == (sx != 0)) ? -1 : 1;"),
+    "typed_sort_desc_reverses_ties": ("    if (oracle_kdesc) c = -c;\n    if (c != 0) return c;\n    return (a->index > b->index) - (a->index < b->index);",
+                                      "    if (oracle_kdesc) c = -c;\n    if (c != 0) return c;\n    return oracle_kdesc ? (a->index < b->index) - (a->index > b->index) : (a->index > b->index) - (a->index < b->index);"),
+    "typed_sort_i32_unsigned": ("const int32_t x = (int32_t)(uint32_t)a, y = (int32_t)(uint32_t)b;",
+                                "const uint32_t x = (uint32_t)a, y = (uint32_t)b;"),
     "topp_strict_comparison": ("if (c >= pd) {", "if (c > pd) {"),
     "topp_default_len": ("int64_t k = len - 1;", "int64_t k = len;"),
     "topp_exclusive_sum": ("            c += (double)row[i];\n            if (c >= pd) {",
