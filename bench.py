@@ -343,6 +343,19 @@ def main():
                 + (" + 4 (histogram)" if bits > 1 else ""),
                 {"mkeys_per_s": round(n5 / (ms * 1e-3) / 1e6, 1), "passes": passes})
             outputs[f"radix{bits}"] = (ko.clone(), po.clone())
+        # float32 keys, descending (the top-p sampler's order), 8-bit digits
+        kf = torch.from_numpy(W.values_f32(n5, seed=2)).to(dev)
+        kfo = torch.empty_like(kf)
+        kft = torch.empty_like(kf)
+        wsx = ops.workspace(_lib.OP_RADIX_SORT, dev, n5, bits=8)
+        a = (P(kf), P(kfo), P(po), P(kft), P(pt), n5, 1, P(wsx), wsx.numel(), sp)
+        ms = T.back_to_back(lambda: check(lib.radix_sort_f32(*a), "radix f32"), max(3, K // 4), 2)
+        bb = n5 * (12 + 16 * 3 + 4)
+        opsd["radix8_f32_desc_n2^26"] = entry(
+            "radix", ms, bb, memcpy_ms(bb), "12 + 16 x 3 + 4 bytes per key (4 passes)",
+            {"mkeys_per_s": round(n5 / (ms * 1e-3) / 1e6, 1), "passes": 4})
+        del kf, kfo, kft
+
         # stable split on its own (flags Bernoulli(1/2)), n = 2^26
         flags = torch.from_numpy(W.mask_u8(n5, seed=1)).to(dev)
         nt = torch.empty(1, dtype=torch.int32, device=dev)

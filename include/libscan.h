@@ -193,6 +193,29 @@ int radix_sort_u32(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out, 
                    int32_t* perm_tmp, int64_t n, int bits_per_pass, void* ws, size_t ws_bytes,
                    void* stream);
 
+/* LSD radix sort of signed and floating-point keys (Section 5 "Radix Sort":
+ * the keys are encoded so that an unsigned sort orders them -- the most
+ * significant bit of non-negative numbers and every bit of negative ones
+ * inverted; for two's-complement integers only the sign bit -- and decoded
+ * afterwards; the paper sorts fp16 this way).  Here the encoding is applied
+ * by the first pass's loads and undone by the last pass's stores, with 8-bit
+ * digits: 4 passes for 32-bit keys, 2 for fp16.  descending != 0 sorts in
+ * descending order (the code inverted).  Stable either way: ties keep index
+ * order.  Floats follow IEEE 754 totalOrder, the order the encoding gives
+ * every bit pattern: -NaN < -Inf < ... < -0 < +0 < ... < +Inf < +NaN.
+ * keys_out, perm_out (nullable: keys only), keys_tmp and perm_tmp as in
+ * radix_sort_u32 (elements of the key type; no two may overlap).
+ * n <= INT32_MAX.  Workspace: LIBSCAN_OP_RADIX_SORT with n and bits = 8. */
+int radix_sort_i32(const int32_t* keys, int32_t* keys_out, int32_t* perm_out, int32_t* keys_tmp,
+                   int32_t* perm_tmp, int64_t n, int descending, void* ws, size_t ws_bytes,
+                   void* stream);
+int radix_sort_f32(const float* keys, float* keys_out, int32_t* perm_out, float* keys_tmp,
+                   int32_t* perm_tmp, int64_t n, int descending, void* ws, size_t ws_bytes,
+                   void* stream);
+int radix_sort_f16(const uint16_t* keys, uint16_t* keys_out, int32_t* perm_out, uint16_t* keys_tmp,
+                   int32_t* perm_tmp, int64_t n, int descending, void* ws, size_t ws_bytes,
+                   void* stream);
+
 #ifdef __cplusplus
 }
 #endif

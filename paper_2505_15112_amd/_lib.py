@@ -42,6 +42,9 @@ SIGNATURES = {
     "compact_by_mask_f32": (_int, [_p, _p, _p, _p, _p, _i64, _p, _sz, _p]),
     "split_by_flags_u32": (_int, [_p, _p, _p, _p, _p, _p, _i64, _p, _sz, _p]),
     "radix_sort_u32": (_int, [_p, _p, _p, _p, _p, _i64, _int, _p, _sz, _p]),
+    "radix_sort_i32": (_int, [_p, _p, _p, _p, _p, _i64, _int, _p, _sz, _p]),
+    "radix_sort_f32": (_int, [_p, _p, _p, _p, _p, _i64, _int, _p, _sz, _p]),
+    "radix_sort_f16": (_int, [_p, _p, _p, _p, _p, _i64, _int, _p, _sz, _p]),
 }
 
 OK, EINVAL, ENOSPACE, EHIP, ERANGE = 0, -1, -2, -3, -4

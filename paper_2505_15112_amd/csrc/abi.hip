@@ -96,6 +96,27 @@ int scan_rows(Kind kind, const void* x, void* y, int64_t rows, int64_t len, int 
                                            (hipStream_t)stream));
 }
 
+int radix_sort_typed(ls::KeyType type, size_t elem, const void* keys, void* keys_out,
+                     int32_t* perm_out, void* keys_tmp, int32_t* perm_tmp, int64_t n,
+                     int descending, void* ws, size_t ws_bytes, void* stream) {
+    if (n < 0) return LIBSCAN_EINVAL;
+    if (n > INT32_MAX) return LIBSCAN_ERANGE;
+    if (n == 0) return LIBSCAN_OK;
+    if (!keys || !keys_out || !keys_tmp || (perm_out && !perm_tmp)) return LIBSCAN_EINVAL;
+    const size_t kb = (size_t)n * elem, pb = (size_t)n * 4;
+    const void* bufs[5] = {keys, keys_out, perm_out, keys_tmp, perm_out ? perm_tmp : nullptr};
+    const size_t len[5] = {kb, kb, perm_out ? pb : 0, kb, perm_out ? pb : 0};
+    for (int i = 0; i < 5; ++i)
+        for (int j = i + 1; j < 5; ++j)
+            if (overlaps(bufs[i], bufs[i] ? len[i] : 0, bufs[j], bufs[j] ? len[j] : 0))
+                return LIBSCAN_EINVAL;
+    const int w = check_ws(ws, ws_bytes, ls::radix_ws_bytes(n, 8));
+    if (w != LIBSCAN_OK) return w;
+    return hip_status(ls::launch_radix_sort_typed(type, descending != 0, keys, keys_out, perm_out,
+                                                  keys_tmp, perm_tmp, n, ws, ws_bytes,
+                                                  (hipStream_t)stream));
+}
+
 }  // namespace
 
 extern "C" {
@@ -298,6 +319,27 @@ int radix_sort_u32(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out, 
     if (w != LIBSCAN_OK) return w;
     return hip_status(ls::launch_radix_sort(keys, keys_out, perm_out, keys_tmp, perm_tmp, n,
                                             bits_per_pass, ws, ws_bytes, (hipStream_t)stream));
+}
+
+int radix_sort_i32(const int32_t* keys, int32_t* keys_out, int32_t* perm_out, int32_t* keys_tmp,
+                   int32_t* perm_tmp, int64_t n, int descending, void* ws, size_t ws_bytes,
+                   void* stream) {
+    return radix_sort_typed(ls::KeyType::I32, 4, keys, keys_out, perm_out, keys_tmp, perm_tmp, n,
+                            descending, ws, ws_bytes, stream);
+}
+
+int radix_sort_f32(const float* keys, float* keys_out, int32_t* perm_out, float* keys_tmp,
+                   int32_t* perm_tmp, int64_t n, int descending, void* ws, size_t ws_bytes,
+                   void* stream) {
+    return radix_sort_typed(ls::KeyType::F32, 4, keys, keys_out, perm_out, keys_tmp, perm_tmp, n,
+                            descending, ws, ws_bytes, stream);
+}
+
+int radix_sort_f16(const uint16_t* keys, uint16_t* keys_out, int32_t* perm_out, uint16_t* keys_tmp,
+                   int32_t* perm_tmp, int64_t n, int descending, void* ws, size_t ws_bytes,
+                   void* stream) {
+    return radix_sort_typed(ls::KeyType::F16, 2, keys, keys_out, perm_out, keys_tmp, perm_tmp, n,
+                            descending, ws, ws_bytes, stream);
 }
 
 }  // extern "C"

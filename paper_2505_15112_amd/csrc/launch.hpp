@@ -48,6 +48,14 @@ hipError_t launch_split(const uint32_t* keys, const int32_t* idx_in, const uint8
                         uint32_t* keys_out, int32_t* idx_out, int32_t* n_true_out, int64_t n,
                         void* ws, size_t ws_bytes, hipStream_t stream);
 
+// Key types of the typed radix sorts (8-bit digits; encoded on the first pass,
+// decoded on the last).
+enum class KeyType { U32, I32, F32, F16 };
+hipError_t launch_radix_sort_typed(KeyType type, bool descending, const void* keys,
+                                   void* keys_out, int32_t* perm_out, void* keys_tmp,
+                                   int32_t* perm_tmp, int64_t n, void* ws, size_t ws_bytes,
+                                   hipStream_t stream);
+
 // LSD radix sort (1, 4 or 8 bits per pass), caller-provided ping-pong buffers.
 size_t radix_ws_bytes(int64_t n, int bits);
 hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out,

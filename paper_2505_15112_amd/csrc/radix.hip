@@ -317,6 +317,29 @@ __global__ __launch_bounds__(kR4Waves* kWave) LS_OCCUPANCY4 void k_radix4_scatte
     }
 }
 
+// ---------------------------------------------------------------- key codes
+
+// Signed and floating-point keys sort as unsigned integers after an encoding
+// (Section 5 "Radix Sort": invert the most significant bit of non-negative
+// numbers and every bit of negative ones; signed integers only need the
+// most significant bit inverted), and are decoded when the last pass writes
+// them.  Descending order inverts every bit of the code as well.  The first
+// pass applies `code` on its loads, the last pass `decode` on its stores;
+// every other pass (and the plain unsigned sort) uses the identity.
+struct KeyCode {
+    uint32_t pos, neg;  // code(k) = k ^ (sign bit of k ? neg : pos)
+    int top;            // sign bit position: 31 (32-bit keys) or 15 (16-bit)
+    __device__ uint32_t apply(uint32_t k) const { return k ^ (((k >> top) & 1u) ? neg : pos); }
+};
+struct KeyDecode {
+    uint32_t pre, one, zero;  // e' = e ^ pre; k = e' ^ (bit top of e' ? one : zero)
+    int top;
+    __device__ uint32_t apply(uint32_t e) const {
+        e ^= pre;
+        return e ^ (((e >> top) & 1u) ? one : zero);
+    }
+};
+
 // ---------------------------------------------------------------- 8-bit pass
 
 // 4 passes of 8-bit digits: the same count -> scan -> scatter structure as the
@@ -350,8 +373,10 @@ __device__ __forceinline__ uint64_t peers8(uint32_t d, bool ok) {
 // with plain LDS atomics, into 4 histograms per wave (picked by lane & 3) so
 // that equal digits in one instruction collide at most 16 ways.
 constexpr int kR8Sub = 4;
+template <class K>
 __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_count(
-    const uint32_t* keys, int64_t n, int shift, bool vec, uint32_t* counts, uint32_t ntiles) {
+    const K* keys, int64_t n, int shift, bool vec, uint32_t* counts, uint32_t ntiles,
+    KeyCode code) {
     __shared__ uint32_t s_h[kR8Waves * kR8Sub][kR8Digits];
     for (int i = threadIdx.x; i < kR8Waves * kR8Sub * kR8Digits; i += kR8Waves * kWave)
         (&s_h[0][0])[i] = 0;
@@ -361,23 +386,23 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_count(
     uint32_t* h = s_h[w * kR8Sub + (lane & (kR8Sub - 1))];
     const int64_t tbase = (int64_t)blockIdx.x * kR8Tile;
     const int64_t wbase = tbase + (int64_t)w * kR8Chunks * kWave;
-    if (vec && tbase + kR8Tile <= n) {  // this wave's 1024 keys as 4 x 16-byte loads per lane
+    if (sizeof(K) == 4 && vec && tbase + kR8Tile <= n) {  // 4 x 16-byte loads per lane
         const u32x4* k4 = reinterpret_cast<const u32x4*>(keys + wbase);
         u32x4 v[kR8Chunks / 4];
 #pragma unroll
         for (int j = 0; j < kR8Chunks / 4; ++j) v[j] = k4[j * kWave + lane];
 #pragma unroll
         for (int j = 0; j < kR8Chunks / 4; ++j) {
-            atomicAdd(&h[(v[j].x >> shift) & 255u], 1u);
-            atomicAdd(&h[(v[j].y >> shift) & 255u], 1u);
-            atomicAdd(&h[(v[j].z >> shift) & 255u], 1u);
-            atomicAdd(&h[(v[j].w >> shift) & 255u], 1u);
+            atomicAdd(&h[(code.apply(v[j].x) >> shift) & 255u], 1u);
+            atomicAdd(&h[(code.apply(v[j].y) >> shift) & 255u], 1u);
+            atomicAdd(&h[(code.apply(v[j].z) >> shift) & 255u], 1u);
+            atomicAdd(&h[(code.apply(v[j].w) >> shift) & 255u], 1u);
         }
     } else {
 #pragma unroll
         for (int j = 0; j < kR8Chunks; ++j) {
             const int64_t i = wbase + j * kWave + lane;
-            if (i < n) atomicAdd(&h[(keys[i] >> shift) & 255u], 1u);
+            if (i < n) atomicAdd(&h[(code.apply((uint32_t)keys[i]) >> shift) & 255u], 1u);
         }
     }
     __syncthreads();
@@ -391,10 +416,10 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_count(
 
 // Rank and scatter one tile of 8192 keys (one key per lane per chunk, so the
 // chunk's index order is the lane order) with the offsets from the spine.
-template <bool HAS_PERM_IN, bool WITH_PERM>
+template <class K, bool HAS_PERM_IN, bool WITH_PERM>
 __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatter(
-    const uint32_t* keys_in, const int32_t* perm_in, uint32_t* keys_out, int32_t* perm_out,
-    int64_t n, int shift, uint32_t* offsets, uint32_t ntiles) {
+    const K* keys_in, const int32_t* perm_in, K* keys_out, int32_t* perm_out, int64_t n,
+    int shift, uint32_t* offsets, uint32_t ntiles, KeyCode code, KeyDecode decode) {
     __shared__ uint32_t s_wh[kR8Waves][kR8Digits];  // wave counts, then each wave's first slot
     __shared__ uint32_t s_tstart[kR8Digits];         // first slot of digit d in the tile
     __shared__ uint32_t s_gbase[kR8Digits];          // global position of that slot
@@ -419,7 +444,7 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
 #pragma unroll
     for (int j = 0; j < kR8Chunks; ++j) {
         const int64_t i = wbase + j * kWave + lane;
-        key[j] = (full || i < n) ? keys_in[i] : 0u;
+        key[j] = (full || i < n) ? code.apply((uint32_t)keys_in[i]) : 0u;
     }
     __syncthreads();
 
@@ -503,7 +528,7 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
         if (t < valid) {
             const uint32_t d = (skey[j] >> shift) & 255u;
             const uint32_t pos = s_gbase[d] + (t - s_tstart[d]);
-            if (pos < (uint64_t)n) keys_out[pos] = skey[j];  // pos < n always; guards a bad count
+            if (pos < (uint64_t)n) keys_out[pos] = (K)decode.apply(skey[j]);  // pos < n always
         }
     }
     if (WITH_PERM) {
@@ -551,6 +576,44 @@ size_t radix_ws_bytes(int64_t n, int bits) {
            (size_t)kHistBlocks * kHistWords * sizeof(uint32_t);
 }
 
+constexpr KeyCode kIdentityCode{0u, 0u, 31};
+constexpr KeyDecode kIdentityDecode{0u, 0u, 0u, 31};
+
+// `passes` 8-bit passes over keys of type K (4 for 32-bit keys, 2 for 16-bit),
+// ping-ponging keys_tmp / keys_out (an even number of passes ends in
+// keys_out); the first pass encodes the keys, the last one decodes them.
+template <class K>
+static hipError_t radix8_sort(const K* keys, K* keys_out, int32_t* perm_out, K* keys_tmp,
+                              int32_t* perm_tmp, int64_t n, int passes, KeyCode code,
+                              KeyDecode decode, void* ws, hipStream_t stream) {
+    const uint32_t nt = (uint32_t)r8_tiles(n);
+    const size_t toff = digit_table_offset(n, 8);
+    uint32_t* counts = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + toff);
+    const K* src_k = keys;
+    const int32_t* src_p = nullptr;
+    for (int p = 0; p < passes; ++p) {
+        K* dk = (p % 2 == 0) ? keys_tmp : keys_out;
+        int32_t* dp = perm_out ? ((p % 2 == 0) ? perm_tmp : perm_out) : nullptr;
+        const KeyCode c = p == 0 ? code : kIdentityCode;
+        const KeyDecode d = p == passes - 1 ? decode : kIdentityDecode;
+        const bool vec = ((uintptr_t)src_k % 16) == 0;
+        hipLaunchKernelGGL(k_radix8_count<K>, dim3(nt), dim3(kR8Waves * kWave), 0, stream, src_k, n,
+                           8 * p, vec, counts, nt, c);
+        hipError_t e = launch_scan1d(Kind::I32, true, counts, counts, digit_table_entries(n, 8),
+                                     nullptr, nullptr, ws, toff, stream);
+        if (e != hipSuccess) return e;
+        auto k = dp ? (src_p ? k_radix8_scatter<K, true, true> : k_radix8_scatter<K, false, true>)
+                    : k_radix8_scatter<K, false, false>;
+        hipLaunchKernelGGL(k, dim3(nt), dim3(kR8Waves * kWave), 0, stream, src_k, src_p, dk, dp, n,
+                           8 * p, counts, nt, c, d);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        src_k = dk;
+        src_p = dp;
+    }
+    return hipSuccess;
+}
+
 hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out,
                              uint32_t* keys_tmp, int32_t* perm_tmp, int64_t n, int bits, void* ws,
                              size_t ws_bytes, hipStream_t stream) {
@@ -592,26 +655,52 @@ hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* 
             e = hipGetLastError();
             if (e != hipSuccess) return e;
         } else {
-            const uint32_t nt = (uint32_t)r8_tiles(n);
-            const size_t toff = digit_table_offset(n, 8);
-            uint32_t* counts = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + toff);
-            const bool vec = ((uintptr_t)src_k % 16) == 0;
-            hipLaunchKernelGGL(k_radix8_count, dim3(nt), dim3(kR8Waves * kWave), 0, stream, src_k, n,
-                               8 * p, vec, counts, nt);
-            hipError_t e = launch_scan1d(Kind::I32, true, counts, counts, digit_table_entries(n, 8),
-                                         nullptr, nullptr, ws, toff, stream);
-            if (e != hipSuccess) return e;
-            auto k = dp ? (src_p ? k_radix8_scatter<true, true> : k_radix8_scatter<false, true>)
-                        : k_radix8_scatter<false, false>;
-            hipLaunchKernelGGL(k, dim3(nt), dim3(kR8Waves * kWave), 0, stream, src_k, src_p, dk, dp,
-                               n, 8 * p, counts, nt);
-            e = hipGetLastError();
-            if (e != hipSuccess) return e;
+            return radix8_sort<uint32_t>(keys, keys_out, perm_out, keys_tmp, perm_tmp, n, 4,
+                                         kIdentityCode, kIdentityDecode, ws, stream);
         }
         src_k = dk;
         src_p = dp;
     }
     return hipSuccess;
+}
+
+hipError_t launch_radix_sort_typed(KeyType type, bool descending, const void* keys,
+                                   void* keys_out, int32_t* perm_out, void* keys_tmp,
+                                   int32_t* perm_tmp, int64_t n, void* ws, size_t ws_bytes,
+                                   hipStream_t stream) {
+    (void)ws_bytes;
+    if (n == 0) return hipSuccess;
+    const bool wide = type != KeyType::F16;
+    const uint32_t all = wide ? 0xFFFFFFFFu : 0xFFFFu;
+    const uint32_t msb = wide ? 0x80000000u : 0x8000u;
+    const int top = wide ? 31 : 15;
+    KeyCode code{0u, 0u, top};
+    KeyDecode decode{0u, 0u, 0u, top};
+    switch (type) {
+        case KeyType::U32:
+            break;
+        case KeyType::I32:  // two's complement: invert the sign bit
+            code.pos = code.neg = msb;
+            decode.one = decode.zero = msb;
+            break;
+        case KeyType::F32:
+        case KeyType::F16:  // sign-magnitude: non-negative -> set the sign bit, negative -> invert all
+            code.pos = msb;
+            code.neg = all;
+            decode.one = msb;   // code with the top bit set came from a non-negative key
+            decode.zero = all;  // code with the top bit clear came from a negative key
+            break;
+    }
+    if (descending) {
+        code.pos ^= all;
+        code.neg ^= all;
+        decode.pre = all;
+    }
+    if (wide)
+        return radix8_sort<uint32_t>((const uint32_t*)keys, (uint32_t*)keys_out, perm_out,
+                                     (uint32_t*)keys_tmp, perm_tmp, n, 4, code, decode, ws, stream);
+    return radix8_sort<uint16_t>((const uint16_t*)keys, (uint16_t*)keys_out, perm_out,
+                                 (uint16_t*)keys_tmp, perm_tmp, n, 2, code, decode, ws, stream);
 }
 
 }  // namespace ls

@@ -250,3 +250,45 @@ def radix_sort_u32(keys, bits_per_pass=8, with_perm=True, keys_out=None, perm_ou
         _lib.call("radix_sort_u32", _ptr(keys), _ptr(keys_out), _ptr(perm_out), _ptr(keys_tmp),
                   _ptr(perm_tmp), n, int(bits_per_pass), _ptr(ws), ws.numel(), _stream(dev))
     return keys_out, perm_out
+
+
+def _radix_sort_typed(cname, keys, dtype, descending, with_perm, keys_out, perm_out, keys_tmp,
+                      perm_tmp, ws):
+    _check(keys, dtype, "keys")
+    n = keys.numel()
+    dev = keys.device
+    keys_out = _out(keys, keys_out, dtype, shape=(n,))
+    keys_tmp = torch.empty(n, dtype=dtype, device=dev) if keys_tmp is None else keys_tmp
+    if with_perm:
+        perm_out = torch.empty(n, dtype=torch.int32, device=dev) if perm_out is None else perm_out
+        perm_tmp = torch.empty(n, dtype=torch.int32, device=dev) if perm_tmp is None else perm_tmp
+    else:
+        perm_out = perm_tmp = None
+    if ws is None:
+        ws = workspace(_lib.OP_RADIX_SORT, dev, n, bits=8)
+    with torch.cuda.device(dev):
+        _lib.call(cname, _ptr(keys), _ptr(keys_out), _ptr(perm_out), _ptr(keys_tmp),
+                  _ptr(perm_tmp), n, int(bool(descending)), _ptr(ws), ws.numel(), _stream(dev))
+    return keys_out, perm_out
+
+
+def radix_sort_i32(keys, descending=False, with_perm=True, keys_out=None, perm_out=None,
+                   keys_tmp=None, perm_tmp=None, ws=None):
+    """Stable sort of int32 keys, ascending or descending.  Returns (keys_out, perm_out or None)."""
+    return _radix_sort_typed("radix_sort_i32", keys, torch.int32, descending, with_perm, keys_out,
+                             perm_out, keys_tmp, perm_tmp, ws)
+
+
+def radix_sort_f32(keys, descending=False, with_perm=True, keys_out=None, perm_out=None,
+                   keys_tmp=None, perm_tmp=None, ws=None):
+    """Stable sort of float32 keys in IEEE 754 totalOrder (-NaN < -Inf < ... < -0 < +0 < ... <
+    +Inf < +NaN), ascending or descending.  Returns (keys_out, perm_out or None)."""
+    return _radix_sort_typed("radix_sort_f32", keys, torch.float32, descending, with_perm,
+                             keys_out, perm_out, keys_tmp, perm_tmp, ws)
+
+
+def radix_sort_f16(keys, descending=False, with_perm=True, keys_out=None, perm_out=None,
+                   keys_tmp=None, perm_tmp=None, ws=None):
+    """Stable sort of float16 keys in IEEE 754 totalOrder, ascending or descending."""
+    return _radix_sort_typed("radix_sort_f16", keys, torch.float16, descending, with_perm,
+                             keys_out, perm_out, keys_tmp, perm_tmp, ws)

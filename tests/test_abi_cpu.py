@@ -162,6 +162,23 @@ def test_split_validation(lib):
     assert fn(None, None, None, None, None, None, 0, None, 0, None) == _lib.OK
 
 
+@pytest.mark.parametrize("name,elem", [("radix_sort_i32", 4), ("radix_sort_f32", 4),
+                                       ("radix_sort_f16", 2)])
+def test_typed_radix_validation(lib, name, elem):
+    fn = getattr(lib, name)
+    KO, PO, KT, PT = P(0x2000000), P(0x3000000), P(0x4000000), P(0x5000000)
+    W2 = P(0x60000000)
+    assert fn(X, KO, PO, KT, PT, -1, 0, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, KO, PO, None, PT, 10, 0, W2, BIG, None) == _lib.EINVAL      # no keys_tmp
+    assert fn(X, KO, PO, KT, None, 10, 1, W2, BIG, None) == _lib.EINVAL      # perm without tmp
+    assert fn(X, X, PO, KT, PT, 10, 0, W2, BIG, None) == _lib.EINVAL         # in place
+    # keys_tmp overlapping keys_out by one element
+    assert fn(X, KO, PO, P(0x2000000 + 9 * elem), PT, 10, 0, W2, BIG, None) == _lib.EINVAL
+    assert fn(XB, YB, None, P(1 << 42), None, 1 << 31, 0, W2, BIG, None) == _lib.ERANGE
+    assert fn(X, KO, PO, KT, PT, 1000, 0, W2, 64, None) == _lib.ENOSPACE
+    assert fn(None, None, None, None, None, 0, 1, None, 0, None) == _lib.OK
+
+
 def test_radix_validation(lib):
     fn = lib.radix_sort_u32
     KO, PO, KT, PT = P(0x2000000), P(0x3000000), P(0x4000000), P(0x5000000)
