@@ -38,6 +38,9 @@ _SIGNATURES = {
     "oracle_sort_i32": ([_p, _p, _p, _i64, ctypes.c_int], ctypes.c_int),
     "oracle_sort_f32": ([_p, _p, _p, _i64, ctypes.c_int], ctypes.c_int),
     "oracle_sort_f16": ([_p, _p, _p, _i64, ctypes.c_int], ctypes.c_int),
+    "oracle_sort_rows_f32": ([_p, _p, _p, _i64, _i64, ctypes.c_int], ctypes.c_int),
+    "oracle_weighted_sample_f32": ([_p, _p, _p, _i64, _i64], None),
+    "oracle_topp_sample_f32": ([_p, _p, ctypes.c_float, _p, _p, _i64, _i64], ctypes.c_int),
     "oracle_topp_cutoff_f32": ([_p, _p, _i64, _i64, ctypes.c_float], None),
     "oracle_half_to_double": ([ctypes.c_uint16], ctypes.c_double),
 }
@@ -177,6 +180,39 @@ class Oracle:
     def sort_f16(self, keys, descending=False):
         """Stable sort of float16 keys in IEEE 754 totalOrder (bit copies)."""
         return self._sort_typed("oracle_sort_f16", keys, np.float16, np.uint16, descending)
+
+    def sort_rows_f32(self, keys, descending=False):
+        """Every row sorted on its own (stable, totalOrder); returns (keys_out, in-row idx)."""
+        keys = _c(keys, np.float32)
+        rows, length = keys.shape
+        b = keys.view(np.uint32)
+        ko = np.empty_like(b)
+        idx = np.empty(keys.shape, np.int32)
+        if self.lib.oracle_sort_rows_f32(_ptr(b), _ptr(ko), _ptr(idx), rows, length,
+                                         int(bool(descending))) != 0:
+            raise MemoryError("oracle_sort_rows_f32: allocation failed")
+        return ko.view(np.float32), idx
+
+    def weighted_sample_f32(self, w, theta):
+        """Appendix "Weighted Sampling": per row, first i with S_i > theta * W."""
+        w = _c(w, np.float32)
+        rows, length = w.shape
+        theta = _c(theta, np.float32)
+        out = np.empty(rows, np.int32)
+        self.lib.oracle_weighted_sample_f32(_ptr(w), _ptr(theta), _ptr(out), rows, length)
+        return out
+
+    def topp_sample_f32(self, probs, theta, p):
+        """Section 5 "Top-p" sampler on unsorted rows: returns (token, cutoff) per row."""
+        probs = _c(probs, np.float32)
+        rows, length = probs.shape
+        theta = _c(theta, np.float32)
+        tok = np.empty(rows, np.int32)
+        cut = np.empty(rows, np.int32)
+        if self.lib.oracle_topp_sample_f32(_ptr(probs), _ptr(theta), float(p), _ptr(tok),
+                                           _ptr(cut), rows, length) != 0:
+            raise MemoryError("oracle_topp_sample_f32: allocation failed")
+        return tok, cut
 
     def topp_cutoff_f32(self, probs, p):
         """Section 5 "Top-p": per row, first index whose float64 running sum >= p."""

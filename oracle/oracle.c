@@ -330,3 +330,72 @@ void oracle_topp_cutoff_f32(const float* probs, int32_t* cutoff, int64_t rows, i
         cutoff[r] = (int32_t)k;
     }
 }
+
+/* ---- Batched sorts and the samplers ------------------------------------ */
+
+int oracle_sort_rows_f32(const uint32_t* keys, uint32_t* keys_out, int32_t* idx_out, int64_t rows,
+                         int64_t len, int descending) {
+    for (int64_t r = 0; r < rows; ++r)
+        if (oracle_sort_f32(keys + r * len, keys_out + r * len, idx_out + r * len, len,
+                            descending) != 0)
+            return -1;
+    return 0;
+}
+
+/* First i in [0, limit] with s[i] > u (running sums in double), else limit. */
+static int64_t oracle_first_above(const float* w, int64_t limit, double u) {
+    double acc = 0.0;
+    for (int64_t i = 0; i <= limit; ++i) {
+        acc += (double)w[i];
+        if (acc > u) return i;
+    }
+    return limit;
+}
+
+void oracle_weighted_sample_f32(const float* w, const float* theta, int32_t* out, int64_t rows,
+                                int64_t len) {
+    for (int64_t r = 0; r < rows; ++r) {
+        const float* row = w + r * len;
+        if (len == 0) {
+            out[r] = -1;
+            continue;
+        }
+        double total = 0.0;
+        for (int64_t i = 0; i < len; ++i) total += (double)row[i];
+        out[r] = (int32_t)oracle_first_above(row, len - 1, (double)theta[r] * total);
+    }
+}
+
+int oracle_topp_sample_f32(const float* probs, const float* theta, float p, int32_t* token_out,
+                           int32_t* cutoff_out, int64_t rows, int64_t len) {
+    if (len == 0) {
+        for (int64_t r = 0; r < rows; ++r) {
+            token_out[r] = -1;
+            if (cutoff_out) cutoff_out[r] = -1;
+        }
+        return 0;
+    }
+    uint32_t* sorted = (uint32_t*)malloc((size_t)len * sizeof(uint32_t));
+    int32_t* idx = (int32_t*)malloc((size_t)len * sizeof(int32_t));
+    if (!sorted || !idx) {
+        free(sorted);
+        free(idx);
+        return -1;
+    }
+    int rc = 0;
+    for (int64_t r = 0; r < rows && rc == 0; ++r) {
+        rc = oracle_sort_f32((const uint32_t*)(probs + r * len), sorted, idx, len, 1);
+        if (rc != 0) break;
+        const float* s = (const float*)sorted;
+        int32_t k;
+        oracle_topp_cutoff_f32(s, &k, 1, len, p);
+        double ck = 0.0;
+        for (int64_t i = 0; i <= k; ++i) ck += (double)s[i];
+        const int64_t j = oracle_first_above(s, k, (double)theta[r] * ck);
+        token_out[r] = idx[j];
+        if (cutoff_out) cutoff_out[r] = k;
+    }
+    free(sorted);
+    free(idx);
+    return rc;
+}

@@ -83,6 +83,29 @@ int oracle_sort_f32(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out,
 int oracle_sort_f16(const uint16_t* keys, uint16_t* keys_out, int32_t* perm_out, int64_t n,
                     int descending);
 
+/* Batched form of the float sort (as the appendix "Multiple (Batched) Scans"
+ * batches scans): every row of a row-major rows x len matrix sorted on its own,
+ * stably; idx_out holds each key's index within its row. */
+int oracle_sort_rows_f32(const uint32_t* keys, uint32_t* keys_out, int32_t* idx_out, int64_t rows,
+                         int64_t len, int descending);
+
+/* Appendix "Weighted Sampling": inverse transform sampling from the scan of
+ * the weights.  Per row, with S_i the inclusive running sum (in double) and
+ * W = S_{len-1}: the first index with S_i > theta * W (len - 1 if rounding
+ * leaves none; -1 for len = 0). */
+void oracle_weighted_sample_f32(const float* w, const float* theta, int32_t* out, int64_t rows,
+                                int64_t len);
+
+/* Section 5 "Top-p or Nucleus Sampling" as a whole sampler: per row of
+ * (unsorted) probabilities, sort them in descending order (stably), take the
+ * cutoff k of the sorted row (oracle_topp_cutoff_f32), and draw one of the
+ * kept tokens 0..k by inverse transform: the first i <= k whose running sum
+ * exceeds theta * C_k (k if rounding leaves none).  token_out is the drawn
+ * token's index in the unsorted row; cutoff_out (nullable) receives k.
+ * len = 0 gives -1 for both.  Returns 0, or -1 on allocation failure. */
+int oracle_topp_sample_f32(const float* probs, const float* theta, float p, int32_t* token_out,
+                           int32_t* cutoff_out, int64_t rows, int64_t len);
+
 /* Section 5 "Top-p or Nucleus Sampling": per row of probabilities already
  * sorted in descending order, the first index whose inclusive running sum
  * (in double) reaches p, or len - 1 if it never does. */

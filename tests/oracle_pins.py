@@ -335,6 +335,65 @@ def check_sort_typed_numpy(o):
             assert np.array_equal(ko, kf[perm]), (dt, desc)
 
 
+def check_sort_rows(o):
+    """Each row equals numpy's stable argsort of that row (finite, no -0)."""
+    rng = np.random.default_rng(23)
+    x = (rng.standard_normal((7, 1000)) * 10).astype(np.float32)
+    x[:, ::4] = np.round(x[:, ::4])
+    x[x == 0] = 1.0
+    for desc in (False, True):
+        ko, idx = o.sort_rows_f32(x, descending=desc)
+        for r in range(x.shape[0]):
+            ref = np.argsort(-x[r] if desc else x[r], kind="stable")
+            assert np.array_equal(idx[r], ref) and np.array_equal(ko[r], x[r][ref]), (r, desc)
+
+
+def check_weighted_sample(o):
+    """Appendix "Weighted Sampling": equal weights give floor(theta * len) in
+    closed form; random weights match numpy's searchsorted(side='right') on
+    the float64 cumulative sum."""
+    for length in (1, 7, 1000):
+        th = np.array([0.0, 0.25, 0.5, 0.999, 0.3], np.float32)
+        w = np.ones((th.size, length), np.float32)
+        got = o.weighted_sample_f32(w, th)
+        want = np.minimum(np.floor(th.astype(np.float64) * length), length - 1).astype(np.int32)
+        assert np.array_equal(got, want), (length, got, want)
+    rng = np.random.default_rng(29)
+    w = rng.random((50, 300)).astype(np.float32)
+    w[:, ::3] = 0  # zero weights are never drawn
+    th = rng.random(50).astype(np.float32)
+    got = o.weighted_sample_f32(w, th)
+    for r in range(50):
+        c = np.cumsum(w[r].astype(np.float64))
+        j = int(np.searchsorted(c, float(th[r]) * c[-1], side="right"))
+        assert got[r] == min(j, 299) and w[r, got[r]] > 0, r
+
+
+def check_topp_sample(o):
+    """The top-p sampler against a numpy composition of its definition:
+    stable descending argsort, float64 cumulative sum, searchsorted cutoff,
+    inverse-transform draw among the kept tokens."""
+    rng = np.random.default_rng(31)
+    probs = W.topp_probs(40, 2048, seed=3)
+    probs = np.stack([r[rng.permutation(r.size)] for r in probs])  # unsorted rows
+    th = rng.random(40).astype(np.float32)
+    for p in (0.9, 0.5, 1e-9, 1.5):
+        tok, cut = o.topp_sample_f32(probs, th, p)
+        pf = float(np.float32(p))
+        for r in range(40):
+            order = np.argsort(-probs[r], kind="stable")
+            c = np.cumsum(probs[r][order].astype(np.float64))
+            k = min(int(np.searchsorted(c, pf, side="left")), 2047)
+            j = min(int(np.searchsorted(c[: k + 1], float(th[r]) * c[k], side="right")), k)
+            assert cut[r] == k and tok[r] == order[j], (p, r)
+    # a hand-worked row: probabilities 0.1 0.4 0.2 0.3, p = 0.65 keeps the
+    # sorted tokens 1 (0.4) and 3 (0.3) (0.4 + 0.3 = 0.7 >= 0.65); theta = 0.6
+    # draws from C = 0.4, 0.7 at u = 0.42: the second kept token, 3.
+    tok, cut = o.topp_sample_f32(np.array([[0.1, 0.4, 0.2, 0.3]], np.float32),
+                                 np.array([0.6], np.float32), 0.65)
+    assert cut.tolist() == [1] and tok.tolist() == [3], (tok, cut)
+
+
 # ---------------------------------------------------------------- top-p
 
 def check_topp(o):

@@ -63,6 +63,12 @@ MUTANTS = {
                                       "    if (oracle_kdesc) c = -c;\n    if (c != 0) return c;\n    return oracle_kdesc ? (a->index < b->index) - (a->index > b->index) : (a->index > b->index) - (a->index < b->index);"),
     "typed_sort_i32_unsigned": ("const int32_t x = (int32_t)(uint32_t)a, y = (int32_t)(uint32_t)b;",
                                 "const uint32_t x = (uint32_t)a, y = (uint32_t)b;"),
+    "weighted_sample_ge": ("        if (acc > u) return i;", "        if (acc >= u) return i;"),
+    "topp_sample_ascending": ("rc = oracle_sort_f32((const uint32_t*)(probs + r * len), sorted, idx, len, 1);",
+                              "rc = oracle_sort_f32((const uint32_t*)(probs + r * len), sorted, idx, len, 0);"),
+    "topp_sample_whole_row_mass": ("for (int64_t i = 0; i <= k; ++i) ck += (double)s[i];",
+                                   "for (int64_t i = 0; i < len; ++i) ck += (double)s[i];"),
+    "topp_sample_sorted_position": ("        token_out[r] = idx[j];", "        token_out[r] = (int32_t)j;"),
     "topp_strict_comparison": ("if (c >= pd) {", "if (c > pd) {"),
     "topp_default_len": ("int64_t k = len - 1;", "int64_t k = len;"),
     "topp_exclusive_sum": ("            c += (double)row[i];\n            if (c >= pd) {",
