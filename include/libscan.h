@@ -67,7 +67,10 @@ int libscan_workspace_init(void* ws, size_t ws_bytes, void* stream);
 #define LIBSCAN_OP_SCAN_RSS 2 /* scan_inclusive_rss_* (reduce-then-scan) */
 #define LIBSCAN_OP_SCAN_ROWS 3 /* scan_rows_* and topp_cutoff_f32 (rows, len) */
 #define LIBSCAN_OP_COMPACT 4   /* compact_by_mask_f32 and split_by_flags_u32 (n) */
-#define LIBSCAN_OP_RADIX_SORT 5 /* radix_sort_u32 (n, bits = bits_per_pass) */
+#define LIBSCAN_OP_RADIX_SORT 5 /* radix_sort_u32 (n, bits = bits_per_pass); typed sorts (bits = 8) */
+#define LIBSCAN_OP_SORT_ROWS 6  /* radix_sort_rows_f32 (rows, len) */
+#define LIBSCAN_OP_WEIGHTED_SAMPLE 7 /* weighted_sample_f32 (rows, len) */
+#define LIBSCAN_OP_TOPP_SAMPLE 8 /* topp_sample_f32 (rows, len) */
 
 /*
  * Workspace size in bytes that op needs for n elements (rows/len/bits are
@@ -187,7 +190,7 @@ int split_by_flags_u32(const uint32_t* keys, const int32_t* idx_in, const uint8_
  * splits); all give the same output.  keys_tmp
  * (and perm_tmp when perm_out is given) are caller-provided n-element
  * ping-pong buffers whose contents are clobbered.  No two of keys, keys_out,
- * perm_out, keys_tmp, perm_tmp may overlap.  n <= INT32_MAX.  Workspace:
+ * perm_out, keys_tmp, perm_tmp may overlap.  n <= 2^30.  Workspace:
  * LIBSCAN_OP_RADIX_SORT with n and bits = bits_per_pass. */
 int radix_sort_u32(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out, uint32_t* keys_tmp,
                    int32_t* perm_tmp, int64_t n, int bits_per_pass, void* ws, size_t ws_bytes,
@@ -205,7 +208,7 @@ int radix_sort_u32(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out, 
  * every bit pattern: -NaN < -Inf < ... < -0 < +0 < ... < +Inf < +NaN.
  * keys_out, perm_out (nullable: keys only), keys_tmp and perm_tmp as in
  * radix_sort_u32 (elements of the key type; no two may overlap).
- * n <= INT32_MAX.  Workspace: LIBSCAN_OP_RADIX_SORT with n and bits = 8. */
+ * n <= 2^30.  Workspace: LIBSCAN_OP_RADIX_SORT with n and bits = 8. */
 int radix_sort_i32(const int32_t* keys, int32_t* keys_out, int32_t* perm_out, int32_t* keys_tmp,
                    int32_t* perm_tmp, int64_t n, int descending, void* ws, size_t ws_bytes,
                    void* stream);
@@ -215,6 +218,50 @@ int radix_sort_f32(const float* keys, float* keys_out, int32_t* perm_out, float*
 int radix_sort_f16(const uint16_t* keys, uint16_t* keys_out, int32_t* perm_out, uint16_t* keys_tmp,
                    int32_t* perm_tmp, int64_t n, int descending, void* ws, size_t ws_bytes,
                    void* stream);
+
+/* Batched sort (Section 5 "Radix Sort" applied to each row, as the top-p
+ * sampler needs it): each of the rows x len rows of fp32 keys sorted on its
+ * own, stably, ascending or (descending != 0) descending, in IEEE 754
+ * totalOrder as radix_sort_f32.  perm_out (nullable) receives each key's index
+ * within its row (0..len-1).  keys_tmp / perm_tmp are rows x len ping-pong
+ * buffers.  No two of keys, keys_out, perm_out, keys_tmp, perm_tmp may
+ * overlap.  rows * len <= 2^30 and rows * ceil(len / 8192) <= 2^24.
+ * Workspace: LIBSCAN_OP_SORT_ROWS with (rows, len). */
+int radix_sort_rows_f32(const float* keys, float* keys_out, int32_t* perm_out, float* keys_tmp,
+                        int32_t* perm_tmp, int64_t rows, int64_t len, int descending, void* ws,
+                        size_t ws_bytes, void* stream);
+
+/* Weighted sampling by inverse transform (Appendix "Weighted Sampling": a scan
+ * of the weights, then the first index whose running sum exceeds theta times
+ * the total).  w: rows x len non-negative fp32 weights; theta_dev (device,
+ * rows floats, each in [0, 1)) the uniform draws; out (device, rows int32)
+ * receives per row the smallest 0-based i with w[r][0] + ... + w[r][i] >
+ * theta[r] * (w[r][0] + ... + w[r][len-1]), the sums taken in fp32; len - 1
+ * when rounding leaves no such i; -1 for len == 0.  Index i is drawn with
+ * probability w[r][i] / total when theta is uniform.  Any row length
+ * (len <= INT32_MAX, limits as scan_rows).  No output may overlap an input.
+ * Workspace: LIBSCAN_OP_WEIGHTED_SAMPLE with (rows, len). */
+int weighted_sample_f32(const float* w, const float* theta_dev, int32_t* out, int64_t rows,
+                        int64_t len, void* ws, size_t ws_bytes, void* stream);
+
+/* Top-p (nucleus) sampling on unsorted rows (Section 5 "Top-p or Nucleus
+ * Sampling": sort each row in descending order keeping the token indices,
+ * take the running sum, cut at p, draw from what is kept).  probs: rows x len
+ * non-negative fp32 probabilities (any order; they need not sum to 1).  Per
+ * row: the stable descending sort S (ties keep index order), the cutoff k as
+ * topp_cutoff_f32 computes it on S, then the draw by inverse transform over
+ * S[0..k]: the smallest j <= k with S[0] + ... + S[j] > theta[r] * C, where C
+ * is the running sum at k (fp32; j = k when rounding leaves none).
+ * token_out (device, rows int32) receives the token index of S[j] in the
+ * original row; cutoff_out (nullable, device, rows int32) receives k.  Both
+ * are -1 for len == 0.  theta_dev as in weighted_sample_f32; p must not be
+ * NaN.  rows * len <= 2^30, rows * ceil(len / 8192) <= 2^24.  The sorted
+ * copies are kept in the workspace, which no input or output may overlap.
+ * Workspace: LIBSCAN_OP_TOPP_SAMPLE with (rows, len) (about 16 bytes per
+ * element). */
+int topp_sample_f32(const float* probs, const float* theta_dev, float p, int32_t* token_out,
+                    int32_t* cutoff_out, int64_t rows, int64_t len, void* ws, size_t ws_bytes,
+                    void* stream);
 
 #ifdef __cplusplus
 }

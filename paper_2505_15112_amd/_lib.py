@@ -45,10 +45,14 @@ SIGNATURES = {
     "radix_sort_i32": (_int, [_p, _p, _p, _p, _p, _i64, _int, _p, _sz, _p]),
     "radix_sort_f32": (_int, [_p, _p, _p, _p, _p, _i64, _int, _p, _sz, _p]),
     "radix_sort_f16": (_int, [_p, _p, _p, _p, _p, _i64, _int, _p, _sz, _p]),
+    "radix_sort_rows_f32": (_int, [_p, _p, _p, _p, _p, _i64, _i64, _int, _p, _sz, _p]),
+    "weighted_sample_f32": (_int, [_p, _p, _p, _i64, _i64, _p, _sz, _p]),
+    "topp_sample_f32": (_int, [_p, _p, ctypes.c_float, _p, _p, _i64, _i64, _p, _sz, _p]),
 }
 
 OK, EINVAL, ENOSPACE, EHIP, ERANGE = 0, -1, -2, -3, -4
 OP_SCAN, OP_SCAN_RSS, OP_SCAN_ROWS, OP_COMPACT, OP_RADIX_SORT = 1, 2, 3, 4, 5
+OP_SORT_ROWS, OP_WEIGHTED_SAMPLE, OP_TOPP_SAMPLE = 6, 7, 8
 
 _LIB = None
 

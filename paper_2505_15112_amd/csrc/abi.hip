@@ -100,7 +100,7 @@ int radix_sort_typed(ls::KeyType type, size_t elem, const void* keys, void* keys
                      int32_t* perm_out, void* keys_tmp, int32_t* perm_tmp, int64_t n,
                      int descending, void* ws, size_t ws_bytes, void* stream) {
     if (n < 0) return LIBSCAN_EINVAL;
-    if (n > INT32_MAX) return LIBSCAN_ERANGE;
+    if (n > ls::kMaxRadixKeys) return LIBSCAN_ERANGE;
     if (n == 0) return LIBSCAN_OK;
     if (!keys || !keys_out || !keys_tmp || (perm_out && !perm_tmp)) return LIBSCAN_EINVAL;
     const size_t kb = (size_t)n * elem, pb = (size_t)n * 4;
@@ -113,8 +113,25 @@ int radix_sort_typed(ls::KeyType type, size_t elem, const void* keys, void* keys
     const int w = check_ws(ws, ws_bytes, ls::radix_ws_bytes(n, 8));
     if (w != LIBSCAN_OK) return w;
     return hip_status(ls::launch_radix_sort_typed(type, descending != 0, keys, keys_out, perm_out,
-                                                  keys_tmp, perm_tmp, n, ws, ws_bytes,
+                                                  keys_tmp, perm_tmp, 1, n, ws, ws_bytes,
                                                   (hipStream_t)stream));
+}
+
+// Per-row sampling ops: rows x len probabilities or weights in, one int32
+// per row out, theta (rows floats) read by the draw.
+int check_sample(const float* x, const float* theta, const int32_t* out, const int32_t* out2,
+                 int64_t rows, int64_t len) {
+    const int r = check_rows(rows, len);
+    if (r != LIBSCAN_OK) return r;
+    if (len > INT32_MAX) return LIBSCAN_ERANGE;
+    if (rows == 0) return LIBSCAN_OK;
+    if (!theta || !out || (len > 0 && !x)) return LIBSCAN_EINVAL;
+    const size_t xb = (size_t)rows * (size_t)len * 4, rb = (size_t)rows * 4;
+    if (overlaps(out, rb, x, xb) || overlaps(out, rb, theta, rb) ||
+        overlaps(out2, out2 ? rb : 0, x, xb) || overlaps(out2, out2 ? rb : 0, theta, rb) ||
+        overlaps(out2, out2 ? rb : 0, out, rb))
+        return LIBSCAN_EINVAL;
+    return LIBSCAN_OK;
 }
 
 }  // namespace
@@ -162,7 +179,7 @@ int libscan_workspace_bytes(int op, int64_t n, int64_t rows, int64_t len, int bi
             *bytes = ls::compact_ws_bytes(n);
             return LIBSCAN_OK;
         case LIBSCAN_OP_RADIX_SORT:
-            if (n > INT32_MAX) return LIBSCAN_ERANGE;
+            if (n > ls::kMaxRadixKeys) return LIBSCAN_ERANGE;
             if (bits != 1 && bits != 4 && bits != 8) return LIBSCAN_EINVAL;
             *bytes = ls::radix_ws_bytes(n, bits);
             return LIBSCAN_OK;
@@ -170,6 +187,23 @@ int libscan_workspace_bytes(int op, int64_t n, int64_t rows, int64_t len, int bi
             const int r = check_rows(rows, len);
             if (r != LIBSCAN_OK) return r;
             *bytes = ls::scan_rows_ws_bytes(rows, len);
+            return LIBSCAN_OK;
+        }
+        case LIBSCAN_OP_SORT_ROWS:
+            if (!ls::radix_rows_fit(rows, len)) return LIBSCAN_ERANGE;
+            *bytes = ls::radix_rows_ws_bytes(rows, len);
+            return LIBSCAN_OK;
+        case LIBSCAN_OP_WEIGHTED_SAMPLE:
+        case LIBSCAN_OP_TOPP_SAMPLE: {
+            const int r = check_rows(rows, len);
+            if (r != LIBSCAN_OK) return r;
+            if (len > INT32_MAX) return LIBSCAN_ERANGE;
+            if (op == LIBSCAN_OP_WEIGHTED_SAMPLE) {
+                *bytes = ls::topp_ws_bytes(rows, len);
+            } else {
+                if (!ls::radix_rows_fit(rows, len)) return LIBSCAN_ERANGE;
+                *bytes = ls::topp_sample_ws_bytes(rows, len);
+            }
             return LIBSCAN_OK;
         }
         default:
@@ -307,7 +341,7 @@ int radix_sort_u32(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out, 
                    void* stream) {
     if (n < 0 || (bits_per_pass != 1 && bits_per_pass != 4 && bits_per_pass != 8))
         return LIBSCAN_EINVAL;
-    if (n > INT32_MAX) return LIBSCAN_ERANGE;
+    if (n > ls::kMaxRadixKeys) return LIBSCAN_ERANGE;
     if (n == 0) return LIBSCAN_OK;
     if (!keys || !keys_out || !keys_tmp || (perm_out && !perm_tmp)) return LIBSCAN_EINVAL;
     const size_t b = (size_t)n * 4;
@@ -340,6 +374,55 @@ int radix_sort_f16(const uint16_t* keys, uint16_t* keys_out, int32_t* perm_out, 
                    void* stream) {
     return radix_sort_typed(ls::KeyType::F16, 2, keys, keys_out, perm_out, keys_tmp, perm_tmp, n,
                             descending, ws, ws_bytes, stream);
+}
+
+int radix_sort_rows_f32(const float* keys, float* keys_out, int32_t* perm_out, float* keys_tmp,
+                        int32_t* perm_tmp, int64_t rows, int64_t len, int descending, void* ws,
+                        size_t ws_bytes, void* stream) {
+    if (rows < 0 || len < 0) return LIBSCAN_EINVAL;
+    if (!ls::radix_rows_fit(rows, len)) return LIBSCAN_ERANGE;
+    if (rows == 0 || len == 0) return LIBSCAN_OK;
+    if (!keys || !keys_out || !keys_tmp || (perm_out && !perm_tmp)) return LIBSCAN_EINVAL;
+    const size_t b = (size_t)rows * (size_t)len * 4;
+    const void* bufs[5] = {keys, keys_out, perm_out, keys_tmp, perm_out ? perm_tmp : nullptr};
+    for (int i = 0; i < 5; ++i)
+        for (int j = i + 1; j < 5; ++j)
+            if (overlaps(bufs[i], bufs[i] ? b : 0, bufs[j], bufs[j] ? b : 0)) return LIBSCAN_EINVAL;
+    const int w = check_ws(ws, ws_bytes, ls::radix_rows_ws_bytes(rows, len));
+    if (w != LIBSCAN_OK) return w;
+    return hip_status(ls::launch_radix_sort_typed(ls::KeyType::F32, descending != 0, keys,
+                                                  keys_out, perm_out, keys_tmp, perm_tmp, rows,
+                                                  len, ws, ws_bytes, (hipStream_t)stream));
+}
+
+int weighted_sample_f32(const float* w, const float* theta_dev, int32_t* out, int64_t rows,
+                        int64_t len, void* ws, size_t ws_bytes, void* stream) {
+    const int c = check_sample(w, theta_dev, out, nullptr, rows, len);
+    if (c != LIBSCAN_OK || rows == 0) return c;
+    const int k = check_ws(ws, ws_bytes, ls::topp_ws_bytes(rows, len));
+    if (k != LIBSCAN_OK) return k;
+    return hip_status(ls::launch_weighted_sample(w, theta_dev, out, rows, len, ws,
+                                                 (hipStream_t)stream));
+}
+
+int topp_sample_f32(const float* probs, const float* theta_dev, float p, int32_t* token_out,
+                    int32_t* cutoff_out, int64_t rows, int64_t len, void* ws, size_t ws_bytes,
+                    void* stream) {
+    if (p != p) return LIBSCAN_EINVAL;  // NaN
+    const int c = check_sample(probs, theta_dev, token_out, cutoff_out, rows, len);
+    if (c != LIBSCAN_OK) return c;
+    if (!ls::radix_rows_fit(rows, len)) return LIBSCAN_ERANGE;
+    if (rows == 0) return LIBSCAN_OK;
+    const size_t need = ls::topp_sample_ws_bytes(rows, len);
+    const int k = check_ws(ws, ws_bytes, need);
+    if (k != LIBSCAN_OK) return k;
+    // the sorted copies live in the workspace: no input or output may lie in it
+    const size_t xb = (size_t)rows * (size_t)len * 4, rb = (size_t)rows * 4;
+    if (overlaps(ws, need, probs, xb) || overlaps(ws, need, theta_dev, rb) ||
+        overlaps(ws, need, token_out, rb) || overlaps(ws, need, cutoff_out, cutoff_out ? rb : 0))
+        return LIBSCAN_EINVAL;
+    return hip_status(ls::launch_topp_sample(probs, theta_dev, p, token_out, cutoff_out, rows, len,
+                                             ws, (hipStream_t)stream));
 }
 
 }  // extern "C"

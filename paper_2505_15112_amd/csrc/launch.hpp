@@ -34,9 +34,23 @@ hipError_t launch_scan1d_rss(Kind kind, const void* x, void* y, int64_t n, void*
 size_t scan_rows_ws_bytes(int64_t rows, int64_t len);
 hipError_t launch_scan_rows(Kind kind, bool exclusive, const void* x, void* y, int64_t rows,
                             int64_t len, void* ws, size_t ws_bytes, hipStream_t stream);
+size_t topp_ws_bytes(int64_t rows, int64_t len);
+bool radix_rows_fit(int64_t rows, int64_t len);
+size_t topp_sample_ws_bytes(int64_t rows, int64_t len);
+hipError_t launch_topp_sample(const float* probs, const float* theta, float p, int32_t* token,
+                              int32_t* cutoff, int64_t rows, int64_t len, void* ws,
+                              hipStream_t stream);
+hipError_t launch_weighted_sample(const float* w, const float* theta, int32_t* out, int64_t rows,
+                                  int64_t len, void* ws, hipStream_t stream);
+hipError_t launch_topp_draw_sorted(const float* sorted, const int32_t* idx, const float* theta,
+                                   float p, int32_t* token, int32_t* cutoff, int64_t rows,
+                                   int64_t len, void* ws, hipStream_t stream);
 hipError_t launch_topp_cutoff(const float* probs, int32_t* cutoff, int64_t rows, int64_t len,
                               float p, void* ws, size_t ws_bytes, hipStream_t stream);
 constexpr int64_t kMaxGridTiles = int64_t(1) << 24;
+// Radix sorts: at most 2^30 keys per call (or rows x len in total), so that
+// every count-table offset, left in the workspace, stays below 2^30.
+constexpr int64_t kMaxRadixKeys = int64_t(1) << 30;
 
 // Compress and split (Section 5).  flags == nullptr in launch_split means
 // "flag = key bit `bit` is 0" (the LSB radix-sort pass).
@@ -51,10 +65,13 @@ hipError_t launch_split(const uint32_t* keys, const int32_t* idx_in, const uint8
 // Key types of the typed radix sorts (8-bit digits; encoded on the first pass,
 // decoded on the last).
 enum class KeyType { U32, I32, F32, F16 };
+// rows = 1: a 1-D sort of len keys; else every row of a rows x len matrix on
+// its own (perm_out: indices within the row).
 hipError_t launch_radix_sort_typed(KeyType type, bool descending, const void* keys,
                                    void* keys_out, int32_t* perm_out, void* keys_tmp,
-                                   int32_t* perm_tmp, int64_t n, void* ws, size_t ws_bytes,
-                                   hipStream_t stream);
+                                   int32_t* perm_tmp, int64_t rows, int64_t len, void* ws,
+                                   size_t ws_bytes, hipStream_t stream);
+size_t radix_rows_ws_bytes(int64_t rows, int64_t len);
 
 // LSD radix sort (1, 4 or 8 bits per pass), caller-provided ping-pong buffers.
 size_t radix_ws_bytes(int64_t n, int bits);

@@ -355,7 +355,6 @@ constexpr int kR8Chunks = 16;
 constexpr int64_t kR8Tile = kR8Waves * kR8Chunks * kWave;  // 8192 keys
 constexpr int kR8Digits = 256;
 
-static inline int64_t r8_tiles(int64_t n) { return (n + kR8Tile - 1) / kR8Tile; }
 
 // Lanes holding the same 8-bit digit as this lane, among the `ok` lanes.
 __device__ __forceinline__ uint64_t peers8(uint32_t d, bool ok) {
@@ -368,14 +367,18 @@ __device__ __forceinline__ uint64_t peers8(uint32_t d, bool ok) {
     return m;
 }
 
-// Per-tile counts of the 256 digits: counts[d * ntiles + tile].  Order does
-// not matter here: keys are read with 16-byte loads when aligned and counted
+// Per-tile counts of the 256 digits.  Keys form rows of `len` (one row of n
+// for a 1-D sort; tiles never straddle rows, tpr tiles per row), and the count
+// of digit d in tile tr of row r goes to counts[(r * 256 + d) * tpr + tr]: per
+// row digit-major, so that one exclusive scan per row turns the table into
+// each (digit, tile)'s first output position in the row.  Order does not
+// matter here: keys are read with 16-byte loads when aligned and counted
 // with plain LDS atomics, into 4 histograms per wave (picked by lane & 3) so
 // that equal digits in one instruction collide at most 16 ways.
 constexpr int kR8Sub = 4;
 template <class K>
 __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_count(
-    const K* keys, int64_t n, int shift, bool vec, uint32_t* counts, uint32_t ntiles,
+    const K* keys, int64_t len, uint32_t tpr, int shift, bool vec, uint32_t* counts,
     KeyCode code) {
     __shared__ uint32_t s_h[kR8Waves * kR8Sub][kR8Digits];
     for (int i = threadIdx.x; i < kR8Waves * kR8Sub * kR8Digits; i += kR8Waves * kWave)
@@ -384,10 +387,12 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_count(
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
     uint32_t* h = s_h[w * kR8Sub + (lane & (kR8Sub - 1))];
-    const int64_t tbase = (int64_t)blockIdx.x * kR8Tile;
-    const int64_t wbase = tbase + (int64_t)w * kR8Chunks * kWave;
-    if (sizeof(K) == 4 && vec && tbase + kR8Tile <= n) {  // 4 x 16-byte loads per lane
-        const u32x4* k4 = reinterpret_cast<const u32x4*>(keys + wbase);
+    const uint32_t row = blockIdx.x / tpr, tr = blockIdx.x - row * tpr;
+    const int64_t tstart = (int64_t)tr * kR8Tile;  // within the row
+    const K* kr = keys + (int64_t)row * len;
+    const int64_t wbase = tstart + (int64_t)w * kR8Chunks * kWave;
+    if (sizeof(K) == 4 && vec && tstart + kR8Tile <= len) {  // 4 x 16-byte loads per lane
+        const u32x4* k4 = reinterpret_cast<const u32x4*>(kr + wbase);
         u32x4 v[kR8Chunks / 4];
 #pragma unroll
         for (int j = 0; j < kR8Chunks / 4; ++j) v[j] = k4[j * kWave + lane];
@@ -402,7 +407,7 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_count(
 #pragma unroll
         for (int j = 0; j < kR8Chunks; ++j) {
             const int64_t i = wbase + j * kWave + lane;
-            if (i < n) atomicAdd(&h[(code.apply((uint32_t)keys[i]) >> shift) & 255u], 1u);
+            if (i < len) atomicAdd(&h[(code.apply((uint32_t)kr[i]) >> shift) & 255u], 1u);
         }
     }
     __syncthreads();
@@ -410,33 +415,39 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_count(
         uint32_t t = 0;
 #pragma unroll
         for (int k = 0; k < kR8Waves * kR8Sub; ++k) t += s_h[k][threadIdx.x];
-        counts[(int64_t)threadIdx.x * ntiles + blockIdx.x] = t;
+        counts[((int64_t)row * kR8Digits + threadIdx.x) * tpr + tr] = t;
     }
 }
 
 // Rank and scatter one tile of 8192 keys (one key per lane per chunk, so the
-// chunk's index order is the lane order) with the offsets from the spine.
+// chunk's index order is the lane order) with the offsets from the scanned
+// table; rows and tiles as in k_radix8_count, the permutation holding indices
+// within the row.
 template <class K, bool HAS_PERM_IN, bool WITH_PERM>
 __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatter(
-    const K* keys_in, const int32_t* perm_in, K* keys_out, int32_t* perm_out, int64_t n,
-    int shift, uint32_t* offsets, uint32_t ntiles, KeyCode code, KeyDecode decode) {
+    const K* keys_in, const int32_t* perm_in, K* keys_out, int32_t* perm_out, int64_t len,
+    uint32_t tpr, int shift, uint32_t* offsets, KeyCode code, KeyDecode decode) {
     __shared__ uint32_t s_wh[kR8Waves][kR8Digits];  // wave counts, then each wave's first slot
     __shared__ uint32_t s_tstart[kR8Digits];         // first slot of digit d in the tile
     __shared__ uint32_t s_gbase[kR8Digits];          // global position of that slot
     __shared__ uint32_t s_part[kR8Digits / kWave];
     __shared__ uint32_t s_stage[kR8Tile];
 
-    const int64_t tile = xcd_tile(blockIdx.x, gridDim.x);
+    const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
-    const int64_t tbase = tile * kR8Tile;
-    const int64_t wbase = tbase + (int64_t)w * kR8Chunks * kWave;
-    const bool full = tbase + kR8Tile <= n;
-    const uint32_t valid = full ? (uint32_t)kR8Tile : (uint32_t)(n - tbase);
+    const uint32_t row = tile / tpr, tr = tile - row * tpr;
+    const int64_t rbase = (int64_t)row * len;
+    const int64_t tstart = (int64_t)tr * kR8Tile;  // within the row
+    const int64_t wbase = tstart + (int64_t)w * kR8Chunks * kWave;
+    const bool full = tstart + kR8Tile <= len;
+    const uint32_t valid = full ? (uint32_t)kR8Tile : (uint32_t)(len - tstart);
+    const K* kin = keys_in + rbase;
+    K* kout = keys_out + rbase;
 
     for (int i = threadIdx.x; i < kR8Waves * kR8Digits; i += kR8Waves * kWave) (&s_wh[0][0])[i] = 0;
     if (threadIdx.x < kR8Digits) {
-        uint32_t* o = offsets + (int64_t)threadIdx.x * ntiles + tile;
+        uint32_t* o = offsets + ((int64_t)row * kR8Digits + threadIdx.x) * tpr + tr;
         s_gbase[threadIdx.x] = *o;
         *o = 0;  // offsets can reach 2^30 and more: leave the workspace word zero
     }
@@ -444,7 +455,7 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
 #pragma unroll
     for (int j = 0; j < kR8Chunks; ++j) {
         const int64_t i = wbase + j * kWave + lane;
-        key[j] = (full || i < n) ? code.apply((uint32_t)keys_in[i]) : 0u;
+        key[j] = (full || i < len) ? code.apply((uint32_t)kin[i]) : 0u;
     }
     __syncthreads();
 
@@ -460,7 +471,7 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
 #pragma unroll
         for (int q = 0; q < kG; ++q) {
             const int64_t i = wbase + (g + q) * kWave + lane;
-            const bool ok = full || i < n;
+            const bool ok = full || i < len;
             const uint64_t peers = peers8((key[g + q] >> shift) & 255u, ok);
             rank[g + q] = lanes_below(peers);
             leader[q] = ok ? ((uint32_t)__builtin_ctzll(peers) |
@@ -484,7 +495,7 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
 #pragma unroll
         for (int j = 0; j < kR8Chunks; ++j) {
             const int64_t i = wbase + j * kWave + lane;
-            perm[j] = HAS_PERM_IN ? ((full || i < n) ? perm_in[i] : 0) : (int32_t)i;
+            perm[j] = HAS_PERM_IN ? ((full || i < len) ? perm_in[rbase + i] : 0) : (int32_t)i;
         }
     }
     __syncthreads();
@@ -517,7 +528,7 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
         const int64_t i = wbase + j * kWave + lane;
         const uint32_t d = (key[j] >> shift) & 255u;
         rank[j] += s_tstart[d] + s_wh[w][d];  // now the slot
-        if ((full || i < n) && rank[j] < kR8Tile) s_stage[rank[j]] = key[j];
+        if ((full || i < len) && rank[j] < kR8Tile) s_stage[rank[j]] = key[j];
     }
     __syncthreads();
     uint32_t skey[kR8Chunks];
@@ -528,7 +539,7 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
         if (t < valid) {
             const uint32_t d = (skey[j] >> shift) & 255u;
             const uint32_t pos = s_gbase[d] + (t - s_tstart[d]);
-            if (pos < (uint64_t)n) keys_out[pos] = (K)decode.apply(skey[j]);  // pos < n always
+            if (pos < (uint64_t)len) kout[pos] = (K)decode.apply(skey[j]);  // pos < len always
         }
     }
     if (WITH_PERM) {
@@ -536,7 +547,7 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
 #pragma unroll
         for (int j = 0; j < kR8Chunks; ++j) {
             const int64_t i = wbase + j * kWave + lane;
-            if ((full || i < n) && rank[j] < kR8Tile) s_stage[rank[j]] = (uint32_t)perm[j];
+            if ((full || i < len) && rank[j] < kR8Tile) s_stage[rank[j]] = (uint32_t)perm[j];
         }
         __syncthreads();
 #pragma unroll
@@ -545,7 +556,7 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
             if (t < valid) {
                 const uint32_t d = (skey[j] >> shift) & 255u;
                 const uint32_t pos = s_gbase[d] + (t - s_tstart[d]);
-                if (pos < (uint64_t)n) perm_out[pos] = (int32_t)s_stage[t];
+                if (pos < (uint64_t)len) perm_out[rbase + pos] = (int32_t)s_stage[t];
             }
         }
     }
@@ -562,16 +573,15 @@ hipError_t launch_radix1_pass(const uint32_t* keys, const int32_t* idx_in, int b
 // 4- and 8-bit: header | the count-table scan's workspace body | count table
 //        (digits x tiles 32-bit counts, 16-byte aligned).
 static int64_t radix1_status_words(int64_t n) { return (n + kR1Tile - 1) / kR1Tile; }
-static int64_t digit_table_entries(int64_t n, int bits) {
-    return bits == 8 ? r8_tiles(n) * kR8Digits : r4_tiles(n) * 16;
-}
-static size_t digit_table_offset(int64_t n, int bits) {
-    return (scan1d_ws_bytes(digit_table_entries(n, bits)) + 15) / 16 * 16;
+static int64_t r4_table_entries(int64_t n) { return r4_tiles(n) * 16; }
+static size_t r4_table_offset(int64_t n) {
+    return (scan1d_ws_bytes(r4_table_entries(n)) + 15) / 16 * 16;
 }
 
 size_t radix_ws_bytes(int64_t n, int bits) {
-    if (bits == 4 || bits == 8)
-        return digit_table_offset(n, bits) + (size_t)digit_table_entries(n, bits) * sizeof(uint32_t);
+    if (bits == 8) return radix_rows_ws_bytes(1, n);
+    if (bits == 4)
+        return r4_table_offset(n) + (size_t)r4_table_entries(n) * sizeof(uint32_t);
     return kRadixStatusOffset + (size_t)radix1_status_words(n) * sizeof(uint64_t) +
            (size_t)kHistBlocks * kHistWords * sizeof(uint32_t);
 }
@@ -579,15 +589,38 @@ size_t radix_ws_bytes(int64_t n, int bits) {
 constexpr KeyCode kIdentityCode{0u, 0u, 31};
 constexpr KeyDecode kIdentityDecode{0u, 0u, 0u, 31};
 
-// `passes` 8-bit passes over keys of type K (4 for 32-bit keys, 2 for 16-bit),
-// ping-ponging keys_tmp / keys_out (an even number of passes ends in
-// keys_out); the first pass encodes the keys, the last one decodes them.
+// Rows of `len` keys (rows = 1: a 1-D sort of n = len keys), each sorted on
+// its own by `passes` 8-bit passes over keys of type K (4 for 32-bit keys, 2
+// for 16-bit), ping-ponging keys_tmp / keys_out (an even number of passes ends
+// in keys_out); the first pass encodes the keys, the last one decodes them.
+// Workspace: header | the table scan's workspace body | the count table.
+static uint32_t r8_tpr(int64_t len) { return (uint32_t)((len + kR8Tile - 1) / kR8Tile); }
+static size_t radix8_table_offset(int64_t rows, int64_t len) {
+    const int64_t entries = (int64_t)kR8Digits * r8_tpr(len);
+    const size_t scan = rows == 1 ? scan1d_ws_bytes(entries) : scan_rows_ws_bytes(rows, entries);
+    return (scan + 15) / 16 * 16;
+}
+// rows x len keys within kMaxRadixKeys and a tile grid that fits one launch
+// (the count table's row scan then fits its limits too).
+bool radix_rows_fit(int64_t rows, int64_t len) {
+    if (rows < 0 || len < 0) return false;
+    if (rows == 0 || len == 0) return true;
+    if (len > kMaxRadixKeys / rows) return false;
+    return rows * (int64_t)r8_tpr(len) <= kMaxGridTiles;
+}
+size_t radix_rows_ws_bytes(int64_t rows, int64_t len) {
+    return radix8_table_offset(rows, len) +
+           (size_t)rows * kR8Digits * r8_tpr(len) * sizeof(uint32_t);
+}
+
 template <class K>
 static hipError_t radix8_sort(const K* keys, K* keys_out, int32_t* perm_out, K* keys_tmp,
-                              int32_t* perm_tmp, int64_t n, int passes, KeyCode code,
-                              KeyDecode decode, void* ws, hipStream_t stream) {
-    const uint32_t nt = (uint32_t)r8_tiles(n);
-    const size_t toff = digit_table_offset(n, 8);
+                              int32_t* perm_tmp, int64_t rows, int64_t len, int passes,
+                              KeyCode code, KeyDecode decode, void* ws, hipStream_t stream) {
+    const uint32_t tpr = r8_tpr(len);
+    const uint32_t nt = (uint32_t)(rows * tpr);
+    const int64_t entries = (int64_t)kR8Digits * tpr;  // per row
+    const size_t toff = radix8_table_offset(rows, len);
     uint32_t* counts = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + toff);
     const K* src_k = keys;
     const int32_t* src_p = nullptr;
@@ -596,16 +629,19 @@ static hipError_t radix8_sort(const K* keys, K* keys_out, int32_t* perm_out, K* 
         int32_t* dp = perm_out ? ((p % 2 == 0) ? perm_tmp : perm_out) : nullptr;
         const KeyCode c = p == 0 ? code : kIdentityCode;
         const KeyDecode d = p == passes - 1 ? decode : kIdentityDecode;
-        const bool vec = ((uintptr_t)src_k % 16) == 0;
-        hipLaunchKernelGGL(k_radix8_count<K>, dim3(nt), dim3(kR8Waves * kWave), 0, stream, src_k, n,
-                           8 * p, vec, counts, nt, c);
-        hipError_t e = launch_scan1d(Kind::I32, true, counts, counts, digit_table_entries(n, 8),
-                                     nullptr, nullptr, ws, toff, stream);
+        const bool vec = ((uintptr_t)src_k % 16) == 0 && (rows == 1 || len % 4 == 0);
+        hipLaunchKernelGGL(k_radix8_count<K>, dim3(nt), dim3(kR8Waves * kWave), 0, stream, src_k,
+                           len, tpr, 8 * p, vec, counts, c);
+        hipError_t e = rows == 1
+                           ? launch_scan1d(Kind::I32, true, counts, counts, entries, nullptr,
+                                           nullptr, ws, toff, stream)
+                           : launch_scan_rows(Kind::I32, true, counts, counts, rows, entries, ws,
+                                              toff, stream);
         if (e != hipSuccess) return e;
         auto k = dp ? (src_p ? k_radix8_scatter<K, true, true> : k_radix8_scatter<K, false, true>)
                     : k_radix8_scatter<K, false, false>;
-        hipLaunchKernelGGL(k, dim3(nt), dim3(kR8Waves * kWave), 0, stream, src_k, src_p, dk, dp, n,
-                           8 * p, counts, nt, c, d);
+        hipLaunchKernelGGL(k, dim3(nt), dim3(kR8Waves * kWave), 0, stream, src_k, src_p, dk, dp,
+                           len, tpr, 8 * p, counts, c, d);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         src_k = dk;
@@ -640,12 +676,12 @@ hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* 
             if (e != hipSuccess) return e;
         } else if (bits == 4) {
             const uint32_t nt = (uint32_t)r4_tiles(n);
-            const size_t toff = digit_table_offset(n, 4);
+            const size_t toff = r4_table_offset(n);
             uint32_t* counts = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + toff);
             const bool vec = ((uintptr_t)src_k % 16) == 0;
             hipLaunchKernelGGL(k_radix4_count, dim3(nt), dim3(kR4Waves * kWave), 0, stream, src_k, n,
                                4 * p, vec, counts, nt);
-            hipError_t e = launch_scan1d(Kind::I32, true, counts, counts, digit_table_entries(n, 4),
+            hipError_t e = launch_scan1d(Kind::I32, true, counts, counts, r4_table_entries(n),
                                          nullptr, nullptr, ws, toff, stream);
             if (e != hipSuccess) return e;
             auto k = dp ? (src_p ? k_radix4_scatter<true, true> : k_radix4_scatter<false, true>)
@@ -655,7 +691,7 @@ hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* 
             e = hipGetLastError();
             if (e != hipSuccess) return e;
         } else {
-            return radix8_sort<uint32_t>(keys, keys_out, perm_out, keys_tmp, perm_tmp, n, 4,
+            return radix8_sort<uint32_t>(keys, keys_out, perm_out, keys_tmp, perm_tmp, 1, n, 4,
                                          kIdentityCode, kIdentityDecode, ws, stream);
         }
         src_k = dk;
@@ -666,10 +702,10 @@ hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* 
 
 hipError_t launch_radix_sort_typed(KeyType type, bool descending, const void* keys,
                                    void* keys_out, int32_t* perm_out, void* keys_tmp,
-                                   int32_t* perm_tmp, int64_t n, void* ws, size_t ws_bytes,
-                                   hipStream_t stream) {
+                                   int32_t* perm_tmp, int64_t rows, int64_t len, void* ws,
+                                   size_t ws_bytes, hipStream_t stream) {
     (void)ws_bytes;
-    if (n == 0) return hipSuccess;
+    if (rows == 0 || len == 0) return hipSuccess;
     const bool wide = type != KeyType::F16;
     const uint32_t all = wide ? 0xFFFFFFFFu : 0xFFFFu;
     const uint32_t msb = wide ? 0x80000000u : 0x8000u;
@@ -698,9 +734,11 @@ hipError_t launch_radix_sort_typed(KeyType type, bool descending, const void* ke
     }
     if (wide)
         return radix8_sort<uint32_t>((const uint32_t*)keys, (uint32_t*)keys_out, perm_out,
-                                     (uint32_t*)keys_tmp, perm_tmp, n, 4, code, decode, ws, stream);
+                                     (uint32_t*)keys_tmp, perm_tmp, rows, len, 4, code, decode, ws,
+                                     stream);
     return radix8_sort<uint16_t>((const uint16_t*)keys, (uint16_t*)keys_out, perm_out,
-                                 (uint16_t*)keys_tmp, perm_tmp, n, 2, code, decode, ws, stream);
+                                 (uint16_t*)keys_tmp, perm_tmp, rows, len, 2, code, decode, ws,
+                                 stream);
 }
 
 }  // namespace ls

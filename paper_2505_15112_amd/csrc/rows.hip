@@ -101,20 +101,25 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_rows_lookback
 // ---------------------------------------------------------------- top-p
 
 // One kernel; no workgroup waits for another's work.  Every tile of a row
-// sums its probabilities, stores the sum (in a workspace word with its two
-// top bits clear, which any look-back reads as "nothing published", and a
-// "set" bit below them) and counts itself in the row's arrival counter.  The
-// row's last tile to arrive -- every other tile has stored its sum by then,
-// it waits only for the stores to become visible -- clears the sums again and
-// scans them in order for the first tile
-// whose inclusive sum reaches p, then re-reads that one tile (just read, so
-// still in the 256 MB Infinity Cache) to locate the index.  p never reached:
-// len - 1.
-// The last tile resets the counter and the sums, so the workspace needs no
-// clearing.
-// (The two phases of the paper's Algorithm 3, MCScan, with the down-sweep cut
-// to the one tile that matters and the second phase run by whichever
-// workgroup finishes a row last.)
+// sums its values, stores the sum (in a workspace word with its two top bits
+// clear, which any look-back reads as "nothing published", and a "set" bit
+// below them) and counts itself in the row's arrival counter.  The row's last
+// tile to arrive -- every other tile has stored its sum by then, it waits only
+// for the stores to become visible -- finishes the row from the tile sums and
+// at most two re-read tiles (just read, so still in the 256 MB Infinity
+// Cache), then clears the sums and the counter, so the workspace needs no
+// clearing.  Three modes:
+//  * cutoff (Section 5 "Top-p"): the first index whose running sum reaches p,
+//    len - 1 if none -- the first tile whose inclusive sum reaches p, then
+//    the index inside it (the two phases of the paper's Algorithm 3, MCScan,
+//    with the down-sweep cut to the one tile that matters);
+//  * weighted sample (appendix "Weighted Sampling"): the first index whose
+//    running sum exceeds theta * W, W the row total;
+//  * top-p sample: the cutoff k, then the first index j <= k whose running
+//    sum exceeds theta * C_k, reported through `idx` (the source index of
+//    each sorted position; null: j itself).
+enum class ToppMode { Cutoff, Weighted, Sample };
+
 // Top-p's workspace words (a published tile sum, a row's arrival count) carry
 // the top three bits 001.  Other ops leave status words with a non-zero state
 // in the top two bits, or counts with the top three bits clear, and cleared
@@ -138,103 +143,232 @@ __device__ __forceinline__ uint32_t topp_arrive(uint64_t* counter) {
     }
 }
 
-template <class TileT, bool VEC>
+__device__ __forceinline__ float topp_sum(const uint64_t* w) {
+    return Bits<float>::from((uint32_t)__hip_atomic_load(w, __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT));
+}
+
+// Wave 0 of the last workgroup: the sum of the row's tile sums, in order.
+__device__ __forceinline__ float topp_total(const uint64_t* rs, uint32_t segs) {
+    float carry = 0.f;
+    for (uint32_t b = 0; b < segs; b += kWave) {
+        const uint32_t s = b + lane_id();
+        carry = carry + wave_sum(s < segs ? topp_sum(&rs[s]) : 0.f);
+    }
+    return carry;
+}
+
+// Wave 0 of the last workgroup: the first tile t < limit whose inclusive sum
+// reaches `thr` (strict: exceeds it), in tile order; -1 if none.  *excl gets
+// the sum of the tiles before t (or of all `limit` tiles when none).
+__device__ __forceinline__ int32_t topp_find_tile(const uint64_t* rs, uint32_t limit, float thr,
+                                                  bool strict, float* excl) {
+    const int lane = lane_id();
+    float carry = 0.f;
+    for (uint32_t b = 0; b < limit; b += kWave) {
+        const uint32_t s = b + lane;
+        const float a = s < limit ? topp_sum(&rs[s]) : 0.f;
+        const float inc = carry + wave_incl_scan(a);
+        const uint64_t hit = __ballot(s < limit && (strict ? inc > thr : inc >= thr));
+        if (hit) {
+            const int l = __builtin_ctzll(hit);
+            *excl = l ? lane_read(inc, l - 1) : carry;
+            return (int32_t)(b + l);
+        }
+        carry = lane_read(inc, kWave - 1);
+    }
+    *excl = carry;
+    return -1;
+}
+
+// The whole workgroup: load the tile at `base`, and find its first index
+// i <= lim whose running sum (excl + the tile prefix) reaches `thr` (STRICT:
+// exceeds it); none (rounding): the tile's last index, capped at lim.
+// Returns the index; `val` gets the running sum there.  Offsets inside the
+// tile are 32-bit, and each lane keeps only the running sums at its candidate
+// and at the cap, so the tile's registers die with the search loop.
+template <class TileT, bool VEC, bool STRICT, bool NEED_VAL>
+__device__ __forceinline__ int64_t topp_find_in_tile(const float* xr, int64_t len, int64_t base,
+                                                     float excl, float thr, int64_t lim,
+                                                     float* s_wtot, int32_t* s_min, float* s_val,
+                                                     float& val, bool& hit) {
+    float v[TileT::J][TileT::V];
+    float wofs;
+    TileT::template load<VEC>(xr, len, base, v);
+    TileT::combine_waves(TileT::template wave_scan<false>(v), s_wtot, &wofs);
+    const float c = excl + wofs;
+    const int64_t last = (base + TileT::kElems < len ? base + TileT::kElems : len) - 1;
+    const int32_t cap = (int32_t)((last < lim ? last : lim) - base);  // in-tile, >= 0
+    int32_t cand = INT_MAX;
+    float cand_val = 0.f, cap_val = 0.f;
+    bool has_cap = false;
+#pragma unroll
+    for (int j = TileT::J - 1; j >= 0; --j) {
+        const int32_t off = (int32_t)TileT::lane_offset(j);
+#pragma unroll
+        for (int e = TileT::V - 1; e >= 0; --e) {
+            const float run = c + v[j][e];
+            if (off + e <= cap && (STRICT ? run > thr : run >= thr)) {
+                cand = off + e;
+                if (NEED_VAL) cand_val = run;
+            }
+            if (NEED_VAL && off + e == cap) {
+                cap_val = run;
+                has_cap = true;
+            }
+        }
+    }
+    const int32_t wm = wave_min(cand);
+    if (lane_id() == 0) s_min[threadIdx.x / kWave] = wm;
+    __syncthreads();
+    int32_t m = INT_MAX;
+    for (int k = 0; k < TileT::WAVES; ++k) m = s_min[k] < m ? s_min[k] : m;
+    const int32_t f = m != INT_MAX ? m : cap;
+    hit = m != INT_MAX;
+    // exactly one lane holds the winner (or, with none, the cap)
+    if (NEED_VAL) {
+        if (m != INT_MAX ? cand == m : has_cap) *s_val = m != INT_MAX ? cand_val : cap_val;
+        __syncthreads();
+        val = *s_val;
+    }
+    __syncthreads();  // s_min / s_val free for the next call
+    return base + f;
+}
+
+// topp_find_in_tile over the tile at `base`; when the running sum is needed
+// and the tile is large, over its two halves in turn (the second only when
+// the first holds no hit and the range goes on), so that half a tile of
+// registers is live at a time.
+template <class TileT, bool VEC, bool STRICT, bool NEED_VAL>
+__device__ __forceinline__ int64_t topp_find(const float* xr, int64_t len, int64_t base,
+                                             float excl, float thr, int64_t lim, float* s_wtot,
+                                             int32_t* s_min, float* s_val, float& val) {
+    bool hit;
+    if constexpr (NEED_VAL && TileT::J > 8) {
+        using H = Tile<float, float, TileT::V, TileT::J / 2, TileT::WAVES>;
+        const int64_t f = topp_find_in_tile<H, VEC, STRICT, true>(xr, len, base, excl, thr, lim,
+                                                                  s_wtot, s_min, s_val, val, hit);
+        if (hit || f != base + H::kElems - 1 || f >= lim || f + 1 >= len) return f;
+        return topp_find_in_tile<H, VEC, STRICT, true>(xr, len, base + H::kElems, val, thr, lim,
+                                                       s_wtot, s_min, s_val, val, hit);
+    } else {
+        return topp_find_in_tile<TileT, VEC, STRICT, NEED_VAL>(xr, len, base, excl, thr, lim,
+                                                               s_wtot, s_min, s_val, val, hit);
+    }
+}
+
+template <class TileT, bool VEC, ToppMode MODE>
 __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp(
-    const float* probs, int32_t* cutoff, int64_t len, uint32_t segs, float p, WsHeader* hdr,
-    uint64_t* sums, uint64_t* arrivals) {
+    const float* probs, const int32_t* idx, const float* theta, int32_t* cutoff, int32_t* token,
+    int64_t len, uint32_t segs, float p, WsHeader* hdr, uint64_t* sums, uint64_t* arrivals) {
     __shared__ float s_wtot[TileT::WAVES];
     __shared__ uint32_t s_last;
-    __shared__ int32_t s_first;
+    __shared__ int32_t s_tile;
     __shared__ float s_excl;
+    __shared__ float s_thr;
     __shared__ int32_t s_min[TileT::WAVES];
+    __shared__ float s_val;
 
     const uint32_t row32 = blockIdx.x / segs;
     const uint32_t seg = blockIdx.x - row32 * segs;
     const int64_t row = row32;
     const float* xr = probs + row * len;
-    float v[TileT::J][TileT::V];
-    TileT::template load<VEC>(xr, len, (int64_t)seg * TileT::kElems, v);
-    float wofs;
-    const float agg = TileT::combine_waves(wave_sum(TileT::lane_sum(v)), s_wtot, &wofs);
-    if (threadIdx.x == 0) {
-        // Relaxed only (a release/acquire pair at device scope would write back
-        // and invalidate L2 in every workgroup): the sum word carries its own
-        // "published" bit, and the last arrival waits for those bits.
-        __hip_atomic_store(&sums[blockIdx.x], kToppTag | Bits<float>::to(agg), __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-        s_last = topp_arrive(&arrivals[row]) == segs - 1;
+    {
+        float v[TileT::J][TileT::V];
+        TileT::template load<VEC>(xr, len, (int64_t)seg * TileT::kElems, v);
+        float wofs;
+        const float agg = TileT::combine_waves(wave_sum(TileT::lane_sum(v)), s_wtot, &wofs);
+        if (threadIdx.x == 0) {
+            // Relaxed only (a release/acquire pair at device scope would write
+            // back and invalidate L2 in every workgroup): the sum word carries
+            // its own "published" bit, and the last arrival waits for it.
+            __hip_atomic_store(&sums[blockIdx.x], kToppTag | Bits<float>::to(agg),
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            // Arrive only once the store is acknowledged: an agent-scope
+            // store is written through to the level every CU reads at agent
+            // scope, so the last arrival can never find an older word (one a
+            // different op left in the workspace) in place of this sum.
+            __builtin_amdgcn_s_waitcnt(0);
+            s_last = topp_arrive(&arrivals[row]) == segs - 1;
+        }
     }
     __syncthreads();
     if (!s_last) return;  // uniform over the workgroup
 
+    uint64_t* rs = sums + (int64_t)row32 * segs;
+    const float th = MODE == ToppMode::Cutoff ? 0.f : theta[row];
+    // Wave 0: wait until every tile sum of the row is visible, then the first
+    // search over the tile sums.
     if (threadIdx.x < kWave) {
         const int lane = lane_id();
-        uint64_t* rs = sums + (int64_t)row32 * segs;
-        float carry = 0.f, excl = 0.f;
-        int32_t first = -1;
         bool failed = false;
         for (uint32_t b = 0; b < segs; b += kWave) {
             const uint32_t s = b + lane;
-            uint64_t word = kToppTag;
             if (s < segs) {
+                uint64_t word;
                 for (uint32_t spins = 0;; ++spins) {  // bounded: every tile has stored already
                     word = __hip_atomic_load(&rs[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     if (topp_word(word) || spins >= kSpinLimit) break;
                     __builtin_amdgcn_s_sleep(1);
                 }
                 failed |= !topp_word(word);
-                // leave the word clear for the next call
-                __hip_atomic_store(&rs[s], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
-            if (first >= 0) continue;  // keep clearing the rest of the row
-            const float a = s < segs ? Bits<float>::from((uint32_t)word) : 0.f;
-            const float inc = carry + wave_incl_scan(a);
-            const uint64_t hit = __ballot(s < segs && inc >= p);
-            if (hit) {
-                const int l = __builtin_ctzll(hit);
-                first = (int32_t)(b + l);
-                excl = l ? lane_read(inc, l - 1) : carry;
-            }
-            carry = lane_read(inc, kWave - 1);
         }
         if (__ballot(failed) && lane == 0)
             __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        float excl = 0.f;
+        const float thr = MODE == ToppMode::Weighted ? th * topp_total(rs, segs) : p;
+        const int32_t t = topp_find_tile(rs, segs, thr, MODE == ToppMode::Weighted, &excl);
         if (lane == 0) {
-            s_first = first;
+            s_tile = t;
             s_excl = excl;
-            __hip_atomic_store(&arrivals[row], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            s_thr = thr;
         }
     }
     __syncthreads();
-    const int32_t first = s_first;
-    if (first < 0) {
-        if (threadIdx.x == 0) cutoff[row] = (int32_t)(len - 1);
-        return;
+    const int32_t t = s_tile;
+    const float excl = s_excl, thr = s_thr;
+    __syncthreads();  // s_tile / s_excl reused below
+    int64_t found;    // the cutoff (cutoff / sample modes) or the weighted draw
+    float at = excl;  // running sum at `found` (no tile: the row total)
+    if (t < 0)
+        found = len - 1;
+    else
+        found = topp_find<TileT, VEC, MODE == ToppMode::Weighted, MODE == ToppMode::Sample>(
+            xr, len, (int64_t)t * TileT::kElems, excl, thr, len - 1, s_wtot, s_min, &s_val, at);
+    if (MODE == ToppMode::Sample) {
+        // second draw: among the kept indices 0..found, u = theta * C_found
+        const float u = th * at;
+        const uint32_t limit = t < 0 ? segs : (uint32_t)t + 1;
+        if (threadIdx.x < kWave) {
+            float e2 = 0.f;
+            const int32_t t2 = topp_find_tile(rs, limit, u, true, &e2);
+            if (lane_id() == 0) {
+                s_tile = t2;
+                s_excl = e2;
+            }
+        }
+        __syncthreads();
+        const int32_t t2 = s_tile;
+        const float e2 = s_excl;
+        int64_t j = found;
+        float at2;
+        if (t2 >= 0)
+            j = topp_find<TileT, VEC, true, false>(xr, len, (int64_t)t2 * TileT::kElems, e2, u,
+                                                    found, s_wtot, s_min, &s_val, at2);
+        if (threadIdx.x == 0) {
+            if (cutoff) cutoff[row] = (int32_t)found;
+            token[row] = idx ? idx[row * len + j] : (int32_t)j;
+        }
+    } else if (threadIdx.x == 0) {
+        (MODE == ToppMode::Cutoff ? cutoff : token)[row] = (int32_t)found;
     }
-    // Re-read the owning tile even when it is this one: keeping this tile's
-    // registers live across the scan of the sums would exceed the register
-    // budget (one tile per row, read moments ago by its own workgroup).
-    const int64_t base = (int64_t)first * TileT::kElems;
-    TileT::template load<VEC>(xr, len, base, v);
-    TileT::combine_waves(TileT::template wave_scan<false>(v), s_wtot, &wofs);
-    const float c = s_excl + wofs;
-    int32_t cand = INT_MAX;
-#pragma unroll
-    for (int j = TileT::J - 1; j >= 0; --j) {
-        const int64_t off = TileT::offset(base, j);
-#pragma unroll
-        for (int e = TileT::V - 1; e >= 0; --e)
-            if (off + e < len && c + v[j][e] >= p) cand = (int32_t)(off + e);
-    }
-    const int32_t wm = wave_min(cand);
-    if (lane_id() == 0) s_min[threadIdx.x / kWave] = wm;
+    // leave the row's sums and counter clear for the next call
     __syncthreads();
-    if (threadIdx.x == 0) {
-        int32_t m = INT_MAX;
-        for (int k = 0; k < TileT::WAVES; ++k) m = s_min[k] < m ? s_min[k] : m;
-        const int64_t last = (base + TileT::kElems < len ? base + TileT::kElems : len) - 1;
-        cutoff[row] = m != INT_MAX ? m : (int32_t)last;  // rounding kept every prefix below p
-    }
+    for (uint32_t s = threadIdx.x; s < segs; s += TileT::kThreads)
+        __hip_atomic_store(&rs[s], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x == 0)
+        __hip_atomic_store(&arrivals[row], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __global__ void k_fill_i32(int32_t* p, int64_t count, int32_t value) {
@@ -304,9 +438,12 @@ __global__ __launch_bounds__(256) void k_rows_wave(const T* x, T* y, int64_t row
 static size_t topp_arrivals_offset(int64_t rows, int64_t len) {
     return kWsHeader + (size_t)rows * (size_t)row_segments(len) * sizeof(uint64_t);
 }
-size_t scan_rows_ws_bytes(int64_t rows, int64_t len) {
-    if (!long_rows(len)) return kWsHeader;
+size_t topp_ws_bytes(int64_t rows, int64_t len) {
     return topp_arrivals_offset(rows, len) + (size_t)rows * sizeof(uint64_t);
+}
+size_t scan_rows_ws_bytes(int64_t rows, int64_t len) {
+    // short rows (one wavefront per row) need no workspace beyond the header
+    return long_rows(len) ? topp_ws_bytes(rows, len) : kWsHeader;
 }
 
 static bool aligned16(const void* p) { return ((uintptr_t)p % 16) == 0; }
@@ -334,10 +471,10 @@ static void rows_long(bool exclusive, bool vec, const T* x, T* y, int64_t rows, 
                        status_words);
 }
 
-template <class G>
-static void topp_long(bool vec, const float* probs, int32_t* cutoff, int64_t rows, int64_t len,
-                      float p, void* ws, size_t ws_bytes, hipStream_t stream) {
-    (void)ws_bytes;
+template <class G, ToppMode MODE>
+static void topp_long(bool vec, const float* probs, const int32_t* idx, const float* theta,
+                      int32_t* cutoff, int32_t* token, int64_t rows, int64_t len, float p,
+                      void* ws, hipStream_t stream) {
     using TV = RowTile<float, G, true>;
     using TU = RowTile<float, G, false>;
     const uint32_t segs = (uint32_t)((len + TV::kElems - 1) / TV::kElems);
@@ -346,9 +483,22 @@ static void topp_long(bool vec, const float* probs, int32_t* cutoff, int64_t row
     uint64_t* sums = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
     uint64_t* arrivals = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) +
                                                      topp_arrivals_offset(rows, len));
-    auto k = vec ? k_topp<TV, true> : k_topp<TU, false>;
-    hipLaunchKernelGGL(k, dim3(nt), dim3(threads), 0, stream, probs, cutoff, len, segs, p,
-                       reinterpret_cast<WsHeader*>(ws), sums, arrivals);
+    auto k = vec ? k_topp<TV, true, MODE> : k_topp<TU, false, MODE>;
+    hipLaunchKernelGGL(k, dim3(nt), dim3(threads), 0, stream, probs, idx, theta, cutoff, token,
+                       len, segs, p, reinterpret_cast<WsHeader*>(ws), sums, arrivals);
+}
+
+template <ToppMode MODE>
+static void topp_any(bool vec, const float* probs, const int32_t* idx, const float* theta,
+                     int32_t* cutoff, int32_t* token, int64_t rows, int64_t len, float p,
+                     void* ws, hipStream_t stream) {
+    const int64_t t = row_tile(len);
+    if (t == 32768)
+        topp_long<RGeomL, MODE>(vec, probs, idx, theta, cutoff, token, rows, len, p, ws, stream);
+    else if (t == 8192)
+        topp_long<RGeomM, MODE>(vec, probs, idx, theta, cutoff, token, rows, len, p, ws, stream);
+    else
+        topp_long<RGeomS, MODE>(vec, probs, idx, theta, cutoff, token, rows, len, p, ws, stream);
 }
 
 template <class T, bool TOPP>
@@ -371,9 +521,8 @@ static hipError_t rows_typed(bool exclusive, const T* x, T* y, int64_t rows, int
     }
     const int64_t t = row_tile(len);
     if constexpr (TOPP) {
-        if (t == 32768) topp_long<RGeomL>(vec, x, cutoff, rows, len, p, ws, ws_bytes, stream);
-        else if (t == 8192) topp_long<RGeomM>(vec, x, cutoff, rows, len, p, ws, ws_bytes, stream);
-        else topp_long<RGeomS>(vec, x, cutoff, rows, len, p, ws, ws_bytes, stream);
+        topp_any<ToppMode::Cutoff>(vec, x, nullptr, nullptr, cutoff, nullptr, rows, len, p, ws,
+                                   stream);
     } else {
         if (t == 32768) rows_long<T, RGeomL>(exclusive, vec, x, y, rows, len, ws, ws_bytes, stream);
         else if (t == 8192) rows_long<T, RGeomM>(exclusive, vec, x, y, rows, len, ws, ws_bytes, stream);
@@ -400,6 +549,73 @@ hipError_t launch_topp_cutoff(const float* probs, int32_t* cutoff, int64_t rows,
                               float p, void* ws, size_t ws_bytes, hipStream_t stream) {
     return rows_typed<float, true>(false, probs, nullptr, rows, len, p, cutoff, ws, ws_bytes,
                                    stream);
+}
+
+// Appendix "Weighted Sampling", per row (any length; workspace
+// topp_ws_bytes(rows, len)).
+hipError_t launch_weighted_sample(const float* w, const float* theta, int32_t* out, int64_t rows,
+                                  int64_t len, void* ws, hipStream_t stream) {
+    if (rows == 0) return hipSuccess;
+    if (len == 0) {
+        hipLaunchKernelGGL(k_fill_i32, dim3(wave_grid(rows)), dim3(256), 0, stream, out, rows,
+                           (int32_t)-1);
+        return hipGetLastError();
+    }
+    const bool vec = (len % 4 == 0) && aligned16(w);
+    topp_any<ToppMode::Weighted>(vec, w, nullptr, theta, nullptr, out, rows, len, 0.f, ws, stream);
+    return hipGetLastError();
+}
+
+// The top-p draw on rows already sorted in descending order: cutoff k, then
+// the draw among 0..k, reported through idx (workspace topp_ws_bytes).
+hipError_t launch_topp_draw_sorted(const float* sorted, const int32_t* idx, const float* theta,
+                                   float p, int32_t* token, int32_t* cutoff, int64_t rows,
+                                   int64_t len, void* ws, hipStream_t stream) {
+    if (rows == 0) return hipSuccess;
+    if (len == 0) {
+        hipLaunchKernelGGL(k_fill_i32, dim3(wave_grid(rows)), dim3(256), 0, stream, token, rows,
+                           (int32_t)-1);
+        if (cutoff)
+            hipLaunchKernelGGL(k_fill_i32, dim3(wave_grid(rows)), dim3(256), 0, stream, cutoff,
+                               rows, (int32_t)-1);
+        return hipGetLastError();
+    }
+    const bool vec = (len % 4 == 0) && aligned16(sorted);
+    topp_any<ToppMode::Sample>(vec, sorted, idx, theta, cutoff, token, rows, len, p, ws, stream);
+    return hipGetLastError();
+}
+
+// The top-p sampler on unsorted rows (Section 5 "Top-p or Nucleus Sampling"):
+// a stable descending radix sort of each row, keeping source indices, then
+// the cutoff and the draw on the sorted row.  Workspace: the sort's and the
+// draw's common head, then four rows x len arrays (sorted keys, their source
+// indices, and the sort's two ping-pong buffers).
+static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+static size_t topp_sample_head(int64_t rows, int64_t len) {
+    const size_t a = radix_rows_ws_bytes(rows, len), b = topp_ws_bytes(rows, len);
+    return align256(a > b ? a : b);
+}
+size_t topp_sample_ws_bytes(int64_t rows, int64_t len) {
+    return topp_sample_head(rows, len) + 4 * align256((size_t)rows * (size_t)len * 4);
+}
+hipError_t launch_topp_sample(const float* probs, const float* theta, float p, int32_t* token,
+                              int32_t* cutoff, int64_t rows, int64_t len, void* ws,
+                              hipStream_t stream) {
+    if (rows == 0) return hipSuccess;
+    if (len == 0)
+        return launch_topp_draw_sorted(probs, nullptr, theta, p, token, cutoff, rows, len, ws,
+                                       stream);
+    const size_t head = topp_sample_head(rows, len);
+    const size_t mb = align256((size_t)rows * (size_t)len * 4);
+    char* base = reinterpret_cast<char*>(ws) + head;
+    float* sorted = reinterpret_cast<float*>(base);
+    int32_t* perm = reinterpret_cast<int32_t*>(base + mb);
+    float* keys_tmp = reinterpret_cast<float*>(base + 2 * mb);
+    int32_t* perm_tmp = reinterpret_cast<int32_t*>(base + 3 * mb);
+    const hipError_t e = launch_radix_sort_typed(KeyType::F32, true, probs, sorted, perm, keys_tmp,
+                                                 perm_tmp, rows, len, ws, head, stream);
+    if (e != hipSuccess) return e;
+    return launch_topp_draw_sorted(sorted, perm, theta, p, token, cutoff, rows, len, ws, stream);
 }
 
 }  // namespace ls

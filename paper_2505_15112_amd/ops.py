@@ -292,3 +292,65 @@ def radix_sort_f16(keys, descending=False, with_perm=True, keys_out=None, perm_o
     """Stable sort of float16 keys in IEEE 754 totalOrder, ascending or descending."""
     return _radix_sort_typed("radix_sort_f16", keys, torch.float16, descending, with_perm,
                              keys_out, perm_out, keys_tmp, perm_tmp, ws)
+
+
+def radix_sort_rows_f32(keys, descending=False, with_perm=True, keys_out=None, perm_out=None,
+                        keys_tmp=None, perm_tmp=None, ws=None):
+    """Stable sort of every row of a 2-D float32 tensor on its own (IEEE 754
+    totalOrder).  perm_out holds indices within the row.  Returns (keys_out,
+    perm_out or None)."""
+    _check(keys, torch.float32, "keys", dims=(2,))
+    rows, length = keys.shape
+    dev = keys.device
+    keys_out = _out(keys, keys_out, torch.float32)
+    keys_tmp = torch.empty_like(keys) if keys_tmp is None else keys_tmp
+    if with_perm:
+        perm_out = _out(keys, perm_out, torch.int32)
+        perm_tmp = torch.empty(keys.shape, dtype=torch.int32, device=dev) if perm_tmp is None \
+            else perm_tmp
+    else:
+        perm_out = perm_tmp = None
+    if ws is None:
+        ws = workspace(_lib.OP_SORT_ROWS, dev, rows=rows, length=length)
+    with torch.cuda.device(dev):
+        _lib.call("radix_sort_rows_f32", _ptr(keys), _ptr(keys_out), _ptr(perm_out),
+                  _ptr(keys_tmp), _ptr(perm_tmp), rows, length, int(bool(descending)), _ptr(ws),
+                  ws.numel(), _stream(dev))
+    return keys_out, perm_out
+
+
+def weighted_sample_f32(w, theta, out=None, ws=None):
+    """Per row of non-negative weights: the index drawn by inverse transform
+    with the uniform draw theta[row] (int32 tensor of shape [rows])."""
+    _check(w, torch.float32, "w", dims=(2,))
+    rows, length = w.shape
+    _check(theta, torch.float32, "theta", dims=(1,))
+    if theta.numel() != rows:
+        raise ValueError(f"theta: expected {rows} draws, got {theta.numel()}")
+    tok = _out(w, out, torch.int32, shape=(rows,))
+    if ws is None:
+        ws = workspace(_lib.OP_WEIGHTED_SAMPLE, w.device, rows=rows, length=length)
+    with torch.cuda.device(w.device):
+        _lib.call("weighted_sample_f32", _ptr(w), _ptr(theta), _ptr(tok), rows, length, _ptr(ws),
+                  ws.numel(), _stream(w.device))
+    return tok
+
+
+def topp_sample_f32(probs, theta, p, with_cutoff=False, out=None, cutoff_out=None, ws=None):
+    """Top-p sampling on unsorted rows: per row, the token drawn with the
+    uniform draw theta[row] from the smallest descending-sorted prefix whose
+    mass reaches p.  Returns the int32 tokens, and the cutoffs (index in the
+    sorted row) when with_cutoff."""
+    _check(probs, torch.float32, "probs", dims=(2,))
+    rows, length = probs.shape
+    _check(theta, torch.float32, "theta", dims=(1,))
+    if theta.numel() != rows:
+        raise ValueError(f"theta: expected {rows} draws, got {theta.numel()}")
+    tok = _out(probs, out, torch.int32, shape=(rows,))
+    cut = _out(probs, cutoff_out, torch.int32, shape=(rows,)) if with_cutoff else None
+    if ws is None:
+        ws = workspace(_lib.OP_TOPP_SAMPLE, probs.device, rows=rows, length=length)
+    with torch.cuda.device(probs.device):
+        _lib.call("topp_sample_f32", _ptr(probs), _ptr(theta), float(p), _ptr(tok), _ptr(cut),
+                  rows, length, _ptr(ws), ws.numel(), _stream(probs.device))
+    return (tok, cut) if with_cutoff else tok

@@ -82,6 +82,34 @@ def topp_probs(rows: int, length: int, seed: int = 0, stream: int = 4,
     return out
 
 
+def sample_probs(rows: int, length: int, seed: int = 0, stream: int = 5,
+                 sigma: float = 2.0) -> np.ndarray:
+    """Rows of a probability vector in token order (unsorted): softmax of
+    N(0, sigma^2) logits, as a sampler receives it."""
+    rng = _rng(seed, stream)
+    out = np.empty((rows, length), np.float32)
+    for r in range(rows):
+        z = sigma * rng.standard_normal(length)
+        z -= z.max()
+        e = np.exp(z)
+        out[r] = (e / e.sum()).astype(np.float32)
+    return out
+
+
+def sample_theta(rows: int, seed: int = 0, stream: int = 6) -> np.ndarray:
+    """One uniform draw in [0, 1) per row (float32)."""
+    return _rng(seed, stream).random(rows, dtype=np.float32)
+
+
+def sample_weights(rows: int, length: int, seed: int = 0, stream: int = 7,
+                   zero_frac: float = 0.25) -> np.ndarray:
+    """Non-negative unnormalised weights: exponential, a fraction exactly 0."""
+    rng = _rng(seed, stream)
+    w = rng.exponential(1.0, (rows, length)).astype(np.float32)
+    w[rng.random((rows, length)) < zero_frac] = 0.0
+    return w
+
+
 # The workloads that tests and the benchmark use, by name.
 METRIC_N = 1 << 28
 CONFIGS = {
@@ -89,6 +117,8 @@ CONFIGS = {
     "scan_f16f32_n2^24": dict(op="scan_inclusive_f16f32", n=1 << 24),
     "compact_n2^28": dict(op="compact_by_mask_f32", n=1 << 28),
     "topp_128x131072": dict(op="topp_cutoff_f32", rows=128, length=131072, p=0.9),
+    "topp_sample_128x131072": dict(op="topp_sample_f32", rows=128, length=131072, p=0.9),
+    "weighted_sample_128x131072": dict(op="weighted_sample_f32", rows=128, length=131072),
     "radix_n2^26": dict(op="radix_sort_u32", n=1 << 26),
     "metric_scan_n2^28": dict(op="scan_inclusive_i32/f32", n=METRIC_N),
 }

@@ -72,3 +72,24 @@ def topp_accept(g: int, k: int, csum: np.ndarray, p: float) -> bool:
     ok_here = csum[g] >= pd - tol[g]
     ok_before = g == 0 or csum[g - 1] < pd + tol[g - 1]
     return bool(ok_here and ok_before)
+
+
+def draw_tol(theta: float, total: float) -> float:
+    """Tolerance of a GPU threshold u = theta * total, where total is an fp32
+    sum carrying the float bound and the product is rounded to fp32."""
+    return theta * (FLOAT_REL * total + FLOAT_ABS) + 2.0**-23 * theta * total
+
+
+def draw_accept(g: int, csum: np.ndarray, u: float, u_tol: float, limit: int) -> bool:
+    """GPU inverse-transform draw g on one row: the first i <= limit whose
+    running sum exceeds u, else limit.  csum is the float64 inclusive prefix
+    of the row (non-negative entries); u the float64 threshold, known to the
+    GPU within u_tol.  g is accepted if it lies in [0, limit], the prefix
+    before it does not exceed u within tolerance, and its own prefix exceeds
+    u within tolerance (or g is the fallback, limit)."""
+    if not (0 <= g <= limit):
+        return False
+    tol = FLOAT_REL * csum + FLOAT_ABS + u_tol
+    ok_here = csum[g] > u - tol[g]
+    ok_before = g == 0 or csum[g - 1] <= u + tol[g - 1]
+    return bool(ok_before and (ok_here or g == limit))

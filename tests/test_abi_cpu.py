@@ -199,3 +199,79 @@ def test_radix_validation(lib):
     assert lib.libscan_workspace_bytes(_lib.OP_RADIX_SORT, 1 << 26, 0, 0, 8, ctypes.byref(out)) == 0
     assert out.value >= 256 + 256 * 4 * ((1 << 26) // 8192)
     assert lib.libscan_workspace_bytes(_lib.OP_RADIX_SORT, 100, 0, 0, 3, ctypes.byref(out)) == _lib.EINVAL
+
+
+def test_radix_key_limit(lib):
+    # at most 2^30 keys per sort, so count-table offsets left in the workspace stay below 2^30
+    KO, KT = P(1 << 42), P(1 << 43)
+    out = ctypes.c_size_t(0)
+    assert lib.radix_sort_u32(XB, KO, None, KT, None, (1 << 30) + 1, 8, WS, BIG, None) == _lib.ERANGE
+    assert lib.radix_sort_f32(XB, KO, None, KT, None, (1 << 30) + 1, 0, WS, BIG, None) == _lib.ERANGE
+    assert lib.libscan_workspace_bytes(_lib.OP_RADIX_SORT, (1 << 30) + 1, 0, 0, 8,
+                                       ctypes.byref(out)) == _lib.ERANGE
+    assert lib.libscan_workspace_bytes(_lib.OP_RADIX_SORT, 1 << 30, 0, 0, 8,
+                                       ctypes.byref(out)) == _lib.OK
+
+
+def test_sort_rows_validation(lib):
+    fn = lib.radix_sort_rows_f32
+    KO, PO, KT, PT = P(0x2000000), P(0x3000000), P(0x4000000), P(0x5000000)
+    W2 = P(0x60000000)
+    assert fn(X, KO, PO, KT, PT, -1, 10, 0, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, KO, PO, KT, PT, 10, -1, 0, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, KO, PO, None, PT, 4, 10, 0, W2, BIG, None) == _lib.EINVAL     # no keys_tmp
+    assert fn(X, KO, PO, KT, None, 4, 10, 1, W2, BIG, None) == _lib.EINVAL     # perm without tmp
+    assert fn(X, X, PO, KT, PT, 4, 10, 0, W2, BIG, None) == _lib.EINVAL        # in place
+    assert fn(X, KO, PO, P(0x2000000 + 39 * 4), PT, 4, 10, 0, W2, BIG, None) == _lib.EINVAL
+    assert fn(XB, YB, None, P(1 << 42), None, 1 << 16, (1 << 14) + 1, 0, W2, BIG,
+              None) == _lib.ERANGE                                              # > 2^30 keys
+    assert fn(XB, YB, None, P(1 << 42), None, (1 << 24) + 1, 8, 0, W2, BIG,
+              None) == _lib.ERANGE                                              # grid too large
+    assert fn(X, KO, PO, KT, PT, 16, 10000, 0, W2, 64, None) == _lib.ENOSPACE
+    assert fn(None, None, None, None, None, 0, 10, 0, None, 0, None) == _lib.OK
+    assert fn(None, None, None, None, None, 10, 0, 0, None, 0, None) == _lib.OK
+    out = ctypes.c_size_t(0)
+    assert lib.libscan_workspace_bytes(_lib.OP_SORT_ROWS, 0, 64, 1 << 17, 0,
+                                       ctypes.byref(out)) == _lib.OK
+    assert out.value >= 256 + 64 * 256 * 4 * ((1 << 17) // 8192)
+
+
+def test_weighted_sample_validation(lib):
+    fn = lib.weighted_sample_f32
+    TH, OUT = P(0x2000000), P(0x3000000)
+    assert fn(X, TH, OUT, -1, 10, WS, BIG, None) == _lib.EINVAL
+    assert fn(None, TH, OUT, 4, 10, WS, BIG, None) == _lib.EINVAL
+    assert fn(X, None, OUT, 4, 10, WS, BIG, None) == _lib.EINVAL               # no theta
+    assert fn(X, TH, None, 4, 10, WS, BIG, None) == _lib.EINVAL
+    assert fn(X, TH, P(0x100008), 4, 10, WS, BIG, None) == _lib.EINVAL         # out inside w
+    assert fn(X, TH, P(0x2000004), 4, 10, WS, BIG, None) == _lib.EINVAL        # out over theta
+    assert fn(XB, TH, OUT, 1, 1 << 31, WS, BIG, None) == _lib.ERANGE
+    assert fn(XB, TH, OUT, 128, 131072, WS, 256, None) == _lib.ENOSPACE
+    assert fn(None, None, None, 0, 10, None, 0, None) == _lib.OK
+    out = ctypes.c_size_t(0)
+    # every length needs the per-tile sums and the per-row arrival counters
+    assert lib.libscan_workspace_bytes(_lib.OP_WEIGHTED_SAMPLE, 0, 1000, 100, 0,
+                                       ctypes.byref(out)) == _lib.OK
+    assert out.value >= 256 + 1000 * 16
+
+
+def test_topp_sample_validation(lib):
+    fn = lib.topp_sample_f32
+    TH, TOK, CUT = P(0x2000000), P(0x3000000), P(0x3100000)
+    W2 = P(0x60000000)
+    assert fn(X, TH, float("nan"), TOK, CUT, 4, 10, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, None, 0.9, TOK, CUT, 4, 10, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, TH, 0.9, None, CUT, 4, 10, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, TH, 0.9, TOK, TOK, 4, 10, W2, BIG, None) == _lib.EINVAL        # cutoff == token
+    assert fn(X, TH, 0.9, TOK, P(0x100004), 4, 10, W2, BIG, None) == _lib.EINVAL
+    # inputs or outputs inside the workspace (it holds the sorted copies)
+    assert fn(X, TH, 0.9, TOK, CUT, 4, 10, P(0x3000000 - 256), BIG, None) == _lib.EINVAL
+    assert fn(X, TH, 0.9, TOK, CUT, 4, 10, W2, 64, None) == _lib.ENOSPACE
+    assert fn(XB, TH, 0.9, TOK, CUT, 1 << 16, (1 << 14) + 1, W2, BIG, None) == _lib.ERANGE
+    assert fn(None, None, 0.9, None, None, 0, 10, None, 0, None) == _lib.OK
+    out = ctypes.c_size_t(0)
+    assert lib.libscan_workspace_bytes(_lib.OP_TOPP_SAMPLE, 0, 64, 1 << 17, 0,
+                                       ctypes.byref(out)) == _lib.OK
+    assert out.value >= 16 * 64 * (1 << 17)
+    assert lib.libscan_workspace_bytes(_lib.OP_TOPP_SAMPLE, 0, 1 << 16, (1 << 14) + 1, 0,
+                                       ctypes.byref(out)) == _lib.ERANGE

@@ -28,7 +28,10 @@ def _big_ws(ops, n):
              _lib.workspace_bytes(_lib.OP_RADIX_SORT, n, bits=8),
              _lib.workspace_bytes(_lib.OP_RADIX_SORT, n, bits=4),
              _lib.workspace_bytes(_lib.OP_RADIX_SORT, n, bits=1),
-             _lib.workspace_bytes(_lib.OP_SCAN_ROWS, rows=16, length=n // 16)]
+             _lib.workspace_bytes(_lib.OP_SCAN_ROWS, rows=16, length=n // 16),
+             _lib.workspace_bytes(_lib.OP_SORT_ROWS, rows=16, length=n // 16),
+             _lib.workspace_bytes(_lib.OP_WEIGHTED_SAMPLE, rows=16, length=n // 16),
+             _lib.workspace_bytes(_lib.OP_TOPP_SAMPLE, rows=16, length=n // 16)]
     nbytes = (max(sizes) + 15) // 16 * 16
     return torch.zeros(nbytes, dtype=torch.uint8, device="cuda")  # zero-filled = ready
 
@@ -60,6 +63,25 @@ def _run_all(ops, ws, n, seed):
     assert_equal_first_diff(to_host(ops.scan_rows_i32(to_dev(xr), ws=ws)), oracle.scan_rows_i32(xr),
                             "rows")
     _check_topp(ops, ws, n, seed)
+    _check_samplers(ops, ws, n, seed)
+
+
+def _check_samplers(ops, ws, n, seed):
+    """The row sort and both samplers, exact cases (integer-valued sums): the
+    sort's count table and the samplers' tile sums share the workspace with
+    everything above."""
+    rng = np.random.default_rng(seed)
+    k = W.values_f32(n, seed=seed).reshape(16, n // 16)
+    ko, po = ops.radix_sort_rows_f32(to_dev(k), descending=True, ws=ws)
+    rk, rp = oracle.sort_rows_f32(k, descending=True)
+    assert_equal_first_diff(to_host(po), rp, "sort rows")
+    w = rng.integers(0, 4, (16, n // 16)).astype(np.float32)
+    theta = (rng.integers(0, 4, 16) / 4.0).astype(np.float32)
+    g = to_host(ops.weighted_sample_f32(to_dev(w), to_dev(theta), ws=ws))
+    assert_equal_first_diff(g, oracle.weighted_sample_f32(w, theta), "weighted")
+    probs = (rng.integers(0, 16, (16, n // 16)) * 2.0**-24).astype(np.float32)
+    tok = to_host(ops.topp_sample_f32(to_dev(probs), to_dev(theta), 2.0**-6, ws=ws))
+    assert_equal_first_diff(tok, oracle.topp_sample_f32(probs, theta, 2.0**-6)[0], "topp sample")
 
 
 def _check_topp(ops, ws, n, seed):
