@@ -190,7 +190,7 @@ int split_by_flags_u32(const uint32_t* keys, const int32_t* idx_in, const uint8_
  * splits); all give the same output.  keys_tmp
  * (and perm_tmp when perm_out is given) are caller-provided n-element
  * ping-pong buffers whose contents are clobbered.  No two of keys, keys_out,
- * perm_out, keys_tmp, perm_tmp may overlap.  n <= 2^30.  Workspace:
+ * perm_out, keys_tmp, perm_tmp may overlap.  n <= INT32_MAX.  Workspace:
  * LIBSCAN_OP_RADIX_SORT with n and bits = bits_per_pass. */
 int radix_sort_u32(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out, uint32_t* keys_tmp,
                    int32_t* perm_tmp, int64_t n, int bits_per_pass, void* ws, size_t ws_bytes,
@@ -208,7 +208,7 @@ int radix_sort_u32(const uint32_t* keys, uint32_t* keys_out, int32_t* perm_out, 
  * every bit pattern: -NaN < -Inf < ... < -0 < +0 < ... < +Inf < +NaN.
  * keys_out, perm_out (nullable: keys only), keys_tmp and perm_tmp as in
  * radix_sort_u32 (elements of the key type; no two may overlap).
- * n <= 2^30.  Workspace: LIBSCAN_OP_RADIX_SORT with n and bits = 8. */
+ * n <= INT32_MAX.  Workspace: LIBSCAN_OP_RADIX_SORT with n and bits = 8. */
 int radix_sort_i32(const int32_t* keys, int32_t* keys_out, int32_t* perm_out, int32_t* keys_tmp,
                    int32_t* perm_tmp, int64_t n, int descending, void* ws, size_t ws_bytes,
                    void* stream);
@@ -225,7 +225,7 @@ int radix_sort_f16(const uint16_t* keys, uint16_t* keys_out, int32_t* perm_out, 
  * totalOrder as radix_sort_f32.  perm_out (nullable) receives each key's index
  * within its row (0..len-1).  keys_tmp / perm_tmp are rows x len ping-pong
  * buffers.  No two of keys, keys_out, perm_out, keys_tmp, perm_tmp may
- * overlap.  rows * len <= 2^30 and rows * ceil(len / 8192) <= 2^24.
+ * overlap.  rows * len <= INT32_MAX and rows * ceil(len / 8192) <= 2^24.
  * Workspace: LIBSCAN_OP_SORT_ROWS with (rows, len). */
 int radix_sort_rows_f32(const float* keys, float* keys_out, int32_t* perm_out, float* keys_tmp,
                         int32_t* perm_tmp, int64_t rows, int64_t len, int descending, void* ws,
@@ -255,7 +255,7 @@ int weighted_sample_f32(const float* w, const float* theta_dev, int32_t* out, in
  * token_out (device, rows int32) receives the token index of S[j] in the
  * original row; cutoff_out (nullable, device, rows int32) receives k.  Both
  * are -1 for len == 0.  theta_dev as in weighted_sample_f32; p must not be
- * NaN.  rows * len <= 2^30, rows * ceil(len / 8192) <= 2^24.  The sorted
+ * NaN.  rows * len <= INT32_MAX, rows * ceil(len / 8192) <= 2^24.  The sorted
  * copies are kept in the workspace, which no input or output may overlap.
  * Workspace: LIBSCAN_OP_TOPP_SAMPLE with (rows, len) (about 16 bytes per
  * element). */

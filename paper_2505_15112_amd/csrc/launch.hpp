@@ -48,9 +48,8 @@ hipError_t launch_topp_draw_sorted(const float* sorted, const int32_t* idx, cons
 hipError_t launch_topp_cutoff(const float* probs, int32_t* cutoff, int64_t rows, int64_t len,
                               float p, void* ws, size_t ws_bytes, hipStream_t stream);
 constexpr int64_t kMaxGridTiles = int64_t(1) << 24;
-// Radix sorts: at most 2^30 keys per call (or rows x len in total), so that
-// every count-table offset, left in the workspace, stays below 2^30.
-constexpr int64_t kMaxRadixKeys = int64_t(1) << 30;
+// Radix sorts: keys per call (rows x len in total), indices being int32.
+constexpr int64_t kMaxRadixKeys = INT32_MAX;
 
 // Compress and split (Section 5).  flags == nullptr in launch_split means
 // "flag = key bit `bit` is 0" (the LSB radix-sort pass).

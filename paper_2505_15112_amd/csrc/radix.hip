@@ -391,24 +391,38 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_count(
     const int64_t tstart = (int64_t)tr * kR8Tile;  // within the row
     const K* kr = keys + (int64_t)row * len;
     const int64_t wbase = tstart + (int64_t)w * kR8Chunks * kWave;
-    if (sizeof(K) == 4 && vec && tstart + kR8Tile <= len) {  // 4 x 16-byte loads per lane
+    if (vec && tstart + kR8Tile <= len) {
+        // 16-byte loads: 4 of 32-bit keys or 2 of 16-bit keys per lane
+        constexpr int kPer = 16 / (int)sizeof(K);
+        constexpr int kLoads = kR8Chunks / kPer;
         const u32x4* k4 = reinterpret_cast<const u32x4*>(kr + wbase);
-        u32x4 v[kR8Chunks / 4];
+        u32x4 v[kLoads];
 #pragma unroll
-        for (int j = 0; j < kR8Chunks / 4; ++j) v[j] = k4[j * kWave + lane];
+        for (int j = 0; j < kLoads; ++j) v[j] = k4[j * kWave + lane];
 #pragma unroll
-        for (int j = 0; j < kR8Chunks / 4; ++j) {
-            atomicAdd(&h[(code.apply(v[j].x) >> shift) & 255u], 1u);
-            atomicAdd(&h[(code.apply(v[j].y) >> shift) & 255u], 1u);
-            atomicAdd(&h[(code.apply(v[j].z) >> shift) & 255u], 1u);
-            atomicAdd(&h[(code.apply(v[j].w) >> shift) & 255u], 1u);
-        }
+        for (int j = 0; j < kLoads; ++j)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const uint32_t word = v[j][c];
+                if (sizeof(K) == 4) {
+                    atomicAdd(&h[(code.apply(word) >> shift) & 255u], 1u);
+                } else {
+                    atomicAdd(&h[(code.apply(word & 0xFFFFu) >> shift) & 255u], 1u);
+                    atomicAdd(&h[(code.apply(word >> 16) >> shift) & 255u], 1u);
+                }
+            }
     } else {
+        // every load issued before the first atomic needs one
+        uint32_t k[kR8Chunks];
 #pragma unroll
         for (int j = 0; j < kR8Chunks; ++j) {
             const int64_t i = wbase + j * kWave + lane;
-            if (i < len) atomicAdd(&h[(code.apply((uint32_t)kr[i]) >> shift) & 255u], 1u);
+            k[j] = i < len ? (uint32_t)kr[i] : 0u;
         }
+#pragma unroll
+        for (int j = 0; j < kR8Chunks; ++j)
+            if (wbase + j * kWave + lane < len)
+                atomicAdd(&h[(code.apply(k[j]) >> shift) & 255u], 1u);
     }
     __syncthreads();
     if (threadIdx.x < kR8Digits) {
@@ -451,12 +465,22 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
         s_gbase[threadIdx.x] = *o;
         *o = 0;  // offsets can reach 2^30 and more: leave the workspace word zero
     }
+    // All loads first, then the encoding: applied inside a per-key branch it
+    // would make each load wait for the one before.  (Lanes past the end get
+    // a code of 0; they are masked out everywhere below.)
     uint32_t key[kR8Chunks];
+    if (full) {
 #pragma unroll
-    for (int j = 0; j < kR8Chunks; ++j) {
-        const int64_t i = wbase + j * kWave + lane;
-        key[j] = (full || i < len) ? code.apply((uint32_t)kin[i]) : 0u;
+        for (int j = 0; j < kR8Chunks; ++j) key[j] = (uint32_t)kin[wbase + j * kWave + lane];
+    } else {
+#pragma unroll
+        for (int j = 0; j < kR8Chunks; ++j) {
+            const int64_t i = wbase + j * kWave + lane;
+            key[j] = i < len ? (uint32_t)kin[i] : 0u;
+        }
     }
+#pragma unroll
+    for (int j = 0; j < kR8Chunks; ++j) key[j] = code.apply(key[j]);
     __syncthreads();
 
     // Chunks in groups of 4: the peer groups of the 4 chunks, their LDS
@@ -629,7 +653,9 @@ static hipError_t radix8_sort(const K* keys, K* keys_out, int32_t* perm_out, K* 
         int32_t* dp = perm_out ? ((p % 2 == 0) ? perm_tmp : perm_out) : nullptr;
         const KeyCode c = p == 0 ? code : kIdentityCode;
         const KeyDecode d = p == passes - 1 ? decode : kIdentityDecode;
-        const bool vec = ((uintptr_t)src_k % 16) == 0 && (rows == 1 || len % 4 == 0);
+        // 16-byte loads need every row start 16-byte aligned
+        const bool vec = ((uintptr_t)src_k % 16) == 0 &&
+                         (rows == 1 || ((size_t)len * sizeof(K)) % 16 == 0);
         hipLaunchKernelGGL(k_radix8_count<K>, dim3(nt), dim3(kR8Waves * kWave), 0, stream, src_k,
                            len, tpr, 8 * p, vec, counts, c);
         hipError_t e = rows == 1

@@ -201,18 +201,6 @@ def test_radix_validation(lib):
     assert lib.libscan_workspace_bytes(_lib.OP_RADIX_SORT, 100, 0, 0, 3, ctypes.byref(out)) == _lib.EINVAL
 
 
-def test_radix_key_limit(lib):
-    # at most 2^30 keys per sort, so count-table offsets left in the workspace stay below 2^30
-    KO, KT = P(1 << 42), P(1 << 43)
-    out = ctypes.c_size_t(0)
-    assert lib.radix_sort_u32(XB, KO, None, KT, None, (1 << 30) + 1, 8, WS, BIG, None) == _lib.ERANGE
-    assert lib.radix_sort_f32(XB, KO, None, KT, None, (1 << 30) + 1, 0, WS, BIG, None) == _lib.ERANGE
-    assert lib.libscan_workspace_bytes(_lib.OP_RADIX_SORT, (1 << 30) + 1, 0, 0, 8,
-                                       ctypes.byref(out)) == _lib.ERANGE
-    assert lib.libscan_workspace_bytes(_lib.OP_RADIX_SORT, 1 << 30, 0, 0, 8,
-                                       ctypes.byref(out)) == _lib.OK
-
-
 def test_sort_rows_validation(lib):
     fn = lib.radix_sort_rows_f32
     KO, PO, KT, PT = P(0x2000000), P(0x3000000), P(0x4000000), P(0x5000000)
@@ -223,8 +211,8 @@ def test_sort_rows_validation(lib):
     assert fn(X, KO, PO, KT, None, 4, 10, 1, W2, BIG, None) == _lib.EINVAL     # perm without tmp
     assert fn(X, X, PO, KT, PT, 4, 10, 0, W2, BIG, None) == _lib.EINVAL        # in place
     assert fn(X, KO, PO, P(0x2000000 + 39 * 4), PT, 4, 10, 0, W2, BIG, None) == _lib.EINVAL
-    assert fn(XB, YB, None, P(1 << 42), None, 1 << 16, (1 << 14) + 1, 0, W2, BIG,
-              None) == _lib.ERANGE                                              # > 2^30 keys
+    assert fn(XB, YB, None, P(1 << 42), None, 1 << 16, 1 << 15, 0, W2, BIG,
+              None) == _lib.ERANGE                                              # > INT32_MAX keys
     assert fn(XB, YB, None, P(1 << 42), None, (1 << 24) + 1, 8, 0, W2, BIG,
               None) == _lib.ERANGE                                              # grid too large
     assert fn(X, KO, PO, KT, PT, 16, 10000, 0, W2, 64, None) == _lib.ENOSPACE
@@ -267,11 +255,11 @@ def test_topp_sample_validation(lib):
     # inputs or outputs inside the workspace (it holds the sorted copies)
     assert fn(X, TH, 0.9, TOK, CUT, 4, 10, P(0x3000000 - 256), BIG, None) == _lib.EINVAL
     assert fn(X, TH, 0.9, TOK, CUT, 4, 10, W2, 64, None) == _lib.ENOSPACE
-    assert fn(XB, TH, 0.9, TOK, CUT, 1 << 16, (1 << 14) + 1, W2, BIG, None) == _lib.ERANGE
+    assert fn(XB, TH, 0.9, TOK, CUT, 1 << 16, 1 << 15, W2, BIG, None) == _lib.ERANGE
     assert fn(None, None, 0.9, None, None, 0, 10, None, 0, None) == _lib.OK
     out = ctypes.c_size_t(0)
     assert lib.libscan_workspace_bytes(_lib.OP_TOPP_SAMPLE, 0, 64, 1 << 17, 0,
                                        ctypes.byref(out)) == _lib.OK
     assert out.value >= 16 * 64 * (1 << 17)
-    assert lib.libscan_workspace_bytes(_lib.OP_TOPP_SAMPLE, 0, 1 << 16, (1 << 14) + 1, 0,
+    assert lib.libscan_workspace_bytes(_lib.OP_TOPP_SAMPLE, 0, 1 << 16, 1 << 15, 0,
                                        ctypes.byref(out)) == _lib.ERANGE
