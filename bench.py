@@ -11,7 +11,9 @@ The same run measures every other operation of the library on its workload
 ("ops"): the fp32 metric scan, the reduce-then-scan check variant, the
 fp16->fp32 scan (n = 2^24), the latency-bound int32 scan (n = 2^16), mask
 compaction (n = 2^28), batched rows and the top-p cutoff (128 x 131072),
-stable split and the 1-, 4- and 8-bit radix sorts (n = 2^26).  Workloads
+the samplers on unsorted rows (top-p sampling, its descending row sort, and
+weighted sampling, 128 x 131072), stable split and the 1-, 4- and 8-bit
+radix sorts (n = 2^26).  Workloads
 that fit in the 256 MB Infinity Cache are timed cold: rounds of (512 MiB
 overwrite, call) enqueued back to back, minus the overwrites alone.
 A sweep of the int32 scan over n = 2^20 .. 2^28 (and 2^k + 17) gives bandwidth
@@ -319,6 +321,45 @@ def main():
                                                  "rows*len*(4+4), cache-flushed")
         outputs["topp"] = (probs_host, cut, yr)
 
+        # config: the samplers on 128 x 131072 unsorted softmax rows (one draw per row)
+        log("samplers")
+        sp_host = W.sample_probs(rows, length, seed=0)
+        th_host = W.sample_theta(rows, seed=0)
+        sprobs = torch.from_numpy(sp_host).to(dev)
+        theta = torch.from_numpy(th_host).to(dev)
+        tok = torch.empty(rows, dtype=torch.int32, device=dev)
+        cut2 = torch.empty(rows, dtype=torch.int32, device=dev)
+        ws_smp = ops.workspace(_lib.OP_TOPP_SAMPLE, dev, rows=rows, length=length)
+        a = (P(sprobs), P(theta), ctypes.c_float(0.9), P(tok), P(cut2), rows, length, P(ws_smp),
+             ws_smp.numel(), sp)
+        ms = T.flushed(lambda: check(lib.topp_sample_f32(*a), "topp sample"), K, Wm)
+        # the descending sort with indices (4 passes: 12 + 16 x 3 + 4 bytes per key) and one
+        # read of the sorted row
+        bb = rows * length * (64 + 4)
+        opsd["topp_sample_128x131072"] = entry(
+            "topp_sample", ms, bb, memcpy_ms(bb, True),
+            "rows*len*(64 sort + 4 draw), cache-flushed",
+            {"p": 0.9, "draws_per_s": round(rows / (ms * 1e-3), 1)})
+        ko2 = torch.empty_like(sprobs)
+        po2 = torch.empty(rows, length, dtype=torch.int32, device=dev)
+        kt2 = torch.empty_like(sprobs)
+        pt2 = torch.empty_like(po2)
+        a = (P(sprobs), P(ko2), P(po2), P(kt2), P(pt2), rows, length, 1, P(ws_smp), ws_smp.numel(), sp)
+        ms = T.flushed(lambda: check(lib.radix_sort_rows_f32(*a), "sort rows"), K, Wm)
+        bb = rows * length * 64
+        opsd["sort_rows_f32_desc_128x131072"] = entry(
+            "sort_rows", ms, bb, memcpy_ms(bb, True), "rows*len*(12 + 16 x 3 + 4), cache-flushed",
+            {"mkeys_per_s": round(rows * length / (ms * 1e-3) / 1e6, 1)})
+        wtok = torch.empty(rows, dtype=torch.int32, device=dev)
+        a = (P(sprobs), P(theta), P(wtok), rows, length, P(ws_smp), ws_smp.numel(), sp)
+        ms = T.flushed(lambda: check(lib.weighted_sample_f32(*a), "weighted"), K, Wm)
+        opsd["weighted_sample_128x131072"] = entry(
+            "weighted_sample", ms, bt, memcpy_ms(bt, True),
+            "weights read once (rows*len*4), cache-flushed",
+            {"draws_per_s": round(rows / (ms * 1e-3), 1)})
+        outputs["samplers"] = (sp_host, th_host, tok, cut2, wtok)
+        del ko2, po2, kt2, pt2
+
         # config: radix sort, n = 2^26 uint32 keys (+ int32 permutation)
         log("radix")
         n5 = 1 << 26
@@ -452,6 +493,16 @@ def cpu_baseline_leg(x_host, y_dev, outputs, np, torch):
         ok = bool(np.all(np.abs(yr.cpu().numpy() - ry) <= 1e-5 * ra + 1e-6))
         res["scan_rows_f32_128x131072"] = {"gbps": round(ph.size * 8 / t / 1e9, 3),
                                            "s": round(t, 4), "matches_gpu": ok}
+        ph, th, tok, cut2, wtok = outputs["samplers"]
+        t, (rt, rc) = timed(lambda: oracle.topp_sample_f32(ph, th, 0.9), reps=1)
+        g, gc = tok.cpu().numpy(), cut2.cpu().numpy()
+        res["topp_sample_128x131072"] = {
+            "draws_per_s": round(ph.shape[0] / t, 1), "s": round(t, 3),
+            "exact_rows": int(np.sum((g == rt) & (gc == rc))), "rows": int(ph.shape[0])}
+        t, rw = timed(lambda: oracle.weighted_sample_f32(ph, th))
+        res["weighted_sample_128x131072"] = {
+            "draws_per_s": round(ph.shape[0] / t, 1), "s": round(t, 4),
+            "exact_rows": int(np.sum(wtok.cpu().numpy() == rw)), "rows": int(ph.shape[0])}
         kh = outputs["radix_keys"]
         sample = kh[: 1 << 22]
         t, _ = timed(lambda: oracle.sort_u32(sample), reps=1)
