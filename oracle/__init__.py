@@ -41,6 +41,7 @@ _SIGNATURES = {
     "oracle_sort_rows_f32": ([_p, _p, _p, _i64, _i64, ctypes.c_int], ctypes.c_int),
     "oracle_weighted_sample_f32": ([_p, _p, _p, _i64, _i64], None),
     "oracle_topp_sample_f32": ([_p, _p, ctypes.c_float, _p, _p, _i64, _i64], ctypes.c_int),
+    "oracle_topk_rows_f32": ([_p, _p, _p, _i64, _i64, _i64, ctypes.c_int], ctypes.c_int),
     "oracle_topp_cutoff_f32": ([_p, _p, _i64, _i64, ctypes.c_float], None),
     "oracle_half_to_double": ([ctypes.c_uint16], ctypes.c_double),
 }
@@ -213,6 +214,20 @@ class Oracle:
                                            _ptr(cut), rows, length) != 0:
             raise MemoryError("oracle_topp_sample_f32: allocation failed")
         return tok, cut
+
+    def topk_rows_f32(self, x, k, largest=True):
+        """Section 5 "Top-k": per row the k largest (or smallest) values in
+        totalOrder, in order, ties by index.  Returns (values rows x k, in-row idx)."""
+        x = _c(x, np.float32)
+        rows, length = x.shape
+        if not 0 <= k <= length:
+            raise ValueError("k must be in [0, len]")
+        vals = np.empty((rows, k), np.uint32)
+        idx = np.empty((rows, k), np.int32)
+        if self.lib.oracle_topk_rows_f32(_ptr(x.view(np.uint32)), _ptr(vals), _ptr(idx), rows,
+                                         length, k, int(bool(largest))) != 0:
+            raise MemoryError("oracle_topk_rows_f32: allocation failed")
+        return vals.view(np.float32), idx
 
     def topp_cutoff_f32(self, probs, p):
         """Section 5 "Top-p": per row, first index whose float64 running sum >= p."""

@@ -342,6 +342,25 @@ int oracle_sort_rows_f32(const uint32_t* keys, uint32_t* keys_out, int32_t* idx_
     return 0;
 }
 
+int oracle_topk_rows_f32(const uint32_t* x, uint32_t* values_out, int32_t* idx_out, int64_t rows,
+                         int64_t len, int64_t k, int largest) {
+    if (k < 0 || k > len) return -1;
+    if (len == 0 || k == 0) return 0;
+    uint32_t* sorted = (uint32_t*)malloc((size_t)len * sizeof(uint32_t));
+    int32_t* idx = (int32_t*)malloc((size_t)len * sizeof(int32_t));
+    int rc = (sorted && idx) ? 0 : -1;
+    for (int64_t r = 0; r < rows && rc == 0; ++r) {
+        rc = oracle_sort_f32(x + r * len, sorted, idx, len, largest != 0);
+        for (int64_t i = 0; i < k && rc == 0; ++i) {
+            values_out[r * k + i] = sorted[i];
+            idx_out[r * k + i] = idx[i];
+        }
+    }
+    free(sorted);
+    free(idx);
+    return rc;
+}
+
 /* First i in [0, limit] with s[i] > u (running sums in double), else limit. */
 static int64_t oracle_first_above(const float* w, int64_t limit, double u) {
     double acc = 0.0;

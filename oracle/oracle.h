@@ -89,6 +89,15 @@ int oracle_sort_f16(const uint16_t* keys, uint16_t* keys_out, int32_t* perm_out,
 int oracle_sort_rows_f32(const uint32_t* keys, uint32_t* keys_out, int32_t* idx_out, int64_t rows,
                          int64_t len, int descending);
 
+/* Section 5 "Top-k": per row, the k largest (largest != 0) or the k smallest
+ * values in IEEE 754 totalOrder, listed in that order (descending or
+ * ascending), equal values by increasing index: the first k entries of the
+ * row's stable sort in that direction.  values_out (bit copies) and idx_out
+ * (indices within the row) are rows x k.  0 <= k <= len.  Returns 0, or -1 on
+ * allocation failure. */
+int oracle_topk_rows_f32(const uint32_t* x, uint32_t* values_out, int32_t* idx_out, int64_t rows,
+                         int64_t len, int64_t k, int largest);
+
 /* Appendix "Weighted Sampling": inverse transform sampling from the scan of
  * the weights.  Per row, with S_i the inclusive running sum (in double) and
  * W = S_{len-1}: the first index with S_i > theta * W (len - 1 if rounding

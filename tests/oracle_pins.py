@@ -394,6 +394,71 @@ def check_topp_sample(o):
     assert cut.tolist() == [1] and tok.tolist() == [3], (tok, cut)
 
 
+# ---------------------------------------------------------------- top-k
+
+def _bits(hexes):
+    return np.array([int(h, 16) for h in hexes], np.uint32)
+
+
+def check_topk_golden(o):
+    """Section 5 "Top-k": hand-worked rows with ties, signed zeros, infinities
+    and NaNs of both signs, both directions, k = 0 and k = len."""
+    for c in _golden("topk.json")["cases"]:
+        x = _bits(c["x"]).view(np.float32).reshape(1, -1)
+        v, i = o.topk_rows_f32(x, c["k"], largest=c["largest"])
+        assert v.view(np.uint32).reshape(-1).tolist() == _bits(c["values"]).tolist(), c["why"]
+        assert i.reshape(-1).tolist() == c["idx"], c["why"]
+
+
+def _totalorder_key(bits):
+    """Unsigned key whose order is IEEE 754 totalOrder on binary32 patterns."""
+    b = bits.astype(np.uint64)
+    return np.where(b >> 31, (~b) & 0xFFFFFFFF, b | 0x80000000)
+
+
+def check_topk_bruteforce(o):
+    """The definition by counting, on tiny rows with many ties: element i is
+    kept iff fewer than k elements come before it in the stable order (larger
+    values, or equal values at lower indices); the kept ones are listed by
+    that rank."""
+    rng = np.random.default_rng(37)
+    for trial in range(40):
+        length = int(rng.integers(1, 12))
+        x = rng.integers(-3, 4, (2, length)).astype(np.float32)
+        x[x == 0] = rng.choice(np.array([0.0, -0.0], np.float32), int((x == 0).sum()))
+        k = int(rng.integers(0, length + 1))
+        for largest in (True, False):
+            v, idx = o.topk_rows_f32(x, k, largest=largest)
+            for r in range(2):
+                key = _totalorder_key(x[r].view(np.uint32))
+                if not largest:
+                    key = (~key) & 0xFFFFFFFF
+                rank = [sum(1 for j in range(length)
+                            if key[j] > key[i] or (key[j] == key[i] and j < i))
+                        for i in range(length)]
+                want = sorted((i for i in range(length) if rank[i] < k), key=lambda i: rank[i])
+                assert idx[r].tolist() == want, (trial, largest, r)
+                assert v[r].view(np.uint32).tolist() == x[r].view(np.uint32)[want].tolist()
+
+
+def check_topk_numpy(o):
+    """numpy's stable argsort of the totalOrder key (complemented for the
+    largest) gives the same indices; values are the row's bits at them."""
+    rng = np.random.default_rng(41)
+    x = rng.standard_normal((6, 3000)).astype(np.float32)
+    x[:, ::7] = np.round(x[:, ::7])  # ties
+    x[1, 5] = np.float32(np.nan)
+    x[2, 9] = -np.float32(np.inf)
+    for k in (1, 17, 3000):
+        for largest in (True, False):
+            v, idx = o.topk_rows_f32(x, k, largest=largest)
+            for r in range(6):
+                key = _totalorder_key(x[r].view(np.uint32)).astype(np.int64)
+                order = np.argsort(-key if largest else key, kind="stable")[:k]
+                assert np.array_equal(idx[r], order), (k, largest, r)
+                assert np.array_equal(v[r].view(np.uint32), x[r].view(np.uint32)[order])
+
+
 # ---------------------------------------------------------------- top-p
 
 def check_topp(o):

@@ -69,6 +69,12 @@ MUTANTS = {
     "topp_sample_whole_row_mass": ("for (int64_t i = 0; i <= k; ++i) ck += (double)s[i];",
                                    "for (int64_t i = 0; i < len; ++i) ck += (double)s[i];"),
     "topp_sample_sorted_position": ("        token_out[r] = idx[j];", "        token_out[r] = (int32_t)j;"),
+    "topk_direction_flipped": ("rc = oracle_sort_f32(x + r * len, sorted, idx, len, largest != 0);",
+                               "rc = oracle_sort_f32(x + r * len, sorted, idx, len, largest == 0);"),
+    "topk_wrong_row": ("rc = oracle_sort_f32(x + r * len, sorted, idx, len, largest != 0);",
+                       "rc = oracle_sort_f32(x + r * k, sorted, idx, len, largest != 0);"),
+    "topk_sorted_position": ("            idx_out[r * k + i] = idx[i];",
+                             "            idx_out[r * k + i] = (int32_t)i;"),
     "topp_strict_comparison": ("if (c >= pd) {", "if (c > pd) {"),
     "topp_default_len": ("int64_t k = len - 1;", "int64_t k = len;"),
     "topp_exclusive_sum": ("            c += (double)row[i];\n            if (c >= pd) {",
