@@ -71,6 +71,7 @@ int libscan_workspace_init(void* ws, size_t ws_bytes, void* stream);
 #define LIBSCAN_OP_SORT_ROWS 6  /* radix_sort_rows_f32 (rows, len) */
 #define LIBSCAN_OP_WEIGHTED_SAMPLE 7 /* weighted_sample_f32 (rows, len) */
 #define LIBSCAN_OP_TOPP_SAMPLE 8 /* topp_sample_f32 (rows, len) */
+#define LIBSCAN_OP_TOPK 9       /* topk_rows_f32 (rows, len, n = k) */
 
 /*
  * Workspace size in bytes that op needs for n elements (rows/len/bits are
@@ -255,13 +256,40 @@ int weighted_sample_f32(const float* w, const float* theta_dev, int32_t* out, in
  * token_out (device, rows int32) receives the token index of S[j] in the
  * original row; cutoff_out (nullable, device, rows int32) receives k.  Both
  * are -1 for len == 0.  theta_dev as in weighted_sample_f32; p must not be
- * NaN.  rows * len <= INT32_MAX, rows * ceil(len / 8192) <= 2^24.  The sorted
- * copies are kept in the workspace, which no input or output may overlap.
- * Workspace: LIBSCAN_OP_TOPP_SAMPLE with (rows, len) (about 16 bytes per
- * element). */
+ * NaN.  rows * len <= INT32_MAX, rows * ceil(len / 8192) <= 2^24.
+ * scratch: caller device memory, 16-byte aligned, of at least
+ * libscan_scratch_bytes(LIBSCAN_OP_TOPP_SAMPLE, rows, len, 0) bytes (16 per
+ * element: the sorted copies and the sort's ping-pong buffers).  Unlike the
+ * workspace it needs no initialisation and carries nothing between calls; it
+ * is clobbered and may not overlap any input, output or the workspace.
+ * Workspace: LIBSCAN_OP_TOPP_SAMPLE with (rows, len). */
 int topp_sample_f32(const float* probs, const float* theta_dev, float p, int32_t* token_out,
-                    int32_t* cutoff_out, int64_t rows, int64_t len, void* ws, size_t ws_bytes,
-                    void* stream);
+                    int32_t* cutoff_out, int64_t rows, int64_t len, void* scratch,
+                    size_t scratch_bytes, void* ws, size_t ws_bytes, void* stream);
+
+/* Top-k of every row (Section 5 "Top-k": selection, a partial quicksort, on
+ * stable splits).  x: rows x len fp32.  Per row, values_out receives the k
+ * largest values (largest != 0) or the k smallest, in IEEE 754 totalOrder
+ * (as radix_sort_f32: +NaN is the largest value, -NaN the smallest), listed
+ * in descending (ascending) order, equal values by increasing index: the
+ * first k entries of the row's stable sort in that direction, as bit
+ * copies; idx_out receives their indices within the row.  values_out and
+ * idx_out are rows x k.  0 <= k <= len (EINVAL otherwise); len <= INT32_MAX,
+ * rows * ceil(len / 4096) <= 2^24, rows * k <= INT32_MAX.  Four rounds of
+ * digit counts find the k-th key of each row, one stable split keeps the
+ * top k in index order, and a row sort of those k orders them.  scratch as
+ * in topp_sample_f32, of libscan_scratch_bytes(LIBSCAN_OP_TOPK, rows, len, k)
+ * bytes (16 per kept element).  No output may overlap an input or the other
+ * output.  Workspace: LIBSCAN_OP_TOPK with (n = k, rows, len). */
+int topk_rows_f32(const float* x, float* values_out, int32_t* idx_out, int64_t rows, int64_t len,
+                  int64_t k, int largest, void* scratch, size_t scratch_bytes, void* ws,
+                  size_t ws_bytes, void* stream);
+
+/* Scratch bytes (see topp_sample_f32) that op needs for rows x len (k: the
+ * top-k count, else ignored).  Writes *bytes and returns LIBSCAN_OK, or
+ * LIBSCAN_EINVAL for an op without scratch / negative size / NULL bytes,
+ * LIBSCAN_ERANGE beyond the op's limits.  Pure host function. */
+int libscan_scratch_bytes(int op, int64_t rows, int64_t len, int64_t k, size_t* bytes);
 
 #ifdef __cplusplus
 }

@@ -47,12 +47,15 @@ SIGNATURES = {
     "radix_sort_f16": (_int, [_p, _p, _p, _p, _p, _i64, _int, _p, _sz, _p]),
     "radix_sort_rows_f32": (_int, [_p, _p, _p, _p, _p, _i64, _i64, _int, _p, _sz, _p]),
     "weighted_sample_f32": (_int, [_p, _p, _p, _i64, _i64, _p, _sz, _p]),
-    "topp_sample_f32": (_int, [_p, _p, ctypes.c_float, _p, _p, _i64, _i64, _p, _sz, _p]),
+    "topp_sample_f32": (_int, [_p, _p, ctypes.c_float, _p, _p, _i64, _i64, _p, _sz, _p, _sz,
+                               _p]),
+    "libscan_scratch_bytes": (_int, [_int, _i64, _i64, _i64, ctypes.POINTER(_sz)]),
+    "topk_rows_f32": (_int, [_p, _p, _p, _i64, _i64, _i64, _int, _p, _sz, _p, _sz, _p]),
 }
 
 OK, EINVAL, ENOSPACE, EHIP, ERANGE = 0, -1, -2, -3, -4
 OP_SCAN, OP_SCAN_RSS, OP_SCAN_ROWS, OP_COMPACT, OP_RADIX_SORT = 1, 2, 3, 4, 5
-OP_SORT_ROWS, OP_WEIGHTED_SAMPLE, OP_TOPP_SAMPLE = 6, 7, 8
+OP_SORT_ROWS, OP_WEIGHTED_SAMPLE, OP_TOPP_SAMPLE, OP_TOPK = 6, 7, 8, 9
 
 _LIB = None
 
@@ -97,6 +100,15 @@ def call(name: str, *args):
     if st != OK:
         raise LibscanError(name, st, lib)
     return st
+
+
+def scratch_bytes(op: int, rows: int, length: int, k: int = 0) -> int:
+    lib = load()
+    out = _sz(0)
+    st = lib.libscan_scratch_bytes(op, rows, length, k, ctypes.byref(out))
+    if st != OK:
+        raise LibscanError("libscan_scratch_bytes", st, lib)
+    return out.value
 
 
 def workspace_bytes(op: int, n: int = 0, rows: int = 0, length: int = 0, bits: int = 0) -> int:

@@ -112,8 +112,8 @@ int radix_sort_typed(ls::KeyType type, size_t elem, const void* keys, void* keys
                 return LIBSCAN_EINVAL;
     const int w = check_ws(ws, ws_bytes, ls::radix_ws_bytes(n, 8));
     if (w != LIBSCAN_OK) return w;
-    return hip_status(ls::launch_radix_sort_typed(type, descending != 0, keys, keys_out, perm_out,
-                                                  keys_tmp, perm_tmp, 1, n, ws, ws_bytes,
+    return hip_status(ls::launch_radix_sort_typed(type, descending != 0, keys, keys_out, nullptr,
+                                                  perm_out, keys_tmp, perm_tmp, 1, n, ws, ws_bytes,
                                                   (hipStream_t)stream));
 }
 
@@ -131,6 +131,16 @@ int check_sample(const float* x, const float* theta, const int32_t* out, const i
         overlaps(out2, out2 ? rb : 0, x, xb) || overlaps(out2, out2 ? rb : 0, theta, rb) ||
         overlaps(out2, out2 ? rb : 0, out, rb))
         return LIBSCAN_EINVAL;
+    return LIBSCAN_OK;
+}
+
+// Top-k sizes: 0 <= k <= len, the row grid as scan_rows, the k kept per row
+// as a row sort.
+int check_topk(int64_t rows, int64_t len, int64_t k) {
+    if (rows < 0 || len < 0 || k < 0 || k > len) return LIBSCAN_EINVAL;
+    const int r = check_rows(rows, len);
+    if (r != LIBSCAN_OK) return r;
+    if (len > INT32_MAX || !ls::radix_rows_fit(rows, k)) return LIBSCAN_ERANGE;
     return LIBSCAN_OK;
 }
 
@@ -193,6 +203,12 @@ int libscan_workspace_bytes(int op, int64_t n, int64_t rows, int64_t len, int bi
             if (!ls::radix_rows_fit(rows, len)) return LIBSCAN_ERANGE;
             *bytes = ls::radix_rows_ws_bytes(rows, len);
             return LIBSCAN_OK;
+        case LIBSCAN_OP_TOPK: {
+            const int r = check_topk(rows, len, n);
+            if (r != LIBSCAN_OK) return r;
+            *bytes = ls::topk_ws_bytes(rows, len, n);
+            return LIBSCAN_OK;
+        }
         case LIBSCAN_OP_WEIGHTED_SAMPLE:
         case LIBSCAN_OP_TOPP_SAMPLE: {
             const int r = check_rows(rows, len);
@@ -391,8 +407,8 @@ int radix_sort_rows_f32(const float* keys, float* keys_out, int32_t* perm_out, f
     const int w = check_ws(ws, ws_bytes, ls::radix_rows_ws_bytes(rows, len));
     if (w != LIBSCAN_OK) return w;
     return hip_status(ls::launch_radix_sort_typed(ls::KeyType::F32, descending != 0, keys,
-                                                  keys_out, perm_out, keys_tmp, perm_tmp, rows,
-                                                  len, ws, ws_bytes, (hipStream_t)stream));
+                                                  keys_out, nullptr, perm_out, keys_tmp, perm_tmp,
+                                                  rows, len, ws, ws_bytes, (hipStream_t)stream));
 }
 
 int weighted_sample_f32(const float* w, const float* theta_dev, int32_t* out, int64_t rows,
@@ -406,23 +422,71 @@ int weighted_sample_f32(const float* w, const float* theta_dev, int32_t* out, in
 }
 
 int topp_sample_f32(const float* probs, const float* theta_dev, float p, int32_t* token_out,
-                    int32_t* cutoff_out, int64_t rows, int64_t len, void* ws, size_t ws_bytes,
-                    void* stream) {
+                    int32_t* cutoff_out, int64_t rows, int64_t len, void* scratch,
+                    size_t scratch_bytes, void* ws, size_t ws_bytes, void* stream) {
     if (p != p) return LIBSCAN_EINVAL;  // NaN
     const int c = check_sample(probs, theta_dev, token_out, cutoff_out, rows, len);
     if (c != LIBSCAN_OK) return c;
     if (!ls::radix_rows_fit(rows, len)) return LIBSCAN_ERANGE;
     if (rows == 0) return LIBSCAN_OK;
-    const size_t need = ls::topp_sample_ws_bytes(rows, len);
-    const int k = check_ws(ws, ws_bytes, need);
+    const size_t need = ls::topp_sample_scratch_bytes(rows, len);
+    if (len > 0) {
+        if (scratch_bytes < need) return LIBSCAN_ENOSPACE;
+        if (!scratch || ((uintptr_t)scratch % 16) != 0) return LIBSCAN_EINVAL;
+        const size_t xb = (size_t)rows * (size_t)len * 4, rb = (size_t)rows * 4;
+        if (overlaps(scratch, need, probs, xb) || overlaps(scratch, need, theta_dev, rb) ||
+            overlaps(scratch, need, token_out, rb) ||
+            overlaps(scratch, need, cutoff_out, cutoff_out ? rb : 0) ||
+            overlaps(scratch, need, ws, ws_bytes))
+            return LIBSCAN_EINVAL;
+    }
+    const int k = check_ws(ws, ws_bytes, ls::topp_sample_ws_bytes(rows, len));
     if (k != LIBSCAN_OK) return k;
-    // the sorted copies live in the workspace: no input or output may lie in it
-    const size_t xb = (size_t)rows * (size_t)len * 4, rb = (size_t)rows * 4;
-    if (overlaps(ws, need, probs, xb) || overlaps(ws, need, theta_dev, rb) ||
-        overlaps(ws, need, token_out, rb) || overlaps(ws, need, cutoff_out, cutoff_out ? rb : 0))
-        return LIBSCAN_EINVAL;
     return hip_status(ls::launch_topp_sample(probs, theta_dev, p, token_out, cutoff_out, rows, len,
-                                             ws, (hipStream_t)stream));
+                                             scratch, ws, (hipStream_t)stream));
+}
+
+int topk_rows_f32(const float* x, float* values_out, int32_t* idx_out, int64_t rows, int64_t len,
+                  int64_t k, int largest, void* scratch, size_t scratch_bytes, void* ws,
+                  size_t ws_bytes, void* stream) {
+    const int r = check_topk(rows, len, k);
+    if (r != LIBSCAN_OK) return r;
+    if (rows == 0 || k == 0) return LIBSCAN_OK;
+    if (!x || !values_out || !idx_out) return LIBSCAN_EINVAL;
+    const size_t xb = (size_t)rows * (size_t)len * 4, ob = (size_t)rows * (size_t)k * 4;
+    const size_t need = ls::topk_scratch_bytes(rows, k);
+    if (scratch_bytes < need) return LIBSCAN_ENOSPACE;
+    if (!scratch || ((uintptr_t)scratch % 16) != 0) return LIBSCAN_EINVAL;
+    if (overlaps(values_out, ob, x, xb) || overlaps(idx_out, ob, x, xb) ||
+        overlaps(values_out, ob, idx_out, ob) || overlaps(scratch, need, x, xb) ||
+        overlaps(scratch, need, values_out, ob) || overlaps(scratch, need, idx_out, ob) ||
+        overlaps(scratch, need, ws, ws_bytes))
+        return LIBSCAN_EINVAL;
+    const int w = check_ws(ws, ws_bytes, ls::topk_ws_bytes(rows, len, k));
+    if (w != LIBSCAN_OK) return w;
+    return hip_status(ls::launch_topk(x, values_out, idx_out, rows, len, k, largest != 0, scratch,
+                                      ws, (hipStream_t)stream));
+}
+
+int libscan_scratch_bytes(int op, int64_t rows, int64_t len, int64_t k, size_t* bytes) {
+    if (!bytes || rows < 0 || len < 0 || k < 0) return LIBSCAN_EINVAL;
+    switch (op) {
+        case LIBSCAN_OP_TOPP_SAMPLE: {
+            const int r = check_rows(rows, len);
+            if (r != LIBSCAN_OK) return r;
+            if (!ls::radix_rows_fit(rows, len)) return LIBSCAN_ERANGE;
+            *bytes = ls::topp_sample_scratch_bytes(rows, len);
+            return LIBSCAN_OK;
+        }
+        case LIBSCAN_OP_TOPK: {
+            const int r = check_topk(rows, len, k);
+            if (r != LIBSCAN_OK) return r;
+            *bytes = ls::topk_scratch_bytes(rows, k);
+            return LIBSCAN_OK;
+        }
+        default:
+            return LIBSCAN_EINVAL;
+    }
 }
 
 }  // extern "C"

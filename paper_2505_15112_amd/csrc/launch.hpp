@@ -37,8 +37,13 @@ hipError_t launch_scan_rows(Kind kind, bool exclusive, const void* x, void* y, i
 size_t topp_ws_bytes(int64_t rows, int64_t len);
 bool radix_rows_fit(int64_t rows, int64_t len);
 size_t topp_sample_ws_bytes(int64_t rows, int64_t len);
+size_t topp_sample_scratch_bytes(int64_t rows, int64_t len);
+size_t topk_ws_bytes(int64_t rows, int64_t len, int64_t k);
+size_t topk_scratch_bytes(int64_t rows, int64_t k);
+hipError_t launch_topk(const float* x, float* values, int32_t* indices, int64_t rows, int64_t len,
+                       int64_t k, bool largest, void* scratch, void* ws, hipStream_t stream);
 hipError_t launch_topp_sample(const float* probs, const float* theta, float p, int32_t* token,
-                              int32_t* cutoff, int64_t rows, int64_t len, void* ws,
+                              int32_t* cutoff, int64_t rows, int64_t len, void* scratch, void* ws,
                               hipStream_t stream);
 hipError_t launch_weighted_sample(const float* w, const float* theta, int32_t* out, int64_t rows,
                                   int64_t len, void* ws, hipStream_t stream);
@@ -65,9 +70,11 @@ hipError_t launch_split(const uint32_t* keys, const int32_t* idx_in, const uint8
 // decoded on the last).
 enum class KeyType { U32, I32, F32, F16 };
 // rows = 1: a 1-D sort of len keys; else every row of a rows x len matrix on
-// its own (perm_out: indices within the row).
+// its own (perm_out: indices within the row).  perm_in (nullable, needs
+// perm_out): the index carried by each key instead of its position.
 hipError_t launch_radix_sort_typed(KeyType type, bool descending, const void* keys,
-                                   void* keys_out, int32_t* perm_out, void* keys_tmp,
+                                   void* keys_out, const int32_t* perm_in, int32_t* perm_out,
+                                   void* keys_tmp,
                                    int32_t* perm_tmp, int64_t rows, int64_t len, void* ws,
                                    size_t ws_bytes, hipStream_t stream);
 size_t radix_rows_ws_bytes(int64_t rows, int64_t len);

@@ -638,7 +638,8 @@ size_t radix_rows_ws_bytes(int64_t rows, int64_t len) {
 }
 
 template <class K>
-static hipError_t radix8_sort(const K* keys, K* keys_out, int32_t* perm_out, K* keys_tmp,
+static hipError_t radix8_sort(const K* keys, K* keys_out, const int32_t* perm_in,
+                              int32_t* perm_out, K* keys_tmp,
                               int32_t* perm_tmp, int64_t rows, int64_t len, int passes,
                               KeyCode code, KeyDecode decode, void* ws, hipStream_t stream) {
     const uint32_t tpr = r8_tpr(len);
@@ -647,7 +648,7 @@ static hipError_t radix8_sort(const K* keys, K* keys_out, int32_t* perm_out, K* 
     const size_t toff = radix8_table_offset(rows, len);
     uint32_t* counts = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + toff);
     const K* src_k = keys;
-    const int32_t* src_p = nullptr;
+    const int32_t* src_p = perm_out ? perm_in : nullptr;
     for (int p = 0; p < passes; ++p) {
         K* dk = (p % 2 == 0) ? keys_tmp : keys_out;
         int32_t* dp = perm_out ? ((p % 2 == 0) ? perm_tmp : perm_out) : nullptr;
@@ -717,8 +718,8 @@ hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* 
             e = hipGetLastError();
             if (e != hipSuccess) return e;
         } else {
-            return radix8_sort<uint32_t>(keys, keys_out, perm_out, keys_tmp, perm_tmp, 1, n, 4,
-                                         kIdentityCode, kIdentityDecode, ws, stream);
+            return radix8_sort<uint32_t>(keys, keys_out, nullptr, perm_out, keys_tmp, perm_tmp, 1,
+                                         n, 4, kIdentityCode, kIdentityDecode, ws, stream);
         }
         src_k = dk;
         src_p = dp;
@@ -727,7 +728,8 @@ hipError_t launch_radix_sort(const uint32_t* keys, uint32_t* keys_out, int32_t* 
 }
 
 hipError_t launch_radix_sort_typed(KeyType type, bool descending, const void* keys,
-                                   void* keys_out, int32_t* perm_out, void* keys_tmp,
+                                   void* keys_out, const int32_t* perm_in, int32_t* perm_out,
+                                   void* keys_tmp,
                                    int32_t* perm_tmp, int64_t rows, int64_t len, void* ws,
                                    size_t ws_bytes, hipStream_t stream) {
     (void)ws_bytes;
@@ -759,10 +761,10 @@ hipError_t launch_radix_sort_typed(KeyType type, bool descending, const void* ke
         decode.pre = all;
     }
     if (wide)
-        return radix8_sort<uint32_t>((const uint32_t*)keys, (uint32_t*)keys_out, perm_out,
+        return radix8_sort<uint32_t>((const uint32_t*)keys, (uint32_t*)keys_out, perm_in, perm_out,
                                      (uint32_t*)keys_tmp, perm_tmp, rows, len, 4, code, decode, ws,
                                      stream);
-    return radix8_sort<uint16_t>((const uint16_t*)keys, (uint16_t*)keys_out, perm_out,
+    return radix8_sort<uint16_t>((const uint16_t*)keys, (uint16_t*)keys_out, perm_in, perm_out,
                                  (uint16_t*)keys_tmp, perm_tmp, rows, len, 2, code, decode, ws,
                                  stream);
 }

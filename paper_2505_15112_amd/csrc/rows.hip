@@ -16,28 +16,9 @@
 #include <limits.h>
 
 #include "launch.hpp"
-#include "tile.hpp"
+#include "rowtile.hpp"
 
 namespace ls {
-
-constexpr int kRVec = 4;
-constexpr int64_t kRowTile = 4096;  // rows up to this length: one wavefront per row
-
-// Long-row tile geometries (waves x chunks x 64 x 4): long rows take big
-// tiles (each tile costs one ticket, about 11 ns serialised on MI355X), rows
-// of a few tiles take smaller ones so that a row still spans several tiles.
-struct RGeomS { static constexpr int W = 4, J = 4; };   //  4096
-struct RGeomM { static constexpr int W = 4, J = 8; };   //  8192
-struct RGeomL { static constexpr int W = 8, J = 16; };  // 32768
-static inline int64_t row_tile(int64_t len) {
-    return len > 65536 ? 32768 : (len > 16384 ? 8192 : 4096);
-}
-static inline int64_t row_segments(int64_t len) { return (len + row_tile(len) - 1) / row_tile(len); }
-// The same tile for misaligned rows (element-wise loads need more registers
-// per element): twice the waves, half the chunks.
-template <class T, class G, bool VEC>
-using RowTile = Tile<T, T, kRVec, VEC ? G::J : G::J / 2, VEC ? G::W : G::W * 2>;
-static inline bool long_rows(int64_t len) { return len > kRowTile; }
 
 // Wavefront minimum with DPP (lanes outside the row / disabled read INT_MAX).
 template <int CTRL, int ROW_MASK>
@@ -119,29 +100,6 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_rows_lookback
 //    sum exceeds theta * C_k, reported through `idx` (the source index of
 //    each sorted position; null: j itself).
 enum class ToppMode { Cutoff, Weighted, Sample };
-
-// Top-p's workspace words (a published tile sum, a row's arrival count) carry
-// the top three bits 001.  Other ops leave status words with a non-zero state
-// in the top two bits, or counts with the top three bits clear, and cleared
-// words are 0, so nothing else can pass for a top-p word.
-constexpr uint64_t kToppTag = 1ull << 61;
-__device__ __forceinline__ bool topp_word(uint64_t w) { return (w >> 61) == 1; }
-
-// Count one arrival in the row's counter; returns the arrivals before it.  A
-// word that is not a top-p word (left by another op sharing the workspace)
-// counts as zero, hence compare-and-swap rather than a plain add.
-__device__ __forceinline__ uint32_t topp_arrive(uint64_t* counter) {
-    uint64_t old = __hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    while (true) {
-        const uint32_t before = topp_word(old) ? (uint32_t)old : 0u;
-        uint64_t expected = old;
-        if (__hip_atomic_compare_exchange_strong(counter, &expected, kToppTag | (before + 1u),
-                                                 __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_AGENT))
-            return before;
-        old = expected;
-    }
-}
 
 __device__ __forceinline__ float topp_sum(const uint64_t* w) {
     return Bits<float>::from((uint32_t)__hip_atomic_load(w, __ATOMIC_RELAXED,
@@ -282,14 +240,14 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp(
             // Relaxed only (a release/acquire pair at device scope would write
             // back and invalidate L2 in every workgroup): the sum word carries
             // its own "published" bit, and the last arrival waits for it.
-            __hip_atomic_store(&sums[blockIdx.x], kToppTag | Bits<float>::to(agg),
+            __hip_atomic_store(&sums[blockIdx.x], kRowTag | Bits<float>::to(agg),
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             // Arrive only once the store is acknowledged: an agent-scope
             // store is written through to the level every CU reads at agent
             // scope, so the last arrival can never find an older word (one a
             // different op left in the workspace) in place of this sum.
             __builtin_amdgcn_s_waitcnt(0);
-            s_last = topp_arrive(&arrivals[row]) == segs - 1;
+            s_last = row_arrive(&arrivals[row]) == segs - 1;
         }
     }
     __syncthreads();
@@ -308,10 +266,10 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp(
                 uint64_t word;
                 for (uint32_t spins = 0;; ++spins) {  // bounded: every tile has stored already
                     word = __hip_atomic_load(&rs[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    if (topp_word(word) || spins >= kSpinLimit) break;
+                    if (row_word(word) || spins >= kSpinLimit) break;
                     __builtin_amdgcn_s_sleep(1);
                 }
-                failed |= !topp_word(word);
+                failed |= !row_word(word);
             }
         }
         if (__ballot(failed) && lane == 0)
@@ -588,32 +546,33 @@ hipError_t launch_topp_draw_sorted(const float* sorted, const int32_t* idx, cons
 // The top-p sampler on unsorted rows (Section 5 "Top-p or Nucleus Sampling"):
 // a stable descending radix sort of each row, keeping source indices, then
 // the cutoff and the draw on the sorted row.  Workspace: the sort's and the
-// draw's common head, then four rows x len arrays (sorted keys, their source
-// indices, and the sort's two ping-pong buffers).
+// draw's common head.  Scratch (caller memory with no invariant, since it
+// ends up holding sort codes): four rows x len arrays -- sorted keys, their
+// source indices, and the sort's two ping-pong buffers.
 static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
-static size_t topp_sample_head(int64_t rows, int64_t len) {
-    const size_t a = radix_rows_ws_bytes(rows, len), b = topp_ws_bytes(rows, len);
-    return align256(a > b ? a : b);
-}
 size_t topp_sample_ws_bytes(int64_t rows, int64_t len) {
-    return topp_sample_head(rows, len) + 4 * align256((size_t)rows * (size_t)len * 4);
+    const size_t a = radix_rows_ws_bytes(rows, len), b = topp_ws_bytes(rows, len);
+    return a > b ? a : b;
+}
+size_t topp_sample_scratch_bytes(int64_t rows, int64_t len) {
+    return 4 * align256((size_t)rows * (size_t)len * 4);
 }
 hipError_t launch_topp_sample(const float* probs, const float* theta, float p, int32_t* token,
-                              int32_t* cutoff, int64_t rows, int64_t len, void* ws,
+                              int32_t* cutoff, int64_t rows, int64_t len, void* scratch, void* ws,
                               hipStream_t stream) {
     if (rows == 0) return hipSuccess;
     if (len == 0)
         return launch_topp_draw_sorted(probs, nullptr, theta, p, token, cutoff, rows, len, ws,
                                        stream);
-    const size_t head = topp_sample_head(rows, len);
     const size_t mb = align256((size_t)rows * (size_t)len * 4);
-    char* base = reinterpret_cast<char*>(ws) + head;
+    char* base = reinterpret_cast<char*>(scratch);
     float* sorted = reinterpret_cast<float*>(base);
     int32_t* perm = reinterpret_cast<int32_t*>(base + mb);
     float* keys_tmp = reinterpret_cast<float*>(base + 2 * mb);
     int32_t* perm_tmp = reinterpret_cast<int32_t*>(base + 3 * mb);
-    const hipError_t e = launch_radix_sort_typed(KeyType::F32, true, probs, sorted, perm, keys_tmp,
-                                                 perm_tmp, rows, len, ws, head, stream);
+    const hipError_t e =
+        launch_radix_sort_typed(KeyType::F32, true, probs, sorted, nullptr, perm, keys_tmp,
+                                perm_tmp, rows, len, ws, topp_sample_ws_bytes(rows, len), stream);
     if (e != hipSuccess) return e;
     return launch_topp_draw_sorted(sorted, perm, theta, p, token, cutoff, rows, len, ws, stream);
 }

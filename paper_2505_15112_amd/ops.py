@@ -336,7 +336,14 @@ def weighted_sample_f32(w, theta, out=None, ws=None):
     return tok
 
 
-def topp_sample_f32(probs, theta, p, with_cutoff=False, out=None, cutoff_out=None, ws=None):
+def scratch(op: int, device, rows: int, length: int, k: int = 0):
+    """Scratch device memory for op at these sizes (no initialisation needed)."""
+    nbytes = max(16, _lib.scratch_bytes(op, rows, length, k))
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def topp_sample_f32(probs, theta, p, with_cutoff=False, out=None, cutoff_out=None, ws=None,
+                    scratch_buf=None):
     """Top-p sampling on unsorted rows: per row, the token drawn with the
     uniform draw theta[row] from the smallest descending-sorted prefix whose
     mass reaches p.  Returns the int32 tokens, and the cutoffs (index in the
@@ -350,7 +357,30 @@ def topp_sample_f32(probs, theta, p, with_cutoff=False, out=None, cutoff_out=Non
     cut = _out(probs, cutoff_out, torch.int32, shape=(rows,)) if with_cutoff else None
     if ws is None:
         ws = workspace(_lib.OP_TOPP_SAMPLE, probs.device, rows=rows, length=length)
+    if scratch_buf is None:
+        scratch_buf = scratch(_lib.OP_TOPP_SAMPLE, probs.device, rows, length)
     with torch.cuda.device(probs.device):
         _lib.call("topp_sample_f32", _ptr(probs), _ptr(theta), float(p), _ptr(tok), _ptr(cut),
-                  rows, length, _ptr(ws), ws.numel(), _stream(probs.device))
+                  rows, length, _ptr(scratch_buf), scratch_buf.numel(), _ptr(ws), ws.numel(),
+                  _stream(probs.device))
     return (tok, cut) if with_cutoff else tok
+
+
+def topk_rows_f32(x, k, largest=True, values_out=None, idx_out=None, ws=None, scratch_buf=None):
+    """Per row of a 2-D float32 tensor, the k largest (or smallest) values in
+    IEEE 754 totalOrder, in order, equal values by index.  Returns (values,
+    int32 indices within the row), both rows x k."""
+    _check(x, torch.float32, "x", dims=(2,))
+    rows, length = x.shape
+    k = int(k)
+    vals = _out(x, values_out, torch.float32, shape=(rows, k))
+    idx = _out(x, idx_out, torch.int32, shape=(rows, k))
+    if ws is None:
+        ws = workspace(_lib.OP_TOPK, x.device, k, rows=rows, length=length)
+    if scratch_buf is None:
+        scratch_buf = scratch(_lib.OP_TOPK, x.device, rows, length, k)
+    with torch.cuda.device(x.device):
+        _lib.call("topk_rows_f32", _ptr(x), _ptr(vals), _ptr(idx), rows, length, k,
+                  int(bool(largest)), _ptr(scratch_buf), scratch_buf.numel(), _ptr(ws), ws.numel(),
+                  _stream(x.device))
+    return vals, idx

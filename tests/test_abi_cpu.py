@@ -246,20 +246,58 @@ def test_weighted_sample_validation(lib):
 def test_topp_sample_validation(lib):
     fn = lib.topp_sample_f32
     TH, TOK, CUT = P(0x2000000), P(0x3000000), P(0x3100000)
-    W2 = P(0x60000000)
-    assert fn(X, TH, float("nan"), TOK, CUT, 4, 10, W2, BIG, None) == _lib.EINVAL
-    assert fn(X, None, 0.9, TOK, CUT, 4, 10, W2, BIG, None) == _lib.EINVAL
-    assert fn(X, TH, 0.9, None, CUT, 4, 10, W2, BIG, None) == _lib.EINVAL
-    assert fn(X, TH, 0.9, TOK, TOK, 4, 10, W2, BIG, None) == _lib.EINVAL        # cutoff == token
-    assert fn(X, TH, 0.9, TOK, P(0x100004), 4, 10, W2, BIG, None) == _lib.EINVAL
-    # inputs or outputs inside the workspace (it holds the sorted copies)
-    assert fn(X, TH, 0.9, TOK, CUT, 4, 10, P(0x3000000 - 256), BIG, None) == _lib.EINVAL
-    assert fn(X, TH, 0.9, TOK, CUT, 4, 10, W2, 64, None) == _lib.ENOSPACE
-    assert fn(XB, TH, 0.9, TOK, CUT, 1 << 16, 1 << 15, W2, BIG, None) == _lib.ERANGE
-    assert fn(None, None, 0.9, None, None, 0, 10, None, 0, None) == _lib.OK
+    SC, W2 = P(0x40000000), P(0x60000000)
+    assert fn(X, TH, float("nan"), TOK, CUT, 4, 10, SC, BIG, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, None, 0.9, TOK, CUT, 4, 10, SC, BIG, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, TH, 0.9, None, CUT, 4, 10, SC, BIG, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, TH, 0.9, TOK, TOK, 4, 10, SC, BIG, W2, BIG, None) == _lib.EINVAL  # cutoff == token
+    assert fn(X, TH, 0.9, TOK, P(0x100004), 4, 10, SC, BIG, W2, BIG, None) == _lib.EINVAL
+    # scratch: required, aligned, large enough, and clear of inputs, outputs and the workspace
+    assert fn(X, TH, 0.9, TOK, CUT, 4, 10, None, BIG, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, TH, 0.9, TOK, CUT, 4, 10, P(0x40000004), BIG, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, TH, 0.9, TOK, CUT, 4, 10, SC, 64, W2, BIG, None) == _lib.ENOSPACE
+    assert fn(X, TH, 0.9, TOK, CUT, 4, 10, P(0x3000000 - 256), 1024, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, TH, 0.9, TOK, CUT, 4, 10, SC, 1 << 20, P(0x40000100), 1 << 20,
+              None) == _lib.EINVAL
+    assert fn(X, TH, 0.9, TOK, CUT, 4, 10, SC, BIG, W2, 64, None) == _lib.ENOSPACE
+    assert fn(XB, TH, 0.9, TOK, CUT, 1 << 16, 1 << 15, SC, BIG, W2, BIG, None) == _lib.ERANGE
+    assert fn(None, None, 0.9, None, None, 0, 10, None, 0, None, 0, None) == _lib.OK
     out = ctypes.c_size_t(0)
     assert lib.libscan_workspace_bytes(_lib.OP_TOPP_SAMPLE, 0, 64, 1 << 17, 0,
                                        ctypes.byref(out)) == _lib.OK
+    assert out.value >= 256 + 64 * 256 * 4 * ((1 << 17) // 8192)
+    assert lib.libscan_scratch_bytes(_lib.OP_TOPP_SAMPLE, 64, 1 << 17, 0,
+                                     ctypes.byref(out)) == _lib.OK
     assert out.value >= 16 * 64 * (1 << 17)
-    assert lib.libscan_workspace_bytes(_lib.OP_TOPP_SAMPLE, 0, 1 << 16, 1 << 15, 0,
-                                       ctypes.byref(out)) == _lib.ERANGE
+    assert lib.libscan_scratch_bytes(_lib.OP_TOPP_SAMPLE, 1 << 16, 1 << 15, 0,
+                                     ctypes.byref(out)) == _lib.ERANGE
+    assert lib.libscan_scratch_bytes(_lib.OP_SCAN, 4, 10, 0, ctypes.byref(out)) == _lib.EINVAL
+    assert lib.libscan_scratch_bytes(_lib.OP_TOPP_SAMPLE, 4, 10, 0, None) == _lib.EINVAL
+
+
+def test_topk_validation(lib):
+    fn = lib.topk_rows_f32
+    VO, IO, SC, W2 = P(0x2000000), P(0x3000000), P(0x40000000), P(0x60000000)
+    assert fn(X, VO, IO, -1, 10, 3, 1, SC, BIG, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, VO, IO, 4, 10, 11, 1, SC, BIG, W2, BIG, None) == _lib.EINVAL   # k > len
+    assert fn(X, VO, IO, 4, 10, -1, 1, SC, BIG, W2, BIG, None) == _lib.EINVAL
+    assert fn(None, VO, IO, 4, 10, 3, 1, SC, BIG, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, VO, None, 4, 10, 3, 1, SC, BIG, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, P(0x100010), IO, 4, 10, 3, 1, SC, BIG, W2, BIG, None) == _lib.EINVAL  # over x
+    assert fn(X, VO, P(0x2000008), 4, 10, 3, 1, SC, BIG, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, VO, IO, 4, 10, 3, 1, None, BIG, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, VO, IO, 4, 10, 3, 1, P(0x40000008), BIG, W2, BIG, None) == _lib.EINVAL
+    assert fn(X, VO, IO, 4, 10, 3, 1, SC, 16, W2, BIG, None) == _lib.ENOSPACE
+    assert fn(X, VO, IO, 4, 10, 3, 1, SC, 1 << 20, P(0x40000100), 1 << 20, None) == _lib.EINVAL
+    assert fn(X, VO, IO, 4, 10, 3, 1, SC, BIG, W2, 64, None) == _lib.ENOSPACE
+    assert fn(XB, VO, IO, 1, 1 << 31, 3, 1, SC, BIG, W2, BIG, None) == _lib.ERANGE
+    assert fn(XB, VO, IO, 1 << 16, 1 << 16, 1 << 15, 1, SC, BIG, W2, BIG, None) == _lib.ERANGE
+    assert fn(None, None, None, 0, 10, 3, 1, None, 0, None, 0, None) == _lib.OK
+    assert fn(None, None, None, 4, 10, 0, 1, None, 0, None, 0, None) == _lib.OK    # k = 0
+    out = ctypes.c_size_t(0)
+    assert lib.libscan_workspace_bytes(_lib.OP_TOPK, 4096, 128, 131072, 0,
+                                       ctypes.byref(out)) == _lib.OK
+    assert out.value >= 256 + 128 * 4 * (16 + 256 * 4)
+    assert lib.libscan_workspace_bytes(_lib.OP_TOPK, 11, 4, 10, 0, ctypes.byref(out)) == _lib.EINVAL
+    assert lib.libscan_scratch_bytes(_lib.OP_TOPK, 128, 131072, 4096, ctypes.byref(out)) == _lib.OK
+    assert out.value >= 16 * 128 * 4096

@@ -21,9 +21,9 @@ import pytest
 from paper_2505_15112_amd import build as B
 
 SOURCES = sorted(f for f in os.listdir(B.CSRC) if f.endswith(".hip"))
-TILE_KERNELS = ("k_scan_lookback", "k_rss_reduce", "k_rss_rescan", "k_rows_lookback",
-                "k_topp_sums", "k_topp_owner", "k_compact", "k_split", "k_radix4_count",
-                "k_radix4_scatter")
+TILE_KERNELS = ("k_scan_lookback", "k_rss_reduce", "k_rss_rescan", "k_rows_lookback", "k_topp",
+                "k_compact", "k_split", "k_radix4_count", "k_radix4_scatter", "k_radix8_count",
+                "k_radix8_scatter", "k_topk_hist", "k_topk_select")
 
 
 def kernel_resources(src, tmp_path):
