@@ -12,8 +12,8 @@ The same run measures every other operation of the library on its workload
 fp16->fp32 scan (n = 2^24), the latency-bound int32 scan (n = 2^16), mask
 compaction (n = 2^28), batched rows and the top-p cutoff (128 x 131072),
 the samplers on unsorted rows (top-p sampling, its descending row sort, and
-weighted sampling, 128 x 131072), stable split and the 1-, 4- and 8-bit
-radix sorts (n = 2^26).  Workloads
+weighted sampling, 128 x 131072), top-k of those rows (k = 64 and 4096),
+stable split and the 1-, 4- and 8-bit radix sorts (n = 2^26).  Workloads
 that fit in the 256 MB Infinity Cache are timed cold: rounds of (512 MiB
 overwrite, call) enqueued back to back, minus the overwrites alone.
 A sweep of the int32 scan over n = 2^20 .. 2^28 (and 2^k + 17) gives bandwidth
@@ -330,8 +330,9 @@ def main():
         tok = torch.empty(rows, dtype=torch.int32, device=dev)
         cut2 = torch.empty(rows, dtype=torch.int32, device=dev)
         ws_smp = ops.workspace(_lib.OP_TOPP_SAMPLE, dev, rows=rows, length=length)
-        a = (P(sprobs), P(theta), ctypes.c_float(0.9), P(tok), P(cut2), rows, length, P(ws_smp),
-             ws_smp.numel(), sp)
+        scr = ops.scratch(_lib.OP_TOPP_SAMPLE, dev, rows, length)
+        a = (P(sprobs), P(theta), ctypes.c_float(0.9), P(tok), P(cut2), rows, length, P(scr),
+             scr.numel(), P(ws_smp), ws_smp.numel(), sp)
         ms = T.flushed(lambda: check(lib.topp_sample_f32(*a), "topp sample"), K, Wm)
         # the descending sort with indices (4 passes: 12 + 16 x 3 + 4 bytes per key) and one
         # read of the sorted row
@@ -358,7 +359,26 @@ def main():
             "weights read once (rows*len*4), cache-flushed",
             {"draws_per_s": round(rows / (ms * 1e-3), 1)})
         outputs["samplers"] = (sp_host, th_host, tok, cut2, wtok)
-        del ko2, po2, kt2, pt2
+        # top-k of the same rows: four digit-count rounds and the split read the
+        # rows (5 x 4 bytes per element), then the k kept per row are sorted
+        topk_out = {}
+        for kq in (64, 4096):
+            wsk = ops.workspace(_lib.OP_TOPK, dev, kq, rows=rows, length=length)
+            sck = ops.scratch(_lib.OP_TOPK, dev, rows, length, kq)
+            tv = torch.empty(rows, kq, dtype=torch.float32, device=dev)
+            ti = torch.empty(rows, kq, dtype=torch.int32, device=dev)
+            a = (P(sprobs), P(tv), P(ti), rows, length, kq, 1, P(sck), sck.numel(), P(wsk),
+                 wsk.numel(), sp)
+            ms = T.flushed(lambda: check(lib.topk_rows_f32(*a), "topk"), K, Wm)
+            bb = rows * length * 20 + rows * kq * 64
+            opsd[f"topk_k{kq}_128x131072"] = entry(
+                "topk", ms, bb, memcpy_ms(bb, True),
+                "rows*len*(4 x 4 counting + 4 split) + rows*k*64 (sort of the kept), cache-flushed",
+                {"k": kq, "rows_per_s": round(rows / (ms * 1e-3), 1)})
+            topk_out[kq] = (tv, ti)
+            del wsk, sck
+        outputs["topk"] = topk_out
+        del ko2, po2, kt2, pt2, scr
 
         # config: radix sort, n = 2^26 uint32 keys (+ int32 permutation)
         log("radix")
@@ -503,6 +523,12 @@ def cpu_baseline_leg(x_host, y_dev, outputs, np, torch):
         res["weighted_sample_128x131072"] = {
             "draws_per_s": round(ph.shape[0] / t, 1), "s": round(t, 4),
             "exact_rows": int(np.sum(wtok.cpu().numpy() == rw)), "rows": int(ph.shape[0])}
+        for kq, (tv, ti) in outputs["topk"].items():
+            t, (rv, ri) = timed(lambda: oracle.topk_rows_f32(ph, kq), reps=1)
+            res[f"topk_k{kq}_128x131072"] = {
+                "rows_per_s": round(ph.shape[0] / t, 1), "s": round(t, 3),
+                "matches_gpu": bool(np.array_equal(ti.cpu().numpy(), ri) and np.array_equal(
+                    tv.cpu().numpy().view(np.uint32), rv.view(np.uint32)))}
         kh = outputs["radix_keys"]
         sample = kh[: 1 << 22]
         t, _ = timed(lambda: oracle.sort_u32(sample), reps=1)

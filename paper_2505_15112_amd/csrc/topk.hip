@@ -55,13 +55,17 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_hist(
     const uint32_t* x, int64_t len, uint32_t segs, uint32_t k, bool largest, uint32_t* hist,
     uint64_t* state, uint64_t* arrivals) {
     constexpr int kWaves = TileT::WAVES;
+    // Several histograms per wave (picked by lane), so that equal digits in
+    // one instruction collide at most 64 / kSub ways: the top digits of
+    // probability-like data take a handful of values.
+    constexpr int kSub = kWaves <= 8 ? 4 : 2;
     static_assert(TileT::kThreads >= kTopkDigits, "one thread per digit");
-    static_assert(TileT::J * TileT::V <= 64, "per-lane element count");
-    __shared__ uint32_t s_h[kWaves][kTopkDigits];
+    __shared__ uint32_t s_h[kWaves * kSub][kTopkDigits];
     __shared__ uint32_t s_part[kTopkDigits / kWave];
     __shared__ uint32_t s_last;
 
-    for (int i = threadIdx.x; i < kWaves * kTopkDigits; i += TileT::kThreads) (&s_h[0][0])[i] = 0;
+    for (int i = threadIdx.x; i < kWaves * kSub * kTopkDigits; i += TileT::kThreads)
+        (&s_h[0][0])[i] = 0;
     const uint32_t row32 = blockIdx.x / segs;
     const uint32_t seg = blockIdx.x - row32 * segs;
     const int64_t row = row32;
@@ -72,6 +76,7 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_hist(
     __syncthreads();  // histograms cleared
 
     const int w = threadIdx.x / kWave;
+    uint32_t* h = s_h[w * kSub + (lane_id() & (kSub - 1))];
     const int32_t valid = (int32_t)(len - base < TileT::kElems ? len - base : TileT::kElems);
     constexpr int kShift = 24 - 8 * R;
 #pragma unroll
@@ -81,14 +86,14 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_hist(
         for (int e = 0; e < TileT::V; ++e) {
             const uint32_t key = topk_key(v[j][e], largest);
             if (off + e < valid && topk_in_bucket<R>(key, prefix))
-                atomicAdd(&s_h[w][(key >> kShift) & 255u], 1u);
+                atomicAdd(&h[(key >> kShift) & 255u], 1u);
         }
     }
     __syncthreads();
     if (threadIdx.x < kTopkDigits) {
         uint32_t t = 0;
 #pragma unroll
-        for (int q = 0; q < kWaves; ++q) t += s_h[q][threadIdx.x];
+        for (int q = 0; q < kWaves * kSub; ++q) t += s_h[q][threadIdx.x];
         // agent scope: written through, so the row's last tile reads it
         __hip_atomic_store(&hist[((int64_t)row32 * segs + seg) * kTopkDigits + threadIdx.x], t,
                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -222,12 +227,56 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_select(
     }
 }
 
+// The kept elements in order, for k <= kTopkSortMax: one workgroup per row
+// sorts the row's k (key, index) pairs in LDS by a bitonic network on the
+// 64-bit composite key << 32 | ~index in descending order -- larger keys
+// first, equal keys by increasing index, so the order is the stable one and
+// unique -- padded with zeros (below every composite, whose low word is at
+// least 2^31) to a power of two.  Values are decoded from the keys.
+constexpr int kTopkSortMax = 8192;
+constexpr int kTopkSortThreads = 512;
+__global__ __launch_bounds__(kTopkSortThreads) void k_topk_sort(
+    const uint32_t* sel_vals, const int32_t* sel_idx, uint32_t* values, int32_t* indices,
+    uint32_t k, uint32_t npow, bool largest) {
+    __shared__ uint64_t s[kTopkSortMax];
+    const int64_t row = blockIdx.x;
+    const uint32_t* sv = sel_vals + row * k;
+    const int32_t* si = sel_idx + row * k;
+    for (uint32_t i = threadIdx.x; i < npow; i += kTopkSortThreads)
+        s[i] = i < k ? ((uint64_t)topk_key(sv[i], largest) << 32) | (uint32_t)~(uint32_t)si[i]
+                     : 0ull;
+    __syncthreads();
+    for (uint32_t size = 2; size <= npow; size <<= 1) {
+        for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
+            for (uint32_t t = threadIdx.x; t < npow / 2; t += kTopkSortThreads) {
+                const uint32_t i = 2 * t - (t & (stride - 1));  // lower end of pair t
+                const uint32_t j = i + stride;
+                const uint64_t a = s[i], b = s[j];
+                // blocks of `size` alternate direction; the last merge is descending
+                if ((a < b) == ((i & size) == 0)) {
+                    s[i] = b;
+                    s[j] = a;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    for (uint32_t i = threadIdx.x; i < k; i += kTopkSortThreads) {
+        const uint64_t c = s[i];
+        const uint32_t key = (uint32_t)(c >> 32);
+        const uint32_t code = largest ? key : ~key;
+        values[row * k + i] = code ^ ((code >> 31) ? 0x80000000u : 0xFFFFFFFFu);
+        indices[row * k + i] = (int32_t)~(uint32_t)c;
+    }
+}
+
 // ---------------------------------------------------------------- launch
 
 // Workspace: header | two look-back chains (rows x segments words each) |
 // digit counts (rows x segments x 256) | row states (2 words) | arrival
-// counters; the final sort reuses the front.  Scratch: the k kept values and
-// indices per row, and the sort's two ping-pong buffers.
+// counters; the final radix sort (k > kTopkSortMax) reuses the front.
+// Scratch: the k kept values and indices per row, and for the radix sort its
+// two ping-pong buffers.
 static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 struct TopkLayout {
     size_t hist, state, arrivals, end;
@@ -242,11 +291,12 @@ static TopkLayout topk_layout(int64_t rows, int64_t len) {
     return l;
 }
 size_t topk_ws_bytes(int64_t rows, int64_t len, int64_t k) {
-    const size_t a = topk_layout(rows, len).end, b = radix_rows_ws_bytes(rows, k);
+    const size_t a = topk_layout(rows, len).end;
+    const size_t b = k > kTopkSortMax ? radix_rows_ws_bytes(rows, k) : 0;
     return a > b ? a : b;
 }
 size_t topk_scratch_bytes(int64_t rows, int64_t k) {
-    return 4 * align256((size_t)rows * (size_t)k * 4);
+    return (k > kTopkSortMax ? 4 : 2) * align256((size_t)rows * (size_t)k * 4);
 }
 
 template <class G>
@@ -302,6 +352,15 @@ hipError_t launch_topk(const float* x, float* values, int32_t* indices, int64_t 
     else
         e = topk_select<RGeomS>(vec, xb, rows, len, k, largest, sel_vals, sel_idx, ws, stream);
     if (e != hipSuccess) return e;
+    if (k <= kTopkSortMax) {
+        uint32_t npow = 1;
+        while (npow < (uint32_t)k) npow <<= 1;
+        hipLaunchKernelGGL(k_topk_sort, dim3((uint32_t)rows), dim3(kTopkSortThreads), 0, stream,
+                           (const uint32_t*)sel_vals, (const int32_t*)sel_idx,
+                           reinterpret_cast<uint32_t*>(values), indices, (uint32_t)k, npow,
+                           largest);
+        return hipGetLastError();
+    }
     // the kept elements in order: a stable sort of each row's k values,
     // carrying their indices (ties keep index order, as the split left them)
     return launch_radix_sort_typed(KeyType::F32, largest, sel_vals, values, sel_idx, indices,

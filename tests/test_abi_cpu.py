@@ -300,4 +300,6 @@ def test_topk_validation(lib):
     assert out.value >= 256 + 128 * 4 * (16 + 256 * 4)
     assert lib.libscan_workspace_bytes(_lib.OP_TOPK, 11, 4, 10, 0, ctypes.byref(out)) == _lib.EINVAL
     assert lib.libscan_scratch_bytes(_lib.OP_TOPK, 128, 131072, 4096, ctypes.byref(out)) == _lib.OK
-    assert out.value >= 16 * 128 * 4096
+    assert out.value >= 8 * 128 * 4096            # the kept values and indices
+    assert lib.libscan_scratch_bytes(_lib.OP_TOPK, 4, 131072, 9000, ctypes.byref(out)) == _lib.OK
+    assert out.value >= 16 * 4 * 9000             # and the row sort's ping-pong buffers

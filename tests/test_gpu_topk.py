@@ -50,7 +50,8 @@ def _rows(rows, length, seed, kind):
 SHAPES = [(1, 1, [1]), (3, 5, [1, 2, 5]), (1000, 100, [1, 10, 100]), (4, 4096, [1, 64, 4096]),
           (3, 4097, [100, 4097]), (7, 10_001, [1, 1000]), (2, 3 * 8192 + 5, [5000]),
           (9, 65_536, [50, 4096]), (3, 65_537, [3]), (16, 131_072, [1, 4096]),
-          (3, 200_003, [2000]), (1, (1 << 20) + 3, [1, 70_000])]
+          (3, 200_003, [2000]), (4, 20_000, [8191, 8192, 8193]), (1, (1 << 20) + 3, [1, 70_000])]
+# k <= 8192: the kept elements are ordered by an LDS sort per row; above, by the row radix sort
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"{s[0]}x{s[1]}")
