@@ -64,13 +64,16 @@ __device__ __forceinline__ void load_vec(const In* p, T (&out)[V]) {
     for (int i = 0; i < V; ++i) out[i] = Conv<In, T>::f(e[i]);
 }
 
-// Aligned vector store of V 32-bit elements (V = 4: one 16-byte store).
+// Aligned vector store of V 32-bit elements (V/4 16-byte stores).
 template <class T, int V>
 __device__ __forceinline__ void store_vec(T* p, const T (&v)[V]) {
-    static_assert(sizeof(T) == 4 && V == 4, "16-byte stores of 32-bit elements");
-    u32x4 r;
-    __builtin_memcpy(&r, v, 16);
-    __builtin_nontemporal_store(r, reinterpret_cast<u32x4*>(p));
+    static_assert(sizeof(T) == 4 && V % 4 == 0, "16-byte stores of 32-bit elements");
+#pragma unroll
+    for (int q = 0; q < V / 4; ++q) {
+        u32x4 r;
+        __builtin_memcpy(&r, v + 4 * q, 16);
+        __builtin_nontemporal_store(r, reinterpret_cast<u32x4*>(p) + q);
+    }
 }
 
 // ---------------------------------------------------------------- the tile

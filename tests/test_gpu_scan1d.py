@@ -189,6 +189,49 @@ def test_large_tiles_ragged(ops, kind, excl, shift):
         assert int(to_host(total)[0]) == rtot
 
 
+# Register + LDS tiles (n >= 2^27, 16-byte aligned 32-bit data): 59392-element
+# integer tiles and 51200-element float tiles.  Sizes: ragged last tile of
+# either kind, an exact multiple of each tile (the last full tile writes the
+# total), and a last tile holding one element.
+LDS_I32_TILE, LDS_F32_TILE = 59392, 51200
+LDS_SIZES = [1 << 27, LDS_I32_TILE * 2260, LDS_I32_TILE * 2260 + 1, LDS_F32_TILE * 2622,
+             LDS_F32_TILE * 2622 + 1]
+
+
+@pytest.mark.skipif(not FULL, reason="full-size cases disabled")
+@pytest.mark.parametrize("n", LDS_SIZES)
+@pytest.mark.parametrize("excl", [False, True])
+def test_lds_tiles_i32(ops, n, excl):
+    """int32 through the large-array kernel, with carry_in and total_out."""
+    import torch
+    announce("lds tiles i32", n, excl)
+    x = W.scan_i32_full_range(n, seed=31)
+    carry = torch.tensor([-123456789], dtype=torch.int32, device="cuda")
+    fn = ops.scan_exclusive_i32_carry if excl else ops.scan_inclusive_i32_carry
+    y, _ = fn(to_dev(x), carry_in=carry, total_out=carry)
+    ref = (oracle.scan_i32(x, exclusive=excl).astype(np.int64) - 123456789).astype(np.int32)
+    assert_equal_first_diff(to_host(y), ref, f"lds i32 n={n}")
+    tot = (int(oracle.scan_i32(x)[-1]) - 123456789 + 2**31) % 2**32 - 2**31
+    assert int(to_host(carry)[0]) == tot
+
+
+@pytest.mark.skipif(not FULL, reason="full-size cases disabled")
+@pytest.mark.parametrize("n", LDS_SIZES)
+@pytest.mark.parametrize("excl", [False, True])
+def test_lds_tiles_f32(ops, n, excl):
+    """fp32 through the large-array kernel: bit-exact on {-1, 0, 1} inputs
+    with an exact carry_in, and the total."""
+    import torch
+    announce("lds tiles f32", n, excl)
+    x = W.exact_pm1(n, seed=32)
+    cf = torch.tensor([0.5], dtype=torch.float32, device="cuda")
+    fn = ops.scan_exclusive_f32_carry if excl else ops.scan_inclusive_f32_carry
+    y, _ = fn(to_dev(x), carry_in=cf, total_out=cf)
+    ref, _ = oracle.scan_f32(x, exclusive=excl)
+    assert_equal_first_diff(to_host(y).astype(np.float64), ref + 0.5, f"lds f32 n={n}")
+    assert float(to_host(cf)[0]) == float(np.sum(x.astype(np.float64))) + 0.5
+
+
 def test_repeat_no_race(ops):
     """The same input 100 times: the look-back must give one result every time."""
     import torch
