@@ -262,8 +262,25 @@ def main():
         b2 = n2 * 6
         ms = T.flushed(scan_call("scan_inclusive_f16f32", x16, y16, n2), K, Wm)
         opsd["scan_f16f32_n2^24"] = entry("f16", ms, b2, memcpy_ms(b2, True),
-                                          "n*(2+4), cache-flushed")
+                                          "n*(2+4), cache-flushed; matrix-core tile scan")
         outputs["f16"] = (x16_host, y16)
+        # the same scan on the wavefront tiles only (the default above runs
+        # its whole 32768-element tiles on the matrix cores), cold at 2^24,
+        # and both back to back at 2^28
+        y16w = torch.empty_like(y16)
+        ms = T.flushed(scan_call("scan_inclusive_f16f32_wave", x16, y16w, n2), K, Wm)
+        opsd["scan_f16f32_wave_n2^24"] = entry("f16 wave", ms, b2, memcpy_ms(b2, True),
+                                               "n*(2+4), cache-flushed; wavefront tiles only")
+        outputs["f16_wave"] = (x16_host, y16w)
+        x16b = torch.from_numpy(W.scan_f16(n, seed=3)).to(dev)
+        y16b = torch.empty(n, dtype=torch.float32, device=dev)
+        b28 = n * 6
+        mc28 = memcpy_ms(b28)
+        for nm in ("scan_inclusive_f16f32", "scan_inclusive_f16f32_wave"):
+            ms = T.back_to_back(scan_call(nm, x16b, y16b, n), K, Wm)
+            key = "scan_f16f32" + ("_wave" if nm.endswith("wave") else "") + "_n2^28"
+            opsd[key] = entry("f16 2^28", ms, b28, mc28, "n*(2+4)")
+        del x16b, y16b
 
         # config: int32, n = 2^16 (latency-bound)
         n1 = 1 << 16
@@ -484,6 +501,9 @@ def cpu_baseline_leg(x_host, y_dev, outputs, np, torch):
         ok = bool(np.all(np.abs(y.cpu().numpy() - r) <= 1e-5 * a + 1e-6))
         res["scan_f16f32_n2^24"] = {"gbps": round(xh.size * 6 / t / 1e9, 3), "s": round(t, 4),
                                     "matches_gpu": ok}
+        xh, y = outputs["f16_wave"]
+        res["scan_f16f32_wave_n2^24"] = {
+            "matches_gpu": bool(np.all(np.abs(y.cpu().numpy() - r) <= 1e-5 * a + 1e-6))}
         xh, y = outputs["c1"]
         t, r = timed(lambda: oracle.scan_i32(xh))
         res["scan_i32_n2^16"] = {"us": round(t * 1e6, 1),

@@ -99,11 +99,35 @@ int scan_exclusive_f32(const float* x, float* y, int64_t n, void* ws, size_t ws_
 
 /* fp16 input (IEEE binary16 bit patterns), fp32 accumulation and output
  * (Section 3.1: the cube takes fp16 in and gives fp32 out; Section 6 scans
- * fp16).  x and y may not overlap. */
+ * fp16).  x and y may not overlap.  The inclusive scan of a 16-byte aligned
+ * x with n >= 32768 takes its tile-local scans on the matrix cores (see
+ * scan_inclusive_f16f32_mfma), otherwise the wavefront tiles. */
 int scan_inclusive_f16f32(const uint16_t* x, float* y, int64_t n, void* ws, size_t ws_bytes,
                           void* stream);
 int scan_exclusive_f16f32(const uint16_t* x, float* y, int64_t n, void* ws, size_t ws_bytes,
                           void* stream);
+
+/* The same inclusive fp16 -> fp32 scan with the tile-local scan on the
+ * matrix cores, as ScanU does it (Section 4.1, Algorithm 1): every block of
+ * 32 x 32 elements, viewed as a row-major matrix A, gives its row scans as
+ * A * U_32 (U_32 upper triangular ones) on v_mfma_f32_32x32x16_f16; rows,
+ * blocks and tiles are then chained as in scan_inclusive_f16f32.  Same
+ * arguments, workspace (LIBSCAN_OP_SCAN) and error behaviour, except that x
+ * must be 16-byte aligned (one matrix operand is one 16-byte load per lane)
+ * and y 4-byte aligned, else LIBSCAN_EINVAL; x and y may not overlap.  Whole
+ * 32768-element tiles take the matrix-core kernel, a shorter tail the
+ * wavefront one.  Results agree with the wavefront scan within the float
+ * tolerance (exactly on {-1, 0, 1} inputs); measured faster than it, which
+ * is why scan_inclusive_f16f32 uses this path when it can. */
+int scan_inclusive_f16f32_mfma(const uint16_t* x, float* y, int64_t n, void* ws,
+                               size_t ws_bytes, void* stream);
+
+/* The inclusive fp16 -> fp32 scan on the wavefront tiles only (lane-serial,
+ * DPP and LDS tile scan), whatever n and the alignment: the baseline the
+ * matrix-core path is measured against.  Arguments and errors as
+ * scan_inclusive_f16f32. */
+int scan_inclusive_f16f32_wave(const uint16_t* x, float* y, int64_t n, void* ws,
+                               size_t ws_bytes, void* stream);
 
 /* 8-bit input summed as unsigned byte values into int32 (Appendix
  * "Exclusive and int8 scan": int8 input, int32 accumulation; used on masks).

@@ -251,6 +251,32 @@ int scan_exclusive_f16f32(const uint16_t* x, float* y, int64_t n, void* ws, size
                           void* stream) {
     return scan1d(Kind::F16F32, true, x, y, n, nullptr, nullptr, ws, ws_bytes, stream);
 }
+
+int scan_inclusive_f16f32_wave(const uint16_t* x, float* y, int64_t n, void* ws, size_t ws_bytes,
+                               void* stream) {
+    if (n < 0) return LIBSCAN_EINVAL;
+    if (n > ls::kMaxScanElems) return LIBSCAN_ERANGE;
+    if (n > 0 && (!x || !y)) return LIBSCAN_EINVAL;
+    if (bad_alias(x, (size_t)n * 2, y, (size_t)n * 4, false)) return LIBSCAN_EINVAL;
+    if (n == 0) return LIBSCAN_OK;
+    const int w = check_ws(ws, ws_bytes, ls::scan1d_ws_bytes(n));
+    if (w != LIBSCAN_OK) return w;
+    return hip_status(ls::launch_scan1d_tiles(Kind::F16F32, false, x, y, n, nullptr, nullptr, ws,
+                                              ws_bytes, (hipStream_t)stream));
+}
+
+int scan_inclusive_f16f32_mfma(const uint16_t* x, float* y, int64_t n, void* ws, size_t ws_bytes,
+                               void* stream) {
+    if (n < 0) return LIBSCAN_EINVAL;
+    if (n > ls::kMaxScanElems) return LIBSCAN_ERANGE;
+    if (n > 0 && (!x || !y)) return LIBSCAN_EINVAL;
+    if (bad_alias(x, (size_t)n * 2, y, (size_t)n * 4, false)) return LIBSCAN_EINVAL;
+    if (n == 0) return LIBSCAN_OK;
+    if (((uintptr_t)x % 16) != 0 || ((uintptr_t)y % 4) != 0) return LIBSCAN_EINVAL;
+    const int w = check_ws(ws, ws_bytes, ls::scan1d_ws_bytes(n));
+    if (w != LIBSCAN_OK) return w;
+    return hip_status(ls::launch_scan1d_mfma_f16(x, y, n, ws, ws_bytes, (hipStream_t)stream));
+}
 int scan_exclusive_u8i32(const uint8_t* x, int32_t* y, int64_t n, int32_t* total_dev, void* ws,
                          size_t ws_bytes, void* stream) {
     return scan1d(Kind::U8I32, true, x, y, n, nullptr, total_dev, ws, ws_bytes, stream);

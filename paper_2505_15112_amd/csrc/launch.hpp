@@ -19,11 +19,23 @@ constexpr int64_t kMaxScanElems = int64_t(1) << 35;
 // Zero-fill a workspace (its first use; see WsHeader in device.hpp).
 hipError_t launch_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream);
 
-// 1-D decoupled look-back scan.
+// 1-D decoupled look-back scan: launch_scan1d picks the kernel (the
+// matrix-core one for inclusive fp16 scans of at least one whole tile),
+// launch_scan1d_tiles always the wavefront tiles.
 size_t scan1d_ws_bytes(int64_t n);
 hipError_t launch_scan1d(Kind kind, bool exclusive, const void* x, void* y, int64_t n,
                          const void* carry_in, void* total_out, void* ws, size_t ws_bytes,
                          hipStream_t stream);
+hipError_t launch_scan1d_tiles(Kind kind, bool exclusive, const void* x, void* y, int64_t n,
+                               const void* carry_in, void* total_out, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
+
+// 1-D inclusive scan of fp16 with the tile-local row scans on the matrix
+// cores (ScanU) on whole tiles of kMfmaTileElems, the tail on the wavefront
+// tiles; same workspace as launch_scan1d.  x 16-byte aligned.
+constexpr int64_t kMfmaTileElems = 32768;
+hipError_t launch_scan1d_mfma_f16(const uint16_t* x, float* y, int64_t n, void* ws,
+                                  size_t ws_bytes, hipStream_t stream);
 
 // 1-D reduce-then-scan (three kernels).
 size_t scan1d_rss_ws_bytes(int64_t n);

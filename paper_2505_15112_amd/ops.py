@@ -93,6 +93,16 @@ def scan_exclusive_f16f32(x, out=None, ws=None):
     return _scan1d("scan_exclusive_f16f32", x, torch.float16, torch.float32, out, ws)
 
 
+def scan_inclusive_f16f32_mfma(x, out=None, ws=None):
+    """Inclusive fp16 -> fp32 scan with the row scans on the matrix cores."""
+    return _scan1d("scan_inclusive_f16f32_mfma", x, torch.float16, torch.float32, out, ws)
+
+
+def scan_inclusive_f16f32_wave(x, out=None, ws=None):
+    """Inclusive fp16 -> fp32 scan on the wavefront tiles only."""
+    return _scan1d("scan_inclusive_f16f32_wave", x, torch.float16, torch.float32, out, ws)
+
+
 def scan_exclusive_u8i32(x, out=None, total=None, ws=None):
     """Returns (y, total) -- total is a 1-element int32 device tensor."""
     if total is None:

@@ -60,7 +60,8 @@ def test_workspace_bytes(lib):
 
 
 SCANS = ["scan_inclusive_i32", "scan_exclusive_i32", "scan_inclusive_f32", "scan_exclusive_f32",
-         "scan_inclusive_f16f32", "scan_exclusive_f16f32", "scan_inclusive_rss_i32",
+         "scan_inclusive_f16f32", "scan_exclusive_f16f32", "scan_inclusive_f16f32_mfma",
+         "scan_inclusive_f16f32_wave", "scan_inclusive_rss_i32",
          "scan_inclusive_rss_f32"]
 
 
@@ -81,6 +82,10 @@ def test_scan_validation(lib, name):
 def test_mixed_type_scans_reject_any_overlap(lib):
     # fp16 in / fp32 out may not alias at all, not even exactly
     assert lib.scan_inclusive_f16f32(X, X, 100, WS, BIG, None) == _lib.EINVAL
+    assert lib.scan_inclusive_f16f32_mfma(X, X, 100, WS, BIG, None) == _lib.EINVAL
+    assert lib.scan_inclusive_f16f32_wave(X, X, 100, WS, BIG, None) == _lib.EINVAL
+    # the matrix-core scan needs a 16-byte aligned input
+    assert lib.scan_inclusive_f16f32_mfma(P(0x100002), Y, 100, WS, BIG, None) == _lib.EINVAL
     assert lib.scan_exclusive_u8i32(X, X, 100, None, WS, BIG, None) == _lib.EINVAL
 
 

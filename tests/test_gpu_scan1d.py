@@ -232,6 +232,60 @@ def test_lds_tiles_f32(ops, n, excl):
     assert float(to_host(cf)[0]) == float(np.sum(x.astype(np.float64))) + 0.5
 
 
+# The matrix-core tile scan (row scans as A * U_32 on MFMA, ScanU): whole
+# 32768-element tiles there, the tail on the wavefront kernel.
+MFMA_SIZES = [1, 1023, 1024, 32767, 32768, 32769, 3 * 32768 + 12345, (1 << 22) + 5, 1 << 24]
+
+
+@pytest.mark.parametrize("n", MFMA_SIZES)
+def test_wave_f16f32(ops, n):
+    """The wavefront-only entry point (the matrix-core path's baseline)."""
+    announce("wave f16f32", n)
+    x = W.scan_f16(n, seed=n + 5)
+    y = to_host(ops.scan_inclusive_f16f32_wave(to_dev(x)))
+    ref, a = oracle.scan_f16(x)
+    assert_float_close(y, ref, a, f"wave f16 n={n}")
+
+
+@pytest.mark.parametrize("n", MFMA_SIZES)
+def test_mfma_f16f32(ops, n):
+    announce("mfma f16f32", n)
+    x = W.scan_f16(n, seed=n + 3)
+    y = to_host(ops.scan_inclusive_f16f32_mfma(to_dev(x)))
+    ref, a = oracle.scan_f16(x)
+    assert_float_close(y, ref, a, f"mfma f16 n={n}")
+    xe = W.exact_pm1(n, seed=n + 4, dtype=np.float16)
+    ye = to_host(ops.scan_inclusive_f16f32_mfma(to_dev(xe)))
+    assert_equal_first_diff(ye.astype(np.float64), oracle.scan_f16(xe)[0], f"mfma exact n={n}")
+
+
+def test_mfma_matches_wavefront_and_repeats(ops):
+    """Exact inputs: the matrix-core and wavefront scans agree bit for bit,
+    call after call on one workspace (the default path is the matrix-core one)."""
+    import torch
+    announce("mfma repeat")
+    n = 64 * 32768 + 777
+    xe = to_dev(W.exact_pm1(n, seed=41, dtype=np.float16))
+    ws = ops.workspace(1, xe.device, n)
+    ref = ops.scan_inclusive_f16f32_wave(xe, ws=ws)
+    assert_equal_first_diff(to_host(ref).astype(np.float64),
+                            oracle.scan_f16(to_host(xe))[0], "wave exact")
+    assert torch.equal(ops.scan_inclusive_f16f32(xe, ws=ws), ref)
+    y = torch.empty_like(ref)
+    bad = 0
+    for _ in range(20):
+        ops.scan_inclusive_f16f32_mfma(xe, out=y, ws=ws)
+        bad += int((y != ref).sum().item())
+    assert bad == 0
+
+
+def test_mfma_rejects_misaligned(ops):
+    announce("mfma misaligned")
+    x = to_dev(W.scan_f16(1001, seed=5))
+    with pytest.raises(Exception):
+        ops.scan_inclusive_f16f32_mfma(x[1:])
+
+
 def test_repeat_no_race(ops):
     """The same input 100 times: the look-back must give one result every time."""
     import torch
