@@ -329,6 +329,114 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp(
         __hip_atomic_store(&arrivals[row], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// ---------------------------------------------------------------- top-p, early exit
+//
+// The cutoff for rows of a few long tiles, reading no more of a row than it
+// needs.  Tiles are taken by ticket in column-major order (tile t of every
+// row before tile t + 1 of any), and tile t of a row first waits for tile
+// t - 1's word in the row's state: the running sum of the tiles before it,
+// or "found".  A tile of a row already found exits without reading its
+// data; otherwise it reads its part, and if the running sum reaches p inside
+// it (or it is the row's last tile) it finds the index in its own registers
+// (no re-read) and marks the row found.  On sorted probabilities the
+// crossing comes early, so most of a row is never read; on any input the
+// result is the cutoff definition's.  A tile only waits for the tile with
+// the previous ticket of its row, which is running or done.
+// State word: [001 | found : 1 | tiles published : 28 | running sum : fp32].
+constexpr uint64_t kFoundBit = 1ull << 60;
+
+template <class TileT, bool VEC>
+__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp_early(
+    const float* probs, int32_t* cutoff, uint32_t rows, int64_t len, uint32_t segs,
+    uint32_t ntiles, float p, WsHeader* hdr, uint64_t* state, uint64_t* arrivals,
+    int64_t ws_words) {
+    __shared__ Ticket s_ticket;
+    __shared__ uint64_t s_state;
+    __shared__ float s_wtot[TileT::WAVES];
+    __shared__ int32_t s_min[TileT::WAVES];
+
+    if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
+    __syncthreads();
+    const uint32_t tile32 = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.tile);
+    const uint32_t epoch = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.epoch);
+    if (tile32 >= ntiles) {  // only with a workspace that was never zero-filled
+        if (threadIdx.x == 0)
+            __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
+    const uint32_t seg = tile32 / rows;
+    const uint32_t row32 = tile32 - seg * rows;
+    const int64_t row = row32;
+
+    if (threadIdx.x == 0) {
+        uint64_t w = kRowTag;  // tile 0: nothing before it
+        if (seg > 0) {
+            for (uint32_t spins = 0;; ++spins) {  // bounded: tile seg - 1 is running or done
+                w = __hip_atomic_load(&state[row], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (row_word(w) && ((w & kFoundBit) || ((uint32_t)(w >> 32) & 0x0FFFFFFFu) >= seg))
+                    break;
+                if (spins >= kSpinLimit) {
+                    __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    w = kRowTag | kFoundBit;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+        }
+        s_state = w;
+    }
+    __syncthreads();
+    const uint64_t st = s_state;
+    if (!(st & kFoundBit)) {  // uniform
+        const float excl = Bits<float>::from((uint32_t)st);
+        const int64_t base = (int64_t)seg * TileT::kElems;
+        const float* xr = probs + row * len;
+        float v[TileT::J][TileT::V];
+        TileT::template load<VEC>(xr, len, base, v);
+        float wofs;
+        const float agg = TileT::combine_waves(TileT::template wave_scan<false>(v), s_wtot, &wofs);
+        const float incl = excl + agg;
+        const bool last = seg == segs - 1;
+        uint64_t out = kRowTag | ((uint64_t)(seg + 1) << 32) | Bits<float>::to(incl);
+        if (incl >= p || last) {
+            // the first index of this tile whose running sum reaches p; none
+            // (rounding, or the row never reaches p): the tile's last index
+            const float c = excl + wofs;
+            const int64_t lastidx = (base + TileT::kElems < len ? base + TileT::kElems : len) - 1;
+            const int32_t cap = (int32_t)(lastidx - base);
+            int32_t cand = INT_MAX;
+#pragma unroll
+            for (int j = TileT::J - 1; j >= 0; --j) {
+                const int32_t off = (int32_t)TileT::lane_offset(j);
+#pragma unroll
+                for (int e = TileT::V - 1; e >= 0; --e)
+                    if (off + e <= cap && c + v[j][e] >= p) cand = off + e;
+            }
+            const int32_t wm = wave_min(cand);
+            if (lane_id() == 0) s_min[threadIdx.x / kWave] = wm;
+            __syncthreads();
+            int32_t m = INT_MAX;
+            for (int k = 0; k < TileT::WAVES; ++k) m = s_min[k] < m ? s_min[k] : m;
+            if (threadIdx.x == 0) cutoff[row] = (int32_t)(base + (m != INT_MAX ? m : cap));
+            out |= kFoundBit;
+        }
+        if (threadIdx.x == 0) {
+            __hip_atomic_store(&state[row], out, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            // arrive only once the word is acknowledged, so that the row's
+            // reset below can never be overtaken by it
+            __builtin_amdgcn_s_waitcnt(0);
+        }
+    }
+    if (threadIdx.x == 0) {
+        // the row's last tile to arrive leaves its words clear for the next call
+        if (row_arrive(&arrivals[row]) == segs - 1) {
+            __hip_atomic_store(&state[row], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&arrivals[row], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        finish_epoch(hdr, epoch, ntiles, state, ws_words);
+    }
+}
+
 __global__ void k_fill_i32(int32_t* p, int64_t count, int32_t value) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) p[i] = value;
@@ -446,10 +554,37 @@ static void topp_long(bool vec, const float* probs, const int32_t* idx, const fl
                        len, segs, p, reinterpret_cast<WsHeader*>(ws), sums, arrivals);
 }
 
+// Rows of 2 to 8 long tiles take the early-exit cutoff kernel.
+static bool topp_early(int64_t len) {
+    return row_tile(len) == 32768 && row_segments(len) <= 8;
+}
+
+static void topp_cutoff_early(bool vec, const float* probs, int32_t* cutoff, int64_t rows,
+                              int64_t len, float p, void* ws, hipStream_t stream) {
+    using TV = RowTile<float, RGeomL, true>;
+    using TU = RowTile<float, RGeomL, false>;
+    const uint32_t segs = (uint32_t)((len + TV::kElems - 1) / TV::kElems);
+    const uint32_t nt = (uint32_t)(rows * segs);
+    uint64_t* state = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
+    uint64_t* arrivals = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) +
+                                                     topp_arrivals_offset(rows, len));
+    // words after the header that the epoch wrap may clear: the state words
+    // and the arrival counters (the arrivals end the workspace)
+    const int64_t words = (int64_t)((topp_ws_bytes(rows, len) - kWsHeader) / sizeof(uint64_t));
+    auto k = vec ? k_topp_early<TV, true> : k_topp_early<TU, false>;
+    hipLaunchKernelGGL(k, dim3(nt), dim3(vec ? TV::kThreads : TU::kThreads), 0, stream, probs,
+                       cutoff, (uint32_t)rows, len, segs, nt, p, reinterpret_cast<WsHeader*>(ws),
+                       state, arrivals, words);
+}
+
 template <ToppMode MODE>
 static void topp_any(bool vec, const float* probs, const int32_t* idx, const float* theta,
                      int32_t* cutoff, int32_t* token, int64_t rows, int64_t len, float p,
                      void* ws, hipStream_t stream) {
+    if (MODE == ToppMode::Cutoff && topp_early(len)) {
+        topp_cutoff_early(vec, probs, cutoff, rows, len, p, ws, stream);
+        return;
+    }
     const int64_t t = row_tile(len);
     if (t == 32768)
         topp_long<RGeomL, MODE>(vec, probs, idx, theta, cutoff, token, rows, len, p, ws, stream);

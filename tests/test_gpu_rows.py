@@ -90,6 +90,25 @@ def test_topp_one_pass_limit(ops, length, p):
     _check_topp(ops, probs, p, f"topp len={length} p={p}")
 
 
+@pytest.mark.parametrize("length", [65_537, 131_072 + 5, 200_003, 262_144, 262_145])
+@pytest.mark.parametrize("p", [0.0, 0.5, 0.9, 0.999, 1.5])
+def test_topp_early_exit_shapes(ops, length, p):
+    """Rows of 3 to 8 long tiles take the early-exit kernel (262145: 9 tiles,
+    the two-phase one); p = 1.5 walks every tile of every row."""
+    announce("topp early", length, p)
+    probs = W.topp_probs(5, length, seed=length % 997)
+    _check_topp(ops, probs, p, f"topp early len={length} p={p}")
+
+
+@pytest.mark.parametrize("p", [0.3, 0.9])
+def test_topp_early_exit_unsorted(ops, p):
+    """The cutoff is defined on any row: unsorted softmax rows put the
+    crossing in any tile, so the row state is passed along tile by tile."""
+    announce("topp early unsorted", p)
+    probs = W.sample_probs(7, 6 * 32768 + 11, seed=3)
+    _check_topp(ops, probs, p, f"topp early unsorted p={p}")
+
+
 def test_topp_misaligned_view(ops):
     announce("topp misaligned")
     probs = W.topp_probs(3, 131_072 + 1, seed=5)
@@ -101,7 +120,7 @@ def test_topp_misaligned_view(ops):
     assert all(topp_accept(int(g[r]), int(k[r]), csum[r], 0.9) for r in range(3)), (g, k)
 
 
-@pytest.mark.parametrize("m", [2, 7, 12, 13, 17])
+@pytest.mark.parametrize("m", [2, 7, 12, 13, 17, 18])
 def test_topp_dyadic_exact(ops, m):
     """2^m equal probabilities 2^-m: every fp32 running sum is exact."""
     announce("topp dyadic", m)

@@ -86,12 +86,15 @@ def _check_samplers(ops, ws, n, seed):
 
 def _check_topp(ops, ws, n, seed):
     from gpu_util import topp_accept
-    probs = W.topp_probs(16, n // 16, seed=seed)
-    g = to_host(ops.topp_cutoff_f32(to_dev(probs), 0.9, ws=ws))
-    k = oracle.topp_cutoff_f32(probs, 0.9)
-    csum, _ = oracle.scan_rows_f32(probs)
-    bad = [r for r in range(16) if not topp_accept(int(g[r]), int(k[r]), csum[r], 0.9)]
-    assert not bad, ("topp", bad, g[bad], k[bad])
+    # 16 rows of n/16 (the two-phase kernel) and 4 rows of 5 long tiles (the
+    # early-exit kernel, whose row state words share the workspace too)
+    for shape in ((16, n // 16), (4, 4 * 32768 + 5)):
+        probs = W.topp_probs(shape[0], shape[1], seed=seed)
+        g = to_host(ops.topp_cutoff_f32(to_dev(probs), 0.9, ws=ws))
+        k = oracle.topp_cutoff_f32(probs, 0.9)
+        csum, _ = oracle.scan_rows_f32(probs)
+        bad = [r for r in range(shape[0]) if not topp_accept(int(g[r]), int(k[r]), csum[r], 0.9)]
+        assert not bad, ("topp", shape, bad, g[bad], k[bad])
 
 
 def test_one_workspace_for_every_op(ops):
