@@ -109,6 +109,25 @@ def test_topp_early_exit_unsorted(ops, p):
     _check_topp(ops, probs, p, f"topp early unsorted p={p}")
 
 
+def test_topp_early_exit_repeat(ops):
+    """The early-exit kernel 30 times on one workspace, alternating p so that
+    rows stop in different tiles: the row words it leaves must read as clear."""
+    from paper_2505_15112_amd import _lib
+    import torch
+    announce("topp early repeat")
+    probs = W.topp_probs(64, 5 * 32768, seed=77)
+    pd = to_dev(probs)
+    ws = ops.workspace(_lib.OP_SCAN_ROWS, torch.device("cuda", 0), rows=64, length=5 * 32768)
+    csum, _ = oracle.scan_rows_f32(probs)
+    for it in range(30):
+        p = (0.5, 0.9, 0.9999, 1.5)[it % 4]
+        g = to_host(ops.topp_cutoff_f32(pd, p, ws=ws))
+        k = oracle.topp_cutoff_f32(probs, p)
+        bad = [r for r in range(64) if not topp_accept(int(g[r]), int(k[r]), csum[r], p)]
+        assert not bad, (it, p, bad[:5])
+    assert int(ws[12:16].cpu().numpy().view(np.int32)[0]) == 0
+
+
 def test_topp_misaligned_view(ops):
     announce("topp misaligned")
     probs = W.topp_probs(3, 131_072 + 1, seed=5)

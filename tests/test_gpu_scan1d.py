@@ -303,6 +303,47 @@ def test_repeat_no_race(ops):
     assert bad == 0
 
 
+@pytest.mark.skipif(not FULL, reason="full-size cases disabled")
+def test_lds_tiles_repeat_no_race(ops):
+    """The register + LDS kernel 20 times on one workspace (int32, ragged
+    last tile): one result every time."""
+    import torch
+    announce("lds tiles repeat x20")
+    n = (1 << 27) + 12345
+    x = W.scan_i32_full_range(n, seed=51)
+    xd = to_dev(x)
+    ref = to_dev(oracle.scan_i32(x))
+    y = torch.empty_like(xd)
+    ws = ops.workspace(1, xd.device, n)
+    bad = 0
+    for _ in range(20):
+        ops.scan_inclusive_i32(xd, out=y, ws=ws)
+        bad += int((y != ref).sum().item())
+    assert bad == 0
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_sizes_and_offsets(ops, seed):
+    """Random lengths (up to 2^23) and element offsets through every 1-D
+    entry point of the three tile kernels (wavefront, register + LDS at the
+    large end is covered above, matrix-core for fp16), against the oracle."""
+    rng = np.random.default_rng(1000 + seed)
+    n = int(rng.integers(1, 1 << 23))
+    off = int(rng.integers(0, 8))
+    announce("random", seed, n, off)
+    xi = W.scan_i32_full_range(n + off, seed=seed)
+    assert_equal_first_diff(to_host(ops.scan_inclusive_i32(to_dev(xi)[off:])),
+                            oracle.scan_i32(xi[off:]), f"random i32 n={n} off={off}")
+    xe = W.exact_pm1(n + off, seed=seed, dtype=np.float16)
+    ref = oracle.scan_f16(xe[off:])[0]
+    for fn in (ops.scan_inclusive_f16f32, ops.scan_inclusive_f16f32_wave):
+        y = to_host(fn(to_dev(xe)[off:]))
+        assert_equal_first_diff(y.astype(np.float64), ref, f"random f16 n={n} off={off}")
+    if off % 8 == 0:
+        y = to_host(ops.scan_inclusive_f16f32_mfma(to_dev(xe)[off:]))
+        assert_equal_first_diff(y.astype(np.float64), ref, f"random mfma n={n}")
+
+
 def test_config_scan_i32_n2_16(ops):
     announce("config i32 n=2^16")
     x = W.scan_i32(1 << 16, seed=0)
