@@ -21,9 +21,28 @@ import pytest
 from paper_2505_15112_amd import build as B
 
 SOURCES = sorted(f for f in os.listdir(B.CSRC) if f.endswith(".hip"))
-TILE_KERNELS = ("k_scan_lookback", "k_rss_reduce", "k_rss_rescan", "k_rows_lookback", "k_topp",
-                "k_compact", "k_split", "k_radix4_count", "k_radix4_scatter", "k_radix8_count",
+TILE_KERNELS = ("k_scan_lookback", "k_scan_lookback_lds", "k_scan_mfma_f16", "k_rss_reduce",
+                "k_rss_rescan", "k_rows_lookback", "k_topp", "k_topp_early", "k_compact",
+                "k_split", "k_radix4_count", "k_radix4_scatter", "k_radix8_count",
                 "k_radix8_scatter", "k_topk_hist", "k_topk_select")
+
+
+def test_two_lds_tile_workgroups_fit_a_cu(tmp_path):
+    """The register + LDS scan tile must leave room for two workgroups per CU
+    (160 KB of LDS)."""
+    src = os.path.join(B.CSRC, "scan1d.hip")
+    out = tmp_path / "scan1d.s"
+    flags = [f for f in B.CFLAGS if f != "-fPIC"]
+    subprocess.run([B.HIPCC, *flags, "--cuda-device-only", "-S", src, "-o", str(out)],
+                   check=True, capture_output=True)
+    meta = out.read_text()
+    meta = meta[meta.index("amdhsa.kernels"):]
+    sizes = []
+    for block in meta.split("  - .agpr_count")[1:]:
+        name = re.search(r"\.name:\s+(\S+)", block).group(1)
+        if "k_scan_lookback_lds" in name:
+            sizes.append(int(re.search(r"\.group_segment_fixed_size:\s+(\d+)", block).group(1)))
+    assert sizes and max(sizes) * 2 <= 160 * 1024, sizes
 
 
 def kernel_resources(src, tmp_path):
