@@ -281,6 +281,20 @@ def main():
             key = "scan_f16f32" + ("_wave" if nm.endswith("wave") else "") + "_n2^28"
             opsd[key] = entry("f16 2^28", ms, b28, mc28, "n*(2+4)")
         del x16b, y16b
+        # the exclusive byte scan (mask counts), n = 2^28: the default
+        # wavefront tiles against the matrix-core variant, 1 + 4 bytes per element
+        xb = torch.from_numpy(W.mask_u8(n, seed=4)).to(dev)
+        yb = torch.empty(n, dtype=torch.int32, device=dev)
+        tb = torch.empty(1, dtype=torch.int32, device=dev)
+        b5 = n * 5
+        mc5 = memcpy_ms(b5)
+        for nm in ("scan_exclusive_u8i32", "scan_exclusive_u8i32_mfma"):
+            fn = getattr(lib, nm)
+            a = (P(xb), P(yb), n, P(tb), wsp, wsb, sp)
+            ms = T.back_to_back(lambda: check(fn(*a), nm), K, Wm)
+            key = "scan_u8i32" + ("_mfma" if nm.endswith("mfma") else "") + "_n2^28"
+            opsd[key] = entry("u8", ms, b5, mc5, "n*(1+4)")
+        del xb, yb, tb
 
         # config: int32, n = 2^16 (latency-bound)
         n1 = 1 << 16

@@ -136,6 +136,25 @@ int scan_inclusive_f16f32_wave(const uint16_t* x, float* y, int64_t n, void* ws,
 int scan_exclusive_u8i32(const uint8_t* x, int32_t* y, int64_t n, int32_t* total_dev, void* ws,
                          size_t ws_bytes, void* stream);
 
+/* The same exclusive byte scan with the tile-local scans on the matrix cores
+ * (Section 4.1's ScanU with the strictly upper triangular ones matrix, which
+ * gives exclusive row scans directly): each block of 32 x 32 bytes is one
+ * v_mfma_i32_32x32x32_i8 product on x - 128 (the signed form of the byte),
+ * corrected by 128 j per column j, exact in int32.  x must be 16-byte aligned
+ * and y 4-byte aligned (else LIBSCAN_EINVAL); otherwise as
+ * scan_exclusive_u8i32.  Whole 32768-byte tiles run on the matrix cores, a
+ * shorter tail on the wavefront tiles.  Measured no faster than the
+ * wavefront tiles, so scan_exclusive_u8i32 does not use it; kept as the
+ * measured alternative. */
+int scan_exclusive_u8i32_mfma(const uint8_t* x, int32_t* y, int64_t n, int32_t* total_dev,
+                              void* ws, size_t ws_bytes, void* stream);
+
+/* The exclusive byte scan on the wavefront tiles only (any n, any
+ * alignment), which is what scan_exclusive_u8i32 runs: the baseline the
+ * matrix-core path is measured against. */
+int scan_exclusive_u8i32_wave(const uint8_t* x, int32_t* y, int64_t n, int32_t* total_dev,
+                              void* ws, size_t ws_bytes, void* stream);
+
 /* Chunked scans (Section 6.1.1, "L2 cache splitting": consecutive chunks
  * scanned one after another, the last value of each carried into the next).
  * carry_in_dev (nullable, device, one element) is added in front of x, i.e.

@@ -32,6 +32,8 @@ SIGNATURES = {
     "scan_inclusive_f16f32_mfma": (_int, [_p, _p, _i64, _p, _sz, _p]),
     "scan_inclusive_f16f32_wave": (_int, [_p, _p, _i64, _p, _sz, _p]),
     "scan_exclusive_u8i32": (_int, [_p, _p, _i64, _p, _p, _sz, _p]),
+    "scan_exclusive_u8i32_mfma": (_int, [_p, _p, _i64, _p, _p, _sz, _p]),
+    "scan_exclusive_u8i32_wave": (_int, [_p, _p, _i64, _p, _p, _sz, _p]),
     "scan_inclusive_i32_carry": (_int, [_p, _p, _i64, _p, _p, _p, _sz, _p]),
     "scan_exclusive_i32_carry": (_int, [_p, _p, _i64, _p, _p, _p, _sz, _p]),
     "scan_inclusive_f32_carry": (_int, [_p, _p, _i64, _p, _p, _p, _sz, _p]),

@@ -144,6 +144,26 @@ int check_topk(int64_t rows, int64_t len, int64_t k) {
     return LIBSCAN_OK;
 }
 
+int scan_u8_variant(bool mfma, const uint8_t* x, int32_t* y, int64_t n, int32_t* total_dev,
+                           void* ws, size_t ws_bytes, void* stream) {
+    if (n < 0) return LIBSCAN_EINVAL;
+    if (n > ls::kMaxScanElems) return LIBSCAN_ERANGE;
+    if (n > 0 && (!x || !y)) return LIBSCAN_EINVAL;
+    if (bad_alias(x, (size_t)n, y, (size_t)n * 4, false)) return LIBSCAN_EINVAL;
+    if (total_dev && overlaps(total_dev, 4, y, (size_t)n * 4)) return LIBSCAN_EINVAL;
+    if (n == 0 && !total_dev) return LIBSCAN_OK;
+    if (mfma && n > 0 && (((uintptr_t)x % 16) != 0 || ((uintptr_t)y % 4) != 0))
+        return LIBSCAN_EINVAL;
+    const int w = check_ws(ws, ws_bytes, ls::scan1d_ws_bytes(n));
+    if (w != LIBSCAN_OK) return w;
+    hipStream_t s = (hipStream_t)stream;
+    if (mfma && n > 0)
+        return hip_status(ls::launch_scan1d_mfma_u8(x, (uint32_t*)y, n, (uint32_t*)total_dev, ws,
+                                                    ws_bytes, s));
+    return hip_status(ls::launch_scan1d_tiles(Kind::U8I32, true, x, y, n, nullptr, total_dev, ws,
+                                              ws_bytes, s));
+}
+
 }  // namespace
 
 extern "C" {
@@ -276,6 +296,16 @@ int scan_inclusive_f16f32_mfma(const uint16_t* x, float* y, int64_t n, void* ws,
     const int w = check_ws(ws, ws_bytes, ls::scan1d_ws_bytes(n));
     if (w != LIBSCAN_OK) return w;
     return hip_status(ls::launch_scan1d_mfma_f16(x, y, n, ws, ws_bytes, (hipStream_t)stream));
+}
+
+int scan_exclusive_u8i32_mfma(const uint8_t* x, int32_t* y, int64_t n, int32_t* total_dev,
+                              void* ws, size_t ws_bytes, void* stream) {
+    return scan_u8_variant(true, x, y, n, total_dev, ws, ws_bytes, stream);
+}
+
+int scan_exclusive_u8i32_wave(const uint8_t* x, int32_t* y, int64_t n, int32_t* total_dev,
+                              void* ws, size_t ws_bytes, void* stream) {
+    return scan_u8_variant(false, x, y, n, total_dev, ws, ws_bytes, stream);
 }
 int scan_exclusive_u8i32(const uint8_t* x, int32_t* y, int64_t n, int32_t* total_dev, void* ws,
                          size_t ws_bytes, void* stream) {

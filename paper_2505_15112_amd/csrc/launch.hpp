@@ -36,6 +36,10 @@ hipError_t launch_scan1d_tiles(Kind kind, bool exclusive, const void* x, void* y
 constexpr int64_t kMfmaTileElems = 32768;
 hipError_t launch_scan1d_mfma_f16(const uint16_t* x, float* y, int64_t n, void* ws,
                                   size_t ws_bytes, hipStream_t stream);
+// The exclusive byte scan the same way (v_mfma_i32_32x32x32_i8); total_out
+// (nullable) gets the sum of all bytes.  x 16-byte aligned.
+hipError_t launch_scan1d_mfma_u8(const uint8_t* x, uint32_t* y, int64_t n, uint32_t* total_out,
+                                 void* ws, size_t ws_bytes, hipStream_t stream);
 
 // 1-D reduce-then-scan (three kernels).
 size_t scan1d_rss_ws_bytes(int64_t n);

@@ -103,15 +103,29 @@ def scan_inclusive_f16f32_wave(x, out=None, ws=None):
     return _scan1d("scan_inclusive_f16f32_wave", x, torch.float16, torch.float32, out, ws)
 
 
-def scan_exclusive_u8i32(x, out=None, total=None, ws=None):
-    """Returns (y, total) -- total is a 1-element int32 device tensor."""
+def _scan_u8(cname, x, out, total, ws):
     if total is None:
         total = torch.empty(1, dtype=torch.int32, device=x.device)
     else:
         _check(total, torch.int32, "total")
-    y = _scan1d("scan_exclusive_u8i32", x, torch.uint8, torch.int32, out, ws,
+    y = _scan1d(cname, x, torch.uint8, torch.int32, out, ws,
                 extra=(ctypes.c_void_p(total.data_ptr()),))
     return y, total
+
+
+def scan_exclusive_u8i32(x, out=None, total=None, ws=None):
+    """Returns (y, total) -- total is a 1-element int32 device tensor."""
+    return _scan_u8("scan_exclusive_u8i32", x, out, total, ws)
+
+
+def scan_exclusive_u8i32_mfma(x, out=None, total=None, ws=None):
+    """The byte scan with the row scans on the matrix cores (x 16-byte aligned)."""
+    return _scan_u8("scan_exclusive_u8i32_mfma", x, out, total, ws)
+
+
+def scan_exclusive_u8i32_wave(x, out=None, total=None, ws=None):
+    """The byte scan on the wavefront tiles only."""
+    return _scan_u8("scan_exclusive_u8i32_wave", x, out, total, ws)
 
 
 def _carry(cname, dtype, x, carry_in, out, total_out, ws):

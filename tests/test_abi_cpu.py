@@ -87,6 +87,16 @@ def test_mixed_type_scans_reject_any_overlap(lib):
     # the matrix-core scan needs a 16-byte aligned input
     assert lib.scan_inclusive_f16f32_mfma(P(0x100002), Y, 100, WS, BIG, None) == _lib.EINVAL
     assert lib.scan_exclusive_u8i32(X, X, 100, None, WS, BIG, None) == _lib.EINVAL
+    for name in ("scan_exclusive_u8i32_mfma", "scan_exclusive_u8i32_wave"):
+        fn = getattr(lib, name)
+        assert fn(X, X, 100, None, WS, BIG, None) == _lib.EINVAL        # overlap
+        assert fn(X, Y, -1, None, WS, BIG, None) == _lib.EINVAL         # negative size
+        assert fn(None, Y, 10, None, WS, BIG, None) == _lib.EINVAL      # NULL input
+        assert fn(X, Y, 1 << 40, None, WS, BIG, None) == _lib.ERANGE    # too long
+        assert fn(X, Y, 1 << 20, None, WS, 8, None) == _lib.ENOSPACE    # workspace too small
+        assert fn(None, None, 0, None, None, 0, None) == _lib.OK        # empty
+    # the matrix-core byte scan needs a 16-byte aligned input
+    assert lib.scan_exclusive_u8i32_mfma(P(0x100001), Y, 100, None, WS, BIG, None) == _lib.EINVAL
 
 
 def test_carry_validation(lib):

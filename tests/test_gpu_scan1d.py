@@ -279,6 +279,36 @@ def test_mfma_matches_wavefront_and_repeats(ops):
     assert bad == 0
 
 
+@pytest.mark.parametrize("n", MFMA_SIZES)
+def test_mfma_u8i32(ops, n):
+    """Bytes 0..255 (the signed MFMA sees x - 128): bit-exact, with the total,
+    through the default (wavefront), matrix-core and wavefront entry points."""
+    announce("mfma u8", n)
+    x = W.bytes_u8(n, seed=n + 6)
+    ref, rtot = oracle.scan_u8(x)
+    for fn in (ops.scan_exclusive_u8i32, ops.scan_exclusive_u8i32_mfma,
+               ops.scan_exclusive_u8i32_wave):
+        y, total = fn(to_dev(x))
+        assert_equal_first_diff(to_host(y), ref, f"{fn.__name__} n={n}")
+        assert int(to_host(total)[0]) == rtot
+
+
+def test_mfma_u8i32_extremes_and_repeats(ops):
+    """All-255 and all-0 bytes (the extremes of the x - 128 correction) and a
+    Bernoulli mask, 10 calls each on one workspace."""
+    import torch
+    announce("mfma u8 extremes")
+    n = 40 * 32768 + 99
+    ws = ops.workspace(1, torch.device("cuda", 0), n)
+    for x in (np.full(n, 255, np.uint8), np.zeros(n, np.uint8), W.mask_u8(n, seed=3)):
+        ref, rtot = oracle.scan_u8(x)
+        xd = to_dev(x)
+        for _ in range(10):
+            y, total = ops.scan_exclusive_u8i32_mfma(xd, ws=ws)
+            assert_equal_first_diff(to_host(y), ref, "u8 extremes")
+            assert int(to_host(total)[0]) == rtot
+
+
 def test_mfma_rejects_misaligned(ops):
     announce("mfma misaligned")
     x = to_dev(W.scan_f16(1001, seed=5))
