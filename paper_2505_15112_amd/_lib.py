@@ -4,12 +4,16 @@ The library is loaded after ``import torch`` so that it binds to the HIP
 runtime torch has already loaded (same soname) instead of a second copy; the
 stream handles torch hands out are then valid inside the library.
 """
+import contextlib
 import ctypes
 import os
 import re
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libscan.so")
+# the same sources with pseudo-random pauses before every inter-workgroup
+# protocol step (adversarial-scheduling tests only)
+LIB_ADV_PATH = os.path.join(PKG, "libscan_adv.so")
 HEADER = os.path.join(os.path.dirname(PKG), "include", "libscan.h")
 
 _p = ctypes.c_void_p
@@ -83,6 +87,11 @@ def load(path: str = LIB_PATH):
     global _LIB
     if _LIB is not None:
         return _LIB
+    _LIB = _open(path)
+    return _LIB
+
+
+def _open(path: str):
     import torch  # noqa: F401  -- bind to torch's HIP runtime (see module docstring)
     if not os.path.exists(path):
         raise RuntimeError(
@@ -93,8 +102,31 @@ def load(path: str = LIB_PATH):
         fn = getattr(lib, name)
         fn.restype = res
         fn.argtypes = args
-    _LIB = lib
     return lib
+
+
+_ADV = None
+
+
+def load_adversarial():
+    """libscan_adv.so (see LIB_ADV_PATH), loaded once beside libscan.so."""
+    global _ADV
+    if _ADV is None:
+        _ADV = _open(LIB_ADV_PATH)
+    return _ADV
+
+
+@contextlib.contextmanager
+def using(lib):
+    """Route every call made through this module to `lib` inside the block."""
+    global _LIB
+    load()
+    saved = _LIB
+    _LIB = lib
+    try:
+        yield lib
+    finally:
+        _LIB = saved
 
 
 def call(name: str, *args):

@@ -3,7 +3,10 @@
     python -m paper_2505_15112_amd.build [-v]
 
 Compiles every csrc/*.hip into _build/ and links paper_2505_15112_amd/libscan.so
-in-tree.  Always recompiles.
+in-tree.  Always recompiles.  Also links libscan_adv.so, the same sources built
+with LS_ADVERSARIAL_DELAYS (pseudo-random pauses before every inter-workgroup
+protocol step) for the adversarial-scheduling tests; it binds its own symbols
+(-Bsymbolic) so that it can be loaded beside libscan.so.
 """
 import concurrent.futures as cf
 import glob
@@ -16,6 +19,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build", "libscan")
 LIB = os.path.join(PKG, "libscan.so")
+LIB_ADV = os.path.join(PKG, "libscan_adv.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
@@ -29,9 +33,9 @@ CFLAGS = [
 ]
 
 
-def _compile(src: str, verbose: bool) -> str:
-    obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *CFLAGS, "-c", src, "-o", obj]
+def _compile(src: str, verbose: bool, build_dir: str, extra=()) -> str:
+    obj = os.path.join(build_dir, os.path.basename(src) + ".o")
+    cmd = [HIPCC, *CFLAGS, *extra, "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -44,19 +48,28 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
-    with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), srcs))
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
+def _link(objs, out: str, verbose: bool, extra=()) -> str:
+    tmp = out + ".tmp"
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *extra, "-o", tmp, *objs]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
+    return out
+
+
+def build(verbose: bool = False) -> str:
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+    adv_dir = BUILD + "_adv"
+    os.makedirs(BUILD, exist_ok=True)
+    os.makedirs(adv_dir, exist_ok=True)
+    jobs = [(s, BUILD, ()) for s in srcs] + [(s, adv_dir, ("-DLS_ADVERSARIAL_DELAYS",)) for s in srcs]
+    with cf.ThreadPoolExecutor(max_workers=min(8, len(jobs))) as ex:
+        objs = list(ex.map(lambda j: _compile(j[0], verbose, j[1], j[2]), jobs))
+    _link(objs[:len(srcs)], LIB, verbose)
+    _link(objs[len(srcs):], LIB_ADV, verbose, ("-Wl,-Bsymbolic",))
     return LIB
 
 

@@ -90,6 +90,27 @@ __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// ---------------------------------------------------------------- test pauses
+
+// Test builds (LS_ADVERSARIAL_DELAYS defined) pause for a pseudo-random time
+// before each step of the inter-workgroup protocols -- after taking a tile
+// ticket, before publishing a status word, before arriving at a row counter
+// -- so that workgroups reach those steps in orders a normal run seldom
+// produces: usually 0-3 us, one time in eight 14-30 us.  Product builds
+// compile it away.  Called by one thread or one wavefront at a time.
+#ifdef LS_ADVERSARIAL_DELAYS
+__device__ __forceinline__ void adversarial_pause(uint32_t key) {
+    uint32_t h = key * 0x9E3779B1u ^ (uint32_t)__builtin_amdgcn_s_memrealtime();
+    h ^= h >> 15;
+    h *= 0x2C1B3C6Du;
+    h ^= h >> 12;
+    const uint32_t rounds = (h & 7u) == 0 ? 64u + ((h >> 3) & 63u) : (h >> 3) & 15u;
+    for (uint32_t i = 0; i < rounds; ++i) __builtin_amdgcn_s_sleep(8);  // 512 cycles
+}
+#else
+__device__ __forceinline__ void adversarial_pause(uint32_t) {}
+#endif
+
 // ---------------------------------------------------------------- workspace
 
 // Every workspace starts with a 256-byte header:
@@ -131,6 +152,7 @@ __device__ __forceinline__ Ticket take_ticket(WsHeader* h, uint32_t nwg) {
     if (t.tile == nwg - 1)  // every other ticket of this launch is taken
         __hip_atomic_store(&h->ticket, (uint64_t)(t.epoch + 1) << 32, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
+    adversarial_pause(t.tile);
     return t;
 }
 
@@ -171,6 +193,7 @@ template <class T, int K = 1>
 __device__ T lookback(uint64_t* status, uint32_t tile, uint32_t first, T agg, T base,
                       uint32_t epoch, WsHeader* h) {
     const int lane = lane_id();
+    if (lane == 0) adversarial_pause(tile);
     if (tile == first) {
         if (lane == 0) status_store(status + tile, status_word(kStateP, epoch, Bits<T>::to(base + agg)));
         return base;
@@ -223,7 +246,10 @@ __device__ T lookback(uint64_t* status, uint32_t tile, uint32_t first, T agg, T 
             __builtin_amdgcn_s_sleep(1);
         }
     }
-    if (lane == 0) status_store(status + tile, status_word(kStateP, epoch, Bits<T>::to(excl + agg)));
+    if (lane == 0) {
+        adversarial_pause(tile ^ 0x5bd1e995u);
+        status_store(status + tile, status_word(kStateP, epoch, Bits<T>::to(excl + agg)));
+    }
     return excl;
 }
 

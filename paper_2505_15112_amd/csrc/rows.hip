@@ -421,6 +421,7 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp_early(
             out |= kFoundBit;
         }
         if (threadIdx.x == 0) {
+            adversarial_pause(tile32);
             __hip_atomic_store(&state[row], out, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             // arrive only once the word is acknowledged, so that the row's
             // reset below can never be overtaken by it

@@ -37,6 +37,7 @@ __device__ __forceinline__ bool row_word(uint64_t w) { return (w >> 61) == 1; }
 // word without the tag (left by another op sharing the workspace) counts as
 // zero, hence compare-and-swap rather than a plain add.
 __device__ __forceinline__ uint32_t row_arrive(uint64_t* counter) {
+    adversarial_pause((uint32_t)(uintptr_t)counter);
     uint64_t old = __hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     while (true) {
         const uint32_t before = row_word(old) ? (uint32_t)old : 0u;

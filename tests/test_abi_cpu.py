@@ -11,7 +11,8 @@ import pytest
 
 from paper_2505_15112_amd import _lib
 
-if not os.path.exists(_lib.LIB_PATH):  # load what is built; build only if nothing is
+if not (os.path.exists(_lib.LIB_PATH) and os.path.exists(_lib.LIB_ADV_PATH)):
+    # load what is built; build only if nothing is
     from paper_2505_15112_amd import build as _build
     _build.build()
 
@@ -36,6 +37,17 @@ def test_every_declared_symbol_is_exported(lib):
         assert hasattr(lib, name), name
         assert name in _lib.SIGNATURES, f"{name} missing from the binding"
     assert sorted(_lib.SIGNATURES) == declared
+
+
+def test_adversarial_build_exports_the_same_symbols_and_checks(lib):
+    """libscan_adv.so (the test build with pauses) loads beside libscan.so,
+    exports the same entry points and validates the same way."""
+    adv = _lib.load_adversarial()
+    assert adv is not lib
+    for name in _lib.header_functions():
+        assert hasattr(adv, name), name
+    assert adv.scan_inclusive_i32(X, Y, -1, WS, BIG, None) == _lib.EINVAL
+    assert adv.scan_inclusive_i32(X, Y, 1 << 20, WS, 8, None) == _lib.ENOSPACE
 
 
 def test_version_and_strings(lib):
