@@ -119,6 +119,30 @@ class Timer:
         return sorted(out)[len(out) // 2]
 
 
+def device_info(torch, dev):
+    """What the runtime reports about the GPU (no clocks: torch does not expose them)."""
+    p = torch.cuda.get_device_properties(dev)
+    return {"name": p.name, "arch": getattr(p, "gcnArchName", ""),
+            "compute_units": p.multi_processor_count,
+            "memory_gib": round(p.total_memory / 2**30, 1),
+            "l2_bytes": getattr(p, "L2_cache_size", None),
+            "hip": torch.version.hip}
+
+
+def host_cpu():
+    """Model name and logical CPU count of the host the oracle runs on."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, os.cpu_count()
+
+
 def entry(name, ms, nbytes, memcpy_ms, unit_note, extra=None):
     gbps = nbytes / (ms * 1e-3) / 1e9
     e = {"ms": round(ms, 5), "gbps": round(gbps, 2), "bytes": nbytes,
@@ -220,6 +244,7 @@ def main():
             "workload": "1-D inclusive prefix sum, n=2^28 int32, x_i iid uniform {0..100}",
             "n": n, "bytes_per_step": nbytes,
         },
+        "device": device_info(torch, dev),
         "pct_of_memcpy": round(100.0 * g_i32 / g_cp, 2),
         "pct_of_peak_hbm": round(100.0 * g_i32 / PEAK_HBM_GBPS, 2),
         "memcpy_gbps": round(g_cp, 2),
@@ -515,6 +540,7 @@ def cpu_baseline_leg(x_host, y_dev, outputs, np, torch):
                   f"(serial C oracle, median of 3 runs, {t:.3f} s each)",
         "matches_gpu": bool(np.array_equal(ref, y_dev.cpu().numpy())),
     }
+    metric["host_cpu_model"], metric["host_logical_cpus"] = host_cpu()
     res = {}
     if "f16" in outputs:
         xh, y = outputs["f16"]
