@@ -356,7 +356,24 @@ constexpr int64_t kR8Tile = kR8Waves * kR8Chunks * kWave;  // 8192 keys
 constexpr int kR8Digits = 256;
 
 
-// Lanes holding the same 8-bit digit as this lane, among the `ok` lanes.
+// Lanes holding the same 8-bit digit as this lane, when every lane of the
+// wave holds a key: the AND over the digit bits of that bit's ballot,
+// complemented where this lane's bit is 0.  Written as m & (ballot ^ e), e
+// all ones for a 0 bit, one three-input bit operation per 32-bit half.
+__device__ __forceinline__ uint64_t peers8_all(uint32_t d) {
+    uint32_t lo = ~0u, hi = ~0u;
+    const uint32_t nd = ~d;
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+        const uint32_t e = (uint32_t)((int32_t)(nd << (31 - b)) >> 31);
+        const uint64_t bb = __ballot(e == 0);
+        lo &= (uint32_t)bb ^ e;
+        hi &= (uint32_t)(bb >> 32) ^ e;
+    }
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// The same among the `ok` lanes (a ragged tile).
 __device__ __forceinline__ uint64_t peers8(uint32_t d, bool ok) {
     uint64_t m = __ballot(ok);
 #pragma unroll
@@ -441,11 +458,14 @@ template <class K, bool HAS_PERM_IN, bool WITH_PERM>
 __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatter(
     const K* keys_in, const int32_t* perm_in, K* keys_out, int32_t* perm_out, int64_t len,
     uint32_t tpr, int shift, uint32_t* offsets, KeyCode code, KeyDecode decode) {
-    __shared__ uint32_t s_wh[kR8Waves][kR8Digits];  // wave counts, then each wave's first slot
-    __shared__ uint32_t s_tstart[kR8Digits];         // first slot of digit d in the tile
-    __shared__ uint32_t s_gbase[kR8Digits];          // global position of that slot
+    // per-wave digit counts during ranking, then each wave's first slot per digit
+    __shared__ uint32_t s_wh[kR8Waves][kR8Digits];
+    __shared__ uint32_t s_off[kR8Digits];  // global row position minus tile slot, per digit
     __shared__ uint32_t s_part[kR8Digits / kWave];
     __shared__ uint32_t s_stage[kR8Tile];
+    // the tile's source indices, loaded straight into LDS at the start (in
+    // the tile's index order) so that they arrive while the keys are ranked
+    __shared__ int32_t s_pin[WITH_PERM && HAS_PERM_IN ? kR8Tile : 1];
 
     const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);
     const int lane = lane_id();
@@ -456,134 +476,130 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
     const int64_t wbase = tstart + (int64_t)w * kR8Chunks * kWave;
     const bool full = tstart + kR8Tile <= len;
     const uint32_t valid = full ? (uint32_t)kR8Tile : (uint32_t)(len - tstart);
-    const K* kin = keys_in + rbase;
+    const K* kw = keys_in + rbase + wbase;  // this wave's keys
     K* kout = keys_out + rbase;
 
     for (int i = threadIdx.x; i < kR8Waves * kR8Digits; i += kR8Waves * kWave) (&s_wh[0][0])[i] = 0;
+    uint32_t gbase = 0;  // thread d < 256: global row position of the tile's first digit-d key
     if (threadIdx.x < kR8Digits) {
         uint32_t* o = offsets + ((int64_t)row * kR8Digits + threadIdx.x) * tpr + tr;
-        s_gbase[threadIdx.x] = *o;
+        gbase = *o;
         *o = 0;  // offsets can reach 2^30 and more: leave the workspace word zero
     }
-    // All loads first, then the encoding: applied inside a per-key branch it
-    // would make each load wait for the one before.  (Lanes past the end get
-    // a code of 0; they are masked out everywhere below.)
-    uint32_t key[kR8Chunks];
-    if (full) {
-#pragma unroll
-        for (int j = 0; j < kR8Chunks; ++j) key[j] = (uint32_t)kin[wbase + j * kWave + lane];
-    } else {
-#pragma unroll
-        for (int j = 0; j < kR8Chunks; ++j) {
-            const int64_t i = wbase + j * kWave + lane;
-            key[j] = i < len ? (uint32_t)kin[i] : 0u;
-        }
-    }
-#pragma unroll
-    for (int j = 0; j < kR8Chunks; ++j) key[j] = code.apply(key[j]);
-    __syncthreads();
 
-    // Chunks in groups of 4: the peer groups of the 4 chunks, their LDS
-    // atomics back to back (they execute in order, so a later chunk sees the
-    // earlier chunks' counts), then the broadcasts from the leaders -- the
-    // atomics' latencies overlap without holding 16 results at once.
-    constexpr int kG = 4;
-    uint32_t rank[kR8Chunks];  // peers in lower lanes, then the rank
-#pragma unroll
-    for (int g = 0; g < kR8Chunks; g += kG) {
-        uint32_t leader[kG];  // leader lane | group size << 8 (size 0: invalid lane)
-#pragma unroll
-        for (int q = 0; q < kG; ++q) {
-            const int64_t i = wbase + (g + q) * kWave + lane;
-            const bool ok = full || i < len;
-            const uint64_t peers = peers8((key[g + q] >> shift) & 255u, ok);
-            rank[g + q] = lanes_below(peers);
-            leader[q] = ok ? ((uint32_t)__builtin_ctzll(peers) |
-                              ((uint32_t)__builtin_popcountll(peers) << 8))
-                           : (uint32_t)lane;
-        }
-        uint32_t before[kG];
-#pragma unroll
-        for (int q = 0; q < kG; ++q) {
-            before[q] = 0;
-            if ((leader[q] & 255u) == (uint32_t)lane && (leader[q] >> 8))
-                before[q] = atomicAdd(&s_wh[w][(key[g + q] >> shift) & 255u], leader[q] >> 8);
-        }
-#pragma unroll
-        for (int q = 0; q < kG; ++q) rank[g + q] += lane_shfl(before[q], (int)(leader[q] & 255u));
-    }
-    // The source indices are needed only when they are staged: load them now
-    // (ranking holds four registers per key), in flight while the keys move.
-    int32_t perm[kR8Chunks];
-    if (WITH_PERM) {
-#pragma unroll
-        for (int j = 0; j < kR8Chunks; ++j) {
-            const int64_t i = wbase + j * kWave + lane;
-            perm[j] = HAS_PERM_IN ? ((full || i < len) ? perm_in[rbase + i] : 0) : (int32_t)i;
-        }
-    }
-    __syncthreads();
+    // The tile body, compiled twice: for full tiles (every lane holds a key,
+    // no per-lane bounds) and for the ragged last tile of a row.
+    auto body = [&](auto full_c) {
+        constexpr bool FULL = decltype(full_c)::value;
+        auto in_range = [&](int j) { return FULL || wbase + j * kWave + lane < len; };
 
-    // Digit d (thread d): the waves' first slots within the digit, the tile
-    // total, and the exclusive scan of the totals over the 256 digits.
-    uint32_t tot = 0, inc = 0;
-    if (threadIdx.x < kR8Digits) {
+        // Source indices first, straight into LDS (no registers: ranking
+        // needs them), then the keys.  The LDS-direct load of a chunk writes
+        // lane l's 4 bytes at the chunk's slot + 4 l; lanes past the end load
+        // nothing and their slots are never read.
+        if (WITH_PERM && HAS_PERM_IN) {
+            const int32_t* pw = perm_in + rbase + wbase;
 #pragma unroll
-        for (int k = 0; k < kR8Waves; ++k) {
-            const uint32_t c = s_wh[k][threadIdx.x];
-            s_wh[k][threadIdx.x] = tot;
-            tot += c;
+            for (int j = 0; j < kR8Chunks; ++j)
+                if (in_range(j))
+                    __builtin_amdgcn_global_load_lds((const void*)(pw + j * kWave + lane),
+                                                     s_pin + (w * kR8Chunks + j) * kWave, 4, 0, 0);
         }
-        inc = wave_incl_scan(tot);
-        if (lane == kWave - 1) s_part[w] = inc;
-    }
-    __syncthreads();
-    if (threadIdx.x < kR8Digits) {
-        uint32_t before = 0;
-        for (int k = 0; k < w; ++k) before += s_part[k];
-        s_tstart[threadIdx.x] = before + inc - tot;
-    }
-    __syncthreads();
-
-    // Sort the tile by digit in LDS, then write it out with consecutive threads
-    // (each digit's keys form one contiguous output run).
+        // All key loads, then the encoding: applied inside a per-key branch
+        // it would make each load wait for the one before.  (Lanes past the
+        // end get a code of 0; they are masked out everywhere below.)
+        uint32_t key[kR8Chunks];
 #pragma unroll
-    for (int j = 0; j < kR8Chunks; ++j) {
-        const int64_t i = wbase + j * kWave + lane;
-        const uint32_t d = (key[j] >> shift) & 255u;
-        rank[j] += s_tstart[d] + s_wh[w][d];  // now the slot
-        if ((full || i < len) && rank[j] < kR8Tile) s_stage[rank[j]] = key[j];
-    }
-    __syncthreads();
-    uint32_t skey[kR8Chunks];
+        for (int j = 0; j < kR8Chunks; ++j) key[j] = in_range(j) ? (uint32_t)kw[j * kWave + lane] : 0u;
 #pragma unroll
-    for (int j = 0; j < kR8Chunks; ++j) {
-        const uint32_t t = (uint32_t)threadIdx.x + j * kR8Waves * kWave;
-        skey[j] = s_stage[t];
-        if (t < valid) {
-            const uint32_t d = (skey[j] >> shift) & 255u;
-            const uint32_t pos = s_gbase[d] + (t - s_tstart[d]);
-            if (pos < (uint64_t)len) kout[pos] = (K)decode.apply(skey[j]);  // pos < len always
-        }
-    }
-    if (WITH_PERM) {
+        for (int j = 0; j < kR8Chunks; ++j) key[j] = code.apply(key[j]);
         __syncthreads();
+
+        // Rank chunk by chunk.  The peer group's lowest lane adds the group
+        // size to the wave's count of the digit (an LDS add that returns
+        // nothing), then every lane reads that count back: LDS carries out a
+        // wave's operations in issue order, so the read sees this chunk's
+        // add and no later one, and the key's rank is the count before the
+        // group plus its peers in lower lanes.  No chunk waits on another.
+        uint32_t rank[kR8Chunks];
 #pragma unroll
         for (int j = 0; j < kR8Chunks; ++j) {
-            const int64_t i = wbase + j * kWave + lane;
-            if ((full || i < len) && rank[j] < kR8Tile) s_stage[rank[j]] = (uint32_t)perm[j];
+            const uint32_t d = (key[j] >> shift) & 255u;
+            const uint64_t peers = FULL ? peers8_all(d) : peers8(d, in_range(j));
+            const uint32_t below = lanes_below(peers);
+            const uint32_t size = (uint32_t)__builtin_popcountll(peers);
+            if (in_range(j) && below == 0) atomicAdd(&s_wh[w][d], size);
+            rank[j] = s_wh[w][d] - size + below;
+        }
+        // the index loads were issued first: long done, and no stores yet
+        if (WITH_PERM && HAS_PERM_IN) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+
+        // Digit d (thread d): the tile's first slot of the digit (exclusive
+        // scan of the totals over the 256 digits), then each wave's first
+        // slot, and the offset from a slot to the global position.
+        uint32_t c[kR8Waves];
+        uint32_t tot = 0, inc = 0;
+        if (threadIdx.x < kR8Digits) {
+#pragma unroll
+            for (int k = 0; k < kR8Waves; ++k) {
+                c[k] = s_wh[k][threadIdx.x];
+                tot += c[k];
+            }
+            inc = wave_incl_scan(tot);
+            if (lane == kWave - 1) s_part[w] = inc;
         }
         __syncthreads();
+        if (threadIdx.x < kR8Digits) {
+            uint32_t first = inc - tot;
+            for (int k = 0; k < w; ++k) first += s_part[k];
+            s_off[threadIdx.x] = gbase - first;
+#pragma unroll
+            for (int k = 0; k < kR8Waves; ++k) {
+                s_wh[k][threadIdx.x] = first;
+                first += c[k];
+            }
+        }
+        __syncthreads();
+
+        // Sort the tile by digit in LDS, then write it out with consecutive
+        // threads (each digit's keys form one contiguous output run).
+#pragma unroll
+        for (int j = 0; j < kR8Chunks; ++j) {
+            rank[j] += s_wh[w][(key[j] >> shift) & 255u];  // now the slot
+            if (FULL || (in_range(j) && rank[j] < kR8Tile)) s_stage[rank[j]] = key[j];
+        }
+        __syncthreads();
+        uint32_t pos[kR8Chunks];
 #pragma unroll
         for (int j = 0; j < kR8Chunks; ++j) {
             const uint32_t t = (uint32_t)threadIdx.x + j * kR8Waves * kWave;
-            if (t < valid) {
-                const uint32_t d = (skey[j] >> shift) & 255u;
-                const uint32_t pos = s_gbase[d] + (t - s_tstart[d]);
-                if (pos < (uint64_t)len) perm_out[rbase + pos] = (int32_t)s_stage[t];
+            const uint32_t sk = s_stage[t];
+            pos[j] = s_off[(sk >> shift) & 255u] + t;
+            // pos < len always; the test guards against a corrupted table
+            if ((FULL || t < valid) && pos[j] < (uint64_t)len) kout[pos[j]] = (K)decode.apply(sk);
+        }
+        if (WITH_PERM) {
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < kR8Chunks; ++j) {
+                const int32_t pv = HAS_PERM_IN ? s_pin[(w * kR8Chunks + j) * kWave + lane]
+                                               : (int32_t)(wbase + j * kWave + lane);
+                if (FULL || (in_range(j) && rank[j] < kR8Tile)) s_stage[rank[j]] = (uint32_t)pv;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < kR8Chunks; ++j) {
+                const uint32_t t = (uint32_t)threadIdx.x + j * kR8Waves * kWave;
+                if ((FULL || t < valid) && pos[j] < (uint64_t)len)
+                    perm_out[rbase + pos[j]] = (int32_t)s_stage[t];
             }
         }
-    }
+    };
+    if (full)
+        body(std::true_type{});
+    else
+        body(std::false_type{});
 }
 
 // ---------------------------------------------------------------- driver
