@@ -358,17 +358,31 @@ constexpr int kR8Digits = 256;
 
 // Lanes holding the same 8-bit digit as this lane, when every lane of the
 // wave holds a key: the AND over the digit bits of that bit's ballot,
-// complemented where this lane's bit is 0.  Written as m & (ballot ^ e), e
-// all ones for a 0 bit, one three-input bit operation per 32-bit half.
+// complemented where this lane's bit is 0.  Per bit: e = all ones if the bit
+// is 0 (a sign-extended bit field of ~d), the ballot of e == 0, and
+// m &= ballot ^ e for each 32-bit half.  The empty asm statements only hide
+// values from the optimiser (they emit nothing): the ballot then stays a
+// test of e, and each m &= ballot ^ e stays one three-input bit operation
+// instead of being regrouped with the next bit into more operations.
 __device__ __forceinline__ uint64_t peers8_all(uint32_t d) {
-    uint32_t lo = ~0u, hi = ~0u;
-    const uint32_t nd = ~d;
+    const int nd = (int)~d;
+    uint32_t e[8];
+    uint64_t bb[8];
 #pragma unroll
     for (int b = 0; b < 8; ++b) {
-        const uint32_t e = (uint32_t)((int32_t)(nd << (31 - b)) >> 31);
-        const uint64_t bb = __ballot(e == 0);
-        lo &= (uint32_t)bb ^ e;
-        hi &= (uint32_t)(bb >> 32) ^ e;
+        e[b] = (uint32_t)__builtin_amdgcn_sbfe(nd, b, 1);
+        asm("" : "+v"(e[b]));
+    }
+    // all ballots first: each is read well after it is written, so no wait
+    // states go in between
+#pragma unroll
+    for (int b = 0; b < 8; ++b) bb[b] = __ballot(e[b] == 0u);
+    uint32_t lo = ~0u, hi = ~0u;
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+        lo &= (uint32_t)bb[b] ^ e[b];
+        hi &= (uint32_t)(bb[b] >> 32) ^ e[b];
+        asm("" : "+v"(lo), "+v"(hi));
     }
     return ((uint64_t)hi << 32) | lo;
 }
@@ -454,6 +468,15 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_count(
 // chunk's index order is the lane order) with the offsets from the scanned
 // table; rows and tiles as in k_radix8_count, the permutation holding indices
 // within the row.
+// A wave's 16 chunks of 64 source indices straight into LDS, chunk j at
+// lds + 64 j: the immediate offset of an LDS-direct load is added to the
+// global and to the LDS address alike, so one address pair serves all 16.
+template <int... J>
+__device__ __forceinline__ void r8_indices_to_lds(const int32_t* lane_src, int32_t* lds,
+                                                  std::integer_sequence<int, J...>) {
+    (__builtin_amdgcn_global_load_lds((const void*)lane_src, lds, 4, J * kWave * 4, 0), ...);
+}
+
 template <class K, bool HAS_PERM_IN, bool WITH_PERM>
 __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatter(
     const K* keys_in, const int32_t* perm_in, K* keys_out, int32_t* perm_out, int64_t len,
@@ -499,11 +522,17 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
         // nothing and their slots are never read.
         if (WITH_PERM && HAS_PERM_IN) {
             const int32_t* pw = perm_in + rbase + wbase;
+            int32_t* lw = s_pin + w * kR8Chunks * kWave;
+            if (FULL) {
+                // one address pair: the immediate offset moves both sides
+                r8_indices_to_lds(pw + lane, lw, std::make_integer_sequence<int, kR8Chunks>{});
+            } else {
 #pragma unroll
-            for (int j = 0; j < kR8Chunks; ++j)
-                if (in_range(j))
-                    __builtin_amdgcn_global_load_lds((const void*)(pw + j * kWave + lane),
-                                                     s_pin + (w * kR8Chunks + j) * kWave, 4, 0, 0);
+                for (int j = 0; j < kR8Chunks; ++j)
+                    if (in_range(j))
+                        __builtin_amdgcn_global_load_lds((const void*)(pw + j * kWave + lane),
+                                                         lw + j * kWave, 4, 0, 0);
+            }
         }
         // All key loads, then the encoding: applied inside a per-key branch
         // it would make each load wait for the one before.  (Lanes past the
@@ -511,8 +540,10 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
         uint32_t key[kR8Chunks];
 #pragma unroll
         for (int j = 0; j < kR8Chunks; ++j) key[j] = in_range(j) ? (uint32_t)kw[j * kWave + lane] : 0u;
+        if (code.pos | code.neg) {  // only the first pass of signed or float keys
 #pragma unroll
-        for (int j = 0; j < kR8Chunks; ++j) key[j] = code.apply(key[j]);
+            for (int j = 0; j < kR8Chunks; ++j) key[j] = code.apply(key[j]);
+        }
         __syncthreads();
 
         // Rank chunk by chunk.  The peer group's lowest lane adds the group
@@ -570,15 +601,26 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
             if (FULL || (in_range(j) && rank[j] < kR8Tile)) s_stage[rank[j]] = key[j];
         }
         __syncthreads();
-        uint32_t pos[kR8Chunks];
+        // All staged keys, then their positions, then the stores: every LDS
+        // read of the write-out in flight at once.  A position is clamped to
+        // the row (it is inside always; the clamp keeps a corrupted offsets
+        // table from writing out of bounds).
+        const uint32_t last = (uint32_t)(len - 1);  // len <= INT32_MAX
+        uint32_t sk[kR8Chunks], pos[kR8Chunks];
+#pragma unroll
+        for (int j = 0; j < kR8Chunks; ++j) sk[j] = s_stage[threadIdx.x + j * kR8Waves * kWave];
 #pragma unroll
         for (int j = 0; j < kR8Chunks; ++j) {
             const uint32_t t = (uint32_t)threadIdx.x + j * kR8Waves * kWave;
-            const uint32_t sk = s_stage[t];
-            pos[j] = s_off[(sk >> shift) & 255u] + t;
-            // pos < len always; the test guards against a corrupted table
-            if ((FULL || t < valid) && pos[j] < (uint64_t)len) kout[pos[j]] = (K)decode.apply(sk);
+            pos[j] = min(s_off[(sk[j] >> shift) & 255u] + t, last);
         }
+        if (decode.pre | decode.one | decode.zero) {  // only the last pass of signed or float keys
+#pragma unroll
+            for (int j = 0; j < kR8Chunks; ++j) sk[j] = decode.apply(sk[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < kR8Chunks; ++j)
+            if (FULL || threadIdx.x + j * kR8Waves * kWave < valid) kout[pos[j]] = (K)sk[j];
         if (WITH_PERM) {
             __syncthreads();
 #pragma unroll
@@ -588,12 +630,12 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
                 if (FULL || (in_range(j) && rank[j] < kR8Tile)) s_stage[rank[j]] = (uint32_t)pv;
             }
             __syncthreads();
+            int32_t* pout = perm_out + rbase;
 #pragma unroll
-            for (int j = 0; j < kR8Chunks; ++j) {
-                const uint32_t t = (uint32_t)threadIdx.x + j * kR8Waves * kWave;
-                if ((FULL || t < valid) && pos[j] < (uint64_t)len)
-                    perm_out[rbase + pos[j]] = (int32_t)s_stage[t];
-            }
+            for (int j = 0; j < kR8Chunks; ++j) sk[j] = s_stage[threadIdx.x + j * kR8Waves * kWave];
+#pragma unroll
+            for (int j = 0; j < kR8Chunks; ++j)
+                if (FULL || threadIdx.x + j * kR8Waves * kWave < valid) pout[pos[j]] = (int32_t)sk[j];
         }
     };
     if (full)
