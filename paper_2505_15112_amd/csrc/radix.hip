@@ -412,9 +412,6 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_count(
     const K* keys, int64_t len, uint32_t tpr, int shift, bool vec, uint32_t* counts,
     KeyCode code) {
     __shared__ uint32_t s_h[kR8Waves * kR8Sub][kR8Digits];
-    for (int i = threadIdx.x; i < kR8Waves * kR8Sub * kR8Digits; i += kR8Waves * kWave)
-        (&s_h[0][0])[i] = 0;
-    __syncthreads();
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
     uint32_t* h = s_h[w * kR8Sub + (lane & (kR8Sub - 1))];
@@ -422,44 +419,60 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_count(
     const int64_t tstart = (int64_t)tr * kR8Tile;  // within the row
     const K* kr = keys + (int64_t)row * len;
     const int64_t wbase = tstart + (int64_t)w * kR8Chunks * kWave;
-    if (vec && tstart + kR8Tile <= len) {
-        // 16-byte loads: 4 of 32-bit keys or 2 of 16-bit keys per lane
-        constexpr int kPer = 16 / (int)sizeof(K);
-        constexpr int kLoads = kR8Chunks / kPer;
+    const bool fast = vec && tstart + kR8Tile <= len;
+    // The key loads first: clearing the histograms runs under their latency.
+    // Fast path: 16-byte loads, 4 of 32-bit keys or 8 of 16-bit keys each.
+    constexpr int kPer = 16 / (int)sizeof(K);
+    constexpr int kLoads = kR8Chunks / kPer;
+    u32x4 v[kLoads];
+    uint32_t k[kR8Chunks];
+    if (fast) {
         const u32x4* k4 = reinterpret_cast<const u32x4*>(kr + wbase);
-        u32x4 v[kLoads];
 #pragma unroll
         for (int j = 0; j < kLoads; ++j) v[j] = k4[j * kWave + lane];
-#pragma unroll
-        for (int j = 0; j < kLoads; ++j)
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const uint32_t word = v[j][c];
-                if (sizeof(K) == 4) {
-                    atomicAdd(&h[(code.apply(word) >> shift) & 255u], 1u);
-                } else {
-                    atomicAdd(&h[(code.apply(word & 0xFFFFu) >> shift) & 255u], 1u);
-                    atomicAdd(&h[(code.apply(word >> 16) >> shift) & 255u], 1u);
-                }
-            }
     } else {
-        // every load issued before the first atomic needs one
-        uint32_t k[kR8Chunks];
 #pragma unroll
         for (int j = 0; j < kR8Chunks; ++j) {
             const int64_t i = wbase + j * kWave + lane;
             k[j] = i < len ? (uint32_t)kr[i] : 0u;
         }
-#pragma unroll
-        for (int j = 0; j < kR8Chunks; ++j)
-            if (wbase + j * kWave + lane < len)
-                atomicAdd(&h[(code.apply(k[j]) >> shift) & 255u], 1u);
     }
+    for (int i = threadIdx.x; i < kR8Waves * kR8Sub * kR8Digits; i += kR8Waves * kWave)
+        (&s_h[0][0])[i] = 0;
+    __syncthreads();
+    // the key encoding (first pass of signed or float keys only) is left out
+    // of the loop when it is the identity
+    auto count_all = [&](auto coded_c) {
+        constexpr bool CODED = decltype(coded_c)::value;
+        auto enc = [&](uint32_t x) { return CODED ? code.apply(x) : x; };
+        if (fast) {
+#pragma unroll
+            for (int j = 0; j < kLoads; ++j)
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const uint32_t word = v[j][c];
+                    if (sizeof(K) == 4) {
+                        atomicAdd(&h[(enc(word) >> shift) & 255u], 1u);
+                    } else {
+                        atomicAdd(&h[(enc(word & 0xFFFFu) >> shift) & 255u], 1u);
+                        atomicAdd(&h[(enc(word >> 16) >> shift) & 255u], 1u);
+                    }
+                }
+        } else {
+#pragma unroll
+            for (int j = 0; j < kR8Chunks; ++j)
+                if (wbase + j * kWave + lane < len) atomicAdd(&h[(enc(k[j]) >> shift) & 255u], 1u);
+        }
+    };
+    if (code.pos | code.neg)
+        count_all(std::true_type{});
+    else
+        count_all(std::false_type{});
     __syncthreads();
     if (threadIdx.x < kR8Digits) {
         uint32_t t = 0;
 #pragma unroll
-        for (int k = 0; k < kR8Waves * kR8Sub; ++k) t += s_h[k][threadIdx.x];
+        for (int q = 0; q < kR8Waves * kR8Sub; ++q) t += s_h[q][threadIdx.x];
         counts[((int64_t)row * kR8Digits + threadIdx.x) * tpr + tr] = t;
     }
 }
