@@ -346,10 +346,11 @@ struct KeyDecode {
 // 4-bit pass, with 256 digits.  Ranking cannot give every digit a lane, so
 // each wave keeps its digit counts in LDS: per chunk of 64 keys, the lanes
 // holding one digit (found with 8 ballots) are a peer group, the group's
-// lowest lane adds the group size to the wave's count of that digit and
-// reads the previous count (one LDS atomic per group, never two lanes on one
-// word), and a key's rank is that count plus its peers in lower lanes.  The
-// wave's atomics execute in order, so ranks follow the index order.
+// lowest lane adds the group size to the wave's count of that digit (one LDS
+// add per group, never two lanes on one word), every lane reads the count
+// back, and a key's rank is that count minus the group size plus its peers
+// in lower lanes.  A wave's LDS operations execute in issue order, so ranks
+// follow the index order.
 constexpr int kR8Waves = 8;
 constexpr int kR8Chunks = 16;
 constexpr int64_t kR8Tile = kR8Waves * kR8Chunks * kWave;  // 8192 keys
