@@ -144,6 +144,15 @@ __device__ __forceinline__ uint32_t lane_shfl(uint32_t v, int src_lane) {
     return (uint32_t)__builtin_amdgcn_ds_bpermute(src_lane << 2, (int)v);
 }
 
+// A wave's chunks of 64 source indices straight into LDS, chunk j at
+// lds + 64 j: the immediate offset of an LDS-direct load is added to the
+// global and to the LDS address alike, so one address pair serves them all.
+template <int... J>
+__device__ __forceinline__ void indices_to_lds(const int32_t* lane_src, int32_t* lds,
+                                               std::integer_sequence<int, J...>) {
+    (__builtin_amdgcn_global_load_lds((const void*)lane_src, lds, 4, J * kWave * 4, 0), ...);
+}
+
 // Per-tile digit counts: counts[d * ntiles + tile] (digit-major, so the
 // spine kernel scans contiguous columns).  Order does not matter here, so the
 // keys are read with 16-byte loads when aligned.
@@ -157,6 +166,29 @@ __global__ __launch_bounds__(kR4Waves* kWave) LS_OCCUPANCY4 void k_radix4_count(
     const int64_t tbase = (int64_t)blockIdx.x * kR4Tile;
     const bool full = tbase + kR4Tile <= n;
     uint32_t run = 0;  // lane L < 16: this wave's count of digit L
+    // every lane holds a key: the lanes holding digit lane & 15 are the AND
+    // over the digit bits of ballot ^ el (el: all ones where lane & 15 has
+    // the bit clear), ballots first (see digit4_masks)
+    uint32_t el[4];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+        el[b] = (uint32_t)__builtin_amdgcn_sbfe((int)~(uint32_t)lane, b, 1);
+        asm("" : "+v"(el[b]));
+    }
+    auto count64_all = [&](uint32_t key) {
+        const uint32_t d = (key >> shift) & 15u;
+        uint64_t bb[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) bb[b] = __ballot((d >> b) & 1u);
+        uint32_t lo = ~0u, hi = ~0u;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            lo &= (uint32_t)bb[b] ^ el[b];
+            hi &= (uint32_t)(bb[b] >> 32) ^ el[b];
+            asm("" : "+v"(lo), "+v"(hi));
+        }
+        run += (uint32_t)__builtin_popcount(lo) + (uint32_t)__builtin_popcount(hi);
+    };
     auto count64 = [&](uint32_t key, bool ok) {
         const uint32_t d = (key >> shift) & 15u;
         const uint64_t valid = __ballot(ok);
@@ -173,10 +205,10 @@ __global__ __launch_bounds__(kR4Waves* kWave) LS_OCCUPANCY4 void k_radix4_count(
         for (int j = 0; j < kR4Chunks / 4; ++j) v[j] = k4[j * kWave + lane];
 #pragma unroll
         for (int j = 0; j < kR4Chunks / 4; ++j) {
-            count64(v[j].x, true);
-            count64(v[j].y, true);
-            count64(v[j].z, true);
-            count64(v[j].w, true);
+            count64_all(v[j].x);
+            count64_all(v[j].y);
+            count64_all(v[j].z);
+            count64_all(v[j].w);
         }
     } else {
         const int64_t wbase = tbase + (int64_t)w * kR4Chunks * kWave;
@@ -197,6 +229,41 @@ __global__ __launch_bounds__(kR4Waves* kWave) LS_OCCUPANCY4 void k_radix4_count(
     }
 }
 
+// Peer masks of a 4-bit digit when every lane of the wave holds a key: the
+// lanes whose digit equals this lane's digit d (`same`) and the lanes whose
+// digit equals this lane's number mod 16 (`of_lane`, for the chunk's count of
+// that digit).  Per digit bit b: the ballot of the lanes with the bit set,
+// and m &= ballot ^ e with e all ones where the wanted digit has the bit
+// clear (ne: this lane's digit, el: its lane number's, a sign-extended bit
+// field of the complement).  All ballots first, so that no read of a ballot
+// waits on its write; the empty asm statements only hide values from the
+// optimiser (they emit nothing), which keeps each m &= ballot ^ e one
+// three-input bit operation.
+__device__ __forceinline__ void digit4_masks(uint32_t d, const uint32_t (&el)[4], uint64_t& same,
+                                             uint64_t& of_lane) {
+    const int nd = (int)~d;
+    uint32_t ne[4];
+    uint64_t bb[4];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+        ne[b] = (uint32_t)__builtin_amdgcn_sbfe(nd, b, 1);
+        asm("" : "+v"(ne[b]));
+    }
+#pragma unroll
+    for (int b = 0; b < 4; ++b) bb[b] = __ballot(ne[b] == 0u);
+    uint32_t slo = ~0u, shi = ~0u, llo = ~0u, lhi = ~0u;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+        slo &= (uint32_t)bb[b] ^ ne[b];
+        shi &= (uint32_t)(bb[b] >> 32) ^ ne[b];
+        llo &= (uint32_t)bb[b] ^ el[b];
+        lhi &= (uint32_t)(bb[b] >> 32) ^ el[b];
+        asm("" : "+v"(slo), "+v"(shi), "+v"(llo), "+v"(lhi));
+    }
+    same = ((uint64_t)shi << 32) | slo;
+    of_lane = ((uint64_t)lhi << 32) | llo;
+}
+
 // Rank and scatter one tile of 8192 keys (one key per lane per chunk, so the
 // chunk's index order is the lane order) with the offsets from the spine.
 template <bool HAS_PERM_IN, bool WITH_PERM>
@@ -205,8 +272,11 @@ __global__ __launch_bounds__(kR4Waves* kWave) LS_OCCUPANCY4 void k_radix4_scatte
     int64_t n, int shift, uint32_t* offsets, uint32_t ntiles) {
     __shared__ uint32_t s_cnt[kR4Waves][16];
     __shared__ uint32_t s_tstart[16];  // first slot of digit d in the tile's digit order
-    __shared__ uint32_t s_gbase[16];   // global position of that slot
+    __shared__ uint32_t s_off[16];     // global position minus tile slot, per digit
     __shared__ uint32_t s_stage[kR4Tile];
+    // the tile's source indices, loaded straight into LDS at the start (in
+    // the tile's index order) so that they cost no registers while ranking
+    __shared__ int32_t s_pin[WITH_PERM && HAS_PERM_IN ? kR4Tile : 1];
 
     const int64_t tile = xcd_tile(blockIdx.x, gridDim.x);
     const int lane = lane_id();
@@ -216,105 +286,148 @@ __global__ __launch_bounds__(kR4Waves* kWave) LS_OCCUPANCY4 void k_radix4_scatte
     const bool full = tbase + kR4Tile <= n;
     const uint32_t valid = full ? (uint32_t)kR4Tile : (uint32_t)(n - tbase);
 
-    uint32_t key[kR4Chunks];
-    int32_t perm[kR4Chunks];
-#pragma unroll
-    for (int j = 0; j < kR4Chunks; ++j) {
-        const int64_t i = wbase + j * kWave + lane;
-        const bool ok = full || i < n;
-        key[j] = ok ? keys_in[i] : 0u;
-        if (WITH_PERM) perm[j] = HAS_PERM_IN ? (ok ? perm_in[i] : 0) : (int32_t)i;
-    }
+    uint32_t gbase = 0;  // lane d < 16 of wave 0: global position of the tile's first digit-d key
     if (threadIdx.x < 16) {
         uint32_t* o = offsets + (int64_t)threadIdx.x * ntiles + tile;
-        s_gbase[threadIdx.x] = *o;
+        gbase = *o;
         *o = 0;  // offsets can reach 2^30 and more: leave the workspace word zero
     }
 
-    // Per-chunk digit counts first (independent), then the stable rank of
-    // each key: its digit's count in the wave's earlier chunks plus the lanes
-    // below it holding the same digit.
-    uint32_t cnt[kR4Chunks];
-    uint32_t rank[kR4Chunks];
+    // The tile body, compiled twice: for full tiles (every lane holds a key,
+    // no per-lane bounds) and for the last, ragged tile.
+    auto body = [&](auto full_c) {
+        constexpr bool FULL = decltype(full_c)::value;
+        auto in_range = [&](int j) { return FULL || wbase + j * kWave + lane < n; };
+        const uint32_t* kw = keys_in + wbase;
+        // Source indices first, straight into LDS; lanes past the end load
+        // nothing and their slots are never read.
+        if (WITH_PERM && HAS_PERM_IN) {
+            const int32_t* pw = perm_in + wbase;
+            int32_t* lw = s_pin + w * kR4Chunks * kWave;
+            if (FULL) {
+                indices_to_lds(pw + lane, lw, std::make_integer_sequence<int, kR4Chunks>{});
+            } else {
 #pragma unroll
-    for (int j = 0; j < kR4Chunks; ++j) {
-        const int64_t i = wbase + j * kWave + lane;
-        const bool ok = full || i < n;
-        const uint32_t d = (key[j] >> shift) & 15u;
-        const uint64_t valid_l = __ballot(ok);
-        const uint64_t b0 = __ballot(ok && (d & 1));
-        const uint64_t b1 = __ballot(ok && (d & 2));
-        const uint64_t b2 = __ballot(ok && (d & 4));
-        const uint64_t b3 = __ballot(ok && (d & 8));
-        rank[j] = lanes_below(digit_lanes(d, valid_l, b0, b1, b2, b3));
-        cnt[j] = (uint32_t)__builtin_popcountll(digit_lanes((uint32_t)(lane & 15), valid_l, b0, b1, b2, b3));
-    }
-    uint32_t run = 0;
-#pragma unroll
-    for (int j = 0; j < kR4Chunks; ++j) {
-        const uint32_t d = (key[j] >> shift) & 15u;
-        rank[j] += lane_shfl(run, (int)d);
-        run += cnt[j];
-    }
-    if (lane < 16) s_cnt[w][lane] = run;
-    __syncthreads();
-
-    // lanes 0..15: count of digit `lane` in earlier waves, and the tile total
-    uint32_t wofs = 0, tot = 0;
-#pragma unroll
-    for (int k = 0; k < kR4Waves; ++k) {
-        const uint32_t c = s_cnt[k][lane & 15];
-        if (k < w) wofs += c;
-        tot += c;
-    }
-    if (w == 0) {
-        const uint32_t t16 = lane < 16 ? tot : 0u;
-        const uint32_t tstart = wave_incl_scan(t16) - t16;
-        if (lane < 16) s_tstart[lane] = tstart;
-    }
-    __syncthreads();
-
-    // Sort the tile by digit in LDS (slot = digit start + earlier waves +
-    // rank), then write each digit's run with consecutive threads.
-    const uint32_t wstart = (lane < 16 ? s_tstart[lane] : 0u) + wofs;  // lane d: this wave's slot 0 for d
-    uint32_t slot[kR4Chunks];
-#pragma unroll
-    for (int j = 0; j < kR4Chunks; ++j) {
-        const uint32_t d = (key[j] >> shift) & 15u;
-        slot[j] = lane_shfl(wstart, (int)d) + rank[j];
-        const int64_t i = wbase + j * kWave + lane;
-        if ((full || i < n) && slot[j] < kR4Tile) s_stage[slot[j]] = key[j];
-    }
-    __syncthreads();
-    uint32_t skey[kR4Chunks];
-#pragma unroll
-    for (int j = 0; j < kR4Chunks; ++j) {
-        const uint32_t t = (uint32_t)threadIdx.x + j * kR4Waves * kWave;
-        skey[j] = s_stage[t];
-        if (t < valid) {
-            const uint32_t d = (skey[j] >> shift) & 15u;
-            const uint32_t pos = s_gbase[d] + (t - s_tstart[d]);
-            if (pos < (uint64_t)n) keys_out[pos] = skey[j];  // pos < n always; guards a bad count
-        }
-    }
-    if (WITH_PERM) {
-        __syncthreads();
-#pragma unroll
-        for (int j = 0; j < kR4Chunks; ++j) {
-            const int64_t i = wbase + j * kWave + lane;
-            if ((full || i < n) && slot[j] < kR4Tile) s_stage[slot[j]] = (uint32_t)perm[j];
-        }
-        __syncthreads();
-#pragma unroll
-        for (int j = 0; j < kR4Chunks; ++j) {
-            const uint32_t t = (uint32_t)threadIdx.x + j * kR4Waves * kWave;
-            if (t < valid) {
-                const uint32_t d = (skey[j] >> shift) & 15u;
-                const uint32_t pos = s_gbase[d] + (t - s_tstart[d]);
-                if (pos < (uint64_t)n) perm_out[pos] = (int32_t)s_stage[t];
+                for (int j = 0; j < kR4Chunks; ++j)
+                    if (in_range(j))
+                        __builtin_amdgcn_global_load_lds((const void*)(pw + j * kWave + lane),
+                                                         lw + j * kWave, 4, 0, 0);
             }
         }
-    }
+        uint32_t key[kR4Chunks];
+#pragma unroll
+        for (int j = 0; j < kR4Chunks; ++j) key[j] = in_range(j) ? kw[j * kWave + lane] : 0u;
+
+        // Per-chunk digit counts first (independent), then the stable rank of
+        // each key: its digit's count in the wave's earlier chunks plus the
+        // lanes below it holding the same digit.
+        uint32_t cnt[kR4Chunks];
+        uint32_t rank[kR4Chunks];
+        if (FULL) {
+            uint32_t el[4];
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                el[b] = (uint32_t)__builtin_amdgcn_sbfe((int)~(uint32_t)lane, b, 1);
+                asm("" : "+v"(el[b]));
+            }
+#pragma unroll
+            for (int j = 0; j < kR4Chunks; ++j) {
+                uint64_t same, of_lane;
+                digit4_masks((key[j] >> shift) & 15u, el, same, of_lane);
+                rank[j] = lanes_below(same);
+                cnt[j] = (uint32_t)__builtin_popcountll(of_lane);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < kR4Chunks; ++j) {
+                const bool ok = in_range(j);
+                const uint32_t d = (key[j] >> shift) & 15u;
+                const uint64_t valid_l = __ballot(ok);
+                const uint64_t b0 = __ballot(ok && (d & 1));
+                const uint64_t b1 = __ballot(ok && (d & 2));
+                const uint64_t b2 = __ballot(ok && (d & 4));
+                const uint64_t b3 = __ballot(ok && (d & 8));
+                rank[j] = lanes_below(digit_lanes(d, valid_l, b0, b1, b2, b3));
+                cnt[j] = (uint32_t)__builtin_popcountll(
+                    digit_lanes((uint32_t)(lane & 15), valid_l, b0, b1, b2, b3));
+            }
+        }
+        uint32_t run = 0;
+#pragma unroll
+        for (int j = 0; j < kR4Chunks; ++j) {
+            const uint32_t d = (key[j] >> shift) & 15u;
+            rank[j] += lane_shfl(run, (int)d);
+            run += cnt[j];
+        }
+        if (lane < 16) s_cnt[w][lane] = run;
+        // the index loads were issued first: long done, and no stores yet
+        if (WITH_PERM && HAS_PERM_IN) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+
+        // lanes 0..15: count of digit `lane` in earlier waves, and the tile total
+        uint32_t wofs = 0, tot = 0;
+#pragma unroll
+        for (int k = 0; k < kR4Waves; ++k) {
+            const uint32_t c = s_cnt[k][lane & 15];
+            if (k < w) wofs += c;
+            tot += c;
+        }
+        if (w == 0) {
+            const uint32_t t16 = lane < 16 ? tot : 0u;
+            const uint32_t tstart = wave_incl_scan(t16) - t16;
+            if (lane < 16) {
+                s_tstart[lane] = tstart;
+                s_off[lane] = gbase - tstart;
+            }
+        }
+        __syncthreads();
+
+        // Sort the tile by digit in LDS (slot = digit start + earlier waves +
+        // rank), then write each digit's run with consecutive threads.
+        const uint32_t wstart = (lane < 16 ? s_tstart[lane] : 0u) + wofs;  // lane d: this wave's slot 0 for d
+        uint32_t slot[kR4Chunks];
+#pragma unroll
+        for (int j = 0; j < kR4Chunks; ++j) {
+            const uint32_t d = (key[j] >> shift) & 15u;
+            slot[j] = lane_shfl(wstart, (int)d) + rank[j];
+            if (FULL || (in_range(j) && slot[j] < kR4Tile)) s_stage[slot[j]] = key[j];
+        }
+        __syncthreads();
+        // All staged keys, then their positions, then the stores.  A position
+        // is clamped to the array (it is inside always; the clamp keeps a
+        // corrupted offsets table from writing out of bounds).
+        const uint32_t last = (uint32_t)(n - 1);  // n <= INT32_MAX
+        uint32_t sk[kR4Chunks], pos[kR4Chunks];
+#pragma unroll
+        for (int j = 0; j < kR4Chunks; ++j) sk[j] = s_stage[threadIdx.x + j * kR4Waves * kWave];
+#pragma unroll
+        for (int j = 0; j < kR4Chunks; ++j)
+            pos[j] = min(s_off[(sk[j] >> shift) & 15u] + (uint32_t)threadIdx.x + j * kR4Waves * kWave,
+                         last);
+#pragma unroll
+        for (int j = 0; j < kR4Chunks; ++j)
+            if (FULL || threadIdx.x + j * kR4Waves * kWave < valid) keys_out[pos[j]] = sk[j];
+        if (WITH_PERM) {
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < kR4Chunks; ++j) {
+                const int32_t pv = HAS_PERM_IN ? s_pin[(w * kR4Chunks + j) * kWave + lane]
+                                               : (int32_t)(wbase + j * kWave + lane);
+                if (FULL || (in_range(j) && slot[j] < kR4Tile)) s_stage[slot[j]] = (uint32_t)pv;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < kR4Chunks; ++j) sk[j] = s_stage[threadIdx.x + j * kR4Waves * kWave];
+#pragma unroll
+            for (int j = 0; j < kR4Chunks; ++j)
+                if (FULL || threadIdx.x + j * kR4Waves * kWave < valid)
+                    perm_out[pos[j]] = (int32_t)sk[j];
+        }
+    };
+    if (full)
+        body(std::true_type{});
+    else
+        body(std::false_type{});
 }
 
 // ---------------------------------------------------------------- key codes
@@ -482,15 +595,6 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_count(
 // chunk's index order is the lane order) with the offsets from the scanned
 // table; rows and tiles as in k_radix8_count, the permutation holding indices
 // within the row.
-// A wave's 16 chunks of 64 source indices straight into LDS, chunk j at
-// lds + 64 j: the immediate offset of an LDS-direct load is added to the
-// global and to the LDS address alike, so one address pair serves all 16.
-template <int... J>
-__device__ __forceinline__ void r8_indices_to_lds(const int32_t* lane_src, int32_t* lds,
-                                                  std::integer_sequence<int, J...>) {
-    (__builtin_amdgcn_global_load_lds((const void*)lane_src, lds, 4, J * kWave * 4, 0), ...);
-}
-
 template <class K, bool HAS_PERM_IN, bool WITH_PERM>
 __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatter(
     const K* keys_in, const int32_t* perm_in, K* keys_out, int32_t* perm_out, int64_t len,
@@ -539,7 +643,7 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_scatte
             int32_t* lw = s_pin + w * kR8Chunks * kWave;
             if (FULL) {
                 // one address pair: the immediate offset moves both sides
-                r8_indices_to_lds(pw + lane, lw, std::make_integer_sequence<int, kR8Chunks>{});
+                indices_to_lds(pw + lane, lw, std::make_integer_sequence<int, kR8Chunks>{});
             } else {
 #pragma unroll
                 for (int j = 0; j < kR8Chunks; ++j)
