@@ -64,6 +64,16 @@ __device__ __forceinline__ void load_vec(const In* p, T (&out)[V]) {
     for (int i = 0; i < V; ++i) out[i] = Conv<In, T>::f(e[i]);
 }
 
+// The same for 16 bytes of 32-bit elements with a nontemporal load: for data
+// read exactly once (the 1-D scan's input), which then does not displace
+// other lines in the caches.
+template <class T>
+__device__ __forceinline__ void load_vec_nt(const T* p, T (&out)[4]) {
+    static_assert(sizeof(T) == 4, "16 bytes of 32-bit elements");
+    const u32x4 r = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    __builtin_memcpy(out, &r, 16);
+}
+
 // Aligned vector store of V 32-bit elements (V/4 16-byte stores).
 template <class T, int V>
 __device__ __forceinline__ void store_vec(T* p, const T (&v)[V]) {
