@@ -63,7 +63,7 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_rows_lookback
     const int64_t base = seg * TileT::kElems;
 
     T v[TileT::J][TileT::V];
-    TileT::template load<VEC>(x + row * len, len, base, v);
+    TileT::template load<VEC, true>(x + row * len, len, base, v);  // read once: nontemporal
     const T wtot = TileT::template wave_scan<EXCL>(v);
     T wofs;
     const T agg = TileT::combine_waves(wtot, s_wtot, &wofs);
@@ -233,7 +233,9 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp(
     const float* xr = probs + row * len;
     {
         float v[TileT::J][TileT::V];
-        TileT::template load<VEC>(xr, len, (int64_t)seg * TileT::kElems, v);
+        // weighted sampling reads the rows once (nontemporal); the top-p modes
+        // re-read a tile or two at the end, which measured faster cached
+        TileT::template load<VEC, MODE == ToppMode::Weighted>(xr, len, (int64_t)seg * TileT::kElems, v);
         float wofs;
         const float agg = TileT::combine_waves(wave_sum(TileT::lane_sum(v)), s_wtot, &wofs);
         if (threadIdx.x == 0) {

@@ -193,7 +193,7 @@ __global__ __launch_bounds__(8 * kWave) LS_OCCUPANCY4 void k_scan_lookback_lds(
                                          lw + c * kWave, 16, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int j = 0; j < J; ++j) load_vec_nt<T>(xw + j * kWave * 4 + lane * 4, v[j]);
+    for (int j = 0; j < J; ++j) load_vec<T, T, 4, true>(xw + j * kWave * 4 + lane * 4, v[j]);
     __builtin_amdgcn_sched_barrier(0);
     // register chunks: the tile scan of Tile::wave_scan
     const T run = Tile<T, T, 4, J, G::W>::template wave_scan<EXCL>(v);
@@ -258,7 +258,7 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_rss_reduce(co
     __shared__ T s_wtot[TileT::WAVES];
     const int64_t base = (int64_t)blockIdx.x * TileT::kElems;
     T v[TileT::J][TileT::V];
-    TileT::template load<VEC>(x, n, base, v);
+    TileT::template load<VEC, true>(x, n, base, v);
     const T wtot = wave_sum(TileT::lane_sum(v));
     T wofs;
     const T agg = TileT::combine_waves(wtot, s_wtot, &wofs);
@@ -312,7 +312,7 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_rss_rescan(co
     const int64_t base = (int64_t)blockIdx.x * TileT::kElems;
     const T carry = partial[blockIdx.x];
     T v[TileT::J][TileT::V];
-    TileT::template load<VEC>(x, n, base, v);
+    TileT::template load<VEC, true>(x, n, base, v);
     const T wtot = TileT::template wave_scan<false>(v);
     T wofs;
     TileT::combine_waves(wtot, s_wtot, &wofs);  // barrier: every thread has read `carry`

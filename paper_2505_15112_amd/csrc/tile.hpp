@@ -43,13 +43,15 @@ struct Conv<uint8_t, uint32_t> {  // unsigned byte value
     __device__ static uint32_t f(uint8_t v) { return v; }
 };
 
-// Aligned vector load of V elements of In, converted to T.
-template <class In, class T, int V>
+// Aligned vector load of V elements of In, converted to T.  NT: 16-byte
+// loads are nontemporal (data read once, kept out of the caches' way).
+template <class In, class T, int V, bool NT = false>
 __device__ __forceinline__ void load_vec(const In* p, T (&out)[V]) {
     constexpr int kBytes = V * (int)sizeof(In);
     In e[V];
     if constexpr (kBytes == 16) {
-        const u32x4 r = *reinterpret_cast<const u32x4*>(p);
+        const u32x4 r = NT ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p))
+                           : *reinterpret_cast<const u32x4*>(p);
         __builtin_memcpy(e, &r, 16);
     } else if constexpr (kBytes == 8) {
         const u32x2 r = *reinterpret_cast<const u32x2*>(p);
@@ -62,16 +64,6 @@ __device__ __forceinline__ void load_vec(const In* p, T (&out)[V]) {
     }
 #pragma unroll
     for (int i = 0; i < V; ++i) out[i] = Conv<In, T>::f(e[i]);
-}
-
-// The same for 16 bytes of 32-bit elements with a nontemporal load: for data
-// read exactly once (the 1-D scan's input), which then does not displace
-// other lines in the caches.
-template <class T>
-__device__ __forceinline__ void load_vec_nt(const T* p, T (&out)[4]) {
-    static_assert(sizeof(T) == 4, "16 bytes of 32-bit elements");
-    const u32x4 r = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-    __builtin_memcpy(out, &r, 16);
 }
 
 // Aligned vector store of V 32-bit elements (V/4 16-byte stores).
@@ -109,12 +101,13 @@ struct Tile {
     __device__ static int64_t offset(int64_t base, int j) { return base + lane_offset(j); }
 
     // Load the tile starting at `base`; elements at or past n read as zero.
-    template <bool VEC>
+    // NT: nontemporal 16-byte loads (see load_vec).
+    template <bool VEC, bool NT = false>
     __device__ static void load(const In* x, int64_t n, int64_t base, T (&v)[J][V]) {
         const In* xt = x + base;  // wave-uniform
         if (VEC && base + kElems <= n) {  // uniform: all vector loads issued back to back
 #pragma unroll
-            for (int j = 0; j < J; ++j) load_vec<In, T, V>(xt + lane_offset(j), v[j]);
+            for (int j = 0; j < J; ++j) load_vec<In, T, V, NT>(xt + lane_offset(j), v[j]);
         } else {
             // Ragged last tile (or unaligned data): per chunk, a lane with all
             // V elements in range loads them without per-element tests (one
@@ -127,7 +120,7 @@ struct Tile {
                 const int32_t rem = valid - off;
                 if (rem >= V) {  // one branch per chunk, not one predicate per element
                     if (VEC) {
-                        load_vec<In, T, V>(xt + off, v[j]);
+                        load_vec<In, T, V, NT>(xt + off, v[j]);
                     } else {
 #pragma unroll
                         for (int e = 0; e < V; ++e) v[j][e] = Conv<In, T>::f(xt[off + e]);
