@@ -83,7 +83,7 @@ __global__ __launch_bounds__(WAVES* kWave) LS_OCCUPANCY4 void k_compact(
         for (int j = 0; j < CHUNKS; ++j)
             kept[j] = nonzero_bytes(*reinterpret_cast<const uint32_t*>(mask + offset(j)));
 #pragma unroll
-        for (int j = 0; j < CHUNKS; ++j) load_vec<float, float, 4>(x + offset(j), xv[j]);
+        for (int j = 0; j < CHUNKS; ++j) load_vec<float, float, 4, true>(x + offset(j), xv[j]);
     } else {
 #pragma unroll
         for (int j = 0; j < CHUNKS; ++j) {
@@ -268,10 +268,10 @@ __global__ __launch_bounds__(kSWaves* kWave) LS_OCCUPANCY4 void k_split(
                 fl[j] = nonzero_bytes(*reinterpret_cast<const uint32_t*>(flags + offset(j)));
         }
 #pragma unroll
-        for (int j = 0; j < CHUNKS; ++j) load_vec<uint32_t, uint32_t, 4>(keys + offset(j), k[j]);
+        for (int j = 0; j < CHUNKS; ++j) load_vec<uint32_t, uint32_t, 4, true>(keys + offset(j), k[j]);
         if (HAS_IDX_IN) {
 #pragma unroll
-            for (int j = 0; j < CHUNKS; ++j) load_vec<int32_t, int32_t, 4>(idx_in + offset(j), iv[j]);
+            for (int j = 0; j < CHUNKS; ++j) load_vec<int32_t, int32_t, 4, true>(idx_in + offset(j), iv[j]);
         }
     } else {
 #pragma unroll
