@@ -166,7 +166,10 @@ __global__ __launch_bounds__(kR4Waves* kWave) LS_OCCUPANCY4 void k_radix4_count(
     __shared__ uint32_t s_cnt[kR4Waves][16];
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
-    const int64_t tbase = (int64_t)blockIdx.x * kR4Tile;
+    // tiles dealt XCD-aware, as in the scatter: neighbouring tiles' count words
+    // share cache lines, which then merge in one L2
+    const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);
+    const int64_t tbase = (int64_t)tile * kR4Tile;
     const bool full = tbase + kR4Tile <= n;
     uint32_t run = 0;  // lane L < 16: this wave's count of digit L
     // every lane holds a key: the lanes holding digit lane & 15 are the AND
@@ -228,7 +231,7 @@ __global__ __launch_bounds__(kR4Waves* kWave) LS_OCCUPANCY4 void k_radix4_count(
         uint32_t t = 0;
 #pragma unroll
         for (int k = 0; k < kR4Waves; ++k) t += s_cnt[k][threadIdx.x];
-        counts[(int64_t)threadIdx.x * ntiles + blockIdx.x] = t;
+        counts[(int64_t)threadIdx.x * ntiles + tile] = t;
     }
 }
 
@@ -533,7 +536,11 @@ __global__ __launch_bounds__(kR8Waves* kWave) LS_OCCUPANCY4 void k_radix8_count(
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
     uint32_t* h = s_h[w * kR8Sub + (lane & (kR8Sub - 1))];
-    const uint32_t row = blockIdx.x / tpr, tr = blockIdx.x - row * tpr;
+    // tiles dealt XCD-aware, as in the scatter: neighbouring tiles' count words
+    // share cache lines, which then merge in one L2 (dealt round-robin by
+    // block index they went to HBM as 8x the table's bytes)
+    const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);
+    const uint32_t row = tile / tpr, tr = tile - row * tpr;
     const int64_t tstart = (int64_t)tr * kR8Tile;  // within the row
     const K* kr = keys + (int64_t)row * len;
     const int64_t wbase = tstart + (int64_t)w * kR8Chunks * kWave;
