@@ -10,8 +10,9 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  *  - Pointers named x, y, keys, mask, out, ... and every *_dev pointer are
- *    DEVICE pointers owned by the caller.  The library keeps no device memory
- *    of its own between calls and never allocates.
+ *    DEVICE pointers owned by the caller.  The library never allocates;
+ *    its only device memory is the static workspace of
+ *    scan_inclusive_i32_noalloc.
  *  - Arrays are dense and contiguous (row-major for rows x len matrices).
  *    Element alignment is enough; 16-byte aligned arrays take the vector path.
  *  - ws / ws_bytes: caller-owned device workspace of at least the size that
@@ -327,6 +328,27 @@ int topp_sample_f32(const float* probs, const float* theta_dev, float p, int32_t
 int topk_rows_f32(const float* x, float* values_out, int32_t* idx_out, int64_t rows, int64_t len,
                   int64_t k, int largest, void* scratch, size_t scratch_bytes, void* ws,
                   size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * inclusive int32 scan of scan_inclusive_i32, same result, same kernels,
+ * but without a workspace argument.  Its workspace is a 4 MiB + 256 B array
+ * in the library's own device memory, one per GPU, set up by the first call
+ * on each device (its address looked up, then zero-filled by a kernel on
+ * `stream`, so make that first call outside graph capture or accept that a
+ * captured graph re-zeroes it on every replay) and held until the process
+ * ends.  The call itself allocates nothing (no hipMalloc, no library
+ * allocation).  n <= LIBSCAN_NOALLOC_MAX_N (2^31) elements, else
+ * LIBSCAN_ERANGE; other argument checks as scan_inclusive_i32 (x == y
+ * allowed); LIBSCAN_EHIP if the array cannot be set up.  x, y and stream
+ * must belong to the current device.  Every call on one GPU shares that
+ * GPU's array: calls that may overlap on one GPU (different streams, other
+ * threads) race and give wrong results; serialise them, or use the
+ * workspace entry points.
+ * ------------------------------------------------------------------------ */
+#define LIBSCAN_NOALLOC_MAX_N (INT64_C(1) << 31)
+int scan_inclusive_i32_noalloc(const int32_t* x, int32_t* y, int64_t n, void* stream);
 
 /* Scratch bytes (see topp_sample_f32) that op needs for rows x len (k: the
  * top-k count, else ignored).  Writes *bytes and returns LIBSCAN_OK, or

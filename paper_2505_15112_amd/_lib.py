@@ -59,6 +59,7 @@ SIGNATURES = {
                                _p]),
     "libscan_scratch_bytes": (_int, [_int, _i64, _i64, _i64, ctypes.POINTER(_sz)]),
     "topk_rows_f32": (_int, [_p, _p, _p, _i64, _i64, _i64, _int, _p, _sz, _p, _sz, _p]),
+    "scan_inclusive_i32_noalloc": (_int, [_p, _p, _i64, _p]),
 }
 
 OK, EINVAL, ENOSPACE, EHIP, ERANGE = 0, -1, -2, -3, -4
