@@ -63,6 +63,24 @@ const char* libscan_status_string(int status);
  */
 int libscan_workspace_init(void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * The workspace's error word (Section 2.1's decoupled look-back waits on
+ * other workgroups; here every such wait is bounded).  Kernels set it to 1,
+ * and carry on with unspecified outputs instead of hanging, when a bounded
+ * wait for another workgroup gives up or a tile ticket lies outside the
+ * launch: what a workspace that was not zero-filled before its first use,
+ * was written by something other than libscan, or was shared by calls that
+ * ran concurrently leads to.  It stays set until reset.  This enqueues on
+ * stream a copy of the word into error_dev (device, one int32: 0 = every call
+ * since the last reset ran its protocol to the end) and, when reset != 0,
+ * clears it; it allocates nothing and does not synchronise (read error_dev
+ * after the stream has reached it).  ws 16-byte aligned and at least 256
+ * bytes (LIBSCAN_ENOSPACE otherwise), error_dev 4-byte aligned and outside
+ * the workspace header, else LIBSCAN_EINVAL.
+ */
+int libscan_workspace_error(void* ws, size_t ws_bytes, int32_t* error_dev, int reset,
+                            void* stream);
+
 /* Operation codes for libscan_workspace_bytes. */
 #define LIBSCAN_OP_SCAN 1     /* every 1-D scan_* entry point (look-back) */
 #define LIBSCAN_OP_SCAN_RSS 2 /* scan_inclusive_rss_* (reduce-then-scan) */

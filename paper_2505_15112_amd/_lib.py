@@ -27,6 +27,7 @@ SIGNATURES = {
     "libscan_status_string": (ctypes.c_char_p, [_int]),
     "libscan_workspace_bytes": (_int, [_int, _i64, _i64, _i64, _int, ctypes.POINTER(_sz)]),
     "libscan_workspace_init": (_int, [_p, _sz, _p]),
+    "libscan_workspace_error": (_int, [_p, _sz, _p, _int, _p]),
     "scan_inclusive_i32": (_int, [_p, _p, _i64, _p, _sz, _p]),
     "scan_exclusive_i32": (_int, [_p, _p, _i64, _p, _sz, _p]),
     "scan_inclusive_f32": (_int, [_p, _p, _i64, _p, _sz, _p]),

@@ -193,6 +193,15 @@ int libscan_workspace_init(void* ws, size_t ws_bytes, void* stream) {
     return hip_status(ls::launch_workspace_init(ws, ws_bytes, (hipStream_t)stream));
 }
 
+int libscan_workspace_error(void* ws, size_t ws_bytes, int32_t* error_dev, int reset,
+                            void* stream) {
+    if (!ws || ((uintptr_t)ws % 16) != 0 || !error_dev || ((uintptr_t)error_dev % 4) != 0)
+        return LIBSCAN_EINVAL;
+    if (ws_bytes < ls::kWsHeader) return LIBSCAN_ENOSPACE;
+    if (overlaps(error_dev, 4, ws, ls::kWsHeader)) return LIBSCAN_EINVAL;
+    return hip_status(ls::launch_workspace_error(ws, error_dev, reset != 0, (hipStream_t)stream));
+}
+
 int libscan_workspace_bytes(int op, int64_t n, int64_t rows, int64_t len, int bits, size_t* bytes) {
     if (!bytes || n < 0 || rows < 0 || len < 0) return LIBSCAN_EINVAL;
     switch (op) {

@@ -18,6 +18,8 @@ constexpr int64_t kMaxScanElems = int64_t(1) << 35;
 
 // Zero-fill a workspace (its first use; see WsHeader in device.hpp).
 hipError_t launch_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream);
+// Copy the workspace's error word into *out (device int32), clearing it if reset.
+hipError_t launch_workspace_error(void* ws, int32_t* out, bool reset, hipStream_t stream);
 
 // 1-D decoupled look-back scan: launch_scan1d picks the kernel (the
 // matrix-core one for inclusive fp16 scans of at least one whole tile),

@@ -484,6 +484,21 @@ __global__ void k_fill_zero(uint64_t* p, int64_t words) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < words; i += stride) p[i] = 0;
 }
 
+// Copy the header's error word to *out and, if `reset`, clear it.
+__global__ void k_workspace_error(WsHeader* hdr, int32_t* out, int reset) {
+    if (threadIdx.x == 0) {
+        const uint32_t e = __hip_atomic_load(&hdr->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *out = (int32_t)e;
+        if (reset) __hip_atomic_store(&hdr->error, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+hipError_t launch_workspace_error(void* ws, int32_t* out, bool reset, hipStream_t stream) {
+    hipLaunchKernelGGL(k_workspace_error, dim3(1), dim3(64), 0, stream,
+                       reinterpret_cast<WsHeader*>(ws), out, reset ? 1 : 0);
+    return hipGetLastError();
+}
+
 hipError_t launch_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream) {
     const int64_t words = (int64_t)(ws_bytes / sizeof(uint64_t));
     if (words == 0) return hipSuccess;

@@ -6,6 +6,7 @@ of the same name on the current torch stream.  Every step of the computation
 runs in libscan's HIP kernels; there is no fallback path.
 """
 import ctypes
+import os
 
 import torch
 
@@ -47,6 +48,34 @@ def workspace(op: int, device, n: int = 0, rows: int = 0, length: int = 0, bits:
     return ws
 
 
+def workspace_error(ws, reset=True):
+    """The workspace's error word (0 or 1), read back to the host (this
+    synchronises the stream); reset clears it.  1 means a call since the last
+    reset gave up a bounded wait for another workgroup, so its outputs are
+    unspecified (a workspace not zero-filled before first use, written by
+    something else, or shared by concurrent calls)."""
+    out = torch.zeros(1, dtype=torch.int32, device=ws.device)
+    with torch.cuda.device(ws.device):
+        _lib.call("libscan_workspace_error", _ptr(ws), ws.numel(),
+                  ctypes.c_void_p(out.data_ptr()), int(bool(reset)), _stream(ws.device))
+    return int(out.item())
+
+
+# Checked mode: every call below then reads the workspace's error word after
+# it (one stream synchronisation per call) and raises if it is set.
+CHECKED = os.environ.get("LIBSCAN_CHECKED", "0") == "1"
+
+
+def set_checked(on: bool):
+    global CHECKED
+    CHECKED = bool(on)
+
+
+def _done(ws, name):
+    if CHECKED and workspace_error(ws) != 0:
+        raise _lib.LibscanError(name + " (workspace error word set)", _lib.EHIP, _lib.load())
+
+
 def _out(x, out, dtype, shape=None):
     shape = x.shape if shape is None else shape
     if out is None:
@@ -66,6 +95,7 @@ def _scan1d(cname, x, in_dtype, out_dtype, out, ws, extra=()):
         ws = workspace(op, x.device, n)
     with torch.cuda.device(x.device):
         _lib.call(cname, _ptr(x), _ptr(y), n, *extra, _ptr(ws), ws.numel(), _stream(x.device))
+        _done(ws, cname)
     return y
 
 
@@ -174,6 +204,7 @@ def _rows(cname, x, dtype, exclusive, out, ws):
     with torch.cuda.device(x.device):
         _lib.call(cname, _ptr(x), _ptr(y), rows, length, int(bool(exclusive)), _ptr(ws),
                   ws.numel(), _stream(x.device))
+        _done(ws, cname)
     return y
 
 
@@ -198,6 +229,7 @@ def topp_cutoff_f32(probs, p, out=None, ws=None):
     with torch.cuda.device(probs.device):
         _lib.call("topp_cutoff_f32", _ptr(probs), _ptr(cut), rows, length, float(p), _ptr(ws),
                   ws.numel(), _stream(probs.device))
+        _done(ws, "topp_cutoff_f32")
     return cut
 
 
@@ -222,6 +254,7 @@ def compact_by_mask_f32(x, mask, with_idx=False, out=None, idx_out=None, count=N
     with torch.cuda.device(x.device):
         _lib.call("compact_by_mask_f32", _ptr(x), _ptr(mask), _ptr(out), _ptr(idx_out),
                   ctypes.c_void_p(count.data_ptr()), n, _ptr(ws), ws.numel(), _stream(x.device))
+        _done(ws, "compact_by_mask_f32")
     return out, idx_out, count
 
 
@@ -250,6 +283,7 @@ def split_by_flags_u32(keys, flags, idx_in=None, with_idx=True, keys_out=None, i
         _lib.call("split_by_flags_u32", _ptr(keys), _ptr(idx_in), _ptr(flags), _ptr(keys_out),
                   _ptr(idx_out), ctypes.c_void_p(n_true.data_ptr()), n, _ptr(ws), ws.numel(),
                   _stream(keys.device))
+        _done(ws, "split_by_flags_u32")
     return keys_out, idx_out, n_true
 
 
@@ -273,6 +307,7 @@ def radix_sort_u32(keys, bits_per_pass=8, with_perm=True, keys_out=None, perm_ou
     with torch.cuda.device(dev):
         _lib.call("radix_sort_u32", _ptr(keys), _ptr(keys_out), _ptr(perm_out), _ptr(keys_tmp),
                   _ptr(perm_tmp), n, int(bits_per_pass), _ptr(ws), ws.numel(), _stream(dev))
+        _done(ws, "radix_sort_u32")
     return keys_out, perm_out
 
 
@@ -293,6 +328,7 @@ def _radix_sort_typed(cname, keys, dtype, descending, with_perm, keys_out, perm_
     with torch.cuda.device(dev):
         _lib.call(cname, _ptr(keys), _ptr(keys_out), _ptr(perm_out), _ptr(keys_tmp),
                   _ptr(perm_tmp), n, int(bool(descending)), _ptr(ws), ws.numel(), _stream(dev))
+        _done(ws, cname)
     return keys_out, perm_out
 
 
@@ -340,6 +376,7 @@ def radix_sort_rows_f32(keys, descending=False, with_perm=True, keys_out=None, p
         _lib.call("radix_sort_rows_f32", _ptr(keys), _ptr(keys_out), _ptr(perm_out),
                   _ptr(keys_tmp), _ptr(perm_tmp), rows, length, int(bool(descending)), _ptr(ws),
                   ws.numel(), _stream(dev))
+        _done(ws, "radix_sort_rows_f32")
     return keys_out, perm_out
 
 
@@ -357,6 +394,7 @@ def weighted_sample_f32(w, theta, out=None, ws=None):
     with torch.cuda.device(w.device):
         _lib.call("weighted_sample_f32", _ptr(w), _ptr(theta), _ptr(tok), rows, length, _ptr(ws),
                   ws.numel(), _stream(w.device))
+        _done(ws, "weighted_sample_f32")
     return tok
 
 
@@ -387,6 +425,7 @@ def topp_sample_f32(probs, theta, p, with_cutoff=False, out=None, cutoff_out=Non
         _lib.call("topp_sample_f32", _ptr(probs), _ptr(theta), float(p), _ptr(tok), _ptr(cut),
                   rows, length, _ptr(scratch_buf), scratch_buf.numel(), _ptr(ws), ws.numel(),
                   _stream(probs.device))
+        _done(ws, "topp_sample_f32")
     return (tok, cut) if with_cutoff else tok
 
 
@@ -407,4 +446,5 @@ def topk_rows_f32(x, k, largest=True, values_out=None, idx_out=None, ws=None, sc
         _lib.call("topk_rows_f32", _ptr(x), _ptr(vals), _ptr(idx), rows, length, k,
                   int(bool(largest)), _ptr(scratch_buf), scratch_buf.numel(), _ptr(ws), ws.numel(),
                   _stream(x.device))
+        _done(ws, "topk_rows_f32")
     return vals, idx

@@ -330,3 +330,46 @@ def test_topk_validation(lib):
     assert out.value >= 8 * 128 * 4096            # the kept values and indices
     assert lib.libscan_scratch_bytes(_lib.OP_TOPK, 4, 131072, 9000, ctypes.byref(out)) == _lib.OK
     assert out.value >= 16 * 4 * 9000             # and the row sort's ping-pong buffers
+
+
+def test_workspace_error_validation(lib):
+    """libscan_workspace_error checks its arguments before enqueueing anything."""
+    E = P(0x200000)
+    assert lib.libscan_workspace_error(None, 4096, E, 1, None) == _lib.EINVAL
+    assert lib.libscan_workspace_error(P(0x4000008), 4096, E, 1, None) == _lib.EINVAL  # alignment
+    assert lib.libscan_workspace_error(WS, 4096, None, 1, None) == _lib.EINVAL
+    assert lib.libscan_workspace_error(WS, 4096, P(0x200002), 1, None) == _lib.EINVAL
+    assert lib.libscan_workspace_error(WS, 255, E, 1, None) == _lib.ENOSPACE
+    assert lib.libscan_workspace_error(WS, 4096, P(0x4000000 + 12), 1, None) == _lib.EINVAL
+
+
+def test_noalloc_validation(lib):
+    """The entry point without a workspace: sizes beyond its static array are
+    rejected before any HIP call, as are negative sizes, NULL data and a
+    partial overlap."""
+    f = lib.scan_inclusive_i32_noalloc
+    assert f(X, Y, -1, None) == _lib.EINVAL
+    assert f(None, Y, 5, None) == _lib.EINVAL
+    assert f(X, None, 5, None) == _lib.EINVAL
+    assert f(X, P(0x100000 + 4), 5, None) == _lib.EINVAL
+    assert f(XB, YB, (1 << 31) + 1, None) == _lib.ERANGE
+    assert f(XB, YB, 1 << 40, None) == _lib.ERANGE
+    assert f(None, None, 0, None) == _lib.OK
+
+
+def _gpu_present():
+    import torch
+    return os.path.exists("/dev/kfd") or torch.cuda.device_count() > 0
+
+
+@pytest.mark.skipif(_gpu_present(), reason="needs a box without a GPU: the calls below launch "
+                    "kernels on fake addresses")
+def test_well_formed_calls_without_a_gpu_return_ehip(lib):
+    """Calls that pass validation reach the HIP launch, which fails on a box
+    without a GPU: the status is LIBSCAN_EHIP, not a crash or a hang."""
+    ws_bytes = 1 << 20
+    assert lib.scan_inclusive_i32(X, Y, 1000, WS, ws_bytes, None) == _lib.EHIP
+    assert lib.scan_exclusive_f32(X, Y, 100_000, WS, ws_bytes, None) == _lib.EHIP
+    assert lib.libscan_workspace_init(WS, ws_bytes, None) == _lib.EHIP
+    assert lib.libscan_workspace_error(WS, ws_bytes, P(0x200000), 1, None) == _lib.EHIP
+    assert lib.scan_inclusive_i32_noalloc(X, Y, 1000, None) == _lib.EHIP

@@ -101,9 +101,13 @@ def test_one_workspace_for_every_op(ops):
     announce("shared workspace, all ops")
     n = 16 * 40_000
     ws = _big_ws(ops, n)
-    for seed in range(3):
-        _run_all(ops, ws, n, seed)
-    assert int(ws[12:16].cpu().numpy().view(np.int32)[0]) == 0
+    ops.set_checked(True)  # every op's call is followed by a read of the error word
+    try:
+        for seed in range(3):
+            _run_all(ops, ws, n, seed)
+    finally:
+        ops.set_checked(False)
+    assert ops.workspace_error(ws) == 0
 
 
 def test_epoch_wrap(ops):
@@ -125,7 +129,7 @@ def test_epoch_wrap(ops):
     assert epoch == 1 << 30
     for seed in (9, 10):
         _run_all(ops, ws, n, seed)
-    assert int(ws[12:16].cpu().numpy().view(np.int32)[0]) == 0
+    assert ops.workspace_error(ws) == 0
 
 
 def test_topp_after_row_scan_at_high_epoch(ops):
@@ -143,7 +147,7 @@ def test_topp_after_row_scan_at_high_epoch(ops):
         assert_equal_first_diff(to_host(ops.scan_rows_i32(to_dev(x), ws=ws)),
                                 oracle.scan_rows_i32(x), "rows at high epoch")
         _check_topp(ops, ws, n, seed)
-    assert int(ws[12:16].cpu().numpy().view(np.int32)[0]) == 0
+    assert ops.workspace_error(ws) == 0
 
 
 def test_uninitialised_header_raises_error_word(ops):
@@ -158,4 +162,15 @@ def test_uninitialised_header_raises_error_word(ops):
     x = to_dev(W.scan_i32(n, seed=1))
     ops.scan_inclusive_i32(x, ws=ws)
     torch.cuda.synchronize()
-    assert int(ws[12:16].cpu().numpy().view(np.int32)[0]) == 1
+    assert ops.workspace_error(ws, reset=False) == 1
+    assert ops.workspace_error(ws) == 1  # read again, then cleared
+    assert ops.workspace_error(ws) == 0
+    ops.scan_inclusive_i32(x, ws=ws)  # the ticket count is still past the grid: set again
+    assert ops.workspace_error(ws) == 1
+    # checked mode: the binding reads the word after the call and raises
+    ops.set_checked(True)
+    try:
+        with pytest.raises(_lib.LibscanError, match="error word"):
+            ops.scan_inclusive_i32(x, ws=ws)
+    finally:
+        ops.set_checked(False)
