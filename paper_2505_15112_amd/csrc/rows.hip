@@ -56,7 +56,6 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_rows_lookback
             __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         return;
     }
-    const int64_t tile = tile32;
     const uint32_t row32 = tile32 / segs;  // 32-bit: no 64-bit division code
     const int64_t row = row32;
     const int64_t seg = tile32 - row32 * segs;
@@ -333,111 +332,195 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp(
 
 // ---------------------------------------------------------------- top-p, early exit
 //
-// The cutoff for rows of a few long tiles, reading no more of a row than it
-// needs.  Tiles are taken by ticket in column-major order (tile t of every
-// row before tile t + 1 of any), and tile t of a row first waits for tile
-// t - 1's word in the row's state: the running sum of the tiles before it,
-// or "found".  A tile of a row already found exits without reading its
-// data; otherwise it reads its part, and if the running sum reaches p inside
-// it (or it is the row's last tile) it finds the index in its own registers
-// (no re-read) and marks the row found.  On sorted probabilities the
-// crossing comes early, so most of a row is never read; on any input the
-// result is the cutoff definition's.  A tile only waits for the tile with
-// the previous ticket of its row, which is running or done.
-// State word: [001 | found : 1 | tiles published : 28 | running sum : fp32].
-constexpr uint64_t kFoundBit = 1ull << 60;
+// The cutoff for rows of 2 to kEarlyMaxSegs tiles of 4096 elements, reading
+// little more of a row than the cutoff needs when the crossing lies in the
+// row's head (as it does on sorted probabilities: the largest ones come
+// first), with no workgroup ever waiting for another.  Two kernels:
+//  * k_topp_head reads the first `heads` tiles of every row, all at once,
+//    and stores for each tile its sum and the largest running sum inside it
+//    (from the tile's start);
+//  * k_topp_finish, one workgroup per row, scans those pairs in tile order:
+//    tile t holds an index whose running sum reaches p exactly when
+//    E_t + M_t >= p (E_t the sum of the tiles before it, M_t its largest
+//    inner running sum; rounding is monotone, so this is exact for the
+//    running sums as computed here), re-reads the first such tile (just
+//    read, so still in L2) and finds the index; if the head holds none, it
+//    walks the rest of the row itself, 16384 elements per step.
+// A running sum is always taken as E + (tile-local inclusive sum), the same
+// in both kernels, so the head's verdict and the search agree.  The result
+// is the definition's on any input.  The head words are plain fp32 values in
+// the low halves of 64-bit workspace words (the top bits clear, as the
+// workspace invariant asks), written before they are read in every call.
+constexpr int64_t kEarlyTile = 4096;
+constexpr int64_t kEarlyMaxSegs = 256;  // rows up to 2^20 elements
+constexpr int kFinishThreads = 512;
+
+// Tiles of a row read by the head kernel: a quarter of the row, at least 8.
+static inline uint32_t topp_heads(int64_t len) {
+    const int64_t segs = (len + kEarlyTile - 1) / kEarlyTile;
+    const int64_t q = (segs + 3) / 4 > 8 ? (segs + 3) / 4 : 8;
+    return (uint32_t)(q < segs ? q : segs);
+}
+
+// Wavefront maximum with DPP (lanes outside the row / disabled read -inf).
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_fmax(float v) {
+    const float o = Bits<float>::from((uint32_t)__builtin_amdgcn_update_dpp(
+        (int)0xff800000u, (int)Bits<float>::to(v), CTRL, ROW_MASK, 0xf, false));
+    return o > v ? o : v;
+}
+__device__ __forceinline__ float wave_fmax(float v) {
+    v = dpp_fmax<0x111, 0xf>(v);
+    v = dpp_fmax<0x112, 0xf>(v);
+    v = dpp_fmax<0x114, 0xf>(v);
+    v = dpp_fmax<0x118, 0xf>(v);
+    v = dpp_fmax<0x142, 0xa>(v);
+    v = dpp_fmax<0x143, 0xc>(v);
+    return lane_read(v, kWave - 1);
+}
 
 template <class TileT, bool VEC>
-__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp_early(
-    const float* probs, int32_t* cutoff, uint32_t rows, int64_t len, uint32_t segs,
-    uint32_t ntiles, float p, WsHeader* hdr, uint64_t* state, uint64_t* arrivals,
-    int64_t ws_words) {
-    __shared__ Ticket s_ticket;
-    __shared__ uint64_t s_state;
+__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp_head(
+    const float* probs, int64_t len, uint32_t rows, uint32_t heads, uint64_t* words) {
     __shared__ float s_wtot[TileT::WAVES];
-    __shared__ int32_t s_min[TileT::WAVES];
-
-    if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
-    __syncthreads();
-    const uint32_t tile32 = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.tile);
-    const uint32_t epoch = (uint32_t)__builtin_amdgcn_readfirstlane(s_ticket.epoch);
-    if (tile32 >= ntiles) {  // only with a workspace that was never zero-filled
-        if (threadIdx.x == 0)
-            __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        return;
+    __shared__ float s_wmax[TileT::WAVES];
+    const uint32_t row32 = blockIdx.x % rows;  // tile t of every row before tile t + 1
+    const uint32_t t = blockIdx.x / rows;
+    const int64_t base = (int64_t)t * TileT::kElems;
+    float v[TileT::J][TileT::V];
+    // plain loads: the finishing kernel re-reads the crossing tile from L2
+    TileT::template load<VEC>(probs + (int64_t)row32 * len, len, base, v);
+    float wofs;
+    const float agg = TileT::combine_waves(TileT::template wave_scan<false>(v), s_wtot, &wofs);
+    const int32_t valid = (int32_t)(len - base < TileT::kElems ? len - base : TileT::kElems);
+    float mx = -__builtin_inff();
+#pragma unroll
+    for (int j = 0; j < TileT::J; ++j) {
+        const int32_t off = (int32_t)TileT::lane_offset(j);
+#pragma unroll
+        for (int e = 0; e < TileT::V; ++e) {
+            const float run = wofs + v[j][e];
+            if (off + e < valid) mx = run > mx ? run : mx;
+        }
     }
-    const uint32_t seg = tile32 / rows;
-    const uint32_t row32 = tile32 - seg * rows;
-    const int64_t row = row32;
-
+    mx = wave_fmax(mx);
+    if (lane_id() == 0) s_wmax[threadIdx.x / kWave] = mx;
+    __syncthreads();
     if (threadIdx.x == 0) {
-        uint64_t w = kRowTag;  // tile 0: nothing before it
-        if (seg > 0) {
-            for (uint32_t spins = 0;; ++spins) {  // bounded: tile seg - 1 is running or done
-                w = __hip_atomic_load(&state[row], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                if (row_word(w) && ((w & kFoundBit) || ((uint32_t)(w >> 32) & 0x0FFFFFFFu) >= seg))
-                    break;
-                if (spins >= kSpinLimit) {
-                    __hip_atomic_store(&hdr->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    w = kRowTag | kFoundBit;
+        float m = s_wmax[0];
+        for (int k = 1; k < TileT::WAVES; ++k) m = s_wmax[k] > m ? s_wmax[k] : m;
+        uint64_t* w = words + ((size_t)row32 * heads + t) * 2;
+        w[0] = Bits<float>::to(agg);
+        w[1] = Bits<float>::to(m);
+    }
+}
+
+// The whole workgroup: the first index i < valid of the tile in v whose
+// running sum e + (wofs + v[i]) reaches p, or INT_MAX.  Contains barriers.
+template <class TileT>
+__device__ __forceinline__ int32_t topp_first_reach(const float (&v)[TileT::J][TileT::V],
+                                                    float e, float wofs, int32_t valid, float p,
+                                                    int32_t* s_min) {
+    int32_t cand = INT_MAX;
+#pragma unroll
+    for (int j = TileT::J - 1; j >= 0; --j) {
+        const int32_t off = (int32_t)TileT::lane_offset(j);
+#pragma unroll
+        for (int k = TileT::V - 1; k >= 0; --k)
+            if (off + k < valid && e + (wofs + v[j][k]) >= p) cand = off + k;
+    }
+    const int32_t wm = wave_min(cand);
+    if (lane_id() == 0) s_min[threadIdx.x / kWave] = wm;
+    __syncthreads();
+    int32_t m = INT_MAX;
+    for (int k = 0; k < TileT::WAVES; ++k) m = s_min[k] < m ? s_min[k] : m;
+    __syncthreads();  // s_min is rewritten by the next call
+    return m;
+}
+
+template <bool VEC>
+__global__ __launch_bounds__(kFinishThreads) LS_OCCUPANCY4 void k_topp_finish(
+    const float* probs, int32_t* cutoff, int64_t len, uint32_t heads, float p,
+    const uint64_t* words) {
+    using H = Tile<float, float, 4, 2, kFinishThreads / kWave>;   // one head tile, 4096
+    using B = Tile<float, float, 4, 8, kFinishThreads / kWave>;  // 16384 per step after the head
+    static_assert(H::kElems == kEarlyTile, "head tile");
+    __shared__ int32_t s_tile;
+    __shared__ float s_e;
+    __shared__ float s_wtot[H::WAVES];
+    __shared__ int32_t s_min[H::WAVES];
+
+    const uint32_t row32 = blockIdx.x;
+    const float* xr = probs + (int64_t)row32 * len;
+    const uint64_t* hw = words + (size_t)row32 * heads * 2;
+    float carry = 0.f;  // sum of the head tiles before `from`
+    uint32_t from = 0;
+    while (true) {
+        if (threadIdx.x < kWave) {
+            // wave 0: the first head tile at or after `from` holding a reach
+            const int lane = lane_id();
+            int32_t found = -1;
+            float e_found = 0.f;
+            for (uint32_t b = from; b < heads; b += kWave) {
+                const uint32_t t = b + lane;
+                const float a = t < heads ? Bits<float>::from((uint32_t)hw[2 * t]) : 0.f;
+                const float m = t < heads ? Bits<float>::from((uint32_t)hw[2 * t + 1]) : 0.f;
+                const float sc = wave_incl_scan(a);
+                const float ex = carry + wave_shr1(sc);  // E_t: the sum of the tiles before t
+                const uint64_t hit = __ballot(t < heads && ex + m >= p);
+                if (hit) {
+                    const int l = __builtin_ctzll(hit);
+                    found = (int32_t)(b + l);
+                    e_found = lane_read(ex, l);
                     break;
                 }
-                __builtin_amdgcn_s_sleep(1);
+                carry = carry + lane_read(sc, kWave - 1);
+            }
+            if (lane == 0) {
+                s_tile = found;
+                s_e = found >= 0 ? e_found : carry;
             }
         }
-        s_state = w;
-    }
-    __syncthreads();
-    const uint64_t st = s_state;
-    if (!(st & kFoundBit)) {  // uniform
-        const float excl = Bits<float>::from((uint32_t)st);
-        const int64_t base = (int64_t)seg * TileT::kElems;
-        const float* xr = probs + row * len;
-        float v[TileT::J][TileT::V];
-        TileT::template load<VEC>(xr, len, base, v);
+        __syncthreads();
+        const int32_t t = s_tile;
+        const float e = s_e;
+        __syncthreads();  // s_tile / s_e are rewritten by the next round
+        if (t < 0) {
+            carry = e;  // the sum of the whole head
+            break;
+        }
+        const int64_t base = (int64_t)t * H::kElems;
+        float v[H::J][H::V];
+        H::template load<VEC>(xr, len, base, v);
         float wofs;
-        const float agg = TileT::combine_waves(TileT::template wave_scan<false>(v), s_wtot, &wofs);
-        const float incl = excl + agg;
-        const bool last = seg == segs - 1;
-        uint64_t out = kRowTag | ((uint64_t)(seg + 1) << 32) | Bits<float>::to(incl);
-        if (incl >= p || last) {
-            // the first index of this tile whose running sum reaches p; none
-            // (rounding, or the row never reaches p): the tile's last index
-            const float c = excl + wofs;
-            const int64_t lastidx = (base + TileT::kElems < len ? base + TileT::kElems : len) - 1;
-            const int32_t cap = (int32_t)(lastidx - base);
-            int32_t cand = INT_MAX;
-#pragma unroll
-            for (int j = TileT::J - 1; j >= 0; --j) {
-                const int32_t off = (int32_t)TileT::lane_offset(j);
-#pragma unroll
-                for (int e = TileT::V - 1; e >= 0; --e)
-                    if (off + e <= cap && c + v[j][e] >= p) cand = off + e;
-            }
-            const int32_t wm = wave_min(cand);
-            if (lane_id() == 0) s_min[threadIdx.x / kWave] = wm;
-            __syncthreads();
-            int32_t m = INT_MAX;
-            for (int k = 0; k < TileT::WAVES; ++k) m = s_min[k] < m ? s_min[k] : m;
-            if (threadIdx.x == 0) cutoff[row] = (int32_t)(base + (m != INT_MAX ? m : cap));
-            out |= kFoundBit;
+        const float agg = H::combine_waves(H::template wave_scan<false>(v), s_wtot, &wofs);
+        const int32_t valid = (int32_t)(len - base < H::kElems ? len - base : H::kElems);
+        const int32_t m = topp_first_reach<H>(v, e, wofs, valid, p, s_min);
+        if (m != INT_MAX) {
+            if (threadIdx.x == 0) cutoff[row32] = (int32_t)(base + m);
+            return;
         }
-        if (threadIdx.x == 0) {
-            adversarial_pause(tile32);
-            __hip_atomic_store(&state[row], out, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            // arrive only once the word is acknowledged, so that the row's
-            // reset below can never be overtaken by it
-            __builtin_amdgcn_s_waitcnt(0);
-        }
+        // (not reached: the head's verdict and this search use the same sums)
+        carry = e + agg;
+        from = (uint32_t)t + 1;
+        __syncthreads();  // s_wtot is rewritten by the next combine
     }
-    if (threadIdx.x == 0) {
-        // the row's last tile to arrive leaves its words clear for the next call
-        if (row_arrive(&arrivals[row]) == segs - 1) {
-            __hip_atomic_store(&state[row], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(&arrivals[row], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // no reach in the head: walk the rest of the row
+    for (int64_t base = (int64_t)heads * kEarlyTile; base < len; base += B::kElems) {
+        float v[B::J][B::V];
+        B::template load<VEC, true>(xr, len, base, v);
+        float wofs;
+        const float agg = B::combine_waves(B::template wave_scan<false>(v), s_wtot, &wofs);
+        const int32_t valid = (int32_t)(len - base < B::kElems ? len - base : B::kElems);
+        const int32_t m = topp_first_reach<B>(v, carry, wofs, valid, p, s_min);
+        if (m != INT_MAX) {
+            if (threadIdx.x == 0) cutoff[row32] = (int32_t)(base + m);
+            return;
         }
-        finish_epoch(hdr, epoch, ntiles, state, ws_words);
+        carry = carry + agg;
+        __syncthreads();  // s_wtot is rewritten by the next combine
     }
+    if (threadIdx.x == 0) cutoff[row32] = (int32_t)(len - 1);
 }
 
 __global__ void k_fill_i32(int32_t* p, int64_t count, int32_t value) {
@@ -510,9 +593,14 @@ static size_t topp_arrivals_offset(int64_t rows, int64_t len) {
 size_t topp_ws_bytes(int64_t rows, int64_t len) {
     return topp_arrivals_offset(rows, len) + (size_t)rows * sizeof(uint64_t);
 }
+static bool topp_early(int64_t len);
+static size_t topp_early_ws_bytes(int64_t rows, int64_t len);
 size_t scan_rows_ws_bytes(int64_t rows, int64_t len) {
     // short rows (one wavefront per row) need no workspace beyond the header
-    return long_rows(len) ? topp_ws_bytes(rows, len) : kWsHeader;
+    if (!long_rows(len)) return kWsHeader;
+    const size_t a = topp_ws_bytes(rows, len);
+    const size_t b = topp_early(len) ? topp_early_ws_bytes(rows, len) : 0;
+    return a > b ? a : b;
 }
 
 static bool aligned16(const void* p) { return ((uintptr_t)p % 16) == 0; }
@@ -557,27 +645,27 @@ static void topp_long(bool vec, const float* probs, const int32_t* idx, const fl
                        len, segs, p, reinterpret_cast<WsHeader*>(ws), sums, arrivals);
 }
 
-// Rows of 2 to 8 long tiles take the early-exit cutoff kernel.
+// Rows of 2 to kEarlyMaxSegs tiles of 4096 take the early-exit cutoff kernels.
 static bool topp_early(int64_t len) {
-    return row_tile(len) == 32768 && row_segments(len) <= 8;
+    return len > kEarlyTile && (len + kEarlyTile - 1) / kEarlyTile <= kEarlyMaxSegs;
+}
+static size_t topp_early_ws_bytes(int64_t rows, int64_t len) {
+    return kWsHeader + (size_t)rows * topp_heads(len) * 2 * sizeof(uint64_t);
 }
 
 static void topp_cutoff_early(bool vec, const float* probs, int32_t* cutoff, int64_t rows,
                               int64_t len, float p, void* ws, hipStream_t stream) {
-    using TV = RowTile<float, RGeomL, true>;
-    using TU = RowTile<float, RGeomL, false>;
-    const uint32_t segs = (uint32_t)((len + TV::kElems - 1) / TV::kElems);
-    const uint32_t nt = (uint32_t)(rows * segs);
-    uint64_t* state = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
-    uint64_t* arrivals = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) +
-                                                     topp_arrivals_offset(rows, len));
-    // words after the header that the epoch wrap may clear: the state words
-    // and the arrival counters (the arrivals end the workspace)
-    const int64_t words = (int64_t)((topp_ws_bytes(rows, len) - kWsHeader) / sizeof(uint64_t));
-    auto k = vec ? k_topp_early<TV, true> : k_topp_early<TU, false>;
-    hipLaunchKernelGGL(k, dim3(nt), dim3(vec ? TV::kThreads : TU::kThreads), 0, stream, probs,
-                       cutoff, (uint32_t)rows, len, segs, nt, p, reinterpret_cast<WsHeader*>(ws),
-                       state, arrivals, words);
+    using TV = RowTile<float, RGeomS, true>;
+    using TU = RowTile<float, RGeomS, false>;
+    static_assert(TV::kElems == kEarlyTile && TU::kElems == kEarlyTile, "early-exit tile");
+    const uint32_t heads = topp_heads(len);
+    uint64_t* words = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
+    auto kh = vec ? k_topp_head<TV, true> : k_topp_head<TU, false>;
+    hipLaunchKernelGGL(kh, dim3((unsigned)(rows * heads)), dim3(vec ? TV::kThreads : TU::kThreads),
+                       0, stream, probs, len, (uint32_t)rows, heads, words);
+    auto kf = vec ? k_topp_finish<true> : k_topp_finish<false>;
+    hipLaunchKernelGGL(kf, dim3((unsigned)rows), dim3(kFinishThreads), 0, stream, probs, cutoff,
+                       len, heads, p, words);
 }
 
 template <ToppMode MODE>

@@ -3,7 +3,7 @@
 libscan_adv.so is the same sources built with LS_ADVERSARIAL_DELAYS: a
 pseudo-random pause (usually 0-3 us, one time in eight 14-30 us) after each
 tile ticket, before each status-word publication of the decoupled look-back,
-before each row-counter arrival and before each early-exit row-state word.
+and before each row-counter arrival.
 Workgroups then reach those steps in orders a normal run seldom produces.
 Every op that crosses workgroups runs here against the oracle: the 1-D scans
 (wavefront, register + LDS and matrix-core tiles), reduce-then-scan,
@@ -109,16 +109,17 @@ def test_lds_tiles(ops, adversarial):
     assert int(to_host(carry)[0]) == (int(oracle.scan_i32(x)[-1]) + 7 + 2**31) % 2**32 - 2**31
 
 
-def test_topp_early_exit_and_sampler(ops, adversarial):
-    """The early-exit cutoff chains tiles through a row state word: unsorted
-    rows put the crossing anywhere; then the sampler on the same rows."""
+def test_topp_cutoff_and_sampler(ops, adversarial):
+    """The cutoff of rows longer than 2^20 (tile sums and a row arrival
+    counter; the last tile to arrive decides), on unsorted rows that put the
+    crossing anywhere; then the sampler."""
     announce("adversarial topp")
-    probs = W.sample_probs(9, 6 * 32768 + 11, seed=8)
+    probs = W.sample_probs(3, (1 << 20) + 4097, seed=8)
     csum, _ = oracle.scan_rows_f32(probs)
     for p in (0.3, 0.9, 1.5):
         g = to_host(ops.topp_cutoff_f32(to_dev(probs), p))
         k = oracle.topp_cutoff_f32(probs, p)
-        bad = [r for r in range(9) if not topp_accept(int(g[r]), int(k[r]), csum[r], p)]
+        bad = [r for r in range(3) if not topp_accept(int(g[r]), int(k[r]), csum[r], p)]
         assert not bad, (p, bad)
     rng = np.random.default_rng(9)
     ex = (rng.integers(0, 16, (6, 70_001)) * 2.0**-24).astype(np.float32)

@@ -90,11 +90,13 @@ def test_topp_one_pass_limit(ops, length, p):
     _check_topp(ops, probs, p, f"topp len={length} p={p}")
 
 
-@pytest.mark.parametrize("length", [65_537, 131_072 + 5, 200_003, 262_144, 262_145])
+@pytest.mark.parametrize("length", [8_191, 65_537, 131_072 + 5, 200_003, 262_145, 1 << 20,
+                                    (1 << 20) + 1])
 @pytest.mark.parametrize("p", [0.0, 0.5, 0.9, 0.999, 1.5])
 def test_topp_early_exit_shapes(ops, length, p):
-    """Rows of 3 to 8 long tiles take the early-exit kernel (262145: 9 tiles,
-    the two-phase one); p = 1.5 walks every tile of every row."""
+    """Rows of 2 to 256 tiles of 4096 take the early-exit kernel (2^20 + 1:
+    the two-phase one); p = 1.5 reads every tile of every row, p = 0 stops in
+    the first."""
     announce("topp early", length, p)
     probs = W.topp_probs(5, length, seed=length % 997)
     _check_topp(ops, probs, p, f"topp early len={length} p={p}")
@@ -103,15 +105,30 @@ def test_topp_early_exit_shapes(ops, length, p):
 @pytest.mark.parametrize("p", [0.3, 0.9])
 def test_topp_early_exit_unsorted(ops, p):
     """The cutoff is defined on any row: unsorted softmax rows put the
-    crossing in any tile, so the row state is passed along tile by tile."""
+    crossing in any tile."""
     announce("topp early unsorted", p)
     probs = W.sample_probs(7, 6 * 32768 + 11, seed=3)
     _check_topp(ops, probs, p, f"topp early unsorted p={p}")
 
 
+@pytest.mark.parametrize("length", [12_289, 300_001])
+def test_topp_early_exit_signed_walk(ops, length):
+    """Rows of -1/0/+1 steps: the running sum crosses p, falls back and crosses
+    again, so several tiles hold indices whose running sum reaches p and the
+    cutoff is the first of them.  Every partial sum is a small integer, exact
+    in fp32, so the GPU must match the oracle exactly."""
+    announce("topp early signed walk", length)
+    x = W.exact_pm1(6 * length, seed=length).reshape(6, length)
+    walk = np.cumsum(x.astype(np.int64), axis=1)
+    for p in (1.0, 3.0, float(max(1, walk.max() // 2)), 1e9):
+        g = to_host(ops.topp_cutoff_f32(to_dev(x), p))
+        k = oracle.topp_cutoff_f32(x, p)
+        assert_equal_first_diff(g, k, f"signed walk len={length} p={p}")
+
+
 def test_topp_early_exit_repeat(ops):
-    """The early-exit kernel 30 times on one workspace, alternating p so that
-    rows stop in different tiles: the row words it leaves must read as clear."""
+    """The early-exit kernels 30 times on one workspace, alternating p so that
+    rows stop in different tiles (and p = 1.5 walks whole rows)."""
     from paper_2505_15112_amd import _lib
     import torch
     announce("topp early repeat")

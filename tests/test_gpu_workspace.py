@@ -86,8 +86,8 @@ def _check_samplers(ops, ws, n, seed):
 
 def _check_topp(ops, ws, n, seed):
     from gpu_util import topp_accept
-    # 16 rows of n/16 (the two-phase kernel) and 4 rows of 5 long tiles (the
-    # early-exit kernel, whose row state words share the workspace too)
+    # 16 rows of n/16 and 4 rows of 32 tiles of 4096 (the early-exit
+    # kernels, whose head words share the workspace too)
     for shape in ((16, n // 16), (4, 4 * 32768 + 5)):
         probs = W.topp_probs(shape[0], shape[1], seed=seed)
         g = to_host(ops.topp_cutoff_f32(to_dev(probs), 0.9, ws=ws))
