@@ -26,7 +26,9 @@
  *    only enqueue work: they return before the GPU finishes and never
  *    synchronise.  Counts and totals are written to device memory.
  *  - Integer sums wrap modulo 2^32 (two's complement).  Floating-point sums are
- *    accumulated in fp32 in an order that can vary from run to run.
+ *    accumulated in fp32 in an order that can vary from run to run;
+ *    infinities and NaNs propagate as in IEEE arithmetic (a running sum is
+ *    NaN once a NaN or both infinities precede it), whatever the order.
  *  - Return value: LIBSCAN_OK, or a negative LIBSCAN_E* code for an argument
  *    or launch error; on error the outputs are unspecified.  Faults inside a
  *    kernel surface at the caller's next synchronisation, not here.
@@ -137,7 +139,9 @@ int scan_exclusive_f16f32(const uint16_t* x, float* y, int64_t n, void* ws, size
  * 32768-element tiles take the matrix-core kernel, a shorter tail the
  * wavefront one.  Results agree with the wavefront scan within the float
  * tolerance (exactly on {-1, 0, 1} inputs); measured faster than it, which
- * is why scan_inclusive_f16f32 uses this path when it can. */
+ * is why scan_inclusive_f16f32 uses this path when it can.  A tile holding
+ * an infinity or a NaN is scanned on the vector units instead (in the
+ * product it would meet the zeros of U_32, and inf * 0 is NaN). */
 int scan_inclusive_f16f32_mfma(const uint16_t* x, float* y, int64_t n, void* ws,
                                size_t ws_bytes, void* stream);
 

@@ -24,7 +24,9 @@
 // matrix operand where the wavefront tile loads 8, and its accumulators leave
 // as 4-byte stores of one matrix column each.  Whole 32768-element tiles run
 // here; a ragged tail (fewer than 32768 elements) is scanned by the
-// wavefront kernel with this launch's total as its carry.
+// wavefront kernel with this launch's total as its carry.  A tile holding an
+// infinity or a NaN is scanned on the vector units (IEEE propagation: the
+// matrix product would multiply it by the zeros of U_s).
 #include "launch.hpp"
 #include "tile.hpp"
 
@@ -58,6 +60,60 @@ __device__ __forceinline__ h8 load_half(const uint16_t* xb, int h) {
     return __builtin_bit_cast(h8, *reinterpret_cast<const u32x4*>(xb + off));
 }
 
+// True if any of the 8 fp16 values is an infinity or a NaN (exponent bits
+// all ones).
+__device__ __forceinline__ bool has_special(h8 v) {
+    const u32x4 r = __builtin_bit_cast(u32x4, v);
+    bool s = false;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const uint32_t e = r[q] & 0x7C007C00u;
+        s |= (e & 0xFFFFu) == 0x7C00u || (e >> 16) == 0x7C00u;
+    }
+    return s;
+}
+
+// A whole tile on the vector units: eight passes of 4096 elements (the
+// wavefront tile scan), swept twice -- the tile's sum for the look-back,
+// then the outputs with the carry -- with the pass sums taken the same way
+// both times.  Used for tiles holding an infinity or a NaN.
+__device__ __forceinline__ void mfma_tile_on_vector_units(
+    const uint16_t* x, float* y, int64_t tbase, uint32_t tile32, uint32_t epoch, WsHeader* hdr,
+    uint64_t* status, int64_t status_words, uint32_t ntiles, float* total_out, float* s_wtot,
+    float* s_carry) {
+    using P = Tile<uint16_t, float, 4, 2, kMfmaWaves>;
+    constexpr int kPasses = (int)(kMfmaTile / P::kElems);
+    const int64_t tend = tbase + kMfmaTile;
+    float agg = 0.f;
+    for (int q = 0; q < kPasses; ++q) {
+        float v[P::J][P::V];
+        P::template load<true>(x, tend, tbase + q * P::kElems, v);
+        float wofs;
+        agg = agg + P::combine_waves(P::template wave_scan<false>(v), s_wtot, &wofs);
+        __syncthreads();  // s_wtot is rewritten by the next pass
+    }
+    if (threadIdx.x < kWave) {
+        const float excl = lookback<float>(status, tile32, 0u, agg, 0.f, epoch, hdr);
+        if (threadIdx.x == 0) {
+            *s_carry = excl;
+            if (total_out && tile32 == ntiles - 1) *total_out = excl + agg;
+            finish_epoch(hdr, epoch, ntiles, status, status_words);
+        }
+    }
+    __syncthreads();
+    float carry = *s_carry;
+    for (int q = 0; q < kPasses; ++q) {
+        float v[P::J][P::V];
+        const int64_t base = tbase + q * P::kElems;
+        P::template load<true>(x, tend, base, v);
+        float wofs;
+        const float pagg = P::combine_waves(P::template wave_scan<false>(v), s_wtot, &wofs);
+        P::template store<true>(y, tend, base, v, carry + wofs);
+        carry = carry + pagg;
+        __syncthreads();
+    }
+}
+
 // Full tiles only (the launcher scans a ragged tail with the wavefront
 // kernel, carrying this launch's total); x 16-byte aligned.  The last tile
 // writes the total to *total_out when total_out is not null.
@@ -87,6 +143,20 @@ __global__ __launch_bounds__(kMfmaWaves * kWave) LS_OCCUPANCY4 void k_scan_mfma_
     for (int b = 0; b < kMfmaBlocks; ++b)
 #pragma unroll
         for (int h = 0; h < 2; ++h) a[b][h] = load_half(x + wbase + b * kBlock, h);
+
+    // An infinity or a NaN would meet the zeros of U_32 (inf * 0 is NaN) and
+    // spoil the sums of the elements before it: such a tile (uniform: one
+    // vote per workgroup) is scanned on the vector units instead.
+    bool special = false;
+#pragma unroll
+    for (int b = 0; b < kMfmaBlocks; ++b)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) special |= has_special(a[b][h]);
+    if (__syncthreads_or(special)) {
+        mfma_tile_on_vector_units(x, y, (int64_t)tile32 * kMfmaTile, tile32, epoch, hdr, status,
+                                  status_words, ntiles, total_out, s_wtot, &s_carry);
+        return;
+    }
 
     // Block by block: the row scans on the matrix cores (acc[b] = A_b * U_32),
     // then every row gets the rows before it and the wave's earlier blocks.

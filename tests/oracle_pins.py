@@ -479,4 +479,39 @@ def check_topp(o):
             assert cut[r] == min(k, probs.shape[1] - 1), (p, r)
 
 
+
+
+# ---------------------------------------------------------------- IEEE special values
+
+def _same_ieee(got, want):
+    got, want = np.asarray(got, np.float64), np.asarray(want, np.float64)
+    return got.shape == want.shape and bool(np.all((got == want) | (np.isnan(got) & np.isnan(want))))
+
+
+def check_scan_float_ieee_specials(o):
+    """Reading A19: infinities and NaNs propagate as in IEEE arithmetic.  The
+    expected running sums are Python's own (IEEE double) sequential sums."""
+    inf, nan = float("inf"), float("nan")
+    for xs in ([0.5, inf, 0.25, -inf, 1.0], [-inf, 1.0, -inf, 2.0], [1.0, nan, 2.0, inf],
+               [inf, inf, -1.0], [0.0, -0.0, -inf, inf]):
+        inc, exc, acc = [], [], 0.0
+        for v in xs:
+            exc.append(acc)
+            acc += v
+            inc.append(acc)
+        for dt, scan in ((np.float32, o.scan_f32), (np.float16, o.scan_f16)):
+            x = np.array(xs, dt)
+            y, _ = scan(x)
+            assert _same_ieee(y, inc), (dt, xs, y, inc)
+            y, _ = scan(x, exclusive=True)
+            assert _same_ieee(y, exc), (dt, xs, y, exc)
+        y, _ = o.scan_rows_f32(np.array([xs, xs[::-1]], np.float32))
+        back = []
+        acc = 0.0
+        for v in xs[::-1]:
+            acc += v
+            back.append(acc)
+        assert _same_ieee(y[0], inc) and _same_ieee(y[1], back), (xs, y)
+
+
 ALL_CHECKS = [v for k, v in sorted(globals().items()) if k.startswith("check_")]
