@@ -68,12 +68,13 @@ def test_compact_misaligned_and_empty(ops):
     assert int(c0.item()) == 0
 
 
-def test_compact_config_n2_28(ops):
-    announce("compact config n=2^28")
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_compact_config_n2_28(ops, seed):
+    announce("compact config n=2^28", seed)
     n = 1 << 28
-    x = W.values_f32(n, seed=0)
-    m = W.mask_u8(n, seed=0)
-    _check_compact(ops, x, m, True, "compact config")
+    x = W.values_f32(n, seed=seed)
+    m = W.mask_u8(n, seed=seed)
+    _check_compact(ops, x, m, True, f"compact config seed={seed}")
 
 
 def _check_split(ops, k, f, idx_in, what):

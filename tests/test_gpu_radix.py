@@ -51,10 +51,11 @@ def test_radix(ops, n, bits):
     _check(ops, W.keys_u32(n, seed=7), bits, False, f"radix{bits} n={n} keys only")
 
 
-def test_radix_config_n2_26(ops):
-    announce("radix config n=2^26")
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_radix_config_n2_26(ops, seed):
+    announce("radix config n=2^26", seed)
     n = 1 << 26
-    keys = W.keys_u32(n, seed=0)
+    keys = W.keys_u32(n, seed=seed)
     rk, rp = oracle.sort_u32(keys)
     outs = {}
     for bits in (8, 4, 1):

@@ -393,23 +393,27 @@ def test_config_f16f32_n2_24(ops):
 
 
 @pytest.mark.skipif(not FULL, reason="full-size cases disabled")
-def test_metric_n2_28_i32(ops):
-    announce("metric i32 n=2^28")
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_metric_n2_28_i32(ops, seed):
+    announce("metric i32 n=2^28", seed)
     n = W.METRIC_N
-    x = W.scan_i32(n, seed=0)
+    x = W.scan_i32(n, seed=seed)
     y = to_host(ops.scan_inclusive_i32(to_dev(x)))
-    assert_equal_first_diff(y, oracle.scan_i32(x), "metric i32")
+    assert_equal_first_diff(y, oracle.scan_i32(x), f"metric i32 seed={seed}")
 
 
 @pytest.mark.skipif(not FULL, reason="full-size cases disabled")
-def test_metric_n2_28_f32(ops):
-    announce("metric f32 n=2^28")
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_metric_n2_28_f32(ops, seed):
+    announce("metric f32 n=2^28", seed)
     n = W.METRIC_N
-    x = W.scan_f32(n, seed=0)
+    x = W.scan_f32(n, seed=seed)
     y = to_host(ops.scan_inclusive_f32(to_dev(x)))
     ref, a = oracle.scan_f32(x)
-    assert_float_close(y, ref, a, "metric f32")
+    assert_float_close(y, ref, a, f"metric f32 seed={seed}")
     del ref, a
+    if seed:
+        return
     xe = W.exact_pm1(n, seed=1)
     ye = to_host(ops.scan_inclusive_f32(to_dev(xe)))
     assert_equal_first_diff(ye.astype(np.float64), oracle.scan_f32(xe)[0], "metric f32 exact")
