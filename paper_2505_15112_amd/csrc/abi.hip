@@ -519,7 +519,7 @@ int topk_rows_f32(const float* x, float* values_out, int32_t* idx_out, int64_t r
     if (rows == 0 || k == 0) return LIBSCAN_OK;
     if (!x || !values_out || !idx_out) return LIBSCAN_EINVAL;
     const size_t xb = (size_t)rows * (size_t)len * 4, ob = (size_t)rows * (size_t)k * 4;
-    const size_t need = ls::topk_scratch_bytes(rows, k);
+    const size_t need = ls::topk_scratch_bytes(rows, len, k);
     if (scratch_bytes < need) return LIBSCAN_ENOSPACE;
     if (!scratch || ((uintptr_t)scratch % 16) != 0) return LIBSCAN_EINVAL;
     if (overlaps(values_out, ob, x, xb) || overlaps(idx_out, ob, x, xb) ||
@@ -546,7 +546,7 @@ int libscan_scratch_bytes(int op, int64_t rows, int64_t len, int64_t k, size_t* 
         case LIBSCAN_OP_TOPK: {
             const int r = check_topk(rows, len, k);
             if (r != LIBSCAN_OK) return r;
-            *bytes = ls::topk_scratch_bytes(rows, k);
+            *bytes = ls::topk_scratch_bytes(rows, len, k);
             return LIBSCAN_OK;
         }
         default:

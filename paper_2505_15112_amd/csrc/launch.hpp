@@ -57,7 +57,7 @@ bool radix_rows_fit(int64_t rows, int64_t len);
 size_t topp_sample_ws_bytes(int64_t rows, int64_t len);
 size_t topp_sample_scratch_bytes(int64_t rows, int64_t len);
 size_t topk_ws_bytes(int64_t rows, int64_t len, int64_t k);
-size_t topk_scratch_bytes(int64_t rows, int64_t k);
+size_t topk_scratch_bytes(int64_t rows, int64_t len, int64_t k);
 hipError_t launch_topk(const float* x, float* values, int32_t* indices, int64_t rows, int64_t len,
                        int64_t k, bool largest, void* scratch, void* ws, hipStream_t stream);
 hipError_t launch_topp_sample(const float* probs, const float* theta, float p, int32_t* token,

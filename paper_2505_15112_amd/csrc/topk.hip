@@ -12,6 +12,14 @@
 // totalOrder codes of the values, complemented when the k smallest are
 // asked for, so that the selection always takes the k largest keys.
 //
+// Rows of up to 2^17 elements with k <= 8192 take a shorter route after the
+// first round: every key whose top digit is at least the chosen bucket's is
+// a candidate, and when a row has at most 16384 of them they are gathered
+// and one workgroup per row sorts them in LDS and keeps the first k (two
+// reads of each row instead of five); a row with more candidates is
+// finished by that workgroup alone (the three further rounds and the
+// selection over its row).
+//
 // No workgroup waits for another during the histogram rounds: each tile
 // writes its 256 digit counts to its own slots, and the row's last tile to
 // arrive (the per-row arrival counter of the row kernels) adds them and
@@ -53,7 +61,7 @@ __device__ __forceinline__ bool topk_in_bucket(uint32_t key, uint32_t prefix) {
 template <class TileT, bool VEC, int R>
 __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_hist(
     const uint32_t* x, int64_t len, uint32_t segs, uint32_t k, bool largest, uint32_t* hist,
-    uint64_t* state, uint64_t* arrivals) {
+    uint64_t* state, uint64_t* arrivals, uint64_t* gather) {
     constexpr int kWaves = TileT::WAVES;
     // Several histograms per wave (picked by lane), so that equal digits in
     // one instruction collide at most 64 / kSub ways: the top digits of
@@ -127,6 +135,12 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_hist(
         if (above < kk && kk <= at_least) {  // exactly one thread
             state[2 * row] = (uint64_t)((prefix << 8) | (uint32_t)(kTopkDigits - 1 - t));
             state[2 * row + 1] = (uint64_t)(kk - above);
+            if (R == 0 && gather) {
+                // the gather route: the row's candidate count, and its
+                // reservation counter cleared for this call
+                gather[2 * row] = at_least;
+                gather[2 * row + 1] = 0;
+            }
         }
     }
     if (t == 0)
@@ -227,6 +241,26 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_select(
     }
 }
 
+// Sorts s[0, npow) (a power of two) in descending order by a bitonic
+// network, `nthreads` threads of the workgroup taking the pairs.
+__device__ __forceinline__ void bitonic_desc(uint64_t* s, uint32_t npow, uint32_t nthreads) {
+    for (uint32_t size = 2; size <= npow; size <<= 1) {
+        for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
+            for (uint32_t t = threadIdx.x; t < npow / 2; t += nthreads) {
+                const uint32_t i = 2 * t - (t & (stride - 1));  // lower end of pair t
+                const uint32_t j = i + stride;
+                const uint64_t a = s[i], b = s[j];
+                // blocks of `size` alternate direction; the last merge is descending
+                if ((a < b) == ((i & size) == 0)) {
+                    s[i] = b;
+                    s[j] = a;
+                }
+            }
+            __syncthreads();
+        }
+    }
+}
+
 // The kept elements in order, for k <= kTopkSortMax: one workgroup per row
 // sorts the row's k (key, index) pairs in LDS by a bitonic network on the
 // 64-bit composite key << 32 | ~index in descending order -- larger keys
@@ -246,21 +280,7 @@ __global__ __launch_bounds__(kTopkSortThreads) void k_topk_sort(
         s[i] = i < k ? ((uint64_t)topk_key(sv[i], largest) << 32) | (uint32_t)~(uint32_t)si[i]
                      : 0ull;
     __syncthreads();
-    for (uint32_t size = 2; size <= npow; size <<= 1) {
-        for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
-            for (uint32_t t = threadIdx.x; t < npow / 2; t += kTopkSortThreads) {
-                const uint32_t i = 2 * t - (t & (stride - 1));  // lower end of pair t
-                const uint32_t j = i + stride;
-                const uint64_t a = s[i], b = s[j];
-                // blocks of `size` alternate direction; the last merge is descending
-                if ((a < b) == ((i & size) == 0)) {
-                    s[i] = b;
-                    s[j] = a;
-                }
-            }
-            __syncthreads();
-        }
-    }
+    bitonic_desc(s, npow, kTopkSortThreads);
     for (uint32_t i = threadIdx.x; i < k; i += kTopkSortThreads) {
         const uint64_t c = s[i];
         const uint32_t key = (uint32_t)(c >> 32);
@@ -268,6 +288,336 @@ __global__ __launch_bounds__(kTopkSortThreads) void k_topk_sort(
         values[row * k + i] = code ^ ((code >> 31) ? 0x80000000u : 0xFFFFFFFFu);
         indices[row * k + i] = (int32_t)~(uint32_t)c;
     }
+}
+
+// ---------------------------------------------------------------- gather route
+
+constexpr int64_t kTopkGatherMaxLen = 1 << 17;
+constexpr uint32_t kTopkCand = 16384;  // candidates sorted in LDS (128 KB)
+constexpr int kTopkFinishThreads = 1024;
+constexpr uint32_t kTopkSortAll = 2048;  // candidates sorted whole, without the cut to k
+static_assert(kTopkSortMax <= kTopkCand, "the k kept fit the finisher's sort");
+
+// The composite sort key of element i with key `key`: larger keys first,
+// equal keys by increasing index.  Every composite is at least 2^31 in its
+// low word, so zero pads sort last.
+__device__ __forceinline__ uint64_t topk_composite(uint32_t key, uint32_t i) {
+    return ((uint64_t)key << 32) | (uint32_t)~i;
+}
+
+// Every key of a row whose top digit is at least the bucket's (state after
+// round 0), to the row's candidate list (cap slots per row), in no
+// particular order: each tile reserves its slots with one atomic add on the
+// row's counter.  Rows with more than cap candidates are left alone.
+template <class TileT, bool VEC>
+__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_gather(
+    const uint32_t* x, int64_t len, uint32_t segs, bool largest, const uint64_t* state,
+    uint64_t* gather, uint64_t* cand, uint32_t cap) {
+    __shared__ uint32_t s_wtot[TileT::WAVES];
+    __shared__ uint32_t s_base;
+    const uint32_t row32 = blockIdx.x / segs;
+    const uint32_t seg = blockIdx.x - row32 * segs;
+    const int64_t row = row32;
+    if ((uint32_t)gather[2 * row] > cap) return;  // uniform: finished the long way
+    const uint32_t d = (uint32_t)state[2 * row] & 255u;
+    const int64_t base = (int64_t)seg * TileT::kElems;
+    uint32_t v[TileT::J][TileT::V];
+    TileT::template load<VEC>(x + row * len, len, base, v);
+    const int32_t valid = (int32_t)(len - base < TileT::kElems ? len - base : TileT::kElems);
+    static_assert(TileT::J * TileT::V <= 64, "per-lane take masks are 64-bit");
+    uint64_t take = 0;
+    uint32_t cnt = 0;
+#pragma unroll
+    for (int j = 0; j < TileT::J; ++j) {
+        const int32_t off = (int32_t)TileT::lane_offset(j);
+#pragma unroll
+        for (int e = 0; e < TileT::V; ++e) {
+            const uint32_t key = topk_key(v[j][e], largest);
+            const bool t = off + e < valid && (key >> 24) >= d;
+            v[j][e] = key;
+            take |= (uint64_t)t << (j * TileT::V + e);
+            cnt += t ? 1u : 0u;
+        }
+    }
+    // this lane's first slot within the tile: lanes before it in its wave,
+    // then the waves before it
+    const uint32_t incl = wave_incl_scan(cnt);
+    const int w = threadIdx.x / kWave;
+    if (lane_id() == kWave - 1) s_wtot[w] = incl;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t total = 0;
+        for (int q = 0; q < TileT::WAVES; ++q) total += s_wtot[q];
+        s_base = total ? (uint32_t)__hip_atomic_fetch_add(&gather[2 * row + 1], (uint64_t)total,
+                                                          __ATOMIC_RELAXED,
+                                                          __HIP_MEMORY_SCOPE_AGENT)
+                       : 0u;
+    }
+    __syncthreads();
+    if (!take) return;
+    uint32_t pos = s_base + incl - cnt;
+    for (int q = 0; q < w; ++q) pos += s_wtot[q];
+    uint64_t* cr = cand + (int64_t)row * cap;
+#pragma unroll
+    for (int j = 0; j < TileT::J; ++j) {
+        const uint32_t off = (uint32_t)(base + TileT::lane_offset(j));
+#pragma unroll
+        for (int e = 0; e < TileT::V; ++e) {
+            if ((take >> (j * TileT::V + e)) & 1u) {
+                // pos < the row's candidate count <= cap; checked all the same
+                if (pos < cap) cr[pos] = topk_composite(v[j][e], off + (uint32_t)e);
+                ++pos;
+            }
+        }
+    }
+}
+
+// The same network on npow keys held in registers, E per thread (thread t:
+// positions t E .. t E + E - 1; positions at or past npow are padding that
+// never meets a real key): strides below E inside the thread, strides below
+// 64 E between the lanes of a wavefront (shuffles, no barrier), larger
+// strides through LDS (s, at least max(npow, E * nthreads) slots).
+template <int E>
+__device__ __forceinline__ void bitonic_desc_regs(uint64_t (&v)[E], uint64_t* s, uint32_t npow,
+                                                  uint32_t nthreads) {
+    const uint32_t t = threadIdx.x;
+    for (uint32_t size = 2; size <= npow; size <<= 1) {
+        uint32_t stride = size >> 1;
+        if (stride >= (uint32_t)(kWave * E)) {  // uniform
+#pragma unroll
+            for (int e = 0; e < E; ++e) s[t * E + e] = v[e];
+            __syncthreads();
+            for (; stride >= (uint32_t)(kWave * E); stride >>= 1) {
+                for (uint32_t q = t; q < npow / 2; q += nthreads) {
+                    const uint32_t i = 2 * q - (q & (stride - 1));
+                    const uint32_t j = i + stride;
+                    const uint64_t a = s[i], b = s[j];
+                    const uint64_t hi = a > b ? a : b, lo = a > b ? b : a;
+                    const bool desc = (i & size) == 0;
+                    s[i] = desc ? hi : lo;
+                    s[j] = desc ? lo : hi;
+                }
+                __syncthreads();
+            }
+#pragma unroll
+            for (int e = 0; e < E; ++e) v[e] = s[t * E + e];  // this thread's own slots
+        }
+        for (; stride >= (uint32_t)E; stride >>= 1) {
+            const int lanes = (int)(stride / E);
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const uint64_t w = __shfl_xor(v[e], lanes);
+                const uint32_t p = t * E + e;
+                // keep the larger of the pair at its lower position in a
+                // descending block ((p & size) == 0), the smaller otherwise
+                const bool keep_max = ((p & stride) == 0) == ((p & size) == 0);
+                const uint64_t hi = v[e] > w ? v[e] : w, lo = v[e] > w ? w : v[e];
+                v[e] = keep_max ? hi : lo;
+            }
+        }
+        // strides below E (those below size), inside the thread
+#pragma unroll
+        for (int st = E / 2; st >= 1; st /= 2) {
+            if ((uint32_t)st < size) {  // uniform
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    if ((e & st) == 0) {
+                        const int e2 = e | st;
+                        const bool desc = ((t * E + e) & size) == 0;
+                        const uint64_t a = v[e], b = v[e2];
+                        const uint64_t hi = a > b ? a : b, lo = a > b ? b : a;
+                        v[e] = desc ? hi : lo;
+                        v[e2] = desc ? lo : hi;
+                    }
+                }
+            }
+        }
+    }
+}
+
+// One workgroup per row: the k largest keys of the row, in order.  A row
+// whose candidates were gathered sorts them and keeps the first k.  Any
+// other row is finished here: three more digit rounds inside the bucket
+// (histograms in LDS, over the row) give the k-th key T and kk, the number
+// of keys equal to T in the top k; a walk over the row in index order takes
+// every key above T and the first kk equal to T; those k are sorted.
+// CAP slots of LDS (a power of two, at least cap) hold the keys to sort.
+template <uint32_t CAP>
+__global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
+    const uint32_t* x, int64_t len, uint32_t k, bool largest, const uint64_t* state,
+    const uint64_t* gather, const uint64_t* cand, uint32_t cap, uint32_t* values,
+    int32_t* indices) {
+    static_assert(CAP <= kTopkCand && (CAP & (CAP - 1)) == 0, "LDS sort size");
+    __shared__ uint64_t s[CAP];
+    __shared__ uint32_t s_h[kTopkDigits];
+    __shared__ uint32_t s_part[kTopkFinishThreads / kWave];
+    __shared__ uint32_t s_prefix, s_kk, s_n, s_qbase;
+    __shared__ uint64_t s_prefix64;
+    constexpr uint32_t kT = kTopkFinishThreads;
+    const int64_t row = blockIdx.x;
+    const int w = threadIdx.x / kWave;
+    const int lane = lane_id();
+    const uint32_t m = (uint32_t)gather[2 * row];
+    if (m <= cap) {
+        // The k largest of the m candidates.  Up to kTopkSortAll of them are
+        // all sorted (the first k are the answer); more are first cut to k:
+        // the k-th largest composite C by seven more digit rounds over the
+        // candidates in LDS (the first digit, the key's top byte, is the
+        // bucket's), then the composites >= C (exactly k: composites are
+        // distinct) to the front.
+        // every candidate load in flight at once, then to LDS for the rounds
+        constexpr int kPer = CAP / kTopkFinishThreads > 0 ? CAP / kTopkFinishThreads : 1;
+        const uint64_t* cr = cand + row * cap;
+        uint64_t mine[kPer];
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            const uint32_t i = threadIdx.x + e * kT;
+            mine[e] = i < m ? cr[i] : 0ull;
+        }
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            const uint32_t i = threadIdx.x + e * kT;
+            if (i < m) s[i] = mine[e];
+        }
+        uint64_t prefix = (uint32_t)state[2 * row] & 255u;
+        uint32_t kk = (uint32_t)state[2 * row + 1];
+        const bool cut = m > k && m > kTopkSortAll;  // uniform
+        for (int r = 1; r < 8 && cut; ++r) {
+            for (uint32_t i = threadIdx.x; i < kTopkDigits; i += kT) s_h[i] = 0;
+            __syncthreads();  // also: the candidates are in LDS
+            const int hs = 64 - 8 * r, ds = 56 - 8 * r;
+            for (uint32_t i = threadIdx.x; i < m; i += kT) {
+                const uint64_t c = s[i];
+                if ((c >> hs) == prefix) atomicAdd(&s_h[(uint32_t)(c >> ds) & 255u], 1u);
+            }
+            __syncthreads();
+            const int t = threadIdx.x;
+            const uint32_t c = t < kTopkDigits ? s_h[kTopkDigits - 1 - t] : 0u;
+            const uint32_t inc = wave_incl_scan(c);
+            if (t < kTopkDigits && lane == kWave - 1) s_part[w] = inc;
+            __syncthreads();
+            if (t < kTopkDigits) {
+                uint32_t before = 0;
+                for (int q = 0; q < w; ++q) before += s_part[q];
+                const uint32_t at_least = before + inc, above = at_least - c;
+                if (above < kk && kk <= at_least) {  // exactly one thread
+                    s_prefix64 = (prefix << 8) | (uint32_t)(kTopkDigits - 1 - t);
+                    s_kk = kk - above;
+                }
+            }
+            __syncthreads();
+            prefix = s_prefix64;
+            kk = s_kk;
+        }
+        // prefix: the k-th largest composite (when m > k); each thread still
+        // holds its candidates in `mine`
+        if (threadIdx.x == 0) s_n = 0;
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            const uint32_t i = threadIdx.x + e * kT;
+            if (i < m && (!cut || mine[e] >= prefix)) {
+                // below n (k, or m when all are sorted); checked all the same
+                const uint32_t pos = atomicAdd(&s_n, 1u);
+                if (pos < cap) s[pos] = mine[e];
+            }
+        }
+    } else {
+        const uint32_t* xr = x + row * len;
+        uint32_t prefix = (uint32_t)state[2 * row];
+        uint32_t kk = (uint32_t)state[2 * row + 1];
+        for (int r = 1; r < 4; ++r) {
+            for (uint32_t i = threadIdx.x; i < kTopkDigits; i += kT) s_h[i] = 0;
+            __syncthreads();
+            const int hs = 32 - 8 * r, ds = 24 - 8 * r;
+            for (int64_t i = threadIdx.x; i < len; i += kT) {
+                const uint32_t key = topk_key(xr[i], largest);
+                if ((key >> hs) == prefix) atomicAdd(&s_h[(key >> ds) & 255u], 1u);
+            }
+            __syncthreads();
+            // thread t takes digit 255 - t: an inclusive scan over t counts the
+            // keys with a digit >= its own
+            const int t = threadIdx.x;
+            const uint32_t c = t < kTopkDigits ? s_h[kTopkDigits - 1 - t] : 0u;
+            const uint32_t inc = wave_incl_scan(c);
+            if (t < kTopkDigits && lane == kWave - 1) s_part[w] = inc;
+            __syncthreads();
+            if (t < kTopkDigits) {
+                uint32_t before = 0;
+                for (int q = 0; q < w; ++q) before += s_part[q];
+                const uint32_t at_least = before + inc, above = at_least - c;
+                if (above < kk && kk <= at_least) {  // exactly one thread
+                    s_prefix = (prefix << 8) | (uint32_t)(kTopkDigits - 1 - t);
+                    s_kk = kk - above;
+                }
+            }
+            __syncthreads();
+            prefix = s_prefix;
+            kk = s_kk;
+            __syncthreads();  // s_prefix / s_kk rewritten by the next round
+        }
+        // prefix is now the k-th key T: take every key above it and the
+        // first kk equal to it, in index order
+        if (threadIdx.x == 0) s_n = s_qbase = 0;
+        __syncthreads();
+        for (int64_t c0 = 0; c0 < len; c0 += kT) {
+            const int64_t i = c0 + threadIdx.x;
+            const uint32_t key = i < len ? topk_key(xr[i], largest) : 0u;
+            const bool a = i < len && key > prefix, q = i < len && key == prefix;
+            const uint64_t qb = __ballot(q);
+            if (lane == 0) s_part[w] = (uint32_t)__builtin_popcountll(qb);
+            __syncthreads();
+            uint32_t r = s_qbase + __builtin_amdgcn_mbcnt_hi((uint32_t)(qb >> 32),
+                                                             __builtin_amdgcn_mbcnt_lo((uint32_t)qb, 0));
+            uint32_t chunk = 0;
+            for (int q2 = 0; q2 < (int)(kT / kWave); ++q2) {
+                if (q2 < w) r += s_part[q2];
+                chunk += s_part[q2];
+            }
+            if (a || (q && r < kk)) {
+                const uint32_t pos = atomicAdd(&s_n, 1u);  // below k; checked all the same
+                if (pos < cap) s[pos] = topk_composite(key, (uint32_t)i);
+            }
+            __syncthreads();
+            if (threadIdx.x == 0) s_qbase += chunk;
+            __syncthreads();
+        }
+    }
+    // the n kept keys are s[0, n) (n >= k): sorted in registers, E per thread
+    const uint32_t n = (m <= cap && m <= kTopkSortAll) ? m : k;
+    uint32_t npow = 1;
+    while (npow < n) npow <<= 1;
+    __syncthreads();
+    auto sort_out = [&](auto e_c) {
+        constexpr int E = decltype(e_c)::value;
+        static_assert((uint32_t)E * kT <= CAP || E == 1, "LDS slots for the register sort");
+        uint64_t v[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const uint32_t p = threadIdx.x * E + e;
+            v[e] = p < n ? s[p] : 0ull;
+        }
+        __syncthreads();  // every kept key read before the sort writes LDS
+        bitonic_desc_regs<E>(v, s, npow, kT);
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const uint32_t p = threadIdx.x * E + e;
+            if (p < k) {
+                const uint32_t key = (uint32_t)(v[e] >> 32);
+                const uint32_t code = largest ? key : ~key;
+                values[row * k + p] = code ^ ((code >> 31) ? 0x80000000u : 0xFFFFFFFFu);
+                indices[row * k + p] = (int32_t)~(uint32_t)v[e];
+            }
+        }
+    };
+    if (npow <= kT)
+        sort_out(std::integral_constant<int, 1>{});
+    else if (npow <= 2 * kT)
+        sort_out(std::integral_constant<int, 2>{});
+    else if (CAP >= 4 * kT && npow <= 4 * kT)
+        sort_out(std::integral_constant<int, (CAP >= 4 * kT ? 4 : 1)>{});
+    else
+        sort_out(std::integral_constant<int, (CAP >= 8 * kT ? 8 : 1)>{});
 }
 
 // ---------------------------------------------------------------- launch
@@ -278,24 +628,37 @@ __global__ __launch_bounds__(kTopkSortThreads) void k_topk_sort(
 // Scratch: the k kept values and indices per row, and for the radix sort its
 // two ping-pong buffers.
 static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+// The gather route: rows of at most kTopkGatherMaxLen with k <= kTopkSortMax,
+// its count round on tiles of at most 8192 (more workgroups for the one read
+// from HBM).
+static bool topk_gather_route(int64_t len, int64_t k) {
+    return len <= kTopkGatherMaxLen && k <= kTopkSortMax;
+}
+static int64_t topk_gather_tile(int64_t len) { return len > 16384 ? 8192 : 4096; }
+static uint32_t topk_cap(int64_t len) {
+    return (uint32_t)(len < (int64_t)kTopkCand ? len : (int64_t)kTopkCand);
+}
 struct TopkLayout {
-    size_t hist, state, arrivals, end;
+    size_t hist, state, arrivals, gather, end;
 };
-static TopkLayout topk_layout(int64_t rows, int64_t len) {
-    const size_t tiles = (size_t)rows * (size_t)row_segments(len);
+static TopkLayout topk_layout(int64_t rows, int64_t len, int64_t k) {
+    const int64_t t = topk_gather_route(len, k) ? topk_gather_tile(len) : row_tile(len);
+    const size_t tiles = (size_t)rows * (size_t)((len + t - 1) / t);
     TopkLayout l;
     l.hist = align256(kWsHeader + 2 * tiles * sizeof(uint64_t));
     l.state = align256(l.hist + tiles * kTopkDigits * sizeof(uint32_t));
     l.arrivals = l.state + (size_t)rows * 2 * sizeof(uint64_t);
-    l.end = l.arrivals + (size_t)rows * sizeof(uint64_t);
+    l.gather = l.arrivals + (size_t)rows * sizeof(uint64_t);
+    l.end = l.gather + (size_t)rows * 2 * sizeof(uint64_t);
     return l;
 }
 size_t topk_ws_bytes(int64_t rows, int64_t len, int64_t k) {
-    const size_t a = topk_layout(rows, len).end;
+    const size_t a = topk_layout(rows, len, k).end;
     const size_t b = k > kTopkSortMax ? radix_rows_ws_bytes(rows, k) : 0;
     return a > b ? a : b;
 }
-size_t topk_scratch_bytes(int64_t rows, int64_t k) {
+size_t topk_scratch_bytes(int64_t rows, int64_t len, int64_t k) {
+    if (topk_gather_route(len, k)) return align256((size_t)rows * topk_cap(len) * sizeof(uint64_t));
     return (k > kTopkSortMax ? 4 : 2) * align256((size_t)rows * (size_t)k * 4);
 }
 
@@ -310,19 +673,23 @@ static hipError_t topk_select(bool vec, const uint32_t* x, int64_t rows, int64_t
     const uint32_t nt = (uint32_t)(rows * segs);
     const unsigned threads = vec ? TV::kThreads : TU::kThreads;
     char* w = reinterpret_cast<char*>(ws);
-    const TopkLayout l = topk_layout(rows, len);
+    const TopkLayout l = topk_layout(rows, len, k);
     uint32_t* hist = reinterpret_cast<uint32_t*>(w + l.hist);
     uint64_t* state = reinterpret_cast<uint64_t*>(w + l.state);
     uint64_t* arrivals = reinterpret_cast<uint64_t*>(w + l.arrivals);
     const uint32_t kk = (uint32_t)k;
     hipLaunchKernelGGL((vec ? k_topk_hist<TV, true, 0> : k_topk_hist<TU, false, 0>), dim3(nt),
-                       dim3(threads), 0, stream, x, len, segs, kk, largest, hist, state, arrivals);
+                       dim3(threads), 0, stream, x, len, segs, kk, largest, hist, state, arrivals,
+                       nullptr);
     hipLaunchKernelGGL((vec ? k_topk_hist<TV, true, 1> : k_topk_hist<TU, false, 1>), dim3(nt),
-                       dim3(threads), 0, stream, x, len, segs, kk, largest, hist, state, arrivals);
+                       dim3(threads), 0, stream, x, len, segs, kk, largest, hist, state, arrivals,
+                       nullptr);
     hipLaunchKernelGGL((vec ? k_topk_hist<TV, true, 2> : k_topk_hist<TU, false, 2>), dim3(nt),
-                       dim3(threads), 0, stream, x, len, segs, kk, largest, hist, state, arrivals);
+                       dim3(threads), 0, stream, x, len, segs, kk, largest, hist, state, arrivals,
+                       nullptr);
     hipLaunchKernelGGL((vec ? k_topk_hist<TV, true, 3> : k_topk_hist<TU, false, 3>), dim3(nt),
-                       dim3(threads), 0, stream, x, len, segs, kk, largest, hist, state, arrivals);
+                       dim3(threads), 0, stream, x, len, segs, kk, largest, hist, state, arrivals,
+                       nullptr);
     // The split keeps its flags and the tile's packed counts in registers as
     // well: it takes the tile shape with half the chunks and twice the waves
     // (16-byte loads still when aligned).
@@ -334,10 +701,71 @@ static hipError_t topk_select(bool vec, const uint32_t* x, int64_t rows, int64_t
     return hipGetLastError();
 }
 
+// The count round on the row kernels' tile (few tiles per row: the row's
+// last arrival is one of few compare-and-swaps on its counter), the gather
+// on tiles of G (more workgroups for reading the rows a second time).
+template <class H>
+static void topk_count_round0(bool vec, const uint32_t* x, int64_t rows, int64_t len, uint32_t k,
+                              bool largest, uint32_t* hist, uint64_t* state, uint64_t* arrivals,
+                              uint64_t* gather, hipStream_t stream) {
+    using TV = RowTile<uint32_t, H, true>;
+    using TU = RowTile<uint32_t, H, false>;
+    const uint32_t segs = (uint32_t)((len + TV::kElems - 1) / TV::kElems);
+    hipLaunchKernelGGL((vec ? k_topk_hist<TV, true, 0> : k_topk_hist<TU, false, 0>),
+                       dim3((uint32_t)(rows * segs)), dim3(vec ? TV::kThreads : TU::kThreads), 0,
+                       stream, x, len, segs, k, largest, hist, state, arrivals, gather);
+}
+
+template <class G>
+static hipError_t topk_gather(bool vec, const uint32_t* x, int64_t rows, int64_t len, int64_t k,
+                              bool largest, uint32_t* values, int32_t* indices, void* scratch,
+                              void* ws, hipStream_t stream) {
+    using TV = RowTile<uint32_t, G, true>;
+    using TU = RowTile<uint32_t, G, false>;
+    static_assert(TV::kElems == TU::kElems, "one tile size per geometry");
+    const uint32_t segs = (uint32_t)((len + TV::kElems - 1) / TV::kElems);
+    const uint32_t nt = (uint32_t)(rows * segs);
+    const unsigned threads = vec ? TV::kThreads : TU::kThreads;
+    char* w = reinterpret_cast<char*>(ws);
+    const TopkLayout l = topk_layout(rows, len, k);
+    uint32_t* hist = reinterpret_cast<uint32_t*>(w + l.hist);
+    uint64_t* state = reinterpret_cast<uint64_t*>(w + l.state);
+    uint64_t* arrivals = reinterpret_cast<uint64_t*>(w + l.arrivals);
+    uint64_t* gather = reinterpret_cast<uint64_t*>(w + l.gather);
+    uint64_t* cand = reinterpret_cast<uint64_t*>(scratch);
+    const uint32_t kk = (uint32_t)k, cap = topk_cap(len);
+    const int64_t h = row_tile(len);
+    if (h == 32768)
+        topk_count_round0<RGeomL>(vec, x, rows, len, kk, largest, hist, state, arrivals, gather, stream);
+    else if (h == 8192)
+        topk_count_round0<RGeomM>(vec, x, rows, len, kk, largest, hist, state, arrivals, gather, stream);
+    else
+        topk_count_round0<RGeomS>(vec, x, rows, len, kk, largest, hist, state, arrivals, gather, stream);
+    hipLaunchKernelGGL((vec ? k_topk_gather<TV, true> : k_topk_gather<TU, false>), dim3(nt),
+                       dim3(threads), 0, stream, x, len, segs, largest, (const uint64_t*)state,
+                       gather, cand, cap);
+    // the LDS sort sized to the row (cap <= CAP)
+    auto kf = cap > 8192 ? k_topk_finish<kTopkCand>
+                         : (cap > 2048 ? k_topk_finish<8192> : k_topk_finish<2048>);
+    hipLaunchKernelGGL(kf, dim3((uint32_t)rows), dim3(kTopkFinishThreads), 0, stream, x, len, kk,
+                       largest, (const uint64_t*)state, (const uint64_t*)gather,
+                       (const uint64_t*)cand, cap, values, indices);
+    return hipGetLastError();
+}
+
 hipError_t launch_topk(const float* x, float* values, int32_t* indices, int64_t rows, int64_t len,
                        int64_t k, bool largest, void* scratch, void* ws, hipStream_t stream) {
     if (rows == 0 || k == 0) return hipSuccess;
     const bool vec = (len % 4 == 0) && ((uintptr_t)x % 16) == 0;
+    if (topk_gather_route(len, k)) {
+        const uint32_t* xb = reinterpret_cast<const uint32_t*>(x);
+        uint32_t* vb = reinterpret_cast<uint32_t*>(values);
+        return topk_gather_tile(len) == 8192
+                   ? topk_gather<RGeomM>(vec, xb, rows, len, k, largest, vb, indices, scratch, ws,
+                                         stream)
+                   : topk_gather<RGeomS>(vec, xb, rows, len, k, largest, vb, indices, scratch, ws,
+                                         stream);
+    }
     const size_t mb = align256((size_t)rows * (size_t)k * 4);
     char* s = reinterpret_cast<char*>(scratch);
     uint32_t* sel_vals = reinterpret_cast<uint32_t*>(s);

@@ -23,7 +23,7 @@ from paper_2505_15112_amd import build as B
 SOURCES = sorted(f for f in os.listdir(B.CSRC) if f.endswith(".hip"))
 TILE_KERNELS = ("k_scan_lookback", "k_scan_lookback_lds", "k_scan_mfma_f16", "k_rss_reduce",
                 "k_rss_rescan", "k_rows_lookback", "k_topp", "k_topp_head", "k_topp_finish", "k_compact",
-                "k_split", "k_radix4_count", "k_radix4_scatter", "k_radix8_count",
+                "k_split", "k_radix4_count", "k_radix4_scatter", "k_radix8_count", "k_topk_gather",
                 "k_radix8_scatter", "k_topk_hist", "k_topk_select")
 
 
