@@ -73,6 +73,7 @@ enum class Mut {
     RowPlainCount,     // the row counter counts whatever the word holds
     RowNoClearCounter, // the last arrival leaves the row counter set
     XcdTickets,        // one ticket counter per XCD: tile = 8 * ticket + xcd
+    PersistentResetAtTiles,  // persistent grid: the count restarts at the last tile's ticket
 };
 Mut g_mut = Mut::None;
 
@@ -89,6 +90,7 @@ const MutName kMutations[] = {
     {"row_plain_count", Mut::RowPlainCount},
     {"row_no_clear_counter", Mut::RowNoClearCounter},
     {"xcd_tickets", Mut::XcdTickets},
+    {"persistent_reset_at_tiles", Mut::PersistentResetAtTiles},
 };
 
 [[noreturn]] void fail(const std::string& what) {
@@ -313,6 +315,42 @@ void scan_launch(Workspace& ws, const std::vector<uint32_t>& x, std::vector<uint
     launch(nwg, slots, dispatch_order(nwg, order_kind, seed), body, seed);
 }
 
+// The same scan by a persistent grid of `grid` workgroups, each holding the
+// ticket of its next tile while it finishes the current one (its next
+// tile's loads in flight meanwhile): take a ticket; while it is a tile, take
+// the next ticket, then scan the tile.  Every workgroup takes exactly one
+// ticket past the last tile, so the count restarts at ticket ntiles + grid - 1.
+void scan_launch_persistent(Workspace& ws, const std::vector<uint32_t>& x, std::vector<uint32_t>& y,
+                            uint32_t ntiles, uint32_t tile_len, uint32_t carry, uint32_t grid,
+                            int slots, uint64_t seed) {
+    const uint32_t len = (uint32_t)x.size();
+    std::atomic<uint64_t>* status = ws.words.data();
+    const size_t nwords = ws.words.size();
+    const uint32_t reset_at = g_mut == Mut::PersistentResetAtTiles ? ntiles : ntiles + grid;
+    auto body = [&](uint32_t block) {
+        Ticket cur = take_ticket(ws, reset_at, block);
+        while (cur.tile < ntiles) {
+            const Ticket next = take_ticket(ws, reset_at, block);
+            const uint64_t lo = (uint64_t)cur.tile * tile_len;
+            const uint64_t hi = std::min<uint64_t>(lo + tile_len, len);
+            uint32_t agg = 0;
+            for (uint64_t i = lo; i < hi; ++i) agg += x[i];
+            const uint32_t base = cur.tile == 0 ? carry : 0;
+            const uint32_t excl = lookback(ws, status, cur.tile, 0, agg, base, cur.epoch);
+            uint32_t run = excl;
+            for (uint64_t i = lo; i < hi; ++i) y[i] = (run += x[i]);
+            if (next.epoch != cur.epoch) {  // a ticket of a later launch: the protocol is broken
+                ws.error.store(1);
+                break;
+            }
+            cur = next;
+        }
+        if (cur.tile >= reset_at && g_mut != Mut::PersistentResetAtTiles) ws.error.store(1);
+        finish_epoch(ws, cur.epoch, grid, status, nwords);
+    };
+    launch(grid, slots, dispatch_order(grid, 0, seed), body, seed);
+}
+
 // ---------------------------------------------------------------- row arrivals
 uint32_t row_arrive(std::atomic<uint64_t>* counter) {
     pause_point();
@@ -422,6 +460,22 @@ struct Runner {
         check_scan(x, y, rows, carry, what);
     }
 
+    void persistent(uint32_t ntiles, uint32_t tile_len, uint32_t grid, int slots) {
+        seed_thread(seed * 7907 + launches);
+        const uint32_t len = ntiles * tile_len - rnd() % tile_len;
+        const uint32_t carry = rnd();
+        auto x = make_input(len, seed * 104723 + launches);
+        std::vector<uint32_t> y(x.size(), 0xDEADBEEFu);
+        const std::string what = "persistent launch " + std::to_string(launches) + " (tiles " +
+                                 std::to_string(ntiles) + ", grid " + std::to_string(grid) +
+                                 ", slots " + std::to_string(slots) + ", epoch " +
+                                 std::to_string(ws.epoch()) + ")";
+        scan_launch_persistent(ws, x, y, ntiles, tile_len, carry, grid, slots, seed + launches);
+        ++launches;
+        check_after_launch(ws, what);
+        check_scan(x, y, 1, carry, what);
+    }
+
     void rows(uint32_t nrows, uint32_t segs, uint32_t tile_len, int slots, int order_kind) {
         const uint32_t len = segs * tile_len - rnd() % tile_len;
         auto x = make_input((size_t)nrows * len, seed * 15485863 + launches);
@@ -512,12 +566,29 @@ void scenario_held_xcd(uint64_t seed, bool) {
     for (int i = 0; i < 4; ++i) r.scan(1, 257 + 64 * i, 5, 24, 2, false);
 }
 
+// Persistent grids (each workgroup holding its next tile's ticket) between
+// ordinary launches on one workspace, across the epoch wrap; grids larger
+// than the resident slots start late and still finish.
+void scenario_persistent(uint64_t seed, bool quick) {
+    Workspace ws(1 << 13);
+    ws.ticket.store((uint64_t)(kEpochMask - 4) << 32);
+    Runner r{ws, seed};
+    const int n = quick ? 6 : 14;
+    for (int i = 0; i < n; ++i) {
+        seed_thread(seed * 733 + i);
+        const uint32_t grid = 1 + rnd() % 40;
+        r.persistent(1 + rnd() % 700, 1 + rnd() % 12, grid, 1 + (int)(rnd() % 40));
+        if (i % 3 == 2) r.scan(1, 1 + rnd() % 200, 1 + rnd() % 9, 8, 0);
+    }
+}
+
 struct Scenario { const char* name; void (*run)(uint64_t, bool); };
 const Scenario kScenarios[] = {
     {"scans", scenario_scans},
     {"mixed", scenario_mixed},
     {"wrap", scenario_wrap},
     {"held_xcd", scenario_held_xcd},
+    {"persistent", scenario_persistent},
 };
 
 }  // namespace

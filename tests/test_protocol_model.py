@@ -23,7 +23,7 @@ pytestmark = pytest.mark.skipif(shutil.which("g++") is None, reason="g++ is need
 
 MUTATIONS = ["blockidx_tiles", "no_ticket_reset", "ignore_epoch", "no_wrap_clear", "x_as_zero",
              "drop_p_lane", "window_from_self", "row_plain_count", "row_no_clear_counter",
-             "xcd_tickets"]
+             "xcd_tickets", "persistent_reset_at_tiles"]
 
 
 def _build(out, *flags):
