@@ -346,6 +346,7 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_gather(
     if (lane_id() == kWave - 1) s_wtot[w] = incl;
     __syncthreads();
     if (threadIdx.x == 0) {
+        adversarial_pause(blockIdx.x);  // reservations in any order
         uint32_t total = 0;
         for (int q = 0; q < TileT::WAVES; ++q) total += s_wtot[q];
         s_base = total ? (uint32_t)__hip_atomic_fetch_add(&gather[2 * row + 1], (uint64_t)total,

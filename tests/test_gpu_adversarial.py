@@ -128,11 +128,16 @@ def test_topp_cutoff_and_sampler(ops, adversarial):
     assert_equal_first_diff(tok, oracle.topp_sample_f32(ex, theta, 2.0**-9)[0], "adv sampler")
 
 
-@pytest.mark.parametrize("k", [64, 9000])
-def test_topk(ops, adversarial, k):
-    """Top-k's digit rounds (arrival counters) and its two-chain split."""
-    announce("adversarial topk", k)
-    x = W.values_f32(12 * 131_072, seed=k).reshape(12, 131_072)
+@pytest.mark.parametrize("k,kind", [(64, "normal"), (4096, "normal"), (64, "ties"), (9000, "normal")])
+def test_topk(ops, adversarial, k, kind):
+    """Top-k's digit rounds (arrival counters), the gather's reservations in
+    any order, the long way for rows with too many candidates (ties), and
+    the two-chain split (k above 8192)."""
+    announce("adversarial topk", k, kind)
+    if kind == "ties":
+        x = np.random.default_rng(k).integers(-3, 4, (12, 131_072)).astype(np.float32)
+    else:
+        x = W.values_f32(12 * 131_072, seed=k).reshape(12, 131_072)
     v, i = ops.topk_rows_f32(to_dev(x), k)
     rv, ri = oracle.topk_rows_f32(x, k)
     assert_equal_first_diff(to_host(i), ri, "adv topk indices")
