@@ -405,15 +405,15 @@ __device__ __forceinline__ void bitonic_desc_regs(uint64_t (&v)[E], uint64_t* s,
         }
         for (; stride >= (uint32_t)E; stride >>= 1) {
             const int lanes = (int)(stride / E);
+            // stride >= E: the thread's positions share their stride and size
+            // bits, so one choice per stage: keep the larger of each pair at
+            // the lower position of a descending block, the smaller otherwise
+            const uint32_t p0 = t * E;
+            const bool keep_max = ((p0 & stride) == 0) == ((p0 & size) == 0);
 #pragma unroll
             for (int e = 0; e < E; ++e) {
                 const uint64_t w = __shfl_xor(v[e], lanes);
-                const uint32_t p = t * E + e;
-                // keep the larger of the pair at its lower position in a
-                // descending block ((p & size) == 0), the smaller otherwise
-                const bool keep_max = ((p & stride) == 0) == ((p & size) == 0);
-                const uint64_t hi = v[e] > w ? v[e] : w, lo = v[e] > w ? w : v[e];
-                v[e] = keep_max ? hi : lo;
+                v[e] = ((v[e] > w) != keep_max) ? w : v[e];
             }
         }
         // strides below E (those below size), inside the thread
@@ -426,9 +426,9 @@ __device__ __forceinline__ void bitonic_desc_regs(uint64_t (&v)[E], uint64_t* s,
                         const int e2 = e | st;
                         const bool desc = ((t * E + e) & size) == 0;
                         const uint64_t a = v[e], b = v[e2];
-                        const uint64_t hi = a > b ? a : b, lo = a > b ? b : a;
-                        v[e] = desc ? hi : lo;
-                        v[e2] = desc ? lo : hi;
+                        const bool sw = (a < b) == desc;
+                        v[e] = sw ? b : a;
+                        v[e2] = sw ? a : b;
                     }
                 }
             }
