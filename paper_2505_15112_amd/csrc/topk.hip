@@ -378,11 +378,16 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_gather(
 // never meets a real key): strides below E inside the thread, strides below
 // 64 E between the lanes of a wavefront (shuffles, no barrier), larger
 // strides through LDS (s, at least max(npow, E * nthreads) slots).
+//
+// `run` (a power of two, at most npow): sort each block of `run` positions,
+// every block descending (run = npow: the whole array).
 template <int E>
 __device__ __forceinline__ void bitonic_desc_regs(uint64_t (&v)[E], uint64_t* s, uint32_t npow,
-                                                  uint32_t nthreads) {
+                                                  uint32_t nthreads, uint32_t run) {
     const uint32_t t = threadIdx.x;
-    for (uint32_t size = 2; size <= npow; size <<= 1) {
+    for (uint32_t size = 2; size <= run; size <<= 1) {
+        // blocks of `size` alternate direction, except in the last merge
+        const bool all_desc = size == run;
         uint32_t stride = size >> 1;
         if (stride >= (uint32_t)(kWave * E)) {  // uniform
 #pragma unroll
@@ -394,7 +399,7 @@ __device__ __forceinline__ void bitonic_desc_regs(uint64_t (&v)[E], uint64_t* s,
                     const uint32_t j = i + stride;
                     const uint64_t a = s[i], b = s[j];
                     const uint64_t hi = a > b ? a : b, lo = a > b ? b : a;
-                    const bool desc = (i & size) == 0;
+                    const bool desc = all_desc || (i & size) == 0;
                     s[i] = desc ? hi : lo;
                     s[j] = desc ? lo : hi;
                 }
@@ -409,7 +414,7 @@ __device__ __forceinline__ void bitonic_desc_regs(uint64_t (&v)[E], uint64_t* s,
             // bits, so one choice per stage: keep the larger of each pair at
             // the lower position of a descending block, the smaller otherwise
             const uint32_t p0 = t * E;
-            const bool keep_max = ((p0 & stride) == 0) == ((p0 & size) == 0);
+            const bool keep_max = ((p0 & stride) == 0) == (all_desc || (p0 & size) == 0);
 #pragma unroll
             for (int e = 0; e < E; ++e) {
                 const uint64_t w = __shfl_xor(v[e], lanes);
@@ -424,7 +429,7 @@ __device__ __forceinline__ void bitonic_desc_regs(uint64_t (&v)[E], uint64_t* s,
                 for (int e = 0; e < E; ++e) {
                     if ((e & st) == 0) {
                         const int e2 = e | st;
-                        const bool desc = ((t * E + e) & size) == 0;
+                        const bool desc = all_desc || ((t * E + e) & size) == 0;
                         const uint64_t a = v[e], b = v[e2];
                         const bool sw = (a < b) == desc;
                         v[e] = sw ? b : a;
@@ -433,6 +438,32 @@ __device__ __forceinline__ void bitonic_desc_regs(uint64_t (&v)[E], uint64_t* s,
                 }
             }
         }
+    }
+}
+
+// Merge path: with runs of L descending keys in src, thread t's E outputs
+// of the merged runs of 2 L (positions t E .. t E + E - 1): the number of
+// them taken from the first run by a binary search, then E merge steps.
+// Keys are distinct (composites), so there are no ties.
+template <int E>
+__device__ __forceinline__ void merge_desc(const uint64_t* src, uint32_t L, uint64_t (&out)[E]) {
+    const uint32_t i0 = threadIdx.x * E;
+    const uint32_t pair = i0 / (2 * L);
+    const uint32_t r = i0 - pair * 2 * L;
+    const uint64_t* A = src + pair * 2 * L;
+    const uint64_t* B = A + L;
+    uint32_t lo = r > L ? r - L : 0, hi = r < L ? r : L;
+    while (lo < hi) {  // A's share of the r largest
+        const uint32_t mid = (lo + hi) / 2;
+        if (A[mid] > B[r - mid - 1]) lo = mid + 1; else hi = mid;
+    }
+    uint32_t a = lo, b = r - lo;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const bool take_a = b >= L || (a < L && A[a] > B[b]);
+        out[e] = take_a ? A[a] : B[b];
+        a += take_a ? 1u : 0u;
+        b += take_a ? 0u : 1u;
     }
 }
 
@@ -599,7 +630,22 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
             v[e] = p < n ? s[p] : 0ull;
         }
         __syncthreads();  // every kept key read before the sort writes LDS
-        bitonic_desc_regs<E>(v, s, npow, kT);
+        const uint32_t wrun = (uint32_t)(kWave * E);
+        if (npow > wrun) {
+            // each wavefront's run of 64 E keys sorted in registers, then
+            // merge levels through LDS (threads past npow merge padding
+            // inside s[0, max(npow, E * kT)) and are never read)
+            bitonic_desc_regs<E>(v, s, npow, kT, wrun);
+            for (uint32_t L = wrun; L < npow; L <<= 1) {
+#pragma unroll
+                for (int e = 0; e < E; ++e) s[threadIdx.x * E + e] = v[e];
+                __syncthreads();
+                merge_desc<E>(s, L, v);
+                __syncthreads();  // s is rewritten by the next level
+            }
+        } else {
+            bitonic_desc_regs<E>(v, s, npow, kT, npow);
+        }
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             const uint32_t p = threadIdx.x * E + e;
