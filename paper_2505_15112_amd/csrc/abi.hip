@@ -244,7 +244,7 @@ int libscan_workspace_bytes(int op, int64_t n, int64_t rows, int64_t len, int bi
             if (r != LIBSCAN_OK) return r;
             if (len > INT32_MAX) return LIBSCAN_ERANGE;
             if (op == LIBSCAN_OP_WEIGHTED_SAMPLE) {
-                *bytes = ls::topp_ws_bytes(rows, len);
+                *bytes = ls::weighted_ws_bytes(rows, len);
             } else {
                 if (!ls::radix_rows_fit(rows, len)) return LIBSCAN_ERANGE;
                 *bytes = ls::topp_sample_ws_bytes(rows, len);
@@ -480,7 +480,7 @@ int weighted_sample_f32(const float* w, const float* theta_dev, int32_t* out, in
                         int64_t len, void* ws, size_t ws_bytes, void* stream) {
     const int c = check_sample(w, theta_dev, out, nullptr, rows, len);
     if (c != LIBSCAN_OK || rows == 0) return c;
-    const int k = check_ws(ws, ws_bytes, ls::topp_ws_bytes(rows, len));
+    const int k = check_ws(ws, ws_bytes, ls::weighted_ws_bytes(rows, len));
     if (k != LIBSCAN_OK) return k;
     return hip_status(ls::launch_weighted_sample(w, theta_dev, out, rows, len, ws,
                                                  (hipStream_t)stream));

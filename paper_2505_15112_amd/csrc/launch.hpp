@@ -53,6 +53,7 @@ size_t scan_rows_ws_bytes(int64_t rows, int64_t len);
 hipError_t launch_scan_rows(Kind kind, bool exclusive, const void* x, void* y, int64_t rows,
                             int64_t len, void* ws, size_t ws_bytes, hipStream_t stream);
 size_t topp_ws_bytes(int64_t rows, int64_t len);
+size_t weighted_ws_bytes(int64_t rows, int64_t len);
 bool radix_rows_fit(int64_t rows, int64_t len);
 size_t topp_sample_ws_bytes(int64_t rows, int64_t len);
 size_t topp_sample_scratch_bytes(int64_t rows, int64_t len);

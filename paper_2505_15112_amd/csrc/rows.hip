@@ -13,6 +13,9 @@
 //    4096 workgroups to fill 256 CUs.
 // The top-p cutoff needs only one index per row: every tile sums its part of
 // the row and the row's last tile to finish locates the index (k_topp).
+// Weighted sampling of rows up to 2^22 and the cutoff of rows up to 2^20 run
+// as two kernels instead (tile sums, then one workgroup per row), with no
+// per-row arrival.
 #include <limits.h>
 
 #include "launch.hpp"
@@ -330,6 +333,72 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp(
         __hip_atomic_store(&arrivals[row], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// ---------------------------------------------------------------- weighted sampling, two kernels
+//
+// Rows of up to kWeightedMaxLen elements: no workgroup waits for another and
+// none counts arrivals.  k_tile_sums stores the sum of every tile of every
+// row (one read of the weights, all tiles at once); k_weighted_finish, one
+// workgroup per row, adds the row's tile sums in tile order into the total
+// W, finds the first tile whose inclusive sum exceeds theta * W (the tile
+// sums are the ones the search below continues from, so the verdict and the
+// search agree), re-reads that one tile and finds the index in it.  The tile
+// sums are plain fp32 values in the low halves of workspace words (the top
+// bits clear, as the workspace invariant asks), written before they are read
+// in every call.  This is k_topp's weighted mode with the row's last-arrival
+// step replaced by a kernel boundary, which costs less than the per-row
+// arrival atomics.
+constexpr int64_t kWeightedMaxLen = int64_t(1) << 22;
+static inline bool weighted_two_kernels(int64_t len) {
+    return len > kRowTile && len <= kWeightedMaxLen;
+}
+static inline int64_t weighted_tile(int64_t len) { return len > 16384 ? 8192 : 4096; }
+
+template <class TileT, bool VEC>
+__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_tile_sums(
+    const float* x, int64_t len, uint32_t segs, uint64_t* sums) {
+    __shared__ float s_wtot[TileT::WAVES];
+    const int64_t row = blockIdx.x / segs;
+    const uint32_t seg = blockIdx.x - (uint32_t)row * segs;
+    float v[TileT::J][TileT::V];
+    TileT::template load<VEC, true>(x + row * len, len, (int64_t)seg * TileT::kElems, v);
+    float wofs;
+    const float agg = TileT::combine_waves(wave_sum(TileT::lane_sum(v)), s_wtot, &wofs);
+    if (threadIdx.x == 0) sums[blockIdx.x] = Bits<float>::to(agg);
+}
+
+template <class TileT, bool VEC>
+__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_weighted_finish(
+    const float* w, const float* theta, int32_t* out, int64_t len, uint32_t segs,
+    const uint64_t* sums) {
+    __shared__ float s_wtot[TileT::WAVES];
+    __shared__ int32_t s_min[TileT::WAVES];
+    __shared__ float s_val;
+    __shared__ int32_t s_tile;
+    __shared__ float s_excl, s_thr;
+    const int64_t row = blockIdx.x;
+    const uint64_t* rs = sums + row * segs;
+    if (threadIdx.x < kWave) {
+        const float thr = theta[row] * topp_total(rs, segs);
+        float excl = 0.f;
+        const int32_t t = topp_find_tile(rs, segs, thr, true, &excl);
+        if (lane_id() == 0) {
+            s_tile = t;
+            s_excl = excl;
+            s_thr = thr;
+        }
+    }
+    __syncthreads();
+    const int32_t t = s_tile;
+    int64_t found = len - 1;  // no tile exceeds theta * W (rounding): the last index
+    if (t >= 0) {
+        float at;
+        found = topp_find<TileT, VEC, true, false>(w + row * len, len, (int64_t)t * TileT::kElems,
+                                                   s_excl, s_thr, len - 1, s_wtot, s_min, &s_val,
+                                                   at);
+    }
+    if (threadIdx.x == 0) out[row] = (int32_t)found;
+}
+
 // ---------------------------------------------------------------- top-p, early exit
 //
 // The cutoff for rows of 2 to kEarlyMaxSegs tiles of 4096 elements, reading
@@ -593,6 +662,15 @@ static size_t topp_arrivals_offset(int64_t rows, int64_t len) {
 size_t topp_ws_bytes(int64_t rows, int64_t len) {
     return topp_arrivals_offset(rows, len) + (size_t)rows * sizeof(uint64_t);
 }
+// Weighted sampling: the top-p layout, or one tile sum per row tile of the
+// two-kernel path.
+size_t weighted_ws_bytes(int64_t rows, int64_t len) {
+    const size_t a = topp_ws_bytes(rows, len);
+    if (!weighted_two_kernels(len)) return a;
+    const int64_t t = weighted_tile(len);
+    const size_t b = kWsHeader + (size_t)rows * (size_t)((len + t - 1) / t) * sizeof(uint64_t);
+    return a > b ? a : b;
+}
 static bool topp_early(int64_t len);
 static size_t topp_early_ws_bytes(int64_t rows, int64_t len);
 size_t scan_rows_ws_bytes(int64_t rows, int64_t len) {
@@ -735,8 +813,24 @@ hipError_t launch_topp_cutoff(const float* probs, int32_t* cutoff, int64_t rows,
                                    stream);
 }
 
+template <class G>
+static void weighted_two(bool vec, const float* w, const float* theta, int32_t* out, int64_t rows,
+                         int64_t len, void* ws, hipStream_t stream) {
+    using TV = RowTile<float, G, true>;
+    using TU = RowTile<float, G, false>;
+    static_assert(TV::kElems == TU::kElems, "one tile size per geometry");
+    const uint32_t segs = (uint32_t)((len + TV::kElems - 1) / TV::kElems);
+    const unsigned threads = vec ? TV::kThreads : TU::kThreads;
+    uint64_t* sums = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
+    hipLaunchKernelGGL((vec ? k_tile_sums<TV, true> : k_tile_sums<TU, false>),
+                       dim3((unsigned)(rows * segs)), dim3(threads), 0, stream, w, len, segs, sums);
+    hipLaunchKernelGGL((vec ? k_weighted_finish<TV, true> : k_weighted_finish<TU, false>),
+                       dim3((unsigned)rows), dim3(threads), 0, stream, w, theta, out, len, segs,
+                       (const uint64_t*)sums);
+}
+
 // Appendix "Weighted Sampling", per row (any length; workspace
-// topp_ws_bytes(rows, len)).
+// weighted_ws_bytes(rows, len)).
 hipError_t launch_weighted_sample(const float* w, const float* theta, int32_t* out, int64_t rows,
                                   int64_t len, void* ws, hipStream_t stream) {
     if (rows == 0) return hipSuccess;
@@ -746,7 +840,15 @@ hipError_t launch_weighted_sample(const float* w, const float* theta, int32_t* o
         return hipGetLastError();
     }
     const bool vec = (len % 4 == 0) && aligned16(w);
-    topp_any<ToppMode::Weighted>(vec, w, nullptr, theta, nullptr, out, rows, len, 0.f, ws, stream);
+    if (weighted_two_kernels(len)) {
+        if (weighted_tile(len) == 8192)
+            weighted_two<RGeomM>(vec, w, theta, out, rows, len, ws, stream);
+        else
+            weighted_two<RGeomS>(vec, w, theta, out, rows, len, ws, stream);
+    } else {
+        topp_any<ToppMode::Weighted>(vec, w, nullptr, theta, nullptr, out, rows, len, 0.f, ws,
+                                     stream);
+    }
     return hipGetLastError();
 }
 
