@@ -18,12 +18,13 @@
 // and one workgroup per row sorts them in LDS and keeps the first k (two
 // reads of each row instead of five); a row with more candidates is
 // finished by that workgroup alone (the three further rounds and the
-// selection over its row).
+// selection over its row).  That route's first round is two kernels: the
+// tiles store their counts, then one workgroup per row adds them.
 //
 // No workgroup waits for another during the histogram rounds: each tile
-// writes its 256 digit counts to its own slots, and the row's last tile to
-// arrive (the per-row arrival counter of the row kernels) adds them and
-// picks the bucket.  The split is a two-chain decoupled look-back (elements
+// writes its 256 digit counts to its own slots, and (on the longer route)
+// the row's last tile to arrive (the per-row arrival counter of the row
+// kernels) adds them and picks the bucket.  The split is a two-chain decoupled look-back (elements
 // above T, elements equal to T), so the output keeps index order.
 #include <limits.h>
 
@@ -61,7 +62,7 @@ __device__ __forceinline__ bool topk_in_bucket(uint32_t key, uint32_t prefix) {
 template <class TileT, bool VEC, int R>
 __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_hist(
     const uint32_t* x, int64_t len, uint32_t segs, uint32_t k, bool largest, uint32_t* hist,
-    uint64_t* state, uint64_t* arrivals, uint64_t* gather) {
+    uint64_t* state, uint64_t* arrivals) {
     constexpr int kWaves = TileT::WAVES;
     // Several histograms per wave (picked by lane), so that equal digits in
     // one instruction collide at most 64 / kSub ways: the top digits of
@@ -135,12 +136,6 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_hist(
         if (above < kk && kk <= at_least) {  // exactly one thread
             state[2 * row] = (uint64_t)((prefix << 8) | (uint32_t)(kTopkDigits - 1 - t));
             state[2 * row + 1] = (uint64_t)(kk - above);
-            if (R == 0 && gather) {
-                // the gather route: the row's candidate count, and its
-                // reservation counter cleared for this call
-                gather[2 * row] = at_least;
-                gather[2 * row + 1] = 0;
-            }
         }
     }
     if (t == 0)
@@ -293,6 +288,7 @@ __global__ __launch_bounds__(kTopkSortThreads) void k_topk_sort(
 // ---------------------------------------------------------------- gather route
 
 constexpr int64_t kTopkGatherMaxLen = 1 << 17;
+constexpr uint32_t kTopkGatherSegs = 16;  // row tiles of the route: 2^17 / 8192 or 16384 / 4096
 constexpr uint32_t kTopkCand = 16384;  // candidates sorted in LDS (128 KB)
 constexpr int kTopkFinishThreads = 1024;
 constexpr uint32_t kTopkSortAll = 2048;  // candidates sorted whole, without the cut to k
@@ -305,24 +301,120 @@ __device__ __forceinline__ uint64_t topk_composite(uint32_t key, uint32_t i) {
     return ((uint64_t)key << 32) | (uint32_t)~i;
 }
 
+// Round 0 of the gather route, in two kernels with no per-row arrival (a
+// kernel boundary costs less than the arrival atomics): k_topk_count0 stores
+// each tile's counts of the top key byte in the tile's own 256 slots, and
+// k_topk_bucket, one workgroup per row, adds the row's tile counts per digit
+// and leaves in the row's state the digit d whose bucket holds the k-th
+// largest key -- fewer than k keys above it, at least k at or above it --
+// and k minus the keys above the bucket, and in its gather words the
+// candidate count (the keys with a top byte >= d) and a cleared reservation
+// counter.  Counting uses one LDS histogram per lane position, shared by the
+// waves and padded by a word (copy c, digit d in bank (c + d) mod 32), so the
+// lanes of an atomic instruction that hold the same digit -- the top bytes of
+// float data take a handful of values -- add to different words.
+constexpr int kTopkCopies = 16;
+constexpr int kTopkCopyStride = kTopkDigits + 1;
+template <class TileT, bool VEC>
+__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_count0(
+    const uint32_t* x, int64_t len, uint32_t segs, bool largest, uint32_t* hist) {
+    static_assert(TileT::kThreads >= kTopkDigits, "one thread per digit");
+    __shared__ uint32_t s_h[kTopkCopies * kTopkCopyStride];
+    for (int i = threadIdx.x; i < kTopkCopies * kTopkCopyStride; i += TileT::kThreads) s_h[i] = 0;
+    const int64_t row = blockIdx.x / segs;
+    const uint32_t seg = blockIdx.x - (uint32_t)row * segs;
+    const int64_t base = (int64_t)seg * TileT::kElems;
+    uint32_t v[TileT::J][TileT::V];
+    TileT::template load<VEC, true>(x + row * len, len, base, v);
+    __syncthreads();  // histograms cleared
+    uint32_t* h = s_h + (lane_id() & (kTopkCopies - 1)) * kTopkCopyStride;
+    const int32_t valid = (int32_t)(len - base < TileT::kElems ? len - base : TileT::kElems);
+#pragma unroll
+    for (int j = 0; j < TileT::J; ++j) {
+        const int32_t off = (int32_t)TileT::lane_offset(j);
+#pragma unroll
+        for (int e = 0; e < TileT::V; ++e)
+            if (off + e < valid) atomicAdd(&h[topk_key(v[j][e], largest) >> 24], 1u);
+    }
+    __syncthreads();
+    if (threadIdx.x < kTopkDigits) {
+        uint32_t t = 0;
+#pragma unroll
+        for (int q = 0; q < kTopkCopies; ++q) t += s_h[q * kTopkCopyStride + threadIdx.x];
+        hist[(int64_t)blockIdx.x * kTopkDigits + threadIdx.x] = t;
+    }
+}
+
+__global__ __launch_bounds__(kTopkDigits) void k_topk_bucket(const uint32_t* hist, uint32_t segs,
+                                                             uint32_t k, uint64_t* state,
+                                                             uint64_t* gather, uint32_t* offs) {
+    __shared__ uint32_t s_part[kTopkDigits / kWave];
+    __shared__ uint32_t s_d;
+    __shared__ uint32_t s_tile[kTopkDigits / kWave][kTopkGatherSegs];
+    const int64_t row = blockIdx.x;
+    // thread t takes digit 255 - t, so an inclusive scan over t counts the
+    // keys with a digit >= its own
+    const int t = threadIdx.x;
+    const int w = t / kWave;
+    const int lane = lane_id();
+    const uint32_t* rh = hist + row * segs * kTopkDigits + (kTopkDigits - 1 - t);
+    uint32_t c[kTopkGatherSegs];
+    uint32_t cnt = 0;
+#pragma unroll
+    for (uint32_t q = 0; q < kTopkGatherSegs; ++q) {
+        c[q] = q < segs ? rh[(int64_t)q * kTopkDigits] : 0u;
+        cnt += c[q];
+    }
+    const uint32_t inc = wave_incl_scan(cnt);
+    if (lane == kWave - 1) s_part[w] = inc;
+    __syncthreads();
+    uint32_t before = 0;
+    for (int q = 0; q < w; ++q) before += s_part[q];
+    const uint32_t at_least = before + inc;  // keys with digit >= 255 - t
+    const uint32_t above = at_least - cnt;   // keys with digit > 255 - t
+    if (above < k && k <= at_least) {       // exactly one thread (k <= len)
+        s_d = (uint32_t)(kTopkDigits - 1 - t);
+        state[2 * row] = (uint64_t)(kTopkDigits - 1 - t);
+        state[2 * row + 1] = (uint64_t)(k - above);
+        gather[2 * row] = at_least;
+    }
+    __syncthreads();
+    // each tile's candidates (its keys with a digit >= d), then their first
+    // slots in the row's list: the tiles in order
+    const bool keep = (uint32_t)(kTopkDigits - 1 - t) >= s_d;
+#pragma unroll
+    for (uint32_t q = 0; q < kTopkGatherSegs; ++q) {
+        const uint32_t n = wave_sum(keep ? c[q] : 0u);
+        if (lane == 0) s_tile[w][q] = n;
+    }
+    __syncthreads();
+    if (t < kWave) {
+        uint32_t n = 0;
+        if ((uint32_t)lane < segs)
+            for (int q = 0; q < kTopkDigits / kWave; ++q) n += s_tile[q][lane];
+        const uint32_t incl = wave_incl_scan(n);
+        if ((uint32_t)lane < segs) offs[row * kTopkGatherSegs + lane] = incl - n;
+    }
+}
+
 // Every key of a row whose top digit is at least the bucket's (state after
-// round 0), to the row's candidate list (cap slots per row), in no
-// particular order: each tile reserves its slots with one atomic add on the
-// row's counter.  Rows with more than cap candidates are left alone.
+// round 0), to the row's candidate list (cap slots per row), tile by tile
+// from the first slots the bucket kernel left for each tile, in index order
+// inside a tile.  Rows with more than cap candidates are left alone.
 template <class TileT, bool VEC>
 __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_gather(
     const uint32_t* x, int64_t len, uint32_t segs, bool largest, const uint64_t* state,
-    uint64_t* gather, uint64_t* cand, uint32_t cap) {
+    const uint64_t* gather, const uint32_t* offs, uint64_t* cand, uint32_t cap) {
     __shared__ uint32_t s_wtot[TileT::WAVES];
-    __shared__ uint32_t s_base;
     const uint32_t row32 = blockIdx.x / segs;
     const uint32_t seg = blockIdx.x - row32 * segs;
     const int64_t row = row32;
     if ((uint32_t)gather[2 * row] > cap) return;  // uniform: finished the long way
     const uint32_t d = (uint32_t)state[2 * row] & 255u;
+    const uint32_t first = offs[row * kTopkGatherSegs + seg];
     const int64_t base = (int64_t)seg * TileT::kElems;
     uint32_t v[TileT::J][TileT::V];
-    TileT::template load<VEC>(x + row * len, len, base, v);
+    TileT::template load<VEC, true>(x + row * len, len, base, v);
     const int32_t valid = (int32_t)(len - base < TileT::kElems ? len - base : TileT::kElems);
     static_assert(TileT::J * TileT::V <= 64, "per-lane take masks are 64-bit");
     uint64_t take = 0;
@@ -345,18 +437,8 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_gather(
     const int w = threadIdx.x / kWave;
     if (lane_id() == kWave - 1) s_wtot[w] = incl;
     __syncthreads();
-    if (threadIdx.x == 0) {
-        adversarial_pause(blockIdx.x);  // reservations in any order
-        uint32_t total = 0;
-        for (int q = 0; q < TileT::WAVES; ++q) total += s_wtot[q];
-        s_base = total ? (uint32_t)__hip_atomic_fetch_add(&gather[2 * row + 1], (uint64_t)total,
-                                                          __ATOMIC_RELAXED,
-                                                          __HIP_MEMORY_SCOPE_AGENT)
-                       : 0u;
-    }
-    __syncthreads();
     if (!take) return;
-    uint32_t pos = s_base + incl - cnt;
+    uint32_t pos = first + incl - cnt;
     for (int q = 0; q < w; ++q) pos += s_wtot[q];
     uint64_t* cr = cand + (int64_t)row * cap;
 #pragma unroll
@@ -686,7 +768,7 @@ static uint32_t topk_cap(int64_t len) {
     return (uint32_t)(len < (int64_t)kTopkCand ? len : (int64_t)kTopkCand);
 }
 struct TopkLayout {
-    size_t hist, state, arrivals, gather, end;
+    size_t hist, state, arrivals, gather, offs, end;
 };
 static TopkLayout topk_layout(int64_t rows, int64_t len, int64_t k) {
     const int64_t t = topk_gather_route(len, k) ? topk_gather_tile(len) : row_tile(len);
@@ -696,7 +778,8 @@ static TopkLayout topk_layout(int64_t rows, int64_t len, int64_t k) {
     l.state = align256(l.hist + tiles * kTopkDigits * sizeof(uint32_t));
     l.arrivals = l.state + (size_t)rows * 2 * sizeof(uint64_t);
     l.gather = l.arrivals + (size_t)rows * sizeof(uint64_t);
-    l.end = l.gather + (size_t)rows * 2 * sizeof(uint64_t);
+    l.offs = l.gather + (size_t)rows * 2 * sizeof(uint64_t);
+    l.end = l.offs + (topk_gather_route(len, k) ? (size_t)rows * kTopkGatherSegs * 4 : 0);
     return l;
 }
 size_t topk_ws_bytes(int64_t rows, int64_t len, int64_t k) {
@@ -726,17 +809,13 @@ static hipError_t topk_select(bool vec, const uint32_t* x, int64_t rows, int64_t
     uint64_t* arrivals = reinterpret_cast<uint64_t*>(w + l.arrivals);
     const uint32_t kk = (uint32_t)k;
     hipLaunchKernelGGL((vec ? k_topk_hist<TV, true, 0> : k_topk_hist<TU, false, 0>), dim3(nt),
-                       dim3(threads), 0, stream, x, len, segs, kk, largest, hist, state, arrivals,
-                       nullptr);
+                       dim3(threads), 0, stream, x, len, segs, kk, largest, hist, state, arrivals);
     hipLaunchKernelGGL((vec ? k_topk_hist<TV, true, 1> : k_topk_hist<TU, false, 1>), dim3(nt),
-                       dim3(threads), 0, stream, x, len, segs, kk, largest, hist, state, arrivals,
-                       nullptr);
+                       dim3(threads), 0, stream, x, len, segs, kk, largest, hist, state, arrivals);
     hipLaunchKernelGGL((vec ? k_topk_hist<TV, true, 2> : k_topk_hist<TU, false, 2>), dim3(nt),
-                       dim3(threads), 0, stream, x, len, segs, kk, largest, hist, state, arrivals,
-                       nullptr);
+                       dim3(threads), 0, stream, x, len, segs, kk, largest, hist, state, arrivals);
     hipLaunchKernelGGL((vec ? k_topk_hist<TV, true, 3> : k_topk_hist<TU, false, 3>), dim3(nt),
-                       dim3(threads), 0, stream, x, len, segs, kk, largest, hist, state, arrivals,
-                       nullptr);
+                       dim3(threads), 0, stream, x, len, segs, kk, largest, hist, state, arrivals);
     // The split keeps its flags and the tile's packed counts in registers as
     // well: it takes the tile shape with half the chunks and twice the waves
     // (16-byte loads still when aligned).
@@ -746,21 +825,6 @@ static hipError_t topk_select(bool vec, const uint32_t* x, int64_t rows, int64_t
                        (const uint64_t*)state, sel_vals, sel_idx, reinterpret_cast<WsHeader*>(ws),
                        status, (int64_t)2 * nt);
     return hipGetLastError();
-}
-
-// The count round on the row kernels' tile (few tiles per row: the row's
-// last arrival is one of few compare-and-swaps on its counter), the gather
-// on tiles of G (more workgroups for reading the rows a second time).
-template <class H>
-static void topk_count_round0(bool vec, const uint32_t* x, int64_t rows, int64_t len, uint32_t k,
-                              bool largest, uint32_t* hist, uint64_t* state, uint64_t* arrivals,
-                              uint64_t* gather, hipStream_t stream) {
-    using TV = RowTile<uint32_t, H, true>;
-    using TU = RowTile<uint32_t, H, false>;
-    const uint32_t segs = (uint32_t)((len + TV::kElems - 1) / TV::kElems);
-    hipLaunchKernelGGL((vec ? k_topk_hist<TV, true, 0> : k_topk_hist<TU, false, 0>),
-                       dim3((uint32_t)(rows * segs)), dim3(vec ? TV::kThreads : TU::kThreads), 0,
-                       stream, x, len, segs, k, largest, hist, state, arrivals, gather);
 }
 
 template <class G>
@@ -777,20 +841,18 @@ static hipError_t topk_gather(bool vec, const uint32_t* x, int64_t rows, int64_t
     const TopkLayout l = topk_layout(rows, len, k);
     uint32_t* hist = reinterpret_cast<uint32_t*>(w + l.hist);
     uint64_t* state = reinterpret_cast<uint64_t*>(w + l.state);
-    uint64_t* arrivals = reinterpret_cast<uint64_t*>(w + l.arrivals);
     uint64_t* gather = reinterpret_cast<uint64_t*>(w + l.gather);
+    uint32_t* offs = reinterpret_cast<uint32_t*>(w + l.offs);
     uint64_t* cand = reinterpret_cast<uint64_t*>(scratch);
     const uint32_t kk = (uint32_t)k, cap = topk_cap(len);
-    const int64_t h = row_tile(len);
-    if (h == 32768)
-        topk_count_round0<RGeomL>(vec, x, rows, len, kk, largest, hist, state, arrivals, gather, stream);
-    else if (h == 8192)
-        topk_count_round0<RGeomM>(vec, x, rows, len, kk, largest, hist, state, arrivals, gather, stream);
-    else
-        topk_count_round0<RGeomS>(vec, x, rows, len, kk, largest, hist, state, arrivals, gather, stream);
+    if (segs > kTopkGatherSegs) return hipErrorInvalidValue;  // not on this route
+    hipLaunchKernelGGL((vec ? k_topk_count0<TV, true> : k_topk_count0<TU, false>), dim3(nt),
+                       dim3(threads), 0, stream, x, len, segs, largest, hist);
+    hipLaunchKernelGGL(k_topk_bucket, dim3((uint32_t)rows), dim3(kTopkDigits), 0, stream,
+                       (const uint32_t*)hist, segs, kk, state, gather, offs);
     hipLaunchKernelGGL((vec ? k_topk_gather<TV, true> : k_topk_gather<TU, false>), dim3(nt),
                        dim3(threads), 0, stream, x, len, segs, largest, (const uint64_t*)state,
-                       gather, cand, cap);
+                       (const uint64_t*)gather, (const uint32_t*)offs, cand, cap);
     // the LDS sort sized to the row (cap <= CAP)
     auto kf = cap > 8192 ? k_topk_finish<kTopkCand>
                          : (cap > 2048 ? k_topk_finish<8192> : k_topk_finish<2048>);
