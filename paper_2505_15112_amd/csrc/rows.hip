@@ -413,7 +413,7 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_weighted_fini
 //    E_t + M_t >= p (E_t the sum of the tiles before it, M_t its largest
 //    inner running sum; rounding is monotone, so this is exact for the
 //    running sums as computed here), re-reads the first such tile (just
-//    read, so still in L2) and finds the index; if the head holds none, it
+//    read) and finds the index; if the head holds none, it
 //    walks the rest of the row itself, 16384 elements per step.
 // A running sum is always taken as E + (tile-local inclusive sum), the same
 // in both kernels, so the head's verdict and the search agree.  The result
@@ -457,8 +457,10 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp_head(
     const uint32_t t = blockIdx.x / rows;
     const int64_t base = (int64_t)t * TileT::kElems;
     float v[TileT::J][TileT::V];
-    // plain loads: the finishing kernel re-reads the crossing tile from L2
-    TileT::template load<VEC>(probs + (int64_t)row32 * len, len, base, v);
+    // nontemporal loads (cold rows are not allocated in the Infinity Cache on
+    // the way): 9.3 against 11.0 us per 128 x 131072 call with cached loads,
+    // the finishing kernel's re-read of one tile per row included
+    TileT::template load<VEC, true>(probs + (int64_t)row32 * len, len, base, v);
     float wofs;
     const float agg = TileT::combine_waves(TileT::template wave_scan<false>(v), s_wtot, &wofs);
     const int32_t valid = (int32_t)(len - base < TileT::kElems ? len - base : TileT::kElems);
