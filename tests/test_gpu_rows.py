@@ -1,8 +1,9 @@
 """GPU parity of the batched row scans and the top-p cutoff (through the C ABI).
 
 Row scans: int32 bit-exact, fp32 within the float bound plus bit-exact runs
-on {-1, 0, 1}.  Shapes cover the one-wave-per-row schedule (len <= 4096) and
-the segmented look-back schedule (len > 4096), ragged and unaligned lengths.
+on {-1, 0, 1}.  Shapes cover the one-wave-per-row schedule (len <= 1024), the
+one-workgroup-per-row schedule (1024 < len <= 4096), the segmented look-back
+schedule (len > 4096), ragged and unaligned lengths.
 Top-p: the cutoff equals the oracle's, or lies inside the tolerance band
 around p; dyadic rows (exact sums) must match exactly.
 """
@@ -16,7 +17,8 @@ from paper_2505_15112_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
 
-SHAPES = [(1, 1), (3, 5), (7, 64), (5, 255), (4, 4096), (3, 4097), (2, 3 * 4096 + 5),
+SHAPES = [(1, 1), (3, 5), (7, 64), (5, 255), (6, 1024), (6, 1025), (33, 3001), (128, 4096),
+          (4, 4096), (3, 4097), (2, 3 * 4096 + 5),
           (1000, 100), (17, 10_001), (9, 65_536), (3, 200_003)]
 
 
@@ -58,6 +60,11 @@ def test_rows_inplace_and_empty(ops):
     z = to_dev(x)
     ops.scan_rows_i32(z, out=z)
     assert_equal_first_diff(to_host(z), oracle.scan_rows_i32(x), "rows in-place")
+    x2 = W.scan_i32_full_range(9 * 3000, seed=2).reshape(9, 3000)  # one workgroup per row
+    z2 = to_dev(x2)
+    ops.scan_rows_i32(z2, out=z2, exclusive=True)
+    assert_equal_first_diff(to_host(z2), oracle.scan_rows_i32(x2, exclusive=True),
+                            "rows in-place, one tile")
     assert ops.scan_rows_f32(torch.empty((0, 7), dtype=torch.float32, device="cuda")).numel() == 0
     assert ops.scan_rows_f32(torch.empty((7, 0), dtype=torch.float32, device="cuda")).numel() == 0
 
