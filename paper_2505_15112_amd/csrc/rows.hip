@@ -510,77 +510,100 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp_head(
 }
 
 // The whole workgroup: the first index i < valid of the tile in v whose
-// running sum e + (wofs + v[i]) reaches p, or INT_MAX.  Contains barriers.
-template <class TileT>
+// running sum e + (wofs + v[i]) reaches p (STRICT: exceeds it), or INT_MAX;
+// *val (when given) gets the running sum there.  Contains barriers.
+template <class TileT, bool STRICT = false>
 __device__ __forceinline__ int32_t topp_first_reach(const float (&v)[TileT::J][TileT::V],
                                                     float e, float wofs, int32_t valid, float p,
-                                                    int32_t* s_min) {
+                                                    int32_t* s_min, float* s_val = nullptr,
+                                                    float* val = nullptr) {
     int32_t cand = INT_MAX;
+    float cand_val = 0.f;
 #pragma unroll
     for (int j = TileT::J - 1; j >= 0; --j) {
         const int32_t off = (int32_t)TileT::lane_offset(j);
 #pragma unroll
-        for (int k = TileT::V - 1; k >= 0; --k)
-            if (off + k < valid && e + (wofs + v[j][k]) >= p) cand = off + k;
+        for (int k = TileT::V - 1; k >= 0; --k) {
+            const float run = e + (wofs + v[j][k]);
+            if (off + k < valid && (STRICT ? run > p : run >= p)) {
+                cand = off + k;
+                cand_val = run;
+            }
+        }
     }
     const int32_t wm = wave_min(cand);
     if (lane_id() == 0) s_min[threadIdx.x / kWave] = wm;
     __syncthreads();
     int32_t m = INT_MAX;
     for (int k = 0; k < TileT::WAVES; ++k) m = s_min[k] < m ? s_min[k] : m;
-    __syncthreads();  // s_min is rewritten by the next call
+    if (val) {
+        if (m != INT_MAX && cand == m) *s_val = cand_val;  // exactly one lane
+        __syncthreads();
+        *val = *s_val;
+    }
+    __syncthreads();  // s_min / s_val are rewritten by the next call
     return m;
 }
 
-template <bool VEC>
-__global__ __launch_bounds__(kFinishThreads) LS_OCCUPANCY4 void k_topp_finish(
-    const float* probs, int32_t* cutoff, int64_t len, uint32_t heads, float p,
-    const uint64_t* words) {
+// Wave 0: the first head tile t in [from, limit) whose largest inner running
+// sum E_t + M_t reaches p (STRICT: exceeds it), -1 if none; *e gets E_t (with
+// none: the sum of the tiles [from, limit) added to carry).
+__device__ __forceinline__ int32_t topp_head_tile(const uint64_t* hw, uint32_t from,
+                                                  uint32_t limit, float carry, float p,
+                                                  bool strict, float* e) {
+    const int lane = lane_id();
+    for (uint32_t b = from; b < limit; b += kWave) {
+        const uint32_t t = b + lane;
+        const float a = t < limit ? Bits<float>::from((uint32_t)hw[2 * t]) : 0.f;
+        const float m = t < limit ? Bits<float>::from((uint32_t)hw[2 * t + 1]) : 0.f;
+        const float sc = wave_incl_scan(a);
+        const float ex = carry + wave_shr1(sc);  // E_t: the sum of the tiles before t
+        const uint64_t hit = __ballot(t < limit && (strict ? ex + m > p : ex + m >= p));
+        if (hit) {
+            const int l = __builtin_ctzll(hit);
+            *e = lane_read(ex, l);
+            return (int32_t)(b + l);
+        }
+        carry = carry + lane_read(sc, kWave - 1);
+    }
+    *e = carry;
+    return -1;
+}
+
+// The whole workgroup: the first index i <= lim of the row at xr whose
+// running sum reaches thr (STRICT: exceeds it), -1 if none.  The head tiles'
+// words pick the first head tile that holds one (E_t + M_t against thr), that
+// tile is re-read and searched; should its sums disagree with the words (they
+// are the same sums, so never), the search goes on from the next head tile.
+// With none in the head, the rest of the row is walked, 16384 elements per
+// step.  *val gets the running sum at the index found, or (none) the sum of
+// every element up to the end of the last tile searched.
+template <bool VEC, bool STRICT>
+__device__ int64_t topp_head_find(const float* xr, int64_t len, const uint64_t* hw, uint32_t heads,
+                                  float thr, int64_t lim, float* val, int32_t* s_tile, float* s_e,
+                                  float* s_wtot, int32_t* s_min, float* s_val) {
     using H = Tile<float, float, 4, 2, kFinishThreads / kWave>;   // one head tile, 4096
     using B = Tile<float, float, 4, 8, kFinishThreads / kWave>;  // 16384 per step after the head
     static_assert(H::kElems == kEarlyTile, "head tile");
-    __shared__ int32_t s_tile;
-    __shared__ float s_e;
-    __shared__ float s_wtot[H::WAVES];
-    __shared__ int32_t s_min[H::WAVES];
-
-    const uint32_t row32 = blockIdx.x;
-    const float* xr = probs + (int64_t)row32 * len;
-    const uint64_t* hw = words + (size_t)row32 * heads * 2;
+    const int64_t lim_tiles = lim / kEarlyTile + 1;  // head tiles holding indices <= lim
+    const uint32_t limit = (uint32_t)(lim_tiles < (int64_t)heads ? lim_tiles : heads);
     float carry = 0.f;  // sum of the head tiles before `from`
     uint32_t from = 0;
     while (true) {
         if (threadIdx.x < kWave) {
-            // wave 0: the first head tile at or after `from` holding a reach
-            const int lane = lane_id();
-            int32_t found = -1;
-            float e_found = 0.f;
-            for (uint32_t b = from; b < heads; b += kWave) {
-                const uint32_t t = b + lane;
-                const float a = t < heads ? Bits<float>::from((uint32_t)hw[2 * t]) : 0.f;
-                const float m = t < heads ? Bits<float>::from((uint32_t)hw[2 * t + 1]) : 0.f;
-                const float sc = wave_incl_scan(a);
-                const float ex = carry + wave_shr1(sc);  // E_t: the sum of the tiles before t
-                const uint64_t hit = __ballot(t < heads && ex + m >= p);
-                if (hit) {
-                    const int l = __builtin_ctzll(hit);
-                    found = (int32_t)(b + l);
-                    e_found = lane_read(ex, l);
-                    break;
-                }
-                carry = carry + lane_read(sc, kWave - 1);
-            }
-            if (lane == 0) {
-                s_tile = found;
-                s_e = found >= 0 ? e_found : carry;
+            float e = 0.f;
+            const int32_t t = topp_head_tile(hw, from, limit, carry, thr, STRICT, &e);
+            if (lane_id() == 0) {
+                *s_tile = t;
+                *s_e = e;
             }
         }
         __syncthreads();
-        const int32_t t = s_tile;
-        const float e = s_e;
+        const int32_t t = *s_tile;
+        const float e = *s_e;
         __syncthreads();  // s_tile / s_e are rewritten by the next round
         if (t < 0) {
-            carry = e;  // the sum of the whole head
+            carry = e;  // the sum of the head tiles searched
             break;
         }
         const int64_t base = (int64_t)t * H::kElems;
@@ -588,33 +611,74 @@ __global__ __launch_bounds__(kFinishThreads) LS_OCCUPANCY4 void k_topp_finish(
         H::template load<VEC>(xr, len, base, v);
         float wofs;
         const float agg = H::combine_waves(H::template wave_scan<false>(v), s_wtot, &wofs);
-        const int32_t valid = (int32_t)(len - base < H::kElems ? len - base : H::kElems);
-        const int32_t m = topp_first_reach<H>(v, e, wofs, valid, p, s_min);
+        const int64_t end = (lim + 1 < len ? lim + 1 : len) - base;  // indices <= lim
+        const int32_t valid = (int32_t)(end < H::kElems ? end : H::kElems);
+        float at;
+        const int32_t m = topp_first_reach<H, STRICT>(v, e, wofs, valid, thr, s_min, s_val, &at);
         if (m != INT_MAX) {
-            if (threadIdx.x == 0) cutoff[row32] = (int32_t)(base + m);
-            return;
+            *val = at;
+            return base + m;
         }
-        // (not reached: the head's verdict and this search use the same sums)
         carry = e + agg;
         from = (uint32_t)t + 1;
         __syncthreads();  // s_wtot is rewritten by the next combine
     }
-    // no reach in the head: walk the rest of the row
-    for (int64_t base = (int64_t)heads * kEarlyTile; base < len; base += B::kElems) {
+    for (int64_t base = (int64_t)limit * kEarlyTile; base <= lim && limit == heads;
+         base += B::kElems) {
         float v[B::J][B::V];
         B::template load<VEC, true>(xr, len, base, v);
         float wofs;
         const float agg = B::combine_waves(B::template wave_scan<false>(v), s_wtot, &wofs);
-        const int32_t valid = (int32_t)(len - base < B::kElems ? len - base : B::kElems);
-        const int32_t m = topp_first_reach<B>(v, carry, wofs, valid, p, s_min);
+        const int64_t end = (lim + 1 < len ? lim + 1 : len) - base;
+        const int32_t valid = (int32_t)(end < B::kElems ? end : B::kElems);
+        float at;
+        const int32_t m = topp_first_reach<B, STRICT>(v, carry, wofs, valid, thr, s_min, s_val, &at);
         if (m != INT_MAX) {
-            if (threadIdx.x == 0) cutoff[row32] = (int32_t)(base + m);
-            return;
+            *val = at;
+            return base + m;
         }
         carry = carry + agg;
         __syncthreads();  // s_wtot is rewritten by the next combine
     }
-    if (threadIdx.x == 0) cutoff[row32] = (int32_t)(len - 1);
+    *val = carry;
+    return -1;
+}
+
+// The cutoff k (len - 1 when no running sum reaches p); SAMPLE: the top-p
+// draw on the sorted rows as well -- with C the running sum at k, the first
+// index j <= k whose running sum exceeds theta * C (j = k when rounding
+// leaves none), found the same way; the token is idx[j] (idx null: j
+// itself), and the cutoff is stored only when asked for.
+template <bool VEC, bool SAMPLE>
+__global__ __launch_bounds__(kFinishThreads) LS_OCCUPANCY4 void k_topp_finish(
+    const float* probs, int32_t* cutoff, int64_t len, uint32_t heads, float p,
+    const uint64_t* words, const int32_t* idx, const float* theta, int32_t* token) {
+    __shared__ int32_t s_tile;
+    __shared__ float s_e;
+    __shared__ float s_wtot[kFinishThreads / kWave];
+    __shared__ int32_t s_min[kFinishThreads / kWave];
+    __shared__ float s_val;
+
+    const uint32_t row32 = blockIdx.x;
+    const float* xr = probs + (int64_t)row32 * len;
+    const uint64_t* hw = words + (size_t)row32 * heads * 2;
+    float c;  // the running sum at k (none reached: the row total)
+    int64_t k = topp_head_find<VEC, false>(xr, len, hw, heads, p, len - 1, &c, &s_tile, &s_e,
+                                           s_wtot, s_min, &s_val);
+    if (k < 0) k = len - 1;
+    if (!SAMPLE) {
+        if (threadIdx.x == 0) cutoff[row32] = (int32_t)k;
+        return;
+    }
+    __syncthreads();
+    float at;
+    int64_t j = topp_head_find<VEC, true>(xr, len, hw, heads, theta[row32] * c, k, &at, &s_tile,
+                                          &s_e, s_wtot, s_min, &s_val);
+    if (j < 0) j = k;
+    if (threadIdx.x == 0) {
+        if (cutoff) cutoff[row32] = (int32_t)k;
+        token[row32] = idx ? idx[(int64_t)row32 * len + j] : (int32_t)j;
+    }
 }
 
 __global__ void k_fill_i32(int32_t* p, int64_t count, int32_t value) {
@@ -766,9 +830,25 @@ static void topp_cutoff_early(bool vec, const float* probs, int32_t* cutoff, int
     auto kh = vec ? k_topp_head<TV, true> : k_topp_head<TU, false>;
     hipLaunchKernelGGL(kh, dim3((unsigned)(rows * heads)), dim3(vec ? TV::kThreads : TU::kThreads),
                        0, stream, probs, len, (uint32_t)rows, heads, words);
-    auto kf = vec ? k_topp_finish<true> : k_topp_finish<false>;
+    auto kf = vec ? k_topp_finish<true, false> : k_topp_finish<false, false>;
     hipLaunchKernelGGL(kf, dim3((unsigned)rows), dim3(kFinishThreads), 0, stream, probs, cutoff,
-                       len, heads, p, words);
+                       len, heads, p, words, nullptr, nullptr, nullptr);
+}
+
+// The top-p draw on sorted rows by the same two kernels (rows as topp_early).
+static void topp_sample_early(bool vec, const float* sorted, const int32_t* idx,
+                              const float* theta, int32_t* cutoff, int32_t* token, int64_t rows,
+                              int64_t len, float p, void* ws, hipStream_t stream) {
+    using TV = RowTile<float, RGeomS, true>;
+    using TU = RowTile<float, RGeomS, false>;
+    const uint32_t heads = topp_heads(len);
+    uint64_t* words = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(ws) + kWsHeader);
+    auto kh = vec ? k_topp_head<TV, true> : k_topp_head<TU, false>;
+    hipLaunchKernelGGL(kh, dim3((unsigned)(rows * heads)), dim3(vec ? TV::kThreads : TU::kThreads),
+                       0, stream, sorted, len, (uint32_t)rows, heads, words);
+    auto kf = vec ? k_topp_finish<true, true> : k_topp_finish<false, true>;
+    hipLaunchKernelGGL(kf, dim3((unsigned)rows), dim3(kFinishThreads), 0, stream, sorted, cutoff,
+                       len, heads, p, words, idx, theta, token);
 }
 
 template <ToppMode MODE>
@@ -777,6 +857,10 @@ static void topp_any(bool vec, const float* probs, const int32_t* idx, const flo
                      void* ws, hipStream_t stream) {
     if (MODE == ToppMode::Cutoff && topp_early(len)) {
         topp_cutoff_early(vec, probs, cutoff, rows, len, p, ws, stream);
+        return;
+    }
+    if (MODE == ToppMode::Sample && topp_early(len)) {
+        topp_sample_early(vec, probs, idx, theta, cutoff, token, rows, len, p, ws, stream);
         return;
     }
     const int64_t t = row_tile(len);
@@ -914,7 +998,7 @@ hipError_t launch_topp_draw_sorted(const float* sorted, const int32_t* idx, cons
 // source indices, and the sort's two ping-pong buffers.
 static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 size_t topp_sample_ws_bytes(int64_t rows, int64_t len) {
-    const size_t a = radix_rows_ws_bytes(rows, len), b = topp_ws_bytes(rows, len);
+    const size_t a = radix_rows_ws_bytes(rows, len), b = scan_rows_ws_bytes(rows, len);
     return a > b ? a : b;
 }
 size_t topp_sample_scratch_bytes(int64_t rows, int64_t len) {
