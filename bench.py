@@ -470,16 +470,17 @@ def main():
             b2 = n2 * 6
             ms = T.flushed(scan_call("scan_inclusive_f16f32", x16, y16, n2), K, Wm)
             opsd["scan_f16f32_n2^24"] = entry("f16", ms, b2, memcpy_ms(b2, True),
-                                              "n*(2+4), cache-flushed; matrix-core tile scan")
+                                              "n*(2+4), cache-flushed; the default dispatch "
+                                              "(wavefront tiles below n = 2^27)")
             outputs["f16"] = (x16_host, y16)
-            # the same scan on the wavefront tiles only (the default above runs
-            # its whole 32768-element tiles on the matrix cores), cold at 2^24,
-            # and both back to back at 2^28
-            y16w = torch.empty_like(y16)
-            ms = T.flushed(scan_call("scan_inclusive_f16f32_wave", x16, y16w, n2), K, Wm)
-            opsd["scan_f16f32_wave_n2^24"] = entry("f16 wave", ms, b2, memcpy_ms(b2, True),
-                                                   "n*(2+4), cache-flushed; wavefront tiles only")
-            outputs["f16_wave"] = (x16_host, y16w)
+            # the same scan with its whole 32768-element tiles on the matrix
+            # cores, cold at 2^24, and both forms back to back at 2^28 (where
+            # the default takes the matrix cores)
+            y16m = torch.empty_like(y16)
+            ms = T.flushed(scan_call("scan_inclusive_f16f32_mfma", x16, y16m, n2), K, Wm)
+            opsd["scan_f16f32_mfma_n2^24"] = entry("f16 mfma", ms, b2, memcpy_ms(b2, True),
+                                                   "n*(2+4), cache-flushed; matrix-core tile scan")
+            outputs["f16_mfma"] = (x16_host, y16m)
             x16b = torch.from_numpy(W.scan_f16(n, seed=3)).to(dev)
             y16b = torch.empty(n, dtype=torch.float32, device=dev)
             b28 = n * 6
@@ -788,8 +789,8 @@ def cpu_baseline_leg(x_host, y_dev, outputs, np, torch):
         ok = bool(np.all(np.abs(y.cpu().numpy() - r) <= 1e-5 * a + 1e-6))
         res["scan_f16f32_n2^24"] = {"gbps": round(xh.size * 6 / t / 1e9, 3), "s": round(t, 4),
                                     "matches_gpu": ok}
-        xh, y = outputs["f16_wave"]
-        res["scan_f16f32_wave_n2^24"] = {
+        xh, y = outputs["f16_mfma"]
+        res["scan_f16f32_mfma_n2^24"] = {
             "matches_gpu": bool(np.all(np.abs(y.cpu().numpy() - r) <= 1e-5 * a + 1e-6))}
     if "c1" in outputs:
         xh, y = outputs["c1"]

@@ -121,7 +121,7 @@ int scan_exclusive_f32(const float* x, float* y, int64_t n, void* ws, size_t ws_
 /* fp16 input (IEEE binary16 bit patterns), fp32 accumulation and output
  * (Section 3.1: the cube takes fp16 in and gives fp32 out; Section 6 scans
  * fp16).  x and y may not overlap.  The inclusive scan of a 16-byte aligned
- * x with n >= 32768 takes its tile-local scans on the matrix cores (see
+ * x with n >= 2^27 takes its tile-local scans on the matrix cores (see
  * scan_inclusive_f16f32_mfma), otherwise the wavefront tiles. */
 int scan_inclusive_f16f32(const uint16_t* x, float* y, int64_t n, void* ws, size_t ws_bytes,
                           void* stream);
@@ -138,8 +138,9 @@ int scan_exclusive_f16f32(const uint16_t* x, float* y, int64_t n, void* ws, size
  * and y 4-byte aligned, else LIBSCAN_EINVAL; x and y may not overlap.  Whole
  * 32768-element tiles take the matrix-core kernel, a shorter tail the
  * wavefront one.  Results agree with the wavefront scan within the float
- * tolerance (exactly on {-1, 0, 1} inputs); measured faster than it, which
- * is why scan_inclusive_f16f32 uses this path when it can.  A tile holding
+ * tolerance (exactly on {-1, 0, 1} inputs); measured faster than it from
+ * n = 2^27 on (slower below), which is why scan_inclusive_f16f32 uses this
+ * path for such arrays.  A tile holding
  * an infinity or a NaN is scanned on the vector units instead (in the
  * product it would meet the zeros of U_32, and inf * 0 is NaN). */
 int scan_inclusive_f16f32_mfma(const uint16_t* x, float* y, int64_t n, void* ws,

@@ -404,13 +404,15 @@ static hipError_t scan1d_typed(bool exclusive, const In* x, T* y, int64_t n, con
 hipError_t launch_scan1d(Kind kind, bool exclusive, const void* x, void* y, int64_t n,
                          const void* carry_in, void* total_out, void* ws, size_t ws_bytes,
                          hipStream_t stream) {
-    // fp16 inclusive scans of at least one whole 32768-element tile run on
-    // the matrix cores (measured faster than the wavefront tiles: 332 against
-    // 350 us at n = 2^28, 30.2 against 31.7 us at 2^24 cold).  The byte scan
-    // on the matrix cores measured no faster (251 against 251 us at 2^28),
-    // so byte scans stay on the wavefront tiles.
-    if (kind == Kind::F16F32 && !exclusive && !carry_in && !total_out && n >= kMfmaTileElems &&
-        aligned(x, 16) && aligned(y, 4))
+    // fp16 inclusive scans of 2^27 elements and more run on the matrix cores:
+    // measured against the wavefront tiles in one process (medians of 9
+    // alternating rounds), 337.0 against 346.8 us at n = 2^28, 152.7 against
+    // 153.7 us at 2^27, but slower below (79.0 against 80.1 us at 2^26, 28.9
+    // against 29.6 at 2^24 cold, 10.2 against 11.0 at 2^22 cold).  The byte
+    // scan on the matrix cores measured no faster (251 against 251 us at
+    // 2^28), so byte scans stay on the wavefront tiles.
+    if (kind == Kind::F16F32 && !exclusive && !carry_in && !total_out &&
+        n >= (int64_t(1) << 27) && aligned(x, 16) && aligned(y, 4))
         return launch_scan1d_mfma_f16(reinterpret_cast<const uint16_t*>(x),
                                       reinterpret_cast<float*>(y), n, ws, ws_bytes, stream);
     return launch_scan1d_tiles(kind, exclusive, x, y, n, carry_in, total_out, ws, ws_bytes,

@@ -84,7 +84,8 @@ def test_scans_mid_sizes(ops, adversarial, n):
                                 f"adv i32 n={n} excl={excl}")
     xe = W.exact_pm1(n, seed=5, dtype=np.float16)
     ref = oracle.scan_f16(xe)[0]
-    for fn in (ops.scan_inclusive_f16f32, ops.scan_inclusive_f16f32_wave):
+    for fn in (ops.scan_inclusive_f16f32, ops.scan_inclusive_f16f32_mfma,
+               ops.scan_inclusive_f16f32_wave):
         assert_equal_first_diff(to_host(fn(to_dev(xe))).astype(np.float64), ref,
                                 f"adv f16 n={n}")
     b = W.bytes_u8(n, seed=6)
