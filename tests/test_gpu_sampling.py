@@ -91,9 +91,11 @@ def _check_weighted(g, w, theta, what):
     return ref
 
 
-@pytest.mark.parametrize("length", [1, 3, 64, 4096, 4097, 10_003, 65_536, 65_537, 131_072,
-                                    (1 << 20) + 3])
+@pytest.mark.parametrize("length", [1, 3, 64, 4096, 4097, 10_003, 16_384, 16_385, 65_536, 65_537,
+                                    131_072, (1 << 20) + 3, 1 << 22, (1 << 22) + 1])
 def test_weighted_sample(ops, length):
+    """Rows of 4097 to 2^22 take the two-kernel path (4096-element tiles up to
+    16384, 8192 above), longer ones the single kernel with per-row arrival."""
     rows = 24 if length < (1 << 20) else 3
     announce("weighted sample", rows, length)
     w = W.sample_weights(rows, length, seed=length)
@@ -179,9 +181,11 @@ def _check_topp_sample(tok, cut, probs, theta, p, what):
 
 
 @pytest.mark.parametrize("length", [1, 3, 100, 4096, 4097, 10_003, 65_536, 65_537, 131_072,
-                                    200_003])
-@pytest.mark.parametrize("p", [0.0, 0.5, 0.9, 1.5])
+                                    200_003, 1 << 20, (1 << 20) + 1])
+@pytest.mark.parametrize("p", [0.0, 0.5, 0.9, 0.99, 1.5])
 def test_topp_sample(ops, length, p):
+    """Rows of 4097 to 2^20 draw on the early-exit kernels (the cutoff and the
+    draw past the head quarter when p is large), others on the single kernel."""
     rows = 8
     announce("topp sample", rows, length, p)
     probs = W.sample_probs(rows, length, seed=length)
