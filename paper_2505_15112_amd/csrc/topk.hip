@@ -292,6 +292,7 @@ constexpr uint32_t kTopkGatherSegs = 16;  // row tiles of the route: 2^17 / 8192
 constexpr uint32_t kTopkCand = 16384;  // candidates sorted in LDS (128 KB)
 constexpr int kTopkFinishThreads = 1024;
 constexpr uint32_t kTopkSortAll = 2048;  // candidates sorted whole, without the cut to k
+constexpr uint32_t kTopkSmallBucket = 128;  // a cut round's bucket finished by one sort
 static_assert(kTopkSortMax <= kTopkCand, "the k kept fit the finisher's sort");
 
 // The composite sort key of element i with key `key`: larger keys first,
@@ -565,8 +566,9 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
     __shared__ uint64_t s[CAP];
     __shared__ uint32_t s_h[kTopkDigits];
     __shared__ uint32_t s_part[kTopkFinishThreads / kWave];
-    __shared__ uint32_t s_prefix, s_kk, s_n, s_qbase;
+    __shared__ uint32_t s_prefix, s_kk, s_n, s_qbase, s_bucket, s_nsmall;
     __shared__ uint64_t s_prefix64;
+    __shared__ uint64_t s_small[kTopkSmallBucket];
     constexpr uint32_t kT = kTopkFinishThreads;
     const int64_t row = blockIdx.x;
     const int w = threadIdx.x / kWave;
@@ -617,11 +619,47 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
                 if (above < kk && kk <= at_least) {  // exactly one thread
                     s_prefix64 = (prefix << 8) | (uint32_t)(kTopkDigits - 1 - t);
                     s_kk = kk - above;
+                    s_bucket = c;
                 }
             }
             __syncthreads();
             prefix = s_prefix64;
             kk = s_kk;
+            if (s_bucket <= kTopkSmallBucket) {  // uniform
+                // A bucket this small is finished in one step instead of
+                // more rounds: its composites are gathered, one wavefront
+                // sorts them in registers and takes the kk-th largest, the
+                // k-th largest composite of the row.
+                const int hs2 = 56 - 8 * r;  // the new prefix's shift
+                if (threadIdx.x == 0) s_nsmall = 0;
+                __syncthreads();
+                for (uint32_t i = threadIdx.x; i < m; i += kT) {
+                    const uint64_t c2 = s[i];
+                    if ((c2 >> hs2) == prefix) {
+                        const uint32_t pos = atomicAdd(&s_nsmall, 1u);
+                        if (pos < kTopkSmallBucket) s_small[pos] = c2;  // below the bucket size
+                    }
+                }
+                __syncthreads();
+                if (threadIdx.x < kWave) {
+                    const uint32_t nb = s_nsmall < kTopkSmallBucket ? s_nsmall : kTopkSmallBucket;
+                    uint64_t v2[2];
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) {
+                        const uint32_t q = (uint32_t)lane * 2 + e;
+                        v2[e] = q < nb ? s_small[q] : 0ull;  // zero pads sort last
+                    }
+                    // 128 slots, 2 per lane: no stride reaches the LDS stages
+                    bitonic_desc_regs<2>(v2, s_small, kTopkSmallBucket, kWave, kTopkSmallBucket);
+                    const uint32_t q = kk - 1;  // kk <= the bucket's size
+#pragma unroll
+                    for (int e = 0; e < 2; ++e)
+                        if ((uint32_t)lane * 2 + e == q) s_prefix64 = v2[e];
+                }
+                __syncthreads();
+                prefix = s_prefix64;
+                break;
+            }
         }
         // prefix: the k-th largest composite (when m > k); each thread still
         // holds its candidates in `mine`
