@@ -26,7 +26,10 @@ chunks through the carry entry points the analogue of its "L2 cache
 splitting"; the fp16 radix sort with indices its radix-sort workload.
 Every back-to-back row reports the batch's time per call and, from a second
 batch with an event between calls, the median and minimum call; cold rows the
-median and minimum of three rounds.  After every row the workspace's error
+median and minimum of three rounds.  Every row but the metric (which takes the
+--warmup calls it is given) warms up for at least 30 ms of GPU time first:
+after the host-side pause of generating a row's inputs the GPU clock needs
+about 10 ms of work to come back up.  After every row the workspace's error
 word is read: a row whose bounded waits gave up fails the run.
 The CPU-baseline leg times the serial oracle on each workload (or a stated
 sample) and checks the GPU outputs against it (the samplers within the
@@ -123,15 +126,38 @@ class Timer:
         self.stream = stream
         self.flush_buf = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
 
-    def back_to_back(self, fn, steps, warmup):
+    def settle(self, body, calls, min_ms):
+        """`calls` untimed calls of body, then more until about `min_ms` of GPU
+        time has gone to warming up: after a host-side pause (input
+        generation between rows) the GPU clock takes about 10 ms of work to
+        ramp up again, and a few warm-up calls of a short op do not cover it
+        (a 2^26-key 8-bit sort measured 1.20-1.29 ms for its first calls after
+        an idle second, 1.15 ms once warm)."""
+        torch = self.torch
+        for _ in range(calls):
+            body()
+        if min_ms <= 0:
+            return
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(self.stream)
+        body()
+        b.record(self.stream)
+        torch.cuda.synchronize()
+        one = max(a.elapsed_time(b), 1e-3)
+        for _ in range(min(int(min_ms / one), 2000)):
+            body()
+
+    def back_to_back(self, fn, steps, warmup, min_warm_ms=0.0):
         """`steps` calls enqueued back to back between two events: the value
         is that batch's time per call.  A second batch of `steps` calls with
         an event between consecutive calls gives each call's own time, for the
         median and the minimum (kept apart so that those events cannot slow
-        the batch the value comes from)."""
+        the batch the value comes from).  The per-op rows also warm up for
+        at least min_warm_ms of GPU time (see settle); the metric takes the
+        warm-up it is given."""
         torch = self.torch
-        for _ in range(warmup):
-            fn()
+        self.settle(fn, warmup, min_warm_ms)
         torch.cuda.synchronize()
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
@@ -150,7 +176,7 @@ class Timer:
         per = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(steps))
         return Stat(mean, per[len(per) // 2], per[0])
 
-    def flushed(self, fn, steps, warmup, reps=3):
+    def flushed(self, fn, steps, warmup, reps=3, min_warm_ms=30.0):
         """Cost of one call on data that is not in any cache: `steps` rounds of
         (overwrite 512 MiB, which evicts L2 and MALL; call) enqueued back to
         back, minus the same number of overwrites alone, per call; median of
@@ -158,9 +184,12 @@ class Timer:
         event-to-kernel launch latency (about 6 us on MI355X) to every call."""
         torch = self.torch
         flush = self.flush_buf.zero_
-        for _ in range(warmup):
+
+        def both():
             flush()
             fn()
+
+        self.settle(both, warmup, min_warm_ms)
         torch.cuda.synchronize()
 
         def timed(body):
@@ -172,10 +201,6 @@ class Timer:
             b.record(self.stream)
             torch.cuda.synchronize()
             return a.elapsed_time(b)
-
-        def both():
-            flush()
-            fn()
 
         out = []
         for _ in range(reps):
@@ -310,7 +335,7 @@ def main():
         src = torch.empty(m, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
         f = lambda: dst.copy_(src)  # noqa: E731
-        return (T.flushed(f, K, Wm) if flushed else T.back_to_back(f, K, Wm))
+        return (T.flushed(f, K, Wm) if flushed else T.back_to_back(f, K, Wm, 30.0))
 
     def streaming_ms(nbytes):
         """torch's elementwise kernel (int32 bitwise_not) moving nbytes in total: a
@@ -319,7 +344,7 @@ def main():
         m = max(1, nbytes // 8)
         src = torch.zeros(m, dtype=torch.int32, device=dev)
         dst = torch.empty_like(src)
-        return T.back_to_back(lambda: torch.bitwise_not(src, out=dst), K, Wm)
+        return T.back_to_back(lambda: torch.bitwise_not(src, out=dst), K, Wm, 30.0)
 
     # ---------------------------------------------------------------- metric
     log("metric inputs")
@@ -416,7 +441,7 @@ def main():
                 f = lambda a=a: check(lib.scan_rows_f32(*a), "rows")  # noqa: E731
                 bb = (rows_b << 16) * 8
                 cold = bb < (512 << 20)
-                ms = T.flushed(f, K, Wm) if cold else T.back_to_back(f, K, Wm)
+                ms = T.flushed(f, K, Wm) if cold else T.back_to_back(f, K, Wm, 30.0)
                 batch.append({"rows": rows_b, "len": 1 << 16, "us": round(ms * 1e3, 2),
                               "us_min": round(ms.min * 1e3, 2),
                               "gbps": round(bb / (ms * 1e-3) / 1e9, 1),
@@ -441,7 +466,7 @@ def main():
                                                           P(cbuf) if c0 else None, P(cbuf), wsp, wsb,
                                                           sp)
                         check(st, "scan_inclusive_i32_carry")
-                ms = T.back_to_back(run_chunks, K, Wm)
+                ms = T.back_to_back(run_chunks, K, Wm, 30.0)
                 chunked.append({"chunk": m, "chunks": n // m, "ms": round(ms, 4),
                                 "ms_min": round(ms.min, 4), "gbps": round(nbytes / (ms * 1e-3) / 1e9, 1),
                                 "vs_one_call": round(ms_i32 / ms, 3),
@@ -454,7 +479,8 @@ def main():
             # reduce-then-scan check variant (3 kernels, x read twice)
             wsr = ops.workspace(_lib.OP_SCAN_RSS, dev, n)
             y_rss = torch.empty_like(x_i32)
-            ms = T.back_to_back(scan_call("scan_inclusive_rss_i32", x_i32, y_rss, n, wsr), K, Wm)
+            ms = T.back_to_back(scan_call("scan_inclusive_rss_i32", x_i32, y_rss, n, wsr), K, Wm,
+                                30.0)
             opsd["scan_rss_i32_n2^28"] = entry("rss", ms, nbytes, ms_cp, "n*(4+4); x is read twice",
                                               {"traffic_ratio_vs_lookback": 1.5})
             outputs["rss_equal"] = bool(torch.equal(y_rss, y_i32))
@@ -486,7 +512,7 @@ def main():
             b28 = n * 6
             mc28 = memcpy_ms(b28)
             for nm in ("scan_inclusive_f16f32", "scan_inclusive_f16f32_wave"):
-                ms = T.back_to_back(scan_call(nm, x16b, y16b, n), K, Wm)
+                ms = T.back_to_back(scan_call(nm, x16b, y16b, n), K, Wm, 30.0)
                 key = "scan_f16f32" + ("_wave" if nm.endswith("wave") else "") + "_n2^28"
                 opsd[key] = entry("f16 2^28", ms, b28, mc28, "n*(2+4)")
             del x16b, y16b
@@ -502,7 +528,7 @@ def main():
             for nm in ("scan_exclusive_u8i32", "scan_exclusive_u8i32_mfma"):
                 fn = getattr(lib, nm)
                 a = (P(xb), P(yb), n, P(tb), wsp, wsb, sp)
-                ms = T.back_to_back(lambda: check(fn(*a), nm), K, Wm)
+                ms = T.back_to_back(lambda: check(fn(*a), nm), K, Wm, 30.0)
                 key = "scan_u8i32" + ("_mfma" if nm.endswith("mfma") else "") + "_n2^28"
                 opsd[key] = entry("u8", ms, b5, mc5, "n*(1+4)")
             ws_clean(ws, "scans")
@@ -515,7 +541,7 @@ def main():
             x1 = torch.from_numpy(x1_host).to(dev)
             y1 = torch.empty_like(x1)
             ms_f = T.flushed(scan_call("scan_inclusive_i32", x1, y1, n1), K, Wm)
-            ms_b = T.back_to_back(scan_call("scan_inclusive_i32", x1, y1, n1), K, Wm)
+            ms_b = T.back_to_back(scan_call("scan_inclusive_i32", x1, y1, n1), K, Wm, 30.0)
             opsd["scan_i32_n2^16"] = entry("c1", ms_f, n1 * 8, memcpy_ms(n1 * 8, True),
                                            "n*(4+4), cache-flushed; latency-bound",
                                            {"us_flushed": round(ms_f * 1e3, 2),
@@ -537,7 +563,7 @@ def main():
             for with_idx in (False, True):
                 a = (P(vals), P(mask), P(out), P(idx) if with_idx else None, P(cnt), n, P(wsc),
                      wsc.numel(), sp)
-                ms = T.back_to_back(lambda: check(fnc(*a), "compact"), K, Wm)
+                ms = T.back_to_back(lambda: check(fnc(*a), "compact"), K, Wm, 30.0)
                 c = int(cnt.item())
                 bb = n * 5 + c * 4 + (c * 4 if with_idx else 0)
                 opsd["compact_n2^28" + ("_idx" if with_idx else "")] = entry(
@@ -674,7 +700,7 @@ def main():
                 wsx = ops.workspace(_lib.OP_RADIX_SORT, dev, n5, bits=bits)
                 a = (P(keys), P(ko), P(po), P(kt), P(pt), n5, bits, P(wsx), wsx.numel(), sp)
                 ms = T.back_to_back(lambda: check(lib.radix_sort_u32(*a), "radix"), max(3, K // 4),
-                                    2)
+                                    2, 30.0)
                 # algorithmic bytes: pass 0 reads keys and writes keys + indices (12 B),
                 # later passes read and write both (16 B); the 4- and 8-bit sorts also
                 # need one histogram read (4 B).  Reads this implementation adds (the
@@ -692,7 +718,8 @@ def main():
             kft = torch.empty_like(kf)
             wsx = ops.workspace(_lib.OP_RADIX_SORT, dev, n5, bits=8)
             a = (P(kf), P(kfo), P(po), P(kft), P(pt), n5, 1, P(wsx), wsx.numel(), sp)
-            ms = T.back_to_back(lambda: check(lib.radix_sort_f32(*a), "radix f32"), max(3, K // 4), 2)
+            ms = T.back_to_back(lambda: check(lib.radix_sort_f32(*a), "radix f32"), max(3, K // 4),
+                                2, 30.0)
             bb = n5 * (12 + 16 * 3 + 4)
             opsd["radix8_f32_desc_n2^26"] = entry(
                 "radix", ms, bb, memcpy_ms(bb), "12 + 16 x 3 + 4 bytes per key (4 passes)",
@@ -707,7 +734,8 @@ def main():
             k16o = torch.empty_like(k16)
             k16t = torch.empty_like(k16)
             a = (P(k16), P(k16o), P(po), P(k16t), P(pt), n5, 0, P(wsx), wsx.numel(), sp)
-            ms = T.back_to_back(lambda: check(lib.radix_sort_f16(*a), "radix f16"), max(3, K // 4), 2)
+            ms = T.back_to_back(lambda: check(lib.radix_sort_f16(*a), "radix f16"), max(3, K // 4),
+                                2, 30.0)
             bb = n5 * (8 + 12)
             opsd["radix8_f16_n2^26"] = entry(
                 "radix", ms, bb, memcpy_ms(bb), "8 + 12 bytes per key (2 passes of 16-bit keys and "
@@ -721,7 +749,7 @@ def main():
             nt = torch.empty(1, dtype=torch.int32, device=dev)
             wss = ops.workspace(_lib.OP_COMPACT, dev, n5)
             a = (P(keys), None, P(flags), P(ko), P(po), P(nt), n5, P(wss), wss.numel(), sp)
-            ms = T.back_to_back(lambda: check(lib.split_by_flags_u32(*a), "split"), K, Wm)
+            ms = T.back_to_back(lambda: check(lib.split_by_flags_u32(*a), "split"), K, Wm, 30.0)
             bb = n5 * (1 + 1 + 4 + 4 + 4)  # count kernel reads flags; split reads flags+keys, writes
             opsd["split_n2^26"] = entry("split", ms, bb, memcpy_ms(bb), "n*(1 count + 1+4 read + "
                                         "4+4 written), no input indices")
@@ -742,7 +770,7 @@ def main():
                     xs, ys = x_i32[:m], y_i32[:m]
                     cold = m * 8 < (512 << 20)
                     f = scan_call("scan_inclusive_i32", xs, ys, m)
-                    ms = T.flushed(f, K, Wm) if cold else T.back_to_back(f, K, Wm)
+                    ms = T.flushed(f, K, Wm) if cold else T.back_to_back(f, K, Wm, 30.0)
                     mc = memcpy_ms(m * 8, cold)
                     sweep.append({"n": m, "us": round(ms * 1e3, 2),
                                   "gbps": round(m * 8 / (ms * 1e-3) / 1e9, 1),
