@@ -362,9 +362,10 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topp(
 // none counts arrivals.  k_tile_sums stores the sum of every tile of every
 // row (one read of the weights, all tiles at once); k_weighted_finish, one
 // workgroup per row, adds the row's tile sums in tile order into the total
-// W, finds the first tile whose inclusive sum exceeds theta * W (the tile
-// sums are the ones the search below continues from, so the verdict and the
-// search agree), re-reads that one tile and finds the index in it.  The tile
+// W, finds the first tile whose inclusive sum exceeds theta * W, re-reads
+// that one tile and finds the index in it (as k_topp does: should rounding
+// leave the tile's running sums short of theta * W, its last index is
+// taken).  The tile
 // sums are plain fp32 values in the low halves of workspace words (the top
 // bits clear, as the workspace invariant asks), written before they are read
 // in every call.  This is k_topp's weighted mode with the row's last-arrival
@@ -437,7 +438,7 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_weighted_fini
 //    inner running sum; rounding is monotone, so this is exact for the
 //    running sums as computed here), re-reads the first such tile (just
 //    read) and finds the index; if the head holds none, it
-//    walks the rest of the row itself, 16384 elements per step.
+//    walks the rest of the row itself, 8192 elements per step.
 // A running sum is always taken as E + (tile-local inclusive sum), the same
 // in both kernels, so the head's verdict and the search agree.  The result
 // is the definition's on any input.  The head words are plain fp32 values in
@@ -445,7 +446,14 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_weighted_fini
 // workspace invariant asks), written before they are read in every call.
 constexpr int64_t kEarlyTile = 4096;
 constexpr int64_t kEarlyMaxSegs = 256;  // rows up to 2^20 elements
-constexpr int kFinishThreads = 512;
+// The finishing kernel re-reads a head tile with the head kernel's own tile
+// geometry (the row tile of 4096: 4 waves of 4 chunks, or 8 waves of 2 for
+// misaligned rows), so that its running sums are bit for bit the ones the
+// head's words were taken from.
+template <bool VEC>
+using HeadTile = RowTile<float, RGeomS, VEC>;
+template <bool VEC>
+constexpr int kFinishThreads = HeadTile<VEC>::kThreads;
 
 // Tiles of a row read by the head kernel: a quarter of the row, at least 8.
 static inline uint32_t topp_heads(int64_t len) {
@@ -573,18 +581,19 @@ __device__ __forceinline__ int32_t topp_head_tile(const uint64_t* hw, uint32_t f
 // The whole workgroup: the first index i <= lim of the row at xr whose
 // running sum reaches thr (STRICT: exceeds it), -1 if none.  The head tiles'
 // words pick the first head tile that holds one (E_t + M_t against thr), that
-// tile is re-read and searched; should its sums disagree with the words (they
-// are the same sums, so never), the search goes on from the next head tile.
-// With none in the head, the rest of the row is walked, 16384 elements per
+// tile is re-read with the head kernel's geometry and searched (the same sums,
+// so the search finds what the words promised; should it not, the search goes
+// on from the next head tile).
+// With none in the head, the rest of the row is walked, 8192 elements per
 // step.  *val gets the running sum at the index found, or (none) the sum of
 // every element up to the end of the last tile searched.
 template <bool VEC, bool STRICT>
 __device__ int64_t topp_head_find(const float* xr, int64_t len, const uint64_t* hw, uint32_t heads,
                                   float thr, int64_t lim, float* val, int32_t* s_tile, float* s_e,
                                   float* s_wtot, int32_t* s_min, float* s_val) {
-    using H = Tile<float, float, 4, 2, kFinishThreads / kWave>;   // one head tile, 4096
-    using B = Tile<float, float, 4, 8, kFinishThreads / kWave>;  // 16384 per step after the head
-    static_assert(H::kElems == kEarlyTile, "head tile");
+    using H = HeadTile<VEC>;  // one head tile, 4096, as the head kernel read it
+    using B = Tile<float, float, 4, 2 * H::J, H::WAVES>;  // 8192 per step after the head
+    static_assert(H::kElems == kEarlyTile && B::kElems == 2 * kEarlyTile, "head tile");
     const int64_t lim_tiles = lim / kEarlyTile + 1;  // head tiles holding indices <= lim
     const uint32_t limit = (uint32_t)(lim_tiles < (int64_t)heads ? lim_tiles : heads);
     float carry = 0.f;  // sum of the head tiles before `from`
@@ -650,13 +659,13 @@ __device__ int64_t topp_head_find(const float* xr, int64_t len, const uint64_t* 
 // leaves none), found the same way; the token is idx[j] (idx null: j
 // itself), and the cutoff is stored only when asked for.
 template <bool VEC, bool SAMPLE>
-__global__ __launch_bounds__(kFinishThreads) LS_OCCUPANCY4 void k_topp_finish(
+__global__ __launch_bounds__(kFinishThreads<VEC>) LS_OCCUPANCY4 void k_topp_finish(
     const float* probs, int32_t* cutoff, int64_t len, uint32_t heads, float p,
     const uint64_t* words, const int32_t* idx, const float* theta, int32_t* token) {
     __shared__ int32_t s_tile;
     __shared__ float s_e;
-    __shared__ float s_wtot[kFinishThreads / kWave];
-    __shared__ int32_t s_min[kFinishThreads / kWave];
+    __shared__ float s_wtot[kFinishThreads<VEC> / kWave];
+    __shared__ int32_t s_min[kFinishThreads<VEC> / kWave];
     __shared__ float s_val;
 
     const uint32_t row32 = blockIdx.x;
@@ -831,7 +840,9 @@ static void topp_cutoff_early(bool vec, const float* probs, int32_t* cutoff, int
     hipLaunchKernelGGL(kh, dim3((unsigned)(rows * heads)), dim3(vec ? TV::kThreads : TU::kThreads),
                        0, stream, probs, len, (uint32_t)rows, heads, words);
     auto kf = vec ? k_topp_finish<true, false> : k_topp_finish<false, false>;
-    hipLaunchKernelGGL(kf, dim3((unsigned)rows), dim3(kFinishThreads), 0, stream, probs, cutoff,
+    hipLaunchKernelGGL(kf, dim3((unsigned)rows),
+                       dim3(vec ? kFinishThreads<true> : kFinishThreads<false>), 0,
+                       stream, probs, cutoff,
                        len, heads, p, words, nullptr, nullptr, nullptr);
 }
 
@@ -847,7 +858,9 @@ static void topp_sample_early(bool vec, const float* sorted, const int32_t* idx,
     hipLaunchKernelGGL(kh, dim3((unsigned)(rows * heads)), dim3(vec ? TV::kThreads : TU::kThreads),
                        0, stream, sorted, len, (uint32_t)rows, heads, words);
     auto kf = vec ? k_topp_finish<true, true> : k_topp_finish<false, true>;
-    hipLaunchKernelGGL(kf, dim3((unsigned)rows), dim3(kFinishThreads), 0, stream, sorted, cutoff,
+    hipLaunchKernelGGL(kf, dim3((unsigned)rows),
+                       dim3(vec ? kFinishThreads<true> : kFinishThreads<false>), 0,
+                       stream, sorted, cutoff,
                        len, heads, p, words, idx, theta, token);
 }
 
