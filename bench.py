@@ -223,6 +223,12 @@ def gpu_clocks():
     """Clock and power readings of the GPU from rocm-smi, or None."""
     import shutil
     import subprocess
+    # Under a profiler its preloaded library initialises the GPU in every
+    # child process, and rocm-smi's launcher hop (a script that re-execs its
+    # interpreter) would then exec from such a process: skip the reading.
+    if "rocprof" in os.environ.get("LD_PRELOAD", "") or any(
+            k.startswith("ROCPROF") for k in os.environ):
+        return None
     exe = shutil.which("rocm-smi") or "/opt/rocm/bin/rocm-smi"
     try:
         r = subprocess.run([exe, "--showclocks", "--showpower", "--json"], capture_output=True,
