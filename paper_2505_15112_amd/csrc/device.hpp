@@ -19,6 +19,10 @@
 // tile's data lives in registers from its loads to its stores, so this is
 // what bounds the bytes in flight per CU.
 #define LS_OCCUPANCY4 __attribute__((amdgpu_waves_per_eu(4)))
+// At most 64 VGPRs (8 waves per SIMD): for short tile kernels launched with
+// about as many workgroups as fit the chip at that occupancy, so that none
+// waits for a free slot.
+#define LS_OCCUPANCY8 __attribute__((amdgpu_waves_per_eu(8)))
 
 namespace ls {
 

@@ -28,6 +28,8 @@
 // above T, elements equal to T), so the output keeps index order.
 #include <limits.h>
 
+#include <type_traits>
+
 #include "launch.hpp"
 #include "rowtile.hpp"
 
@@ -293,6 +295,7 @@ constexpr uint32_t kTopkCand = 16384;  // candidates sorted in LDS (128 KB)
 constexpr int kTopkFinishThreads = 1024;
 constexpr uint32_t kTopkSortAll = 2048;  // candidates sorted whole, without the cut to k
 constexpr uint32_t kTopkSmallBucket = 128;  // a cut round's bucket finished by one sort
+constexpr uint32_t kTopkRankMax = 256;  // kept keys placed by rank instead of sorted
 static_assert(kTopkSortMax <= kTopkCand, "the k kept fit the finisher's sort");
 
 // The composite sort key of element i with key `key`: larger keys first,
@@ -456,6 +459,162 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_gather(
     }
 }
 
+// The route for small k (rows of up to 2^17 elements, k <= kTopkTileK): one
+// read of each row.  Every tile keeps as candidates its keys whose top 16
+// bits are at least those of the tile's own k-th largest key.  That is a
+// superset of the tile's share of the row's top k: a key below it has k keys
+// of its own tile above it.  Two digit rounds over the tile, held in
+// registers, find that 16-bit prefix (LDS histograms as in k_topk_count0);
+// the tile writes its candidates to its own kTopkTileSlots slots (keys and
+// complemented indices, the two halves of their composites) and their number
+// to tcount (more than the slots: none written, and the row is finished the
+// long way).
+constexpr uint32_t kTopkTileK = 256;
+constexpr uint32_t kTopkTileSlots = 1024;
+static_assert(kTopkTileSlots * kTopkGatherSegs <= kTopkCand, "a row's candidates fit the LDS sort");
+
+// Thread t takes digit 255 - t, the sum of its COPIES histogram copies; an
+// inclusive scan over the threads counts the keys with a digit >= its own.
+// The thread whose digit's bucket holds the need-th largest counted key (1 <=
+// need <= the keys counted) writes the digit and need minus the keys above
+// the bucket to *s_out, as digit | rest << 8.
+template <int COPIES>
+__device__ __forceinline__ void tile_bucket(const uint32_t* s_h, uint32_t need, uint32_t* s_part,
+                                            uint32_t* s_out) {
+    const int t = threadIdx.x;
+    const int w = t / kWave;
+    uint32_t c = 0;
+    if (t < kTopkDigits) {
+#pragma unroll
+        for (int q = 0; q < COPIES; ++q) c += s_h[q * kTopkCopyStride + (kTopkDigits - 1 - t)];
+    }
+    const uint32_t inc = wave_incl_scan(c);
+    if (t < kTopkDigits && lane_id() == kWave - 1) s_part[w] = inc;
+    __syncthreads();
+    if (t < kTopkDigits) {
+        uint32_t before = 0;
+        for (int q = 0; q < w; ++q) before += s_part[q];
+        const uint32_t at_least = before + inc, above = at_least - c;
+        if (above < need && need <= at_least)
+            *s_out = (uint32_t)(kTopkDigits - 1 - t) | ((need - above) << 8);
+    }
+}
+
+template <class TileT, bool VEC>
+__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY8 void k_topk_tilesel(
+    const uint32_t* x, int64_t len, uint32_t segs, uint32_t k, bool largest, uint64_t* cand,
+    uint32_t* tcount) {
+    static_assert(TileT::kThreads >= kTopkDigits, "one thread per digit");
+    // round 1 counts only the keys of one round-0 bucket: fewer copies, so
+    // that the LDS of 8 workgroups fits a CU (with at most 64 VGPRs, 8 waves
+    // per SIMD: every tile of a 128 x 131072 call resident at once)
+    constexpr int kCopies1 = 2;
+    constexpr int kHist = kTopkCopies * kTopkCopyStride, kHist1 = kCopies1 * kTopkCopyStride;
+    __shared__ uint32_t s_h[kHist];
+    __shared__ uint32_t s_h1[kHist1];
+    __shared__ uint32_t s_part[kTopkDigits / kWave];
+    __shared__ uint32_t s_wtot[TileT::WAVES];
+    __shared__ uint32_t s_sel;
+    for (int i = threadIdx.x; i < kHist; i += TileT::kThreads) s_h[i] = 0;
+    for (int i = threadIdx.x; i < kHist1; i += TileT::kThreads) s_h1[i] = 0;
+    const int64_t row = blockIdx.x / segs;
+    const uint32_t seg = blockIdx.x - (uint32_t)row * segs;
+    const int64_t base = (int64_t)seg * TileT::kElems;
+    uint32_t v[TileT::J][TileT::V];
+    TileT::template load<VEC, true>(x + row * len, len, base, v);
+    const int32_t valid = (int32_t)(len - base < TileT::kElems ? len - base : TileT::kElems);
+    __syncthreads();  // histograms cleared
+    uint32_t* h = s_h + (lane_id() & (kTopkCopies - 1)) * kTopkCopyStride;
+    // bit j V + e: element (j, e) of this lane lies in the row (one register;
+    // opaque, so that the compiler keeps no per-element flags beside it)
+    using Mask = typename std::conditional<(TileT::J * TileT::V > 32), uint64_t, uint32_t>::type;
+    static_assert(TileT::J * TileT::V <= 64, "per-lane masks of at most 64 bits");
+    Mask inrow = 0;
+#pragma unroll
+    for (int j = 0; j < TileT::J; ++j) {
+        const int32_t off = (int32_t)TileT::lane_offset(j);
+#pragma unroll
+        for (int e = 0; e < TileT::V; ++e) inrow |= (Mask)(off + e < valid ? 1u : 0u) << (j * TileT::V + e);
+    }
+    asm volatile("" : "+v"(inrow));
+    // round 0: the top byte of every key of the tile.  Positions past the
+    // row's end count as key 0, the smallest: need <= valid, so they do not
+    // move the need-th largest key, and the candidates are taken below with
+    // the bound checked.
+#pragma unroll
+    for (int j = 0; j < TileT::J; ++j) {
+#pragma unroll
+        for (int e = 0; e < TileT::V; ++e) {
+            const uint32_t key = topk_key(v[j][e], largest);
+            v[j][e] = (inrow >> (j * TileT::V + e)) & 1u ? key : 0u;
+            asm volatile("" : "+v"(v[j][e]));  // the unmasked key is dead here
+            atomicAdd(&h[v[j][e] >> 24], 1u);
+        }
+    }
+    __syncthreads();
+    const uint32_t need = k < (uint32_t)valid ? k : (uint32_t)valid;
+    tile_bucket<kTopkCopies>(s_h, need, s_part, &s_sel);
+    __syncthreads();  // s_sel written
+    const uint32_t d = s_sel & 255u, need1 = s_sel >> 8;
+    // round 1: the second byte of the keys in bucket d
+    uint32_t* h1 = s_h1 + (lane_id() & (kCopies1 - 1)) * kTopkCopyStride;
+#pragma unroll
+    for (int j = 0; j < TileT::J; ++j) {
+#pragma unroll
+        for (int e = 0; e < TileT::V; ++e)
+            if ((v[j][e] >> 24) == d) atomicAdd(&h1[(v[j][e] >> 16) & 255u], 1u);
+    }
+    __syncthreads();
+    tile_bucket<kCopies1>(s_h1, need1, s_part, &s_sel);
+    __syncthreads();
+    const uint32_t p16 = (d << 8) | (s_sel & 255u);
+    Mask take = 0;
+    uint32_t cnt = 0;
+#pragma unroll
+    for (int j = 0; j < TileT::J; ++j) {
+#pragma unroll
+        for (int e = 0; e < TileT::V; ++e) {
+            const bool t = ((inrow >> (j * TileT::V + e)) & 1u) && (v[j][e] >> 16) >= p16;
+            take |= (Mask)(t ? 1u : 0u) << (j * TileT::V + e);
+            cnt += t ? 1u : 0u;
+        }
+    }
+    // this lane's first slot within the tile: lanes before it in its wave,
+    // then the waves before it
+    const uint32_t incl = wave_incl_scan(cnt);
+    const int w = threadIdx.x / kWave;
+    if (lane_id() == kWave - 1) s_wtot[w] = incl;
+    __syncthreads();
+    uint32_t pos = incl - cnt, total = 0;
+    for (int q = 0; q < TileT::WAVES; ++q) {
+        pos += q < w ? s_wtot[q] : 0u;
+        total += s_wtot[q];
+    }
+    if (threadIdx.x == 0) tcount[blockIdx.x] = total;
+    if (total > kTopkTileSlots || !take) return;
+    // The tile's slots: kTopkTileSlots keys, then as many complemented
+    // indices (two arrays rather than 64-bit composites, so that no key needs
+    // an aligned register pair of its own).
+    uint32_t* ck = reinterpret_cast<uint32_t*>(cand + (int64_t)blockIdx.x * kTopkTileSlots);
+    uint32_t* ci = ck + kTopkTileSlots;
+    // the row index of element (j, e): lane0 + j 64 V + e (computed here,
+    // opaque, so that no per-chunk offsets stay live from the loads)
+    uint32_t lane0 = (uint32_t)base + (uint32_t)TileT::lane_offset(0);
+    asm volatile("" : "+v"(lane0));
+#pragma unroll
+    for (int j = 0; j < TileT::J; ++j) {
+        const uint32_t off = lane0 + (uint32_t)(TileT::lane_offset(j) - TileT::lane_offset(0));
+#pragma unroll
+        for (int e = 0; e < TileT::V; ++e) {
+            if ((take >> (j * TileT::V + e)) & 1u) {
+                ck[pos] = v[j][e];  // pos < total
+                ci[pos] = ~(off + (uint32_t)e);
+                ++pos;
+            }
+        }
+    }
+}
+
 // The same network on npow keys held in registers, E per thread (thread t:
 // positions t E .. t E + E - 1; positions at or past npow are padding that
 // never meets a real key): strides below E inside the thread, strides below
@@ -550,6 +709,45 @@ __device__ __forceinline__ void merge_desc(const uint64_t* src, uint32_t L, uint
     }
 }
 
+// For i < n (1 <= n <= kTopkRankMax, a holding at least n rounded up to a
+// power of two >= 64 slots, distinct keys): s_rank[i] = the number of keys
+// of a[0, n) above a[i], its place in descending order.  Each of the
+// workgroup's kTopkFinishThreads threads counts over one of kT / P slices
+// for one key (P: n rounded up to a power of two, at least 64), so that all
+// waves share the work and the slice loads of a wave are one address.  Ends
+// with a barrier.
+template <uint32_t P>
+__device__ __forceinline__ void rank_keys_p(const uint64_t* a, uint32_t n, uint32_t* s_rank) {
+    constexpr uint32_t kT = kTopkFinishThreads;
+    constexpr uint32_t L = P * P / kT;  // 64: 4, 128: 16, 256: 64
+    static_assert(P <= kT && L >= 1, "every key with a thread");
+    const uint32_t i = threadIdx.x % P, q = threadIdx.x / P;
+    if (threadIdx.x < P) s_rank[threadIdx.x] = 0;
+    const uint64_t me = a[i];
+    __syncthreads();  // s_rank cleared
+    uint32_t above = 0;
+    const uint32_t j0 = q * L;
+    if (j0 < n) {  // uniform in the wave
+#pragma unroll
+        for (uint32_t u = 0; u < L; ++u) {
+            const uint32_t j = j0 + u;  // < P
+            const uint64_t o = a[j];
+            above += (j < n && o > me) ? 1u : 0u;
+        }
+    }
+    if (i < n && above) atomicAdd(&s_rank[i], above);
+    __syncthreads();
+}
+__device__ __forceinline__ void rank_keys(const uint64_t* a, uint32_t n, uint32_t* s_rank) {
+    static_assert(kTopkRankMax == 256, "the sizes below");
+    if (n <= 64)
+        rank_keys_p<64>(a, n, s_rank);
+    else if (n <= 128)
+        rank_keys_p<128>(a, n, s_rank);
+    else
+        rank_keys_p<256>(a, n, s_rank);
+}
+
 // One workgroup per row: the k largest keys of the row, in order.  A row
 // whose candidates were gathered sorts them and keeps the first k.  Any
 // other row is finished here: three more digit rounds inside the bucket
@@ -557,24 +755,67 @@ __device__ __forceinline__ void merge_desc(const uint64_t* src, uint32_t L, uint
 // of keys equal to T in the top k; a walk over the row in index order takes
 // every key above T and the first kk equal to T; those k are sorted.
 // CAP slots of LDS (a power of two, at least cap) hold the keys to sort.
-template <uint32_t CAP>
+//
+// TILES (the small-k route): the candidates are the row's tiles' lists
+// (tcount: each tile's count, cand: kTopkTileSlots slots per tile, as
+// k_topk_tilesel lays them out), and no digit of the k-th key is known yet,
+// so the rounds start from the top byte.
+template <uint32_t CAP, bool TILES>
 __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
     const uint32_t* x, int64_t len, uint32_t k, bool largest, const uint64_t* state,
-    const uint64_t* gather, const uint64_t* cand, uint32_t cap, uint32_t* values,
-    int32_t* indices) {
+    const uint64_t* gather, const uint64_t* cand, uint32_t cap, uint32_t segs,
+    const uint32_t* tcount, uint32_t* values, int32_t* indices) {
     static_assert(CAP <= kTopkCand && (CAP & (CAP - 1)) == 0, "LDS sort size");
     __shared__ uint64_t s[CAP];
-    __shared__ uint32_t s_h[kTopkDigits];
+    // digit counts: one copy per lane position, as in k_topk_count0 (the
+    // keys of a round share few digits)
+    __shared__ uint32_t s_h[kTopkCopies * kTopkCopyStride];
     __shared__ uint32_t s_part[kTopkFinishThreads / kWave];
-    __shared__ uint32_t s_prefix, s_kk, s_n, s_qbase, s_bucket, s_nsmall;
+    __shared__ uint32_t s_prefix, s_kk, s_n, s_qbase, s_bucket, s_nsmall, s_m, s_over;
     __shared__ uint64_t s_prefix64;
     __shared__ uint64_t s_small[kTopkSmallBucket];
+    __shared__ uint32_t s_off[kTopkGatherSegs], s_cnt[kTopkGatherSegs];
+    __shared__ uint32_t s_rank[kTopkRankMax];
     constexpr uint32_t kT = kTopkFinishThreads;
+    static_assert(!TILES || kTopkTileSlots <= kT, "one tile slot per thread");
     const int64_t row = blockIdx.x;
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
-    const uint32_t m = (uint32_t)gather[2 * row];
-    if (m <= cap) {
+    uint32_t* hcopy = s_h + (lane & (kTopkCopies - 1)) * kTopkCopyStride;
+    auto digit_count = [&](int t) {  // thread t: digit 255 - t, all copies
+        uint32_t c = 0;
+        if (t < kTopkDigits) {
+#pragma unroll
+            for (int q = 0; q < kTopkCopies; ++q) c += s_h[q * kTopkCopyStride + (kTopkDigits - 1 - t)];
+        }
+        return c;
+    };
+    uint32_t m;
+    bool fits;
+    if constexpr (TILES) {
+        // the row's candidates: each tile's count and first slot in LDS
+        if (threadIdx.x < kWave) {
+            const uint32_t c = (uint32_t)lane < segs ? tcount[row * segs + lane] : 0u;
+            const uint64_t over = __ballot(c > kTopkTileSlots);
+            const uint32_t incl = wave_incl_scan(c);
+            if ((uint32_t)lane < kTopkGatherSegs) {
+                s_off[lane] = incl - c;
+                s_cnt[lane] = c;
+            }
+            if (lane == kWave - 1) {
+                s_m = incl;
+                s_over = over != 0 ? 1u : 0u;
+            }
+        }
+        __syncthreads();
+        m = s_m;
+        fits = s_over == 0;
+    } else {
+        m = (uint32_t)gather[2 * row];
+        fits = m <= cap;
+    }
+    const uint32_t sort_all = TILES ? kTopkRankMax : kTopkSortAll;
+    if (fits) {
         // The k largest of the m candidates.  Up to kTopkSortAll of them are
         // all sorted (the first k are the answer); more are first cut to k:
         // the k-th largest composite C by seven more digit rounds over the
@@ -582,33 +823,55 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
         // bucket's), then the composites >= C (exactly k: composites are
         // distinct) to the front.
         // every candidate load in flight at once, then to LDS for the rounds
+        // Slot e of this thread: candidate t + e kT of the row's list, or
+        // (TILES) candidate t of tile e, which goes to LDS slot off_e + t.
         constexpr int kPer = CAP / kTopkFinishThreads > 0 ? CAP / kTopkFinishThreads : 1;
-        const uint64_t* cr = cand + row * cap;
+        auto slot_valid = [&](int e) {
+            if constexpr (TILES)
+                return (uint32_t)e < segs && threadIdx.x < s_cnt[e];
+            else
+                return threadIdx.x + e * kT < m;
+        };
+        auto slot_lds = [&](int e) {
+            if constexpr (TILES)
+                return s_off[e] + threadIdx.x;
+            else
+                return threadIdx.x + e * kT;
+        };
         uint64_t mine[kPer];
+        uint32_t vmask = 0;  // bit e: slot e holds a candidate
 #pragma unroll
         for (int e = 0; e < kPer; ++e) {
-            const uint32_t i = threadIdx.x + e * kT;
-            mine[e] = i < m ? cr[i] : 0ull;
+            mine[e] = 0ull;
+            if (slot_valid(e)) {
+                vmask |= 1u << e;
+                if constexpr (TILES) {
+                    // tile e's slot t: its key and complemented index
+                    const uint32_t* ck = reinterpret_cast<const uint32_t*>(
+                        cand + ((int64_t)row * segs + e) * kTopkTileSlots);
+                    mine[e] = ((uint64_t)ck[threadIdx.x] << 32) | ck[kTopkTileSlots + threadIdx.x];
+                } else
+                    mine[e] = cand[row * cap + threadIdx.x + e * kT];
+            }
         }
 #pragma unroll
-        for (int e = 0; e < kPer; ++e) {
-            const uint32_t i = threadIdx.x + e * kT;
-            if (i < m) s[i] = mine[e];
-        }
-        uint64_t prefix = (uint32_t)state[2 * row] & 255u;
-        uint32_t kk = (uint32_t)state[2 * row + 1];
-        const bool cut = m > k && m > kTopkSortAll;  // uniform
-        for (int r = 1; r < 8 && cut; ++r) {
-            for (uint32_t i = threadIdx.x; i < kTopkDigits; i += kT) s_h[i] = 0;
+        for (int e = 0; e < kPer; ++e)
+            if ((vmask >> e) & 1u) s[slot_lds(e)] = mine[e];
+        uint64_t prefix = TILES ? 0ull : ((uint32_t)state[2 * row] & 255u);
+        uint32_t kk = TILES ? k : (uint32_t)state[2 * row + 1];
+        const bool cut = m > k && m > sort_all;  // uniform
+        for (int r = TILES ? 0 : 1; r < 8 && cut; ++r) {
+            for (uint32_t i = threadIdx.x; i < kTopkCopies * kTopkCopyStride; i += kT) s_h[i] = 0;
             __syncthreads();  // also: the candidates are in LDS
             const int hs = 64 - 8 * r, ds = 56 - 8 * r;
             for (uint32_t i = threadIdx.x; i < m; i += kT) {
                 const uint64_t c = s[i];
-                if ((c >> hs) == prefix) atomicAdd(&s_h[(uint32_t)(c >> ds) & 255u], 1u);
+                if (r == 0 || (c >> hs) == prefix)
+                    atomicAdd(&hcopy[(uint32_t)(c >> ds) & 255u], 1u);
             }
             __syncthreads();
             const int t = threadIdx.x;
-            const uint32_t c = t < kTopkDigits ? s_h[kTopkDigits - 1 - t] : 0u;
+            const uint32_t c = digit_count(t);
             const uint32_t inc = wave_incl_scan(c);
             if (t < kTopkDigits && lane == kWave - 1) s_part[w] = inc;
             __syncthreads();
@@ -627,10 +890,11 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
             kk = s_kk;
             if (s_bucket <= kTopkSmallBucket) {  // uniform
                 // A bucket this small is finished in one step instead of
-                // more rounds: its composites are gathered, one wavefront
-                // sorts them in registers and takes the kk-th largest, the
-                // k-th largest composite of the row.
+                // more rounds: its composites are gathered and ranked, and
+                // the one with kk - 1 above it is the k-th largest composite
+                // of the row.
                 const int hs2 = 56 - 8 * r;  // the new prefix's shift
+                const uint32_t nb = s_bucket;  // >= kk >= 1
                 if (threadIdx.x == 0) s_nsmall = 0;
                 __syncthreads();
                 for (uint32_t i = threadIdx.x; i < m; i += kT) {
@@ -641,56 +905,57 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
                     }
                 }
                 __syncthreads();
-                if (threadIdx.x < kWave) {
-                    const uint32_t nb = s_nsmall < kTopkSmallBucket ? s_nsmall : kTopkSmallBucket;
-                    uint64_t v2[2];
-#pragma unroll
-                    for (int e = 0; e < 2; ++e) {
-                        const uint32_t q = (uint32_t)lane * 2 + e;
-                        v2[e] = q < nb ? s_small[q] : 0ull;  // zero pads sort last
-                    }
-                    // 128 slots, 2 per lane: no stride reaches the LDS stages
-                    bitonic_desc_regs<2>(v2, s_small, kTopkSmallBucket, kWave, kTopkSmallBucket);
-                    const uint32_t q = kk - 1;  // kk <= the bucket's size
-#pragma unroll
-                    for (int e = 0; e < 2; ++e)
-                        if ((uint32_t)lane * 2 + e == q) s_prefix64 = v2[e];
-                }
+                rank_keys(s_small, nb, s_rank);
+                if (threadIdx.x < nb && s_rank[threadIdx.x] == kk - 1)  // exactly one
+                    s_prefix64 = s_small[threadIdx.x];
                 __syncthreads();
                 prefix = s_prefix64;
                 break;
             }
         }
-        // prefix: the k-th largest composite (when m > k); each thread still
-        // holds its candidates in `mine`
-        if (threadIdx.x == 0) s_n = 0;
-        __syncthreads();
+        // prefix: the k-th largest composite; each thread still holds its
+        // candidates in `mine`.  Cut: the k at or above it go to s[0, k), each
+        // thread's after those of the threads before it (a workgroup scan).
+        // Otherwise all m are in s[0, m) already.
+        if (cut) {
+            uint32_t keep = 0, cnt = 0;
 #pragma unroll
-        for (int e = 0; e < kPer; ++e) {
-            const uint32_t i = threadIdx.x + e * kT;
-            if (i < m && (!cut || mine[e] >= prefix)) {
-                // below n (k, or m when all are sorted); checked all the same
-                const uint32_t pos = atomicAdd(&s_n, 1u);
-                if (pos < cap) s[pos] = mine[e];
+            for (int e = 0; e < kPer; ++e) {
+                const bool kp = ((vmask >> e) & 1u) && mine[e] >= prefix;
+                keep |= (kp ? 1u : 0u) << e;
+                cnt += kp ? 1u : 0u;
+            }
+            const uint32_t inc = wave_incl_scan(cnt);
+            if (lane == kWave - 1) s_part[w] = inc;
+            __syncthreads();  // also: every round's reads of s are done
+            uint32_t pos = inc - cnt;
+#pragma unroll
+            for (int q = 0; q < (int)(kT / kWave); ++q) pos += q < w ? s_part[q] : 0u;
+#pragma unroll
+            for (int e = 0; e < kPer; ++e) {
+                if ((keep >> e) & 1u) {
+                    if (pos < cap) s[pos] = mine[e];  // pos < k; checked all the same
+                    ++pos;
+                }
             }
         }
     } else {
         const uint32_t* xr = x + row * len;
-        uint32_t prefix = (uint32_t)state[2 * row];
-        uint32_t kk = (uint32_t)state[2 * row + 1];
-        for (int r = 1; r < 4; ++r) {
-            for (uint32_t i = threadIdx.x; i < kTopkDigits; i += kT) s_h[i] = 0;
+        uint32_t prefix = TILES ? 0u : (uint32_t)state[2 * row];
+        uint32_t kk = TILES ? k : (uint32_t)state[2 * row + 1];
+        for (int r = TILES ? 0 : 1; r < 4; ++r) {
+            for (uint32_t i = threadIdx.x; i < kTopkCopies * kTopkCopyStride; i += kT) s_h[i] = 0;
             __syncthreads();
             const int hs = 32 - 8 * r, ds = 24 - 8 * r;
             for (int64_t i = threadIdx.x; i < len; i += kT) {
                 const uint32_t key = topk_key(xr[i], largest);
-                if ((key >> hs) == prefix) atomicAdd(&s_h[(key >> ds) & 255u], 1u);
+                if (r == 0 || (key >> hs) == prefix) atomicAdd(&hcopy[(key >> ds) & 255u], 1u);
             }
             __syncthreads();
             // thread t takes digit 255 - t: an inclusive scan over t counts the
             // keys with a digit >= its own
             const int t = threadIdx.x;
-            const uint32_t c = t < kTopkDigits ? s_h[kTopkDigits - 1 - t] : 0u;
+            const uint32_t c = digit_count(t);
             const uint32_t inc = wave_incl_scan(c);
             if (t < kTopkDigits && lane == kWave - 1) s_part[w] = inc;
             __syncthreads();
@@ -735,11 +1000,29 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
             __syncthreads();
         }
     }
-    // the n kept keys are s[0, n) (n >= k): sorted in registers, E per thread
-    const uint32_t n = (m <= cap && m <= kTopkSortAll) ? m : k;
+    // the n kept keys are s[0, n) (n >= k)
+    const uint32_t n = (fits && m <= sort_all) ? m : k;
+    auto emit = [&](uint32_t p, uint64_t c) {  // output p (< k): composite c
+        const uint32_t key = (uint32_t)(c >> 32);
+        const uint32_t code = largest ? key : ~key;
+        values[row * k + p] = code ^ ((code >> 31) ? 0x80000000u : 0xFFFFFFFFu);
+        indices[row * k + p] = (int32_t)~(uint32_t)c;
+    };
+    __syncthreads();
+    if (n <= kTopkRankMax) {  // uniform
+        // Few keys: each goes straight to its rank, the number of kept keys
+        // above it (the composites are distinct).
+        rank_keys(s, n, s_rank);
+        if (threadIdx.x < n) {
+            const uint32_t r = s_rank[threadIdx.x];
+            if (r < k) emit(r, s[threadIdx.x]);
+        }
+        return;
+    }
+    if constexpr (TILES) return;  // n <= k <= kTopkRankMax
+    // more: sorted in registers, E per thread
     uint32_t npow = 1;
     while (npow < n) npow <<= 1;
-    __syncthreads();
     auto sort_out = [&](auto e_c) {
         constexpr int E = decltype(e_c)::value;
         static_assert((uint32_t)E * kT <= CAP || E == 1, "LDS slots for the register sort");
@@ -769,12 +1052,7 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             const uint32_t p = threadIdx.x * E + e;
-            if (p < k) {
-                const uint32_t key = (uint32_t)(v[e] >> 32);
-                const uint32_t code = largest ? key : ~key;
-                values[row * k + p] = code ^ ((code >> 31) ? 0x80000000u : 0xFFFFFFFFu);
-                indices[row * k + p] = (int32_t)~(uint32_t)v[e];
-            }
+            if (p < k) emit(p, v[e]);
         }
     };
     if (npow <= kT)
@@ -802,6 +1080,13 @@ static bool topk_gather_route(int64_t len, int64_t k) {
     return len <= kTopkGatherMaxLen && k <= kTopkSortMax;
 }
 static int64_t topk_gather_tile(int64_t len) { return len > 16384 ? 8192 : 4096; }
+// The small-k route (one read of each row): the gather route's rows and tiles.
+static bool topk_tiles_route(int64_t len, int64_t k) {
+    return topk_gather_route(len, k) && k <= kTopkTileK;
+}
+static uint32_t topk_tiles_segs(int64_t len) {
+    return (uint32_t)((len + topk_gather_tile(len) - 1) / topk_gather_tile(len));
+}
 static uint32_t topk_cap(int64_t len) {
     return (uint32_t)(len < (int64_t)kTopkCand ? len : (int64_t)kTopkCand);
 }
@@ -826,6 +1111,8 @@ size_t topk_ws_bytes(int64_t rows, int64_t len, int64_t k) {
     return a > b ? a : b;
 }
 size_t topk_scratch_bytes(int64_t rows, int64_t len, int64_t k) {
+    if (topk_tiles_route(len, k))
+        return align256((size_t)rows * topk_tiles_segs(len) * kTopkTileSlots * sizeof(uint64_t));
     if (topk_gather_route(len, k)) return align256((size_t)rows * topk_cap(len) * sizeof(uint64_t));
     return (k > kTopkSortMax ? 4 : 2) * align256((size_t)rows * (size_t)k * 4);
 }
@@ -892,11 +1179,46 @@ static hipError_t topk_gather(bool vec, const uint32_t* x, int64_t rows, int64_t
                        dim3(threads), 0, stream, x, len, segs, largest, (const uint64_t*)state,
                        (const uint64_t*)gather, (const uint32_t*)offs, cand, cap);
     // the LDS sort sized to the row (cap <= CAP)
-    auto kf = cap > 8192 ? k_topk_finish<kTopkCand>
-                         : (cap > 2048 ? k_topk_finish<8192> : k_topk_finish<2048>);
+    auto kf = cap > 8192 ? k_topk_finish<kTopkCand, false>
+                         : (cap > 2048 ? k_topk_finish<8192, false> : k_topk_finish<2048, false>);
     hipLaunchKernelGGL(kf, dim3((uint32_t)rows), dim3(kTopkFinishThreads), 0, stream, x, len, kk,
                        largest, (const uint64_t*)state, (const uint64_t*)gather,
-                       (const uint64_t*)cand, cap, values, indices);
+                       (const uint64_t*)cand, cap, segs, (const uint32_t*)nullptr, values,
+                       indices);
+    return hipGetLastError();
+}
+
+template <class G>
+static hipError_t topk_tiles(bool vec, const uint32_t* x, int64_t rows, int64_t len, int64_t k,
+                             bool largest, uint32_t* values, int32_t* indices, void* scratch,
+                             void* ws, hipStream_t stream) {
+    using TV = RowTile<uint32_t, G, true>;
+    using TU = RowTile<uint32_t, G, false>;
+    static_assert(TV::kElems == TU::kElems, "one tile size per geometry");
+    const uint32_t segs = (uint32_t)((len + TV::kElems - 1) / TV::kElems);
+    const uint32_t nt = (uint32_t)(rows * segs);
+    const unsigned threads = vec ? TV::kThreads : TU::kThreads;
+    const TopkLayout l = topk_layout(rows, len, k);
+    uint32_t* tcount = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + l.offs);
+    uint64_t* cand = reinterpret_cast<uint64_t*>(scratch);
+    const uint32_t kk = (uint32_t)k;
+    // every candidate in the finisher's LDS, every tile list on one slot per
+    // finisher thread (CAP / kTopkFinishThreads of them)
+    const uint32_t cap = (uint32_t)(len < (int64_t)segs * kTopkTileSlots
+                                        ? len : (int64_t)segs * kTopkTileSlots);
+    const uint32_t fcap = cap > 8192 ? kTopkCand : (cap > 2048 ? 8192 : 2048);
+    if (segs != topk_tiles_segs(len) || segs > kTopkGatherSegs ||
+        segs > fcap / kTopkFinishThreads)
+        return hipErrorInvalidValue;  // not on this route
+    hipLaunchKernelGGL((vec ? k_topk_tilesel<TV, true> : k_topk_tilesel<TU, false>), dim3(nt),
+                       dim3(threads), 0, stream, x, len, segs, kk, largest, cand, tcount);
+    auto kf = fcap == kTopkCand ? k_topk_finish<kTopkCand, true>
+                                : (fcap == 8192 ? k_topk_finish<8192, true>
+                                                : k_topk_finish<2048, true>);
+    hipLaunchKernelGGL(kf, dim3((uint32_t)rows), dim3(kTopkFinishThreads), 0, stream, x, len, kk,
+                       largest, (const uint64_t*)nullptr, (const uint64_t*)nullptr,
+                       (const uint64_t*)cand, cap, segs, (const uint32_t*)tcount, values,
+                       indices);
     return hipGetLastError();
 }
 
@@ -904,6 +1226,15 @@ hipError_t launch_topk(const float* x, float* values, int32_t* indices, int64_t 
                        int64_t k, bool largest, void* scratch, void* ws, hipStream_t stream) {
     if (rows == 0 || k == 0) return hipSuccess;
     const bool vec = (len % 4 == 0) && ((uintptr_t)x % 16) == 0;
+    if (topk_tiles_route(len, k)) {
+        const uint32_t* xb = reinterpret_cast<const uint32_t*>(x);
+        uint32_t* vb = reinterpret_cast<uint32_t*>(values);
+        return topk_gather_tile(len) == 8192
+                   ? topk_tiles<RGeomM>(vec, xb, rows, len, k, largest, vb, indices, scratch, ws,
+                                        stream)
+                   : topk_tiles<RGeomS>(vec, xb, rows, len, k, largest, vb, indices, scratch, ws,
+                                        stream);
+    }
     if (topk_gather_route(len, k)) {
         const uint32_t* xb = reinterpret_cast<const uint32_t*>(x);
         uint32_t* vb = reinterpret_cast<uint32_t*>(values);

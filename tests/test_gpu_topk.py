@@ -50,7 +50,12 @@ def _rows(rows, length, seed, kind):
 SHAPES = [(1, 1, [1]), (3, 5, [1, 2, 5]), (1000, 100, [1, 10, 100]), (4, 4096, [1, 64, 4096]),
           (3, 4097, [100, 4097]), (7, 10_001, [1, 1000]), (2, 3 * 8192 + 5, [5000]),
           (9, 65_536, [50, 4096]), (3, 65_537, [3]), (16, 131_072, [1, 4096]),
-          (3, 200_003, [2000]), (4, 20_000, [8191, 8192, 8193]), (1, (1 << 20) + 3, [1, 70_000])]
+          (3, 200_003, [2000]), (4, 20_000, [8191, 8192, 8193]), (1, (1 << 20) + 3, [1, 70_000]),
+          # the small-k route (k <= 256, rows up to 2^17): ragged last tiles
+          # with fewer keys than k, its boundary at k = 256 / 257, and the
+          # finisher's three LDS sizes
+          (2, 3 * 8192 + 5, [7, 256]), (5, 16_385, [256, 257]), (3, 16_384, [200]),
+          (2, 2048, [256]), (6, 131_072, [256, 257])]
 # k <= 8192: the kept elements are ordered by an LDS sort per row; above, by the row radix sort
 
 
@@ -84,6 +89,40 @@ def test_topk_misaligned(ops):
     rv, ri = oracle.topk_rows_f32(flat[1:].reshape(4, 40_000), 333)
     assert_equal_first_diff(to_host(i), ri, "misaligned indices")
     assert_equal_first_diff(to_host(v).view(np.uint32), rv.view(np.uint32), "misaligned values")
+
+
+def test_topk_misaligned_small_k(ops):
+    """The small-k route on misaligned rows (element-wise loads, twice the
+    waves per tile)."""
+    announce("topk misaligned small k")
+    flat = _rows(1, 3 * 70_000 + 1, seed=12, kind="normal").reshape(-1)
+    d = to_dev(flat)[1:].reshape(3, 70_000)
+    assert d.data_ptr() % 16 != 0
+    for k in (1, 50, 256):
+        v, i = ops.topk_rows_f32(d, k)
+        rv, ri = oracle.topk_rows_f32(flat[1:].reshape(3, 70_000), k)
+        assert_equal_first_diff(to_host(i), ri, f"misaligned k={k} indices")
+        assert_equal_first_diff(to_host(v).view(np.uint32), rv.view(np.uint32),
+                                f"misaligned k={k} values")
+
+
+@pytest.mark.parametrize("n_t", [1024, 1025])
+@pytest.mark.parametrize("largest", [True, False])
+def test_topk_tile_slot_edges(ops, n_t, largest):
+    """On the small-k route every 8192-element tile keeps its keys whose top 16
+    key bits are at least its own k-th key's, in 1024 slots; a tile with more
+    sends its row the long way.  Here one tile of the middle row holds n_t
+    values sharing their top 16 bits (2 + i * 2^-20), with ties among them,
+    above (below, for the smallest k) the rest of the row, which is normal
+    data of small magnitude."""
+    announce("topk tile slots", n_t, largest)
+    rows, length, k = 3, 131_072, 100
+    rng = np.random.default_rng(n_t)
+    x = (W.values_f32(rows * length, seed=n_t).reshape(rows, length) * 0.1).astype(np.float32)
+    pos = 5 * 8192 + rng.choice(8192, n_t, replace=False)
+    big = (2.0 + rng.integers(0, 64, n_t) * 2.0**-20).astype(np.float32)
+    x[1, pos] = big if largest else -big
+    _check(ops, x, k, largest, f"tile slots n_t={n_t} largest={largest}")
 
 
 @pytest.mark.parametrize("k", [64, 4096])
