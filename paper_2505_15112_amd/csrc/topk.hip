@@ -406,7 +406,7 @@ __global__ __launch_bounds__(kTopkDigits) void k_topk_bucket(const uint32_t* his
 // from the first slots the bucket kernel left for each tile, in index order
 // inside a tile.  Rows with more than cap candidates are left alone.
 template <class TileT, bool VEC>
-__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_gather(
+__global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY8 void k_topk_gather(
     const uint32_t* x, int64_t len, uint32_t segs, bool largest, const uint64_t* state,
     const uint64_t* gather, const uint32_t* offs, uint64_t* cand, uint32_t cap) {
     __shared__ uint32_t s_wtot[TileT::WAVES];
@@ -443,16 +443,26 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_gather(
     __syncthreads();
     if (!take) return;
     uint32_t pos = first + incl - cnt;
-    for (int q = 0; q < w; ++q) pos += s_wtot[q];
-    uint64_t* cr = cand + (int64_t)row * cap;
+#pragma unroll
+    for (int q = 0; q < TileT::WAVES; ++q) pos += q < w ? s_wtot[q] : 0u;
+    // the row's list: cap keys, then as many complemented indices (the two
+    // halves of the composites, in two arrays so that no key needs an aligned
+    // register pair of its own)
+    uint32_t* ck = reinterpret_cast<uint32_t*>(cand + (int64_t)row * cap);
+    uint32_t* ci = ck + cap;
+    uint32_t lane0 = (uint32_t)base + (uint32_t)TileT::lane_offset(0);
+    asm volatile("" : "+v"(lane0));  // no per-chunk offsets kept live from the loads
 #pragma unroll
     for (int j = 0; j < TileT::J; ++j) {
-        const uint32_t off = (uint32_t)(base + TileT::lane_offset(j));
+        const uint32_t off = lane0 + (uint32_t)(TileT::lane_offset(j) - TileT::lane_offset(0));
 #pragma unroll
         for (int e = 0; e < TileT::V; ++e) {
             if ((take >> (j * TileT::V + e)) & 1u) {
                 // pos < the row's candidate count <= cap; checked all the same
-                if (pos < cap) cr[pos] = topk_composite(v[j][e], off + (uint32_t)e);
+                if (pos < cap) {
+                    ck[pos] = v[j][e];
+                    ci[pos] = ~(off + (uint32_t)e);
+                }
                 ++pos;
             }
         }
@@ -850,8 +860,12 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
                     const uint32_t* ck = reinterpret_cast<const uint32_t*>(
                         cand + ((int64_t)row * segs + e) * kTopkTileSlots);
                     mine[e] = ((uint64_t)ck[threadIdx.x] << 32) | ck[kTopkTileSlots + threadIdx.x];
-                } else
-                    mine[e] = cand[row * cap + threadIdx.x + e * kT];
+                } else {
+                    // the row's list: cap keys, then the complemented indices
+                    const uint32_t* ck = reinterpret_cast<const uint32_t*>(cand + row * cap);
+                    const uint32_t i = threadIdx.x + e * kT;
+                    mine[e] = ((uint64_t)ck[i] << 32) | ck[cap + i];
+                }
             }
         }
 #pragma unroll
