@@ -405,11 +405,56 @@ __global__ __launch_bounds__(kTopkDigits) void k_topk_bucket(const uint32_t* his
 // round 0), to the row's candidate list (cap slots per row), tile by tile
 // from the first slots the bucket kernel left for each tile, in index order
 // inside a tile.  Rows with more than cap candidates are left alone.
+// Write a tile's candidates -- element (j, e) of this lane when bit j V + e
+// of `take` is set, the lane's first at tile slot lpos, total in the tile --
+// as keys to ck[0, total) and complemented row indices (base + the element's
+// tile offset) to ci[0, total), both clipped to `room` slots.  Up to
+// kTopkStage of them are gathered in LDS first (s_ck, s_ci) and written by
+// consecutive threads; more go straight from each lane (a uniform choice).
+// Every thread of the workgroup calls it.
+constexpr uint32_t kTopkStage = 1024;
+template <class TileT, class V, class Mask>
+__device__ __forceinline__ void stage_candidates(const V& v, Mask take, uint32_t lpos,
+                                                 uint32_t total, uint32_t base, uint32_t* ck,
+                                                 uint32_t* ci, uint32_t room, uint32_t* s_ck,
+                                                 uint32_t* s_ci) {
+    const bool staged = total <= kTopkStage;  // uniform
+    uint32_t* dk = staged ? s_ck : ck;
+    uint32_t* di = staged ? s_ci : ci;
+    const uint32_t lim = staged ? kTopkStage : room;
+    uint32_t lane0 = base + (uint32_t)TileT::lane_offset(0);
+    asm volatile("" : "+v"(lane0));  // no per-chunk offsets kept live from the loads
+    if (take) {
+#pragma unroll
+        for (int j = 0; j < TileT::J; ++j) {
+            const uint32_t off = lane0 + (uint32_t)(TileT::lane_offset(j) - TileT::lane_offset(0));
+#pragma unroll
+            for (int e = 0; e < TileT::V; ++e) {
+                if ((take >> (j * TileT::V + e)) & 1u) {
+                    if (lpos < lim) {  // lpos < total; checked all the same
+                        dk[lpos] = v[j][e];
+                        di[lpos] = ~(off + (uint32_t)e);
+                    }
+                    ++lpos;
+                }
+            }
+        }
+    }
+    if (!staged) return;
+    __syncthreads();
+    const uint32_t n = total < room ? total : room;
+    for (uint32_t i = threadIdx.x; i < n; i += TileT::kThreads) {
+        ck[i] = s_ck[i];
+        ci[i] = s_ci[i];
+    }
+}
+
 template <class TileT, bool VEC>
 __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY8 void k_topk_gather(
     const uint32_t* x, int64_t len, uint32_t segs, bool largest, const uint64_t* state,
     const uint64_t* gather, const uint32_t* offs, uint64_t* cand, uint32_t cap) {
     __shared__ uint32_t s_wtot[TileT::WAVES];
+    __shared__ uint32_t s_ck[kTopkStage], s_ci[kTopkStage];
     const uint32_t row32 = blockIdx.x / segs;
     const uint32_t seg = blockIdx.x - row32 * segs;
     const int64_t row = row32;
@@ -441,32 +486,19 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY8 void k_topk_gather(
     const int w = threadIdx.x / kWave;
     if (lane_id() == kWave - 1) s_wtot[w] = incl;
     __syncthreads();
-    if (!take) return;
-    uint32_t pos = first + incl - cnt;
+    uint32_t lpos = incl - cnt, total = 0;  // this lane's first slot in the tile
 #pragma unroll
-    for (int q = 0; q < TileT::WAVES; ++q) pos += q < w ? s_wtot[q] : 0u;
+    for (int q = 0; q < TileT::WAVES; ++q) {
+        lpos += q < w ? s_wtot[q] : 0u;
+        total += s_wtot[q];
+    }
     // the row's list: cap keys, then as many complemented indices (the two
     // halves of the composites, in two arrays so that no key needs an aligned
     // register pair of its own)
     uint32_t* ck = reinterpret_cast<uint32_t*>(cand + (int64_t)row * cap);
     uint32_t* ci = ck + cap;
-    uint32_t lane0 = (uint32_t)base + (uint32_t)TileT::lane_offset(0);
-    asm volatile("" : "+v"(lane0));  // no per-chunk offsets kept live from the loads
-#pragma unroll
-    for (int j = 0; j < TileT::J; ++j) {
-        const uint32_t off = lane0 + (uint32_t)(TileT::lane_offset(j) - TileT::lane_offset(0));
-#pragma unroll
-        for (int e = 0; e < TileT::V; ++e) {
-            if ((take >> (j * TileT::V + e)) & 1u) {
-                // pos < the row's candidate count <= cap; checked all the same
-                if (pos < cap) {
-                    ck[pos] = v[j][e];
-                    ci[pos] = ~(off + (uint32_t)e);
-                }
-                ++pos;
-            }
-        }
-    }
+    stage_candidates<TileT>(v, take, lpos, total, (uint32_t)base, ck + first, ci + first,
+                            cap - (first < cap ? first : cap), s_ck, s_ci);
 }
 
 // The route for small k (rows of up to 2^17 elements, k <= kTopkTileK): one
@@ -595,34 +627,22 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY8 void k_topk_tilesel(
     const int w = threadIdx.x / kWave;
     if (lane_id() == kWave - 1) s_wtot[w] = incl;
     __syncthreads();
-    uint32_t pos = incl - cnt, total = 0;
+    uint32_t lpos = incl - cnt, total = 0;  // this lane's first slot in the tile
+#pragma unroll
     for (int q = 0; q < TileT::WAVES; ++q) {
-        pos += q < w ? s_wtot[q] : 0u;
+        lpos += q < w ? s_wtot[q] : 0u;
         total += s_wtot[q];
     }
     if (threadIdx.x == 0) tcount[blockIdx.x] = total;
-    if (total > kTopkTileSlots || !take) return;
+    if (total > kTopkTileSlots) return;  // uniform: the row goes the long way
     // The tile's slots: kTopkTileSlots keys, then as many complemented
     // indices (two arrays rather than 64-bit composites, so that no key needs
-    // an aligned register pair of its own).
+    // an aligned register pair of its own); staged in the round-0 histogram's
+    // LDS, which is free by now.
+    static_assert(kTopkTileSlots <= kTopkStage && 2 * kTopkStage <= kHist, "staging room");
     uint32_t* ck = reinterpret_cast<uint32_t*>(cand + (int64_t)blockIdx.x * kTopkTileSlots);
-    uint32_t* ci = ck + kTopkTileSlots;
-    // the row index of element (j, e): lane0 + j 64 V + e (computed here,
-    // opaque, so that no per-chunk offsets stay live from the loads)
-    uint32_t lane0 = (uint32_t)base + (uint32_t)TileT::lane_offset(0);
-    asm volatile("" : "+v"(lane0));
-#pragma unroll
-    for (int j = 0; j < TileT::J; ++j) {
-        const uint32_t off = lane0 + (uint32_t)(TileT::lane_offset(j) - TileT::lane_offset(0));
-#pragma unroll
-        for (int e = 0; e < TileT::V; ++e) {
-            if ((take >> (j * TileT::V + e)) & 1u) {
-                ck[pos] = v[j][e];  // pos < total
-                ci[pos] = ~(off + (uint32_t)e);
-                ++pos;
-            }
-        }
-    }
+    stage_candidates<TileT>(v, take, lpos, total, (uint32_t)base, ck, ck + kTopkTileSlots,
+                            kTopkTileSlots, s_h, s_h + kTopkStage);
 }
 
 // The same network on npow keys held in registers, E per thread (thread t:
