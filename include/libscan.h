@@ -343,16 +343,23 @@ int topp_sample_f32(const float* probs, const float* theta_dev, float p, int32_t
  * copies; idx_out receives their indices within the row.  values_out and
  * idx_out are rows x k.  0 <= k <= len (EINVAL otherwise); len <= INT32_MAX,
  * rows * ceil(len / 4096) <= 2^24, rows * k <= INT32_MAX.  Rows of at most
- * 2^17 elements with k <= 8192: one round of 8-bit digit counts finds the
- * key byte of each row's k-th largest, the keys at or above it are gathered
- * and one workgroup per row sorts them (at most 16384 per row; a row with
- * more is finished by its workgroup with three more rounds over the row);
- * other shapes: four rounds of digit counts find the k-th key, one stable
- * split keeps the top k in index order, and a row sort orders them.  scratch
- * as in topp_sample_f32, of libscan_scratch_bytes(LIBSCAN_OP_TOPK, rows,
- * len, k) bytes (8 * min(len, 16384) per row for the first route, 16 per
- * kept element for the second).  No output may overlap an input or the
- * other output.  Workspace: LIBSCAN_OP_TOPK with (n = k, rows, len). */
+ * 2^17 elements with k <= 256: each tile of the row (8192 elements, 4096
+ * for rows of at most 16384) keeps its keys whose top 16 bits are at least
+ * those of its own k-th largest, and one workgroup per row selects the k
+ * largest of those and places them by rank (one read of the row; a tile
+ * with more than 1024 such keys sends its row the long way: four digit
+ * rounds over the row, then a selection in index order).  Rows of at most
+ * 2^17 elements with 256 < k <= 8192: one round of 8-bit digit counts finds
+ * the key byte of each row's k-th largest, the keys at or above it are
+ * gathered and one workgroup per row sorts them (at most 16384 per row; a
+ * row with more is finished by its workgroup with three more rounds over
+ * the row).  Other shapes: four rounds of digit counts find the k-th key,
+ * one stable split keeps the top k in index order, and a row sort orders
+ * them.  scratch as in topp_sample_f32, of libscan_scratch_bytes(
+ * LIBSCAN_OP_TOPK, rows, len, k) bytes (8192 per tile for the first route,
+ * 8 * min(len, 16384) per row for the second, 16 per kept element for the
+ * third).  No output may overlap an input or the other output.  Workspace:
+ * LIBSCAN_OP_TOPK with (n = k, rows, len). */
 int topk_rows_f32(const float* x, float* values_out, int32_t* idx_out, int64_t rows, int64_t len,
                   int64_t k, int largest, void* scratch, size_t scratch_bytes, void* ws,
                   size_t ws_bytes, void* stream);

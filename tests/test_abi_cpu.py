@@ -330,6 +330,11 @@ def test_topk_validation(lib):
     assert out.value >= 8 * 128 * 4096            # the kept values and indices
     assert lib.libscan_scratch_bytes(_lib.OP_TOPK, 4, 131072, 9000, ctypes.byref(out)) == _lib.OK
     assert out.value >= 16 * 4 * 9000             # and the row sort's ping-pong buffers
+    # k <= 256: 1024 candidate slots (keys and indices) per tile of the row
+    assert lib.libscan_scratch_bytes(_lib.OP_TOPK, 128, 131072, 64, ctypes.byref(out)) == _lib.OK
+    assert out.value >= 128 * 16 * 8192           # 8192-element tiles
+    assert lib.libscan_scratch_bytes(_lib.OP_TOPK, 3, 16384, 256, ctypes.byref(out)) == _lib.OK
+    assert out.value >= 3 * 4 * 8192              # 4096-element tiles up to 16384
 
 
 def test_workspace_error_validation(lib):
