@@ -19,7 +19,9 @@
 // reads of each row instead of five); a row with more candidates is
 // finished by that workgroup alone (the three further rounds and the
 // selection over its row).  That route's first round is two kernels: the
-// tiles store their counts, then one workgroup per row adds them.
+// tiles store their counts, then one workgroup per row adds them.  With
+// k <= 256 the candidates come from one read instead: each tile keeps its
+// keys at or above its own k-th key's top 16 bits (k_topk_tilesel).
 //
 // No workgroup waits for another during the histogram rounds: each tile
 // writes its 256 digit counts to its own slots, and (on the longer route)
