@@ -160,14 +160,14 @@ def test_topk_repeated_calls_share_workspace(ops):
 @pytest.mark.parametrize("n_top", [16_383, 16_384, 16_385])
 @pytest.mark.parametrize("largest", [True, False])
 def test_topk_candidate_capacity_edges(ops, n_top, largest):
-    """Rows of up to 2^17 elements and k <= 8192 keep the keys whose top 8
-    key bits are at least the k-th largest key's, sorted in LDS, when there
+    """Rows of up to 2^17 elements and 256 < k <= 8192 keep the keys whose top
+    8 key bits are at least the k-th largest key's, sorted in LDS, when there
     are at most 16384 of them, and are finished the long way otherwise.  Here
     n_top elements of a row share the top key byte of the k-th (values 2 + i
     * 2^-20, all with the same exponent), the rest lie below it (or above it,
     for the smallest k); ties of equal values mixed in."""
     announce("topk capacity edge", n_top, largest)
-    rows, length, k = 3, 131_072, 100
+    rows, length, k = 3, 131_072, 300
     rng = np.random.default_rng(n_top)
     x = np.full((rows, length), 0.5 if largest else 8.0, np.float32)
     for r in range(rows):
@@ -179,8 +179,10 @@ def test_topk_candidate_capacity_edges(ops, n_top, largest):
 @pytest.mark.parametrize("k", [1, 37, 4096, 8192])
 def test_topk_long_way_close_values(ops, k):
     """Every key of the row in one top byte (values in [1, 2): one exponent):
-    the rows are finished the long way, whose three further digit rounds must
-    separate values that differ only in their low mantissa bits."""
+    at k = 4096 and 8192 the rows are finished the long way, whose three
+    further digit rounds must separate values that differ only in their low
+    mantissa bits; at k = 1 and 37 each tile's candidates share the top 16
+    bits of its k-th key and the finisher's rounds separate the rest."""
     announce("topk long way", k)
     rng = np.random.default_rng(k)
     x = (1.0 + rng.integers(0, 1 << 23, (4, 65_536)) * 2.0**-23).astype(np.float32)
