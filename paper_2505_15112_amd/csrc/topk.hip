@@ -298,6 +298,13 @@ constexpr int kTopkFinishThreads = 1024;
 constexpr uint32_t kTopkSortAll = 2048;  // candidates sorted whole, without the cut to k
 constexpr uint32_t kTopkSmallBucket = 128;  // a cut round's bucket finished by one sort
 constexpr uint32_t kTopkRankMax = 256;  // kept keys placed by rank instead of sorted
+// Outputs per finishing workgroup on the gather route: a row with larger k
+// is finished by topk_parts(k) workgroups, each cutting and sorting one
+// slice of ranks (smaller sorts, and the chip's other CUs put to work).
+constexpr uint32_t kTopkPartKeys = 2048;
+__host__ __device__ inline uint32_t topk_parts(uint32_t k) {
+    return k > kTopkPartKeys ? (k + kTopkPartKeys - 1) / kTopkPartKeys : 1u;
+}
 static_assert(kTopkSortMax <= kTopkCand, "the k kept fit the finisher's sort");
 
 // The composite sort key of element i with key `key`: larger keys first,
@@ -810,7 +817,13 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
     __shared__ uint32_t s_rank[kTopkRankMax];
     constexpr uint32_t kT = kTopkFinishThreads;
     static_assert(!TILES || kTopkTileSlots <= kT, "one tile slot per thread");
-    const int64_t row = blockIdx.x;
+    // A row's outputs are split between topk_parts(k) workgroups: part q
+    // writes ranks [lo, hi) = [q P, min((q + 1) P, k)), P = kTopkPartKeys.
+    const uint32_t parts = TILES ? 1u : topk_parts(k);
+    const int64_t row = blockIdx.x / parts;
+    const uint32_t part = blockIdx.x - (uint32_t)row * parts;
+    uint32_t lo = part * kTopkPartKeys;
+    uint32_t hi = k - lo < kTopkPartKeys ? k : lo + kTopkPartKeys;
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
     uint32_t* hcopy = s_h + (lane & (kTopkCopies - 1)) * kTopkCopyStride;
@@ -845,6 +858,10 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
     } else {
         m = (uint32_t)gather[2 * row];
         fits = m <= cap;
+        if (!fits) {  // uniform: part 0 finishes the row the long way, all k ranks
+            if (part != 0) return;
+            hi = k;
+        }
     }
     const uint32_t sort_all = TILES ? kTopkRankMax : kTopkSortAll;
     if (fits) {
@@ -893,10 +910,12 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
 #pragma unroll
         for (int e = 0; e < kPer; ++e)
             if ((vmask >> e) & 1u) s[slot_lds(e)] = mine[e];
-        uint64_t prefix = TILES ? 0ull : ((uint32_t)state[2 * row] & 255u);
-        uint32_t kk = TILES ? k : (uint32_t)state[2 * row + 1];
-        const bool cut = m > k && m > sort_all;  // uniform
-        for (int r = TILES ? 0 : 1; r < 8 && cut; ++r) {
+        // The kk-th largest of the candidates whose top 8 r0 bits are
+        // `prefix`: digit rounds from digit r0 on, each keeping the bucket
+        // that holds it, until the last digit or a bucket small enough to
+        // rank.
+        auto find_kth = [&](uint32_t kk, int r0, uint64_t prefix) -> uint64_t {
+        for (int r = r0; r < 8; ++r) {
             for (uint32_t i = threadIdx.x; i < kTopkCopies * kTopkCopyStride; i += kT) s_h[i] = 0;
             __syncthreads();  // also: the candidates are in LDS
             const int hs = 64 - 8 * r, ds = 56 - 8 * r;
@@ -949,15 +968,32 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
                 break;
             }
         }
-        // prefix: the k-th largest composite; each thread still holds its
-        // candidates in `mine`.  Cut: the k at or above it go to s[0, k), each
-        // thread's after those of the threads before it (a workgroup scan).
-        // Otherwise all m are in s[0, m) already.
+        return prefix;
+        };
+        const bool cut = parts > 1 || (m > k && m > sort_all);  // uniform
+        // Cut: the composites of ranks [lo, hi), those in [C_hi, C_lo) with
+        // C_r the r-th largest (C_0 above every key).  C_k from the bucket
+        // the count round chose (TILES: from the top byte on), other ranks
+        // from the top byte on.
+        uint64_t c_hi = 0, c_lo = ~0ull;
+        if (cut) {
+            if (TILES)
+                c_hi = find_kth(k, 0, 0ull);
+            else if (hi == k)
+                c_hi = find_kth((uint32_t)state[2 * row + 1], 1, (uint32_t)state[2 * row] & 255u);
+            else
+                c_hi = find_kth(hi, 0, 0ull);
+            if (part != 0) c_lo = find_kth(lo, 0, 0ull);
+        }
+        // Each thread still holds its candidates in `mine`.  Cut: the kept
+        // ones go to s[0, hi - lo), each thread's after those of the threads
+        // before it (a workgroup scan).  Otherwise all m are in s[0, m)
+        // already.
         if (cut) {
             uint32_t keep = 0, cnt = 0;
 #pragma unroll
             for (int e = 0; e < kPer; ++e) {
-                const bool kp = ((vmask >> e) & 1u) && mine[e] >= prefix;
+                const bool kp = ((vmask >> e) & 1u) && mine[e] >= c_hi && mine[e] < c_lo;
                 keep |= (kp ? 1u : 0u) << e;
                 cnt += kp ? 1u : 0u;
             }
@@ -970,7 +1006,7 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
 #pragma unroll
             for (int e = 0; e < kPer; ++e) {
                 if ((keep >> e) & 1u) {
-                    if (pos < cap) s[pos] = mine[e];  // pos < k; checked all the same
+                    if (pos < cap) s[pos] = mine[e];  // pos < hi - lo; checked all the same
                     ++pos;
                 }
             }
@@ -1036,9 +1072,11 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
             __syncthreads();
         }
     }
-    // the n kept keys are s[0, n) (n >= k)
-    const uint32_t n = (fits && m <= sort_all) ? m : k;
-    auto emit = [&](uint32_t p, uint64_t c) {  // output p (< k): composite c
+    // the n kept keys are s[0, n): this part's hi - lo (all of them, n >= k,
+    // when the candidates were sorted whole); outputs from rank lo on
+    const uint32_t n = (fits && m <= sort_all) ? m : hi - lo;
+    auto emit = [&](uint32_t p0, uint64_t c) {  // output lo + p0 (< k): composite c
+        const uint32_t p = lo + p0;
         const uint32_t key = (uint32_t)(c >> 32);
         const uint32_t code = largest ? key : ~key;
         values[row * k + p] = code ^ ((code >> 31) ? 0x80000000u : 0xFFFFFFFFu);
@@ -1051,7 +1089,7 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
         rank_keys(s, n, s_rank);
         if (threadIdx.x < n) {
             const uint32_t r = s_rank[threadIdx.x];
-            if (r < k) emit(r, s[threadIdx.x]);
+            if (r < hi - lo) emit(r, s[threadIdx.x]);
         }
         return;
     }
@@ -1088,7 +1126,7 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             const uint32_t p = threadIdx.x * E + e;
-            if (p < k) emit(p, v[e]);
+            if (p < hi - lo) emit(p, v[e]);
         }
     };
     if (npow <= kT)
@@ -1217,10 +1255,10 @@ static hipError_t topk_gather(bool vec, const uint32_t* x, int64_t rows, int64_t
     // the LDS sort sized to the row (cap <= CAP)
     auto kf = cap > 8192 ? k_topk_finish<kTopkCand, false>
                          : (cap > 2048 ? k_topk_finish<8192, false> : k_topk_finish<2048, false>);
-    hipLaunchKernelGGL(kf, dim3((uint32_t)rows), dim3(kTopkFinishThreads), 0, stream, x, len, kk,
-                       largest, (const uint64_t*)state, (const uint64_t*)gather,
-                       (const uint64_t*)cand, cap, segs, (const uint32_t*)nullptr, values,
-                       indices);
+    hipLaunchKernelGGL(kf, dim3((uint32_t)rows * topk_parts(kk)), dim3(kTopkFinishThreads), 0,
+                       stream, x, len, kk, largest, (const uint64_t*)state,
+                       (const uint64_t*)gather, (const uint64_t*)cand, cap, segs,
+                       (const uint32_t*)nullptr, values, indices);
     return hipGetLastError();
 }
 
