@@ -585,7 +585,8 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY8 void k_topk_tilesel(
     for (int j = 0; j < TileT::J; ++j) {
         const int32_t off = (int32_t)TileT::lane_offset(j);
 #pragma unroll
-        for (int e = 0; e < TileT::V; ++e) inrow |= (Mask)(off + e < valid ? 1u : 0u) << (j * TileT::V + e);
+        for (int e = 0; e < TileT::V; ++e)
+            inrow |= (Mask)(off + e < valid ? 1u : 0u) << (j * TileT::V + e);
     }
     asm volatile("" : "+v"(inrow));
     // round 0: the top byte of every key of the tile.  Positions past the
@@ -915,60 +916,61 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
         // that holds it, until the last digit or a bucket small enough to
         // rank.
         auto find_kth = [&](uint32_t kk, int r0, uint64_t prefix) -> uint64_t {
-        for (int r = r0; r < 8; ++r) {
-            for (uint32_t i = threadIdx.x; i < kTopkCopies * kTopkCopyStride; i += kT) s_h[i] = 0;
-            __syncthreads();  // also: the candidates are in LDS
-            const int hs = 64 - 8 * r, ds = 56 - 8 * r;
-            for (uint32_t i = threadIdx.x; i < m; i += kT) {
-                const uint64_t c = s[i];
-                if (r == 0 || (c >> hs) == prefix)
-                    atomicAdd(&hcopy[(uint32_t)(c >> ds) & 255u], 1u);
-            }
-            __syncthreads();
-            const int t = threadIdx.x;
-            const uint32_t c = digit_count(t);
-            const uint32_t inc = wave_incl_scan(c);
-            if (t < kTopkDigits && lane == kWave - 1) s_part[w] = inc;
-            __syncthreads();
-            if (t < kTopkDigits) {
-                uint32_t before = 0;
-                for (int q = 0; q < w; ++q) before += s_part[q];
-                const uint32_t at_least = before + inc, above = at_least - c;
-                if (above < kk && kk <= at_least) {  // exactly one thread
-                    s_prefix64 = (prefix << 8) | (uint32_t)(kTopkDigits - 1 - t);
-                    s_kk = kk - above;
-                    s_bucket = c;
-                }
-            }
-            __syncthreads();
-            prefix = s_prefix64;
-            kk = s_kk;
-            if (s_bucket <= kTopkSmallBucket) {  // uniform
-                // A bucket this small is finished in one step instead of
-                // more rounds: its composites are gathered and ranked, and
-                // the one with kk - 1 above it is the k-th largest composite
-                // of the row.
-                const int hs2 = 56 - 8 * r;  // the new prefix's shift
-                const uint32_t nb = s_bucket;  // >= kk >= 1
-                if (threadIdx.x == 0) s_nsmall = 0;
-                __syncthreads();
+            for (int r = r0; r < 8; ++r) {
+                for (uint32_t i = threadIdx.x; i < kTopkCopies * kTopkCopyStride; i += kT)
+                    s_h[i] = 0;
+                __syncthreads();  // also: the candidates are in LDS
+                const int hs = 64 - 8 * r, ds = 56 - 8 * r;
                 for (uint32_t i = threadIdx.x; i < m; i += kT) {
-                    const uint64_t c2 = s[i];
-                    if ((c2 >> hs2) == prefix) {
-                        const uint32_t pos = atomicAdd(&s_nsmall, 1u);
-                        if (pos < kTopkSmallBucket) s_small[pos] = c2;  // below the bucket size
+                    const uint64_t c = s[i];
+                    if (r == 0 || (c >> hs) == prefix)
+                        atomicAdd(&hcopy[(uint32_t)(c >> ds) & 255u], 1u);
+                }
+                __syncthreads();
+                const int t = threadIdx.x;
+                const uint32_t c = digit_count(t);
+                const uint32_t inc = wave_incl_scan(c);
+                if (t < kTopkDigits && lane == kWave - 1) s_part[w] = inc;
+                __syncthreads();
+                if (t < kTopkDigits) {
+                    uint32_t before = 0;
+                    for (int q = 0; q < w; ++q) before += s_part[q];
+                    const uint32_t at_least = before + inc, above = at_least - c;
+                    if (above < kk && kk <= at_least) {  // exactly one thread
+                        s_prefix64 = (prefix << 8) | (uint32_t)(kTopkDigits - 1 - t);
+                        s_kk = kk - above;
+                        s_bucket = c;
                     }
                 }
                 __syncthreads();
-                rank_keys(s_small, nb, s_rank);
-                if (threadIdx.x < nb && s_rank[threadIdx.x] == kk - 1)  // exactly one
-                    s_prefix64 = s_small[threadIdx.x];
-                __syncthreads();
                 prefix = s_prefix64;
-                break;
+                kk = s_kk;
+                if (s_bucket <= kTopkSmallBucket) {  // uniform
+                    // A bucket this small is finished in one step instead of
+                    // more rounds: its composites are gathered and ranked, and
+                    // the one with kk - 1 above it is the k-th largest composite
+                    // of the row.
+                    const int hs2 = 56 - 8 * r;  // the new prefix's shift
+                    const uint32_t nb = s_bucket;  // >= kk >= 1
+                    if (threadIdx.x == 0) s_nsmall = 0;
+                    __syncthreads();
+                    for (uint32_t i = threadIdx.x; i < m; i += kT) {
+                        const uint64_t c2 = s[i];
+                        if ((c2 >> hs2) == prefix) {
+                            const uint32_t pos = atomicAdd(&s_nsmall, 1u);
+                            if (pos < kTopkSmallBucket) s_small[pos] = c2;  // below the bucket size
+                        }
+                    }
+                    __syncthreads();
+                    rank_keys(s_small, nb, s_rank);
+                    if (threadIdx.x < nb && s_rank[threadIdx.x] == kk - 1)  // exactly one
+                        s_prefix64 = s_small[threadIdx.x];
+                    __syncthreads();
+                    prefix = s_prefix64;
+                    break;
+                }
             }
-        }
-        return prefix;
+            return prefix;
         };
         const bool cut = parts > 1 || (m > k && m > sort_all);  // uniform
         // Cut: the composites of ranks [lo, hi), those in [C_hi, C_lo) with
