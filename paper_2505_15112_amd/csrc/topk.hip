@@ -360,7 +360,8 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_topk_count0(
 
 __global__ __launch_bounds__(kTopkDigits) void k_topk_bucket(const uint32_t* hist, uint32_t segs,
                                                              uint32_t k, uint64_t* state,
-                                                             uint64_t* gather, uint32_t* offs) {
+                                                             uint64_t* gather, uint32_t* offs,
+                                                             uint32_t* rowhist) {
     __shared__ uint32_t s_part[kTopkDigits / kWave];
     __shared__ uint32_t s_d;
     __shared__ uint32_t s_tile[kTopkDigits / kWave][kTopkGatherSegs];
@@ -378,6 +379,7 @@ __global__ __launch_bounds__(kTopkDigits) void k_topk_bucket(const uint32_t* his
         c[q] = q < segs ? rh[(int64_t)q * kTopkDigits] : 0u;
         cnt += c[q];
     }
+    rowhist[row * kTopkDigits + t] = cnt;  // the row's count of digit 255 - t
     const uint32_t inc = wave_incl_scan(cnt);
     if (lane == kWave - 1) s_part[w] = inc;
     __syncthreads();
@@ -804,7 +806,7 @@ template <uint32_t CAP, bool TILES>
 __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
     const uint32_t* x, int64_t len, uint32_t k, bool largest, const uint64_t* state,
     const uint64_t* gather, const uint64_t* cand, uint32_t cap, uint32_t segs,
-    const uint32_t* tcount, uint32_t* values, int32_t* indices) {
+    const uint32_t* tcount, const uint32_t* rowhist, uint32_t* values, int32_t* indices) {
     static_assert(CAP <= kTopkCand && (CAP & (CAP - 1)) == 0, "LDS sort size");
     __shared__ uint64_t s[CAP];
     // digit counts: one copy per lane position, as in k_topk_count0 (the
@@ -813,6 +815,7 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
     __shared__ uint32_t s_part[kTopkFinishThreads / kWave];
     __shared__ uint32_t s_prefix, s_kk, s_n, s_qbase, s_bucket, s_nsmall, s_m, s_over;
     __shared__ uint64_t s_prefix64;
+    __shared__ uint32_t s_dig[2], s_dkk[2];
     __shared__ uint64_t s_small[kTopkSmallBucket];
     __shared__ uint32_t s_off[kTopkGatherSegs], s_cnt[kTopkGatherSegs];
     __shared__ uint32_t s_rank[kTopkRankMax];
@@ -825,6 +828,13 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
     const uint32_t part = blockIdx.x - (uint32_t)row * parts;
     uint32_t lo = part * kTopkPartKeys;
     uint32_t hi = k - lo < kTopkPartKeys ? k : lo + kTopkPartKeys;
+    // the row's top-byte counts (thread t: digit 255 - t), loaded under the
+    // candidate loads: they place a slice's boundaries without a digit round
+    // over the candidates (the keys with the top byte of the k-th or more are
+    // all candidates, and every boundary rank is at most k)
+    uint32_t rh = 0;
+    if (!TILES && parts > 1 && threadIdx.x < kTopkDigits)
+        rh = rowhist[row * kTopkDigits + threadIdx.x];
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
     uint32_t* hcopy = s_h + (lane & (kTopkCopies - 1)) * kTopkCopyStride;
@@ -978,14 +988,35 @@ __global__ __launch_bounds__(kTopkFinishThreads) void k_topk_finish(
         // the count round chose (TILES: from the top byte on), other ranks
         // from the top byte on.
         uint64_t c_hi = 0, c_lo = ~0ull;
-        if (cut) {
-            if (TILES)
-                c_hi = find_kth(k, 0, 0ull);
-            else if (hi == k)
-                c_hi = find_kth((uint32_t)state[2 * row + 1], 1, (uint32_t)state[2 * row] & 255u);
-            else
-                c_hi = find_kth(hi, 0, 0ull);
-            if (part != 0) c_lo = find_kth(lo, 0, 0ull);
+        if (cut && parts > 1) {
+            // the top bytes of C_hi and C_lo and their ranks within those
+            // bytes' buckets, from the row's counts
+            const int t = threadIdx.x;
+            const uint32_t c = t < kTopkDigits ? rh : 0u;
+            const uint32_t inc = wave_incl_scan(c);
+            if (t < kTopkDigits && lane == kWave - 1) s_part[w] = inc;
+            __syncthreads();
+            if (t < kTopkDigits) {
+                uint32_t before = 0;
+                for (int q = 0; q < w; ++q) before += s_part[q];
+                const uint32_t at_least = before + inc, above = at_least - c;
+                const uint32_t tgt[2] = {hi, lo};
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+                    if (above < tgt[q] && tgt[q] <= at_least) {  // one thread each (lo: if > 0)
+                        s_dig[q] = (uint32_t)(kTopkDigits - 1 - t);
+                        s_dkk[q] = tgt[q] - above;
+                    }
+                }
+            }
+            __syncthreads();
+            const uint32_t d_hi = s_dig[0], kk_hi = s_dkk[0], d_lo = s_dig[1], kk_lo = s_dkk[1];
+            c_hi = find_kth(kk_hi, 1, d_hi);
+            if (part != 0) c_lo = find_kth(kk_lo, 1, d_lo);
+        } else if (cut) {
+            c_hi = TILES ? find_kth(k, 0, 0ull)
+                         : find_kth((uint32_t)state[2 * row + 1], 1,
+                                    (uint32_t)state[2 * row] & 255u);
         }
         // Each thread still holds its candidates in `mine`.  Cut: the kept
         // ones go to s[0, hi - lo), each thread's after those of the threads
@@ -1167,7 +1198,7 @@ static uint32_t topk_cap(int64_t len) {
     return (uint32_t)(len < (int64_t)kTopkCand ? len : (int64_t)kTopkCand);
 }
 struct TopkLayout {
-    size_t hist, state, arrivals, gather, offs, end;
+    size_t hist, state, arrivals, gather, offs, rowhist, end;
 };
 static TopkLayout topk_layout(int64_t rows, int64_t len, int64_t k) {
     const int64_t t = topk_gather_route(len, k) ? topk_gather_tile(len) : row_tile(len);
@@ -1178,7 +1209,9 @@ static TopkLayout topk_layout(int64_t rows, int64_t len, int64_t k) {
     l.arrivals = l.state + (size_t)rows * 2 * sizeof(uint64_t);
     l.gather = l.arrivals + (size_t)rows * sizeof(uint64_t);
     l.offs = l.gather + (size_t)rows * 2 * sizeof(uint64_t);
-    l.end = l.offs + (topk_gather_route(len, k) ? (size_t)rows * kTopkGatherSegs * 4 : 0);
+    const bool g = topk_gather_route(len, k);
+    l.rowhist = l.offs + (g ? (size_t)rows * kTopkGatherSegs * 4 : 0);
+    l.end = l.rowhist + (g ? (size_t)rows * kTopkDigits * 4 : 0);
     return l;
 }
 size_t topk_ws_bytes(int64_t rows, int64_t len, int64_t k) {
@@ -1249,8 +1282,9 @@ static hipError_t topk_gather(bool vec, const uint32_t* x, int64_t rows, int64_t
     if (segs > kTopkGatherSegs) return hipErrorInvalidValue;  // not on this route
     hipLaunchKernelGGL((vec ? k_topk_count0<TV, true> : k_topk_count0<TU, false>), dim3(nt),
                        dim3(threads), 0, stream, x, len, segs, largest, hist);
+    uint32_t* rowhist = reinterpret_cast<uint32_t*>(w + l.rowhist);
     hipLaunchKernelGGL(k_topk_bucket, dim3((uint32_t)rows), dim3(kTopkDigits), 0, stream,
-                       (const uint32_t*)hist, segs, kk, state, gather, offs);
+                       (const uint32_t*)hist, segs, kk, state, gather, offs, rowhist);
     hipLaunchKernelGGL((vec ? k_topk_gather<TV, true> : k_topk_gather<TU, false>), dim3(nt),
                        dim3(threads), 0, stream, x, len, segs, largest, (const uint64_t*)state,
                        (const uint64_t*)gather, (const uint32_t*)offs, cand, cap);
@@ -1260,7 +1294,7 @@ static hipError_t topk_gather(bool vec, const uint32_t* x, int64_t rows, int64_t
     hipLaunchKernelGGL(kf, dim3((uint32_t)rows * topk_parts(kk)), dim3(kTopkFinishThreads), 0,
                        stream, x, len, kk, largest, (const uint64_t*)state,
                        (const uint64_t*)gather, (const uint64_t*)cand, cap, segs,
-                       (const uint32_t*)nullptr, values, indices);
+                       (const uint32_t*)nullptr, (const uint32_t*)rowhist, values, indices);
     return hipGetLastError();
 }
 
@@ -1293,8 +1327,8 @@ static hipError_t topk_tiles(bool vec, const uint32_t* x, int64_t rows, int64_t 
                                                 : k_topk_finish<2048, true>);
     hipLaunchKernelGGL(kf, dim3((uint32_t)rows), dim3(kTopkFinishThreads), 0, stream, x, len, kk,
                        largest, (const uint64_t*)nullptr, (const uint64_t*)nullptr,
-                       (const uint64_t*)cand, cap, segs, (const uint32_t*)tcount, values,
-                       indices);
+                       (const uint64_t*)cand, cap, segs, (const uint32_t*)tcount,
+                       (const uint32_t*)nullptr, values, indices);
     return hipGetLastError();
 }
 
