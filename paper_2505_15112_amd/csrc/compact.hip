@@ -46,6 +46,7 @@ constexpr int kCountBlocks = 256;
 // registers and the per-tile look-back is paid rarely.
 constexpr int kPWaves = 8;
 constexpr int kPChunks = 16;
+constexpr int kPStage = 4;  // chunks staged per write-out (with indices)
 constexpr int64_t kPTile = kPWaves * kPChunks * kWave * 4;
 
 template <bool VEC, bool WITH_IDX, int WAVES, int CHUNKS>
@@ -56,8 +57,13 @@ __global__ __launch_bounds__(WAVES* kWave) LS_OCCUPANCY4 void k_compact(
     __shared__ Ticket s_ticket;
     __shared__ uint32_t s_wtot[WAVES];
     __shared__ uint32_t s_carry;
-    __shared__ float s_val[WAVES][kWave * 4];
-    __shared__ int32_t s_idx[WITH_IDX ? WAVES : 1][kWave * 4];
+    // STAGE chunks of kept values (and indices) per wave between stores: as
+    // many as leave room in LDS for two workgroups per CU (values only on the
+    // 8-wave tile: twice as many)
+    constexpr int STAGE = WAVES > kPWaves ? kPStage / 2 : (WITH_IDX ? kPStage : 2 * kPStage);
+    static_assert(CHUNKS % STAGE == 0, "whole batches of chunks");
+    __shared__ float s_val[WAVES][kWave * 4 * STAGE];
+    __shared__ int32_t s_idx[WITH_IDX ? WAVES : 1][kWave * 4 * STAGE];
 
     if (threadIdx.x == 0) s_ticket = take_ticket(hdr, ntiles);
     __syncthreads();
@@ -127,25 +133,30 @@ __global__ __launch_bounds__(WAVES* kWave) LS_OCCUPANCY4 void k_compact(
         }
     }
     __syncthreads();
-    // The kept elements of one chunk form one contiguous output run: gather
-    // them in this wave's LDS slot, then write the run with consecutive lanes.
+    // The kept elements of a batch of STAGE consecutive chunks form one
+    // contiguous output run: gather them in this wave's LDS slot, then write
+    // the run with consecutive lanes (one LDS round trip per batch).
     const uint32_t c0 = s_carry + wofs;
     float* st = s_val[w];
     int32_t* si = s_idx[WITH_IDX ? w : 0];
 #pragma unroll
-    for (int j = 0; j < CHUNKS; ++j) {
-        const int64_t off = offset(j);
-        const uint32_t run0 = lane_read(lane_off[j], 0);  // kept before this chunk, in the wave
-        uint32_t r = lane_off[j] - run0;
+    for (int j0 = 0; j0 < CHUNKS; j0 += STAGE) {
+        const uint32_t run0 = lane_read(lane_off[j0], 0);  // kept before this batch, in the wave
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            if ((kept[j] >> (8 * e)) & 1u) {
-                st[r] = xv[j][e];
-                if (WITH_IDX) si[r] = (int32_t)(off + e);
-                ++r;
+        for (int j = j0; j < j0 + STAGE; ++j) {
+            const int64_t off = offset(j);
+            uint32_t r = lane_off[j] - run0;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if ((kept[j] >> (8 * e)) & 1u) {
+                    st[r] = xv[j][e];
+                    if (WITH_IDX) si[r] = (int32_t)(off + e);
+                    ++r;
+                }
             }
         }
-        const uint32_t cnt = (j + 1 < CHUNKS ? lane_read(lane_off[j + 1], 0) : run) - run0;
+        const uint32_t cnt =
+            (j0 + STAGE < CHUNKS ? lane_read(lane_off[j0 + STAGE], 0) : run) - run0;
         wave_lds_sync();
         const uint32_t dst = c0 + run0;
         for (uint32_t t = lane; t < cnt; t += kWave) {
