@@ -51,6 +51,28 @@ def test_compact(ops, n):
     _check_compact(ops, x, W.mask_u8(n, seed=1), False, f"compact n={n} no idx")
 
 
+@pytest.mark.parametrize("which", ["out", "idx"])
+def test_compact_outputs_not_16_byte_aligned(ops, which):
+    """Aligned input, an output 4 bytes off 16-byte alignment: the kept runs
+    are written element by element instead of as aligned 16-byte quads."""
+    import torch
+    announce("compact unaligned output", which)
+    n = 3 * 32768 + 5
+    x = W.values_f32(n, seed=9)
+    m = W.mask_u8(n, seed=9)
+    ob = torch.empty(n + 1, dtype=torch.float32, device="cuda")
+    ib = torch.empty(n + 1, dtype=torch.int32, device="cuda")
+    out = ob[1:] if which == "out" else ob[:n]
+    idx = ib[1:] if which == "idx" else ib[:n]
+    out, idx, cnt = ops.compact_by_mask_f32(to_dev(x), to_dev(m), with_idx=True, out=out,
+                                            idx_out=idx)
+    ro, ri = oracle.compact_f32(x, m)
+    c = int(cnt.item())
+    assert c == ro.size
+    assert_equal_first_diff(to_host(out)[:c].view(np.uint32), ro.view(np.uint32), which + " values")
+    assert_equal_first_diff(to_host(idx)[:c], ri, which + " idx")
+
+
 def test_compact_misaligned_and_empty(ops):
     import torch
     announce("compact misaligned/empty")
