@@ -157,23 +157,25 @@ def test_topk_repeated_calls_share_workspace(ops):
     assert ops.workspace_error(ws) == 0
 
 
+@pytest.mark.parametrize("k", [300, 4096])
 @pytest.mark.parametrize("n_top", [16_383, 16_384, 16_385])
 @pytest.mark.parametrize("largest", [True, False])
-def test_topk_candidate_capacity_edges(ops, n_top, largest):
+def test_topk_candidate_capacity_edges(ops, n_top, largest, k):
     """Rows of up to 2^17 elements and 256 < k <= 8192 keep the keys whose top
     8 key bits are at least the k-th largest key's, sorted in LDS, when there
     are at most 16384 of them, and are finished the long way otherwise.  Here
     n_top elements of a row share the top key byte of the k-th (values 2 + i
     * 2^-20, all with the same exponent), the rest lie below it (or above it,
-    for the smallest k); ties of equal values mixed in."""
-    announce("topk capacity edge", n_top, largest)
-    rows, length, k = 3, 131_072, 300
+    for the smallest k); ties of equal values mixed in.  At k = 4096 the rows
+    that fit are finished by two workgroups, one per 2048 ranks."""
+    announce("topk capacity edge", n_top, largest, k)
+    rows, length = 3, 131_072
     rng = np.random.default_rng(n_top)
     x = np.full((rows, length), 0.5 if largest else 8.0, np.float32)
     for r in range(rows):
         pos = rng.choice(length, n_top, replace=False)
         x[r, pos] = (2.0 + rng.integers(0, 64, n_top) * 2.0**-20).astype(np.float32)
-    _check(ops, x, k, largest, f"capacity edge n_top={n_top} largest={largest}")
+    _check(ops, x, k, largest, f"capacity edge n_top={n_top} largest={largest} k={k}")
 
 
 @pytest.mark.parametrize("k", [1, 37, 4096, 8192])
