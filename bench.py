@@ -413,8 +413,8 @@ def main():
             "pct_of_memcpy": round(100.0 * g_f32 / g_cp, 2),
         },
         "roofline": {
-            "kernel": "k_scan_lookback_lds<u32,20,9> (int32 inclusive, 59392-element tiles: "
-                      "20 register + 9 LDS chunks of 1 KB per wave, 16-byte vector path)",
+            "kernel": "k_scan_lookback_lds<u32,19,9,16> (int32 inclusive, 114688-element tiles: "
+                      "16 waves x (19 register + 9 LDS chunks of 1 KB), 16-byte vector path)",
             "bound": "hbm",
             "achieved": round(g_i32, 2),
             "peak": PEAK_HBM_GBPS,

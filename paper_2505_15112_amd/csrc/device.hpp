@@ -15,9 +15,9 @@
 #include <stdint.h>
 
 // Register budget of the tile kernels: at least 4 waves per SIMD, i.e. at
-// most 128 VGPRs, so two 8-wave (or four 4-wave) workgroups share a CU.  A
-// tile's data lives in registers from its loads to its stores, so this is
-// what bounds the bytes in flight per CU.
+// most 128 VGPRs, so 16 waves share a CU (two 8-wave workgroups, four 4-wave
+// ones or one of 16).  A tile's data lives in registers from its loads to its
+// stores, so this is what bounds the bytes in flight per CU.
 #define LS_OCCUPANCY4 __attribute__((amdgpu_waves_per_eu(4)))
 // At most 64 VGPRs (8 waves per SIMD): for short tile kernels launched with
 // about as many workgroups as fit the chip at that occupancy, so that none

@@ -23,7 +23,7 @@ namespace ls {
 // and 32768-element tiles match it.  A tile's data stays in registers from
 // its loads until its stores, so the bytes in flight per CU are set by how
 // much of the register file holds data: the large integer tile keeps 80 of
-// at most 128 VGPRs per lane as data (two 8-wave workgroups per CU); the
+// at most 128 VGPRs per lane as data (16 waves per CU); the
 // float scans need more scratch registers and keep 64.  Small arrays want
 // more, smaller tiles to occupy the 256 CUs.  Between 2^22 and 2^27 integer
 // elements the 32768-element tile is faster than the 40960-element one
@@ -101,27 +101,31 @@ __global__ __launch_bounds__(TileT::kThreads) LS_OCCUPANCY4 void k_scan_lookback
 // Same single pass, but each wave also owns L further 1 KB chunks that are
 // loaded straight into LDS (global_load_lds_dwordx4, no VGPRs) and read back
 // only for the chunk totals and for the stores.  Registers cap what a tile
-// can hold while it waits for its predecessors; LDS adds 72 KB per workgroup
-// (two workgroups per CU still fit), so the same number of tiles in flight
-// carries 45 % more bytes.  Measured at n = 2^28: int32 420 -> 405 us, fp32
-// 426 -> 410 us.  Wave w owns chunks [w*JT, (w+1)*JT) of the tile (JT = J+L),
+// can hold while it waits for its predecessors; LDS adds 9 KB per wave, so
+// the same number of tiles in flight carries 45 % more bytes.  Measured at
+// n = 2^28: int32 420 -> 405 us, fp32 426 -> 410 us (two 8-wave workgroups
+// per CU).  One 16-wave workgroup per CU (144 KB of LDS), with the same
+// chunks per wave, halves the tiles and with them the tickets and the
+// look-back chain: 402 -> 393 us (int32, 19 register chunks: 20 spill) and
+// 410 -> 402 us (fp32); 4-wave workgroups, four per CU, took 428 us and
+// 2-wave ones 479.  Wave w owns chunks [w*JT, (w+1)*JT) of the tile (JT = J+L),
 // register chunks first.  Only full tiles take this path; a ragged last tile
 // scans its elements in at most two passes of register-only sub-tiles, the
 // first one loaded before its look-back (no tile waits on the last one).
-template <class T, int J, int L>
+template <class T, int J, int L, int WV>
 struct LdsGeom {
-    static constexpr int W = 8, JT = J + L;
+    static constexpr int W = WV, JT = J + L;
     static constexpr int kThreads = W * kWave;
     static constexpr int64_t kElems = (int64_t)W * JT * kWave * 4;
 };
 
-template <class T, int J, int L, bool EXCL>
-__global__ __launch_bounds__(8 * kWave) LS_OCCUPANCY4 void k_scan_lookback_lds(
+template <class T, int J, int L, int WV, bool EXCL>
+__global__ __launch_bounds__(WV * kWave) LS_OCCUPANCY4 void k_scan_lookback_lds(
     const T* x, T* y, int64_t n, WsHeader* hdr, uint64_t* status, int64_t status_words,
     uint32_t ntiles, const T* carry_in, T* total_out) {
-    using G = LdsGeom<T, J, L>;
-    static_assert(G::kThreads == 8 * kWave, "launch bounds");
-    using Sub = Tile<T, T, 4, 16, G::W>;  // passes over a ragged last tile (32768 elements)
+    using G = LdsGeom<T, J, L, WV>;
+    static_assert(G::kThreads == WV * kWave, "launch bounds");
+    using Sub = Tile<T, T, 4, 16, G::W>;  // passes over a ragged last tile (65536 elements)
     static_assert(2 * Sub::kElems >= G::kElems, "a ragged tile takes at most two passes");
     __shared__ u32x4 s_buf[G::W * L * kWave];
     __shared__ Ticket s_ticket;
@@ -345,22 +349,22 @@ static void scan1d_geom(bool exclusive, const In* x, T* y, int64_t n, const T* c
                        status_words, nt, carry_in, total_out);
 }
 
-// Register + LDS tiles for the largest 32-bit arrays: 59392 (integer) or
-// 51200 (float) elements per tile, the most that fits 128 VGPRs and 72 KB of
-// LDS per workgroup.
+// Register + LDS tiles for the largest 32-bit arrays: 114688 (integer) or
+// 102400 (float) elements per tile, one 16-wave workgroup per CU, the most
+// that fits 128 VGPRs per lane without spilling and 160 KB of LDS.
 template <class T>
 struct LdsChunks {
-    static constexpr int J = std::is_same<T, float>::value ? 16 : 20, L = 9;
+    static constexpr int J = std::is_same<T, float>::value ? 16 : 19, L = 9, W = 16;
 };
 
 template <class T>
 static void scan1d_lds(bool exclusive, const T* x, T* y, int64_t n, const T* carry_in,
                        T* total_out, WsHeader* hdr, uint64_t* status, int64_t status_words,
                        hipStream_t stream) {
-    constexpr int J = LdsChunks<T>::J, L = LdsChunks<T>::L;
-    using G = LdsGeom<T, J, L>;
+    constexpr int J = LdsChunks<T>::J, L = LdsChunks<T>::L, WV = LdsChunks<T>::W;
+    using G = LdsGeom<T, J, L, WV>;
     const uint32_t nt = (uint32_t)num_tiles(n, G::kElems);
-    auto k = exclusive ? k_scan_lookback_lds<T, J, L, true> : k_scan_lookback_lds<T, J, L, false>;
+    auto k = exclusive ? k_scan_lookback_lds<T, J, L, WV, true> : k_scan_lookback_lds<T, J, L, WV, false>;
     hipLaunchKernelGGL(k, dim3(nt), dim3(G::kThreads), 0, stream, x, y, n, hdr, status,
                        status_words, nt, carry_in, total_out);
 }

@@ -177,6 +177,15 @@ struct Tile {
         const int w = threadIdx.x / kWave;
         if (lane_id() == 0) s_wtot[w] = wave_total;
         __syncthreads();
+        if constexpr (WAVES > 8) {
+            // Many waves: the wave totals are scanned across lanes instead of
+            // summed by every lane in a loop, which holds one register per
+            // wave total (and spills the 16-wave tiles).
+            const T inc = wave_incl_scan(lane_id() < WAVES ? s_wtot[lane_id()] : T(0));
+            const int wu = __builtin_amdgcn_readfirstlane(w);
+            *wofs = wu > 0 ? lane_read(inc, wu - 1) : T(0);
+            return lane_read(inc, WAVES - 1);
+        }
         T before = T(0), agg = T(0);
 #pragma unroll
         for (int k = 0; k < WAVES; ++k) {

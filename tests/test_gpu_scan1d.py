@@ -189,13 +189,15 @@ def test_large_tiles_ragged(ops, kind, excl, shift):
         assert int(to_host(total)[0]) == rtot
 
 
-# Register + LDS tiles (n >= 2^27, 16-byte aligned 32-bit data): 59392-element
-# integer tiles and 51200-element float tiles.  Sizes: ragged last tile of
-# either kind, an exact multiple of each tile (the last full tile writes the
-# total), and a last tile holding one element.
-LDS_I32_TILE, LDS_F32_TILE = 59392, 51200
-LDS_SIZES = [1 << 27, LDS_I32_TILE * 2260, LDS_I32_TILE * 2260 + 1, LDS_F32_TILE * 2622,
-             LDS_F32_TILE * 2622 + 1]
+# Register + LDS tiles (n >= 2^27, 16-byte aligned 32-bit data): 114688-element
+# integer tiles and 102400-element float tiles; a ragged last tile is scanned
+# in passes of 65536.  Sizes: ragged last tiles of one pass (2^27 for integers,
+# a last tile of one element) and of two (2^27 for floats, 100000 elements
+# past a multiple of the integer tile), and an exact multiple of each tile
+# (the last full tile writes the total).
+LDS_I32_TILE, LDS_F32_TILE = 114688, 102400
+LDS_SIZES = [1 << 27, LDS_I32_TILE * 1170 + 100000, LDS_I32_TILE * 1171,
+             LDS_I32_TILE * 1171 + 1, LDS_F32_TILE * 1311, LDS_F32_TILE * 1311 + 1]
 
 
 @pytest.mark.skipif(not FULL, reason="full-size cases disabled")
